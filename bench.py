@@ -1,0 +1,374 @@
+#!/usr/bin/env python3
+"""Benchmark of the datapath executor on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input:
+
+  1. ReduceScatter, P=8 ranks, bf16, 134217728 elements (256 MiB) per rank,
+     chunk 1 MiB                               (one executor launch)
+  2. AllGather of its result (RS then AG = AllReduce), same shape (one launch)
+  3. MoE dispatch: pack 4096 x 7168 bf16 tokens, top-8 Zipf(1.1) routing over
+     256 experts on 8 ranks                     (three launches)
+  4. MoE combine of 32768 x 7168 bf16 expert outputs with fp32 gates
+                                                (one launch)
+
+Plans are built once per shape (host orchestration, like the paper's
+compile-time specialisation) and reused; every step re-executes them.
+
+value = algorithmic bytes of a step (reads + writes each op must make at
+least once) / wall time of a step, in GB/s (1e9 bytes/s).  Per-op times come
+from HIP events recorded on the stream the kernels run on.  The decode-size
+AllReduce (P=8, bf16, 128 x 8192 per rank) is timed separately as latency:
+128 calls captured in a graph, one warm-up replay, eight timed replays,
+time / 1024 (the paper's methodology, Section 5).
+
+Prints ONE JSON line.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "datapath GB/s (read+write) and % of HBM peak; small-message latency µs"
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+KERNEL_SOURCES = ["paper_2609_36954_amd/csrc/exec.hip", "paper_2609_36954_amd/csrc/moe.hip"]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def collective_bytes(op, P, N, s):
+    """Algorithmic bytes: every input byte read once, every output byte written once."""
+    if op == "reduce_scatter":
+        return P * N * s + N * s
+    if op == "allgather":
+        return N * s + P * N * s
+    if op in ("allreduce", "alltoall"):
+        return 2 * P * N * s
+    raise ValueError(op)
+
+
+def pack_bytes(T, H, K, E, P):
+    return T * H * 2 + T * K * H * 2 + T * K * 4 + T * K * 4 + (2 * P + 2 * E) * 4
+
+
+def unpack_bytes(T, H, K):
+    return T * K * H * 2 + T * H * 2 + T * K * 4 + T * K * 4
+
+
+def to_dev(torch, a):
+    a = np.ascontiguousarray(a)
+    return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to("cuda")
+
+
+def load_traffic(src_hash):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they
+    were taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("kernel_source_hash") != src_hash:
+        return None
+    return t
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--latency-sweep", action="store_true", help="also time AllReduce P=8 bf16 at 1 KiB..512 KiB per rank")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(json.dumps({"error": "this build runs on one GPU: the P ranks are P buffers on that GPU; "
+                          "--gpus above 1 is not supported"}))
+        return 2
+
+    import torch
+
+    from paper_2609_36954_amd import purlin as PL
+    from paper_2609_36954_amd import workloads as W
+
+    PL.lib()  # fail loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    dev_name = torch.cuda.get_device_name(0)
+    src_hash = kernel_source_hash()
+
+    # ---------------- inputs (seeded, synthetic) ----------------
+    c3 = W.COLLECTIVE_CONFIGS[3]
+    P, N, s = c3.P, c3.count, 2
+    M = N // P
+    moe = W.MOE_CONFIG
+    T, H, E, K = moe.T, moe.H, moe.E, moe.K
+    t0 = time.time()
+    log(f"bench: generating inputs (RS/AG P={P} N={N} bf16; MoE T={T} H={H} E={E} K={K})")
+    ins_np = W.collective_inputs(c3)
+    ids_np = W.zipf_topk_ids(T, E, K, moe.zipf_s, moe.seed_ids)
+    x_np = W.moe_tokens(moe)
+    y_np = W.moe_expert_outputs(moe)
+    g_np = W.softmax_gates(T, K, moe.seed_gates)
+    log(f"bench: inputs ready in {time.time() - t0:.1f}s; uploading")
+
+    ins = [to_dev(torch, a) for a in ins_np]
+    rs_out = [torch.empty(M, dtype=torch.int16, device="cuda") for _ in range(P)]
+    ag_out = [torch.empty(N, dtype=torch.int16, device="cuda") for _ in range(P)]
+    x, ids, y, g = to_dev(torch, x_np), to_dev(torch, ids_np), to_dev(torch, y_np), to_dev(torch, g_np)
+    pack_out = dict(
+        packed=torch.empty((T * K, H), dtype=torch.int16, device="cuda"),
+        dest_counts=torch.empty(P, dtype=torch.int32, device="cuda"),
+        dest_offsets=torch.empty(P, dtype=torch.int32, device="cuda"),
+        expert_counts=torch.empty(E, dtype=torch.int32, device="cuda"),
+        expert_offsets=torch.empty(E, dtype=torch.int32, device="cuda"),
+        pos=torch.empty((T, K), dtype=torch.int32, device="cuda"),
+    )
+    ws = torch.empty(PL.purlin_pack_workspace_size(T, K, E), dtype=torch.uint8, device="cuda")
+    comb_out = torch.empty((T, H), dtype=torch.int16, device="cuda")
+
+    # ---------------- plans (host orchestration, once per shape) ----------------
+    tp = time.perf_counter()
+    rs_plan = PL.Plan("reduce_scatter", P, N, "bf16", c3.chunk)
+    ag_plan = PL.Plan("allgather", P, N, "bf16", c3.chunk)
+    plan_ms = (time.perf_counter() - tp) * 1e3
+
+    ops = [
+        ("reduce_scatter", collective_bytes("reduce_scatter", P, N, s), rs_plan.sched_bytes),
+        ("allgather", collective_bytes("allgather", P, N, s), ag_plan.sched_bytes),
+        ("moe_pack", pack_bytes(T, H, K, E, P), pack_bytes(T, H, K, E, P)),
+        ("moe_combine", unpack_bytes(T, H, K), unpack_bytes(T, H, K)),
+    ]
+    step_bytes = sum(b for _, b, _ in ops)
+
+    def step(evs=None):
+        if evs is not None:
+            evs[0].record()
+        rs_plan.exec(ins, rs_out)
+        if evs is not None:
+            evs[1].record()
+        ag_plan.exec(rs_out, ag_out)
+        if evs is not None:
+            evs[2].record()
+        PL.purlin_pack(x, ids, E, P, out=pack_out, workspace=ws)
+        if evs is not None:
+            evs[3].record()
+        PL.purlin_unpack(y, pack_out["pos"], g, out=comb_out)
+        if evs is not None:
+            evs[4].record()
+
+    log("bench: warmup")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    log(f"bench: timing {args.steps} steps")
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms_per_step = wall * 1e3 / args.steps
+
+    per_op = {}
+    for j, (name, bmin, bsched) in enumerate(ops):
+        ts = [events[i][j].elapsed_time(events[i][j + 1]) for i in range(args.steps)]
+        avg_ms = float(np.mean(ts))
+        per_op[name] = {
+            "avg_us": round(avg_ms * 1e3, 2),
+            "min_us": round(float(np.min(ts)) * 1e3, 2),
+            "bytes_min": int(bmin),
+            "bytes_sched": int(bsched),
+            "GBps_min": round(bmin / (avg_ms * 1e-3) / 1e9, 1),
+            "frac_of_hbm_peak": round(bmin / (avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        }
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
+
+    # dominant single-kernel op (RS, AG and combine are one launch each)
+    single = ["reduce_scatter", "allgather", "moe_combine"]
+    dom = max(single, key=lambda n: per_op[n]["avg_us"])
+    kernel_of = {"reduce_scatter": "exec_reduce<8, bf16>", "allgather": "exec_copy", "moe_combine": "unpack_rows"}
+    achieved = per_op[dom]["bytes_min"] / (per_op[dom]["avg_us"] * 1e-6) / 1e9
+    traffic = None
+    tr = load_traffic(src_hash)
+    if tr and dom in tr.get("ops", {}):
+        traffic = tr["ops"][dom].get("hbm_bytes_per_launch")
+    roofline = {
+        "bound": "hbm",
+        "kernel": kernel_of[dom],
+        "op": dom,
+        "achieved": round(achieved, 1),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": traffic,
+    }
+
+    # ---------------- latency: decode-size AllReduce ----------------
+    def graph_latency_us(plan, lin, lout, calls=128, reps=8):
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            plan.exec(lin, lout, stream=side)
+        torch.cuda.synchronize()
+        gph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gph, stream=side):
+            for _ in range(calls):
+                plan.exec(lin, lout, stream=side)
+        gph.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            gph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / (calls * reps)
+
+    c2 = W.COLLECTIVE_CONFIGS[2]
+    lat_in = [to_dev(torch, a) for a in W.collective_inputs(c2)]
+    lat_out = [torch.empty(c2.count, dtype=torch.int16, device="cuda") for _ in range(c2.P)]
+    ar2 = PL.Plan("allreduce", c2.P, c2.count, "bf16", c2.chunk)
+    lat_us = graph_latency_us(ar2, lat_in, lat_out)
+    latency = {
+        "allreduce_p8_bf16_128x8192": {
+            "us": round(lat_us, 2),
+            "GBps_min": round(collective_bytes("allreduce", c2.P, c2.count, 2) / (lat_us * 1e-6) / 1e9, 1),
+            "algbw_GBps": round(c2.count * 2 / (lat_us * 1e-6) / 1e9, 1),
+        }
+    }
+    if args.latency_sweep:
+        sweep = {}
+        for kib in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512):
+            n = kib * 1024 // 2
+            li = [torch.randn(n, device="cuda").to(torch.bfloat16).view(torch.int16) for _ in range(8)]
+            lo = [torch.empty(n, dtype=torch.int16, device="cuda") for _ in range(8)]
+            pl = PL.Plan("allreduce", 8, n, "bf16", 65536)
+            sweep[f"{kib}KiB"] = round(graph_latency_us(pl, li, lo), 2)
+        latency["allreduce_p8_bf16_sweep_us"] = sweep
+    del lat_in, lat_out
+
+    # ---------------- CPU baseline: the oracle on a bounded sample ----------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_out, comb_out, P, N, M, E, K)
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; shapes of the paper's prefill collectives and MoE dispatch/combine)",
+        "config": {
+            "workload": "ReduceScatter then AllGather P=8 bf16 256MiB/rank chunk 1MiB; MoE pack + combine "
+                        "4096x7168 bf16, E=256 over P=8, top-8 Zipf(1.1)",
+            "ranks_simulated": P,
+            "elements_per_rank": N,
+            "moe": {"T": T, "H": H, "E": E, "K": K},
+            "step_bytes_min": step_bytes,
+        },
+        "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "ops": per_op,
+        "latency_us": latency,
+        "plan_ms": round(plan_ms, 3),
+        "device": dev_name,
+        "kernel_source_hash": src_hash,
+    }
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_out, comb_out, P, N, M, E, K):
+    """Time the oracle (as it stands, single-threaded numpy) on a bounded
+    sample of the same step, and compare the GPU's outputs on that sample."""
+    import oracle
+
+    def down(t, dt):
+        return t.contiguous().view(torch.uint8).cpu().numpy().view(dt)
+
+    log("bench: cpu baseline (oracle on a sample)")
+    frac = 16  # 1/16 of each partition of the collectives
+    m = M // frac
+    ok = True
+    t_total, bytes_total = 0.0, 0
+    # ReduceScatter on the first m elements of every partition
+    sub = [np.concatenate([a[k * M:k * M + m] for k in range(P)]) for a in ins_np]
+    t = time.perf_counter()
+    rs_want = oracle.reduce_scatter(sub, "bf16")
+    t_total += time.perf_counter() - t
+    bytes_total += collective_bytes("reduce_scatter", P, P * m, 2)
+    for r in range(P):
+        ok &= bool(np.array_equal(down(rs_out[r][:m], np.uint16), rs_want[r]))
+    # AllGather of those
+    t = time.perf_counter()
+    ag_want = oracle.all_gather(rs_want, "bf16")
+    t_total += time.perf_counter() - t
+    bytes_total += collective_bytes("allgather", P, P * m, 2)
+    for r in (0, P - 1):
+        got = np.concatenate([down(ag_out[r][k * M:k * M + m], np.uint16) for k in range(P)])
+        ok &= bool(np.array_equal(got, ag_want[r]))
+    # MoE pack and combine on the first 512 tokens (positions for the combine
+    # come from the oracle's own pack of the full routing)
+    Ts = 512
+    H = x_np.shape[1]
+    t = time.perf_counter()
+    oracle.pack(x_np[:Ts], ids_np[:Ts], E, P)
+    t_total += time.perf_counter() - t
+    bytes_total += pack_bytes(Ts, H, K, E, P)
+    pos_want = oracle.pack(np.zeros((ids_np.shape[0], 1), np.uint16), ids_np, E, P)["pos"]
+    ok &= bool(np.array_equal(down(pack_out["pos"], np.int32).reshape(-1, K), pos_want))
+    t = time.perf_counter()
+    cw = oracle.unpack(y_np, pos_want[:Ts], g_np[:Ts])
+    t_total += time.perf_counter() - t
+    bytes_total += unpack_bytes(Ts, H, K)
+    ok &= bool(np.array_equal(down(comb_out[:Ts], np.uint16).reshape(Ts, H), cw))
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count()
+    return {
+        "value": round(bytes_total / t_total / 1e9, 3),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"ReduceScatter+AllGather on 1/{frac} of each 32 MiB partition (P=8, bf16); "
+                  f"MoE pack and combine of the first {Ts} of 4096 tokens",
+        "seconds": round(t_total, 3),
+        "host_cores_available": cores,
+        "cpu": platform.processor() or platform.machine(),
+        "numpy": np.__version__,
+        "gpu_matches_oracle_on_sample": ok,
+    }
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,261 @@
+/*
+ * purlin.h -- C ABI of an MI355X (gfx950) datapath executor for collectives.
+ *
+ * The operations follow "Purlin: Separating Orchestration from the Datapath
+ * of Collectives" (arXiv 2609.36954):
+ *
+ *   - collective semantics: Section 2.1 ("Stable communication semantics");
+ *   - collectives as layout transformations with a consume op (copy or
+ *     reduce) between packed / scattered / transposed layouts, and
+ *     AllReduce = compose<ReduceScatter, AllGather>: Section 3.1, Listing 1;
+ *   - chunk-level consumption and its address rule (packed output: dst +
+ *     offset; scattered/transposed output: dst + peer * partBytes + offset):
+ *     Section 3.2, Listing 2;
+ *   - copy and reduce of the datapath, the reduction summing in FP32 in
+ *     ascending rank order from zero (Eq. 2): Section 3.3, Listing 3.
+ *
+ * On one GPU, the P ranks of a collective are P separate device buffers.  A
+ * host-side planner (purlin_plan) turns (op, P, count, dtype, chunk) into a
+ * table of chunk descriptors; purlin_exec binds 2P buffer pointers and runs
+ * the table with hand-written HIP kernels.  purlin_pack / purlin_unpack are
+ * the MoE dispatch and combine of expert parallelism (Section 2, Table 2).
+ *
+ * Conventions shared by every entry point:
+ *   - Status codes only: nothing throws or aborts across this ABI.
+ *   - Arguments are validated on the host before anything is enqueued; a
+ *     call that returns anything but PURLIN_OK has enqueued nothing.
+ *   - Device work is asynchronous on the given stream (a hipStream_t passed
+ *     as void*; NULL = the default stream).  The caller owns every data
+ *     buffer and keeps it alive until the stream has finished with it.
+ *   - Device pointers must be 16-byte aligned.
+ *   - bf16 data is the 16-bit encoding (upper half of a binary32 encoding).
+ */
+#ifndef PURLIN_H
+#define PURLIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define PURLIN_API __attribute__((visibility("default")))
+#else
+#define PURLIN_API
+#endif
+
+typedef enum purlin_status {
+    PURLIN_OK = 0,
+    PURLIN_ERR_INVALID = 1,     /* a bad argument; nothing was enqueued */
+    PURLIN_ERR_UNSUPPORTED = 2, /* valid request this build does not implement */
+    PURLIN_ERR_NOMEM = 3,       /* descriptor table too large, or an allocation failed */
+    PURLIN_ERR_DEVICE = 4       /* a HIP call or kernel launch failed */
+} purlin_status;
+
+/* Collectives (Section 2.1; Listing 1 gives consume op and layouts):
+ *   ALLREDUCE      reduce, scattered -> scattered  (compose<RS, AG>)
+ *   REDUCE_SCATTER reduce, scattered -> packed
+ *   ALLGATHER      copy,   packed    -> scattered
+ *   ALLTOALL       copy,   scattered -> transposed                       */
+typedef enum purlin_op {
+    PURLIN_ALLREDUCE = 0,
+    PURLIN_REDUCE_SCATTER = 1,
+    PURLIN_ALLGATHER = 2,
+    PURLIN_ALLTOALL = 3
+} purlin_op;
+
+typedef enum purlin_dtype { PURLIN_FP32 = 0, PURLIN_BF16 = 1 } purlin_dtype;
+
+/* Consume op of a descriptor (Section 3.1, "copy" and "reduce"). */
+typedef enum purlin_kind { PURLIN_KIND_COPY = 0, PURLIN_KIND_REDUCE = 1 } purlin_kind;
+
+/* One chunk descriptor (64 bytes).  Buffer indices refer to the bufs[]
+ * array given to purlin_exec: bufs[0..P-1] are the inputs in_0..in_{P-1},
+ * bufs[P..2P-1] the outputs out_0..out_{P-1}.
+ *
+ *   COPY:   for every destination j < ndst:
+ *             bufs[dst_buf + j*dst_step][dst_off .. +bytes) =
+ *             bufs[src_buf][src_off .. +bytes)                  (bit copy)
+ *   REDUCE: for every element i of the byte range and every j < ndst:
+ *             acc = +0.0f;
+ *             for p = 0 .. nsrc-1: acc += widen(bufs[src_buf + p*src_step][src_off + i]);
+ *             bufs[dst_buf + j*dst_step][dst_off + i] = narrow(acc)
+ *           in binary32, round to nearest even, no flush of denormals
+ *           (Eq. 2); widen/narrow are the identity for fp32 and exact
+ *           widening / round-to-nearest-even narrowing for bf16.
+ *
+ * phase: descriptors of phase 1 start only after every descriptor of phase
+ * 0 has completed (stream order between two launches).  A multi-destination
+ * descriptor (ndst > 1) reads its sources once and writes every destination. */
+typedef struct purlin_desc {
+    uint32_t kind;     /* purlin_kind */
+    uint32_t phase;    /* 0 or 1 */
+    uint32_t nsrc;     /* 1 for COPY; number of summed sources for REDUCE */
+    uint32_t src_buf;  /* bufs[] index of source 0 */
+    uint32_t src_step; /* bufs[] index stride between successive sources */
+    uint32_t ndst;     /* number of destinations written */
+    uint32_t dst_buf;  /* bufs[] index of destination 0 */
+    uint32_t dst_step; /* bufs[] index stride between successive destinations */
+    uint64_t src_off;  /* byte offset into every source */
+    uint64_t dst_off;  /* byte offset into every destination */
+    uint64_t bytes;    /* length in bytes (a multiple of the element size) */
+    uint32_t part;     /* partition k the range belongs to */
+    uint32_t chunk;    /* chunk c within the partition */
+} purlin_desc;
+
+/* Planning policy (the paper's codesign policies, Section 3.2/3.3): how the
+ * descriptors are split into work items and how AllGather / AllReduce are
+ * scheduled.  Zero in a field means "choose automatically". */
+typedef struct purlin_policy {
+    uint64_t item_bytes; /* bytes of one work item (a multiple of 16; 0 = auto) */
+    uint32_t fanout;     /* 0 auto, 1 = one COPY descriptor per destination,
+                            2 = one multi-destination COPY per source chunk   */
+    uint32_t ar_mode;    /* AllReduce: 0 auto, 1 = two phases (ReduceScatter
+                            into out_k's partition k, then copies of it to
+                            every other rank: the in-place compose of
+                            Section 3.1), 2 = one phase (each chunk reduced
+                            once and written to all P outputs)               */
+    uint32_t reserved[4];/* must be zero */
+} purlin_policy;
+
+#define PURLIN_PLAN_HOST_ONLY 1u /* build the tables on the host only (no device
+                                    upload); such a plan can be inspected but
+                                    not executed */
+
+#define PURLIN_MAX_RANKS 16
+#define PURLIN_MAX_ITEMS (1ull << 24)
+
+typedef struct purlin_plan_s* purlin_plan_t;
+
+/* Build a plan for `op` over P ranks (1..16) of `count` elements per rank
+ * on the scattered side (the paper's message-size convention, Section 5
+ * "Microbenchmark methodology"):
+ *     ALLREDUCE      in: count      out: count        elements per rank
+ *     REDUCE_SCATTER in: count      out: count / P
+ *     ALLGATHER      in: count / P  out: count
+ *     ALLTOALL       in: count      out: count
+ * `count` must be a multiple of P (uniform slices, Section 2.1); count = 0
+ * is a valid plan whose exec is a no-op.  `chunk_bytes` (>= element size and
+ * a multiple of it) is the chunk of Section 3.2: every partition of M =
+ * count/P elements is cut into ceil(M*s / chunk_bytes) chunks, the last one
+ * possibly shorter; the result does not depend on it.
+ * The plan owns a host descriptor table and its device copy (uploaded
+ * synchronously here, once).  Errors: PURLIN_ERR_INVALID (bad op, dtype,
+ * P, count, chunk, null out_plan), PURLIN_ERR_NOMEM (more than
+ * PURLIN_MAX_ITEMS work items, or an allocation failed), PURLIN_ERR_DEVICE
+ * (the device upload failed).  *out_plan is NULL on error. */
+PURLIN_API purlin_status purlin_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype,
+                          uint64_t chunk_bytes, purlin_plan_t* out_plan);
+
+/* purlin_plan with an explicit policy (NULL = automatic) and flags
+ * (0 or PURLIN_PLAN_HOST_ONLY).  PURLIN_ERR_INVALID also for a policy with
+ * item_bytes not a multiple of 16, fanout > 2, ar_mode > 2 or nonzero
+ * reserved fields, and for unknown flags. */
+PURLIN_API purlin_status purlin_plan_ex(purlin_op op, int P, uint64_t count, purlin_dtype dtype,
+                             uint64_t chunk_bytes, const purlin_policy* policy, uint32_t flags,
+                             purlin_plan_t* out_plan);
+
+/* Sizes of a plan (any output pointer may be NULL):
+ *   n_desc             chunk descriptors;
+ *   in_bytes_per_rank  bytes each bufs[p], p < P, must hold;
+ *   out_bytes_per_rank bytes each bufs[P + r] must hold;
+ *   sched_bytes        bytes the schedule reads plus writes,
+ *                      sum over descriptors of (nsrc + ndst) * bytes. */
+PURLIN_API purlin_status purlin_plan_info(purlin_plan_t plan, uint64_t* n_desc, uint64_t* in_bytes_per_rank,
+                               uint64_t* out_bytes_per_rank, uint64_t* sched_bytes);
+
+/* The chunk descriptor table (host memory owned by the plan, valid until
+ * purlin_plan_destroy): *n entries of *stride bytes each, phase 0 first. */
+PURLIN_API purlin_status purlin_plan_descriptors(purlin_plan_t plan, const purlin_desc** table, uint64_t* n,
+                                      uint64_t* stride);
+
+/* The work items the kernels execute: the descriptors cut at item_bytes
+ * boundaries, one item per wavefront (host copy, owned by the plan).
+ * phase_begin[0..2] (optional, may be NULL) receives the first item of
+ * phase 0, of phase 1, and the item count. */
+PURLIN_API purlin_status purlin_plan_items(purlin_plan_t plan, const purlin_desc** items, uint64_t* n,
+                                uint64_t phase_begin[3]);
+
+/* Run the plan: bufs[] holds 2P device pointers, in_0..in_{P-1} then
+ * out_0..out_{P-1}, sized per purlin_plan_info.  Each phase is one kernel
+ * launch on `stream`; no host-device copy, no allocation, no
+ * synchronisation (graph-capturable).  Errors (nothing enqueued):
+ * PURLIN_ERR_INVALID for a NULL or host-only plan, NULL bufs, a NULL or
+ * misaligned pointer, an input range overlapping an output range, or two
+ * output ranges overlapping; PURLIN_ERR_DEVICE if a launch fails.
+ * Inputs may alias each other.  For count = 0 it returns PURLIN_OK and
+ * ignores bufs.  A plan is immutable: concurrent execs on different
+ * streams with distinct buffers are safe. */
+PURLIN_API purlin_status purlin_exec(purlin_plan_t plan, void* const* bufs, void* stream);
+
+/* Free a plan (NULL-safe).  Does not synchronise: the caller keeps the plan
+ * alive until work queued with it has finished. */
+PURLIN_API void purlin_plan_destroy(purlin_plan_t plan);
+
+/* Workspace bytes purlin_pack needs for T tokens, K slots, E experts. */
+PURLIN_API purlin_status purlin_pack_workspace_size(int T, int K, int E, uint64_t* bytes);
+
+/* MoE dispatch (pack).  Expert parallelism dispatches tokens to the ranks
+ * that own their experts (Section 2, Table 2); the variable-size segments
+ * are the scatteredV layout of Section 3.1.  With L = E / P experts per
+ * rank, expert e belongs to rank e / L, and
+ *   expert_counts[e]  = #{(t,k) : ids[t,k] == e}
+ *   expert_offsets[e] = sum of expert_counts[0..e)  (exclusive prefix sum)
+ *   dest_counts[r]    = sum of expert_counts over rank r's experts
+ *   dest_offsets[r]   = expert_offsets[r * L]
+ *   pos[t,k]          = expert_offsets[e] + #{t' < t : e in ids[t',:]},  e = ids[t,k]
+ *   packed[pos[t,k], :] = x[t, :]                              (bit copy)
+ * so rows are grouped by destination rank, then expert, then token.
+ *   x        bf16 [T, H] device, row-major
+ *   ids      int32 [T, K] device; each id in [0, E), distinct within a token
+ *   packed   bf16 [T*K, H] device (output)
+ *   dest_counts, dest_offsets  int32 [P] device (output)
+ *   expert_counts              int32 [E] device (output)
+ *   expert_offsets             int32 [E] device (output, optional: NULL)
+ *   pos      int32 [T, K] device (output)
+ *   dev_status int32 device (optional: NULL): set to 0, or to 1 when an id
+ *            is out of range or repeated within a token; then counts and
+ *            positions are unspecified, pos holds -1 for out-of-range ids,
+ *            and no row is written outside packed.
+ *   workspace >= purlin_pack_workspace_size bytes of device memory, owned
+ *            by the caller; its contents on entry do not matter.
+ * Limits: T >= 0, H >= 1, 1 <= K <= 64, 1 <= E <= 4096, 1 <= P <= E,
+ * E % P == 0, T*K < 2^31.  Errors: PURLIN_ERR_INVALID (limits, NULL or
+ * misaligned pointer, small workspace), PURLIN_ERR_DEVICE. */
+PURLIN_API purlin_status purlin_pack(int T, int H, int K, int E, int P, const void* x, const int32_t* ids,
+                          void* packed, int32_t* dest_counts, int32_t* dest_offsets,
+                          int32_t* expert_counts, int32_t* expert_offsets, int32_t* pos,
+                          int32_t* dev_status, void* workspace, uint64_t workspace_bytes,
+                          void* stream);
+
+/* MoE combine (unpack), the inverse of purlin_pack weighted by gates:
+ *   acc = +0.0f;
+ *   for k = 0 .. K-1:  acc = acc + (gates[t,k] * widen(y[pos[t,k], h]));
+ *   out[t, h] = narrow(acc)
+ * each multiply and add a separately rounded binary32 operation (never
+ * fused), slots summed in ascending order (the slot analogue of the rank
+ * order of Eq. 2).
+ *   y      bf16 [T*K, H] device (rows in purlin_pack's layout)
+ *   pos    int32 [T, K] device, each in [0, T*K)
+ *   gates  fp32 [T, K] device
+ *   out    bf16 [T, H] device (output)
+ *   dev_status int32 device (optional: NULL): set to 0, or to 1 if some pos
+ *          is out of range (that slot then contributes nothing).
+ * Limits: T >= 0, H >= 1, 1 <= K <= 64, T*K < 2^31.  Errors:
+ * PURLIN_ERR_INVALID, PURLIN_ERR_DEVICE. */
+PURLIN_API purlin_status purlin_unpack(int T, int H, int K, const void* y, const int32_t* pos,
+                            const float* gates, void* out, int32_t* dev_status, void* stream);
+
+/* Static text for a status code ("unknown status" for others). */
+PURLIN_API const char* purlin_status_string(purlin_status status);
+
+/* Library version, e.g. "0.1.0" (static text). */
+PURLIN_API const char* purlin_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PURLIN_H */

@@ -1,0 +1,208 @@
+// extern "C" entry points declared in include/purlin.h: host-side argument
+// validation (always complete before anything is enqueued), plan lifetime,
+// and the launches.  Status codes only: no exception crosses the ABI.
+
+#include <cstdint>
+#include <new>
+
+#include "kernels.h"
+#include "plan.h"
+#include "purlin.h"
+
+struct purlin_plan_s {
+    purlin::Plan plan;
+};
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// [a, a + na) and [b, b + nb) share a byte.
+bool overlaps(const void* a, uint64_t na, const void* b, uint64_t nb) {
+    if (na == 0 || nb == 0) return false;
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + nb && y < x + na;
+}
+
+purlin_status make_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype, uint64_t chunk,
+                        const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan) {
+    if (!out_plan) return PURLIN_ERR_INVALID;
+    *out_plan = nullptr;
+    purlin_plan_s* h = new (std::nothrow) purlin_plan_s;
+    if (!h) return PURLIN_ERR_NOMEM;
+    purlin_status st;
+    try {
+        st = purlin::build_plan(op, P, count, dtype, chunk, policy, flags, h->plan);
+    } catch (...) {
+        st = PURLIN_ERR_NOMEM;
+    }
+    if (st != PURLIN_OK) {
+        delete h;
+        return st;
+    }
+    purlin::Plan& pl = h->plan;
+    if (!(flags & PURLIN_PLAN_HOST_ONLY) && !pl.items.empty()) {
+        const size_t bytes = pl.items.size() * sizeof(purlin_desc);
+        if (hipMalloc(reinterpret_cast<void**>(&pl.d_items), bytes) != hipSuccess) {
+            pl.d_items = nullptr;
+            delete h;
+            return PURLIN_ERR_NOMEM;
+        }
+        if (hipMemcpy(pl.d_items, pl.items.data(), bytes, hipMemcpyHostToDevice) != hipSuccess) {
+            (void)hipFree(pl.d_items);
+            delete h;
+            return PURLIN_ERR_DEVICE;
+        }
+    }
+    *out_plan = h;
+    return PURLIN_OK;
+}
+
+bool pack_limits_ok(int T, int H, int K, int E) {
+    if (T < 0 || H < 1 || K < 1 || K > 64 || E < 1 || E > 4096) return false;
+    return static_cast<int64_t>(T) * K < (int64_t(1) << 31);
+}
+
+}  // namespace
+
+extern "C" {
+
+purlin_status purlin_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype, uint64_t chunk_bytes,
+                          purlin_plan_t* out_plan) {
+    return make_plan(op, P, count, dtype, chunk_bytes, nullptr, 0, out_plan);
+}
+
+purlin_status purlin_plan_ex(purlin_op op, int P, uint64_t count, purlin_dtype dtype, uint64_t chunk_bytes,
+                             const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan) {
+    return make_plan(op, P, count, dtype, chunk_bytes, policy, flags, out_plan);
+}
+
+purlin_status purlin_plan_info(purlin_plan_t plan, uint64_t* n_desc, uint64_t* in_bytes_per_rank,
+                               uint64_t* out_bytes_per_rank, uint64_t* sched_bytes) {
+    if (!plan) return PURLIN_ERR_INVALID;
+    const purlin::Plan& p = plan->plan;
+    if (n_desc) *n_desc = p.descs.size();
+    if (in_bytes_per_rank) *in_bytes_per_rank = p.in_bytes;
+    if (out_bytes_per_rank) *out_bytes_per_rank = p.out_bytes;
+    if (sched_bytes) *sched_bytes = p.sched_bytes;
+    return PURLIN_OK;
+}
+
+purlin_status purlin_plan_descriptors(purlin_plan_t plan, const purlin_desc** table, uint64_t* n, uint64_t* stride) {
+    if (!plan || !table || !n) return PURLIN_ERR_INVALID;
+    *table = plan->plan.descs.data();
+    *n = plan->plan.descs.size();
+    if (stride) *stride = sizeof(purlin_desc);
+    return PURLIN_OK;
+}
+
+purlin_status purlin_plan_items(purlin_plan_t plan, const purlin_desc** items, uint64_t* n, uint64_t phase_begin[3]) {
+    if (!plan || !items || !n) return PURLIN_ERR_INVALID;
+    const purlin::Plan& p = plan->plan;
+    *items = p.items.data();
+    *n = p.items.size();
+    if (phase_begin) {
+        // phase 0 always comes first; a plan has a phase 1 only as its second launch
+        phase_begin[0] = 0;
+        phase_begin[1] = p.nphases == 2 ? p.phases[1].begin : p.items.size();
+        phase_begin[2] = p.items.size();
+    }
+    return PURLIN_OK;
+}
+
+purlin_status purlin_exec(purlin_plan_t plan, void* const* bufs, void* stream) {
+    if (!plan) return PURLIN_ERR_INVALID;
+    const purlin::Plan& p = plan->plan;
+    if (p.count == 0) return PURLIN_OK;
+    if (p.flags & PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
+    if (!bufs) return PURLIN_ERR_INVALID;
+    const int P = p.P;
+    for (int i = 0; i < 2 * P; ++i)
+        if (!bufs[i] || !aligned16(bufs[i])) return PURLIN_ERR_INVALID;
+    for (int i = 0; i < P; ++i)
+        for (int r = 0; r < P; ++r)
+            if (overlaps(bufs[i], p.in_bytes, bufs[P + r], p.out_bytes)) return PURLIN_ERR_INVALID;
+    for (int r = 0; r < P; ++r)
+        for (int q = r + 1; q < P; ++q)
+            if (overlaps(bufs[P + r], p.out_bytes, bufs[P + q], p.out_bytes)) return PURLIN_ERR_INVALID;
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    for (int i = 0; i < p.nphases; ++i) {
+        const purlin::Phase& ph = p.phases[i];
+        const hipError_t e = purlin::launch_phase(p.d_items + ph.begin, ph.count, ph.kind, ph.nsrc, ph.src_buf,
+                                                  ph.src_step, p.dtype, bufs, 2 * P, s);
+        if (e != hipSuccess) return PURLIN_ERR_DEVICE;
+    }
+    return PURLIN_OK;
+}
+
+void purlin_plan_destroy(purlin_plan_t plan) {
+    if (!plan) return;
+    if (plan->plan.d_items) (void)hipFree(plan->plan.d_items);
+    delete plan;
+}
+
+purlin_status purlin_pack_workspace_size(int T, int K, int E, uint64_t* bytes) {
+    if (!bytes || T < 0 || K < 1 || K > 64 || E < 1 || E > 4096) return PURLIN_ERR_INVALID;
+    if (static_cast<int64_t>(T) * K >= (int64_t(1) << 31)) return PURLIN_ERR_INVALID;
+    *bytes = purlin::pack_workspace_bytes(T, K, E);
+    return PURLIN_OK;
+}
+
+purlin_status purlin_pack(int T, int H, int K, int E, int P, const void* x, const int32_t* ids, void* packed,
+                          int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts,
+                          int32_t* expert_offsets, int32_t* pos, int32_t* dev_status, void* workspace,
+                          uint64_t workspace_bytes, void* stream) {
+    if (!pack_limits_ok(T, H, K, E)) return PURLIN_ERR_INVALID;
+    if (P < 1 || P > E || E % P != 0) return PURLIN_ERR_INVALID;
+    if (!dest_counts || !dest_offsets || !expert_counts) return PURLIN_ERR_INVALID;
+    if (!aligned16(dest_counts) || !aligned16(dest_offsets) || !aligned16(expert_counts)) return PURLIN_ERR_INVALID;
+    if (expert_offsets && !aligned16(expert_offsets)) return PURLIN_ERR_INVALID;
+    if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    const uint64_t need = purlin::pack_workspace_bytes(T, K, E);
+    if (workspace_bytes < need || (need && (!workspace || !aligned16(workspace)))) return PURLIN_ERR_INVALID;
+    if (T > 0) {
+        if (!x || !ids || !packed || !pos) return PURLIN_ERR_INVALID;
+        if (!aligned16(x) || !aligned16(ids) || !aligned16(packed) || !aligned16(pos)) return PURLIN_ERR_INVALID;
+        const uint64_t xb = uint64_t(T) * H * 2, pb = xb * K;
+        if (overlaps(x, xb, packed, pb)) return PURLIN_ERR_INVALID;
+    }
+    const purlin::PackWorkspace ws = purlin::pack_workspace_carve(workspace, T, K, E);
+    const hipError_t e = purlin::launch_pack(T, H, K, E, P, static_cast<const uint16_t*>(x), ids,
+                                             static_cast<uint16_t*>(packed), dest_counts, dest_offsets,
+                                             expert_counts, expert_offsets, pos, dev_status, ws,
+                                             static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
+purlin_status purlin_unpack(int T, int H, int K, const void* y, const int32_t* pos, const float* gates, void* out,
+                            int32_t* dev_status, void* stream) {
+    if (T < 0 || H < 1 || K < 1 || K > 64) return PURLIN_ERR_INVALID;
+    if (static_cast<int64_t>(T) * K >= (int64_t(1) << 31)) return PURLIN_ERR_INVALID;
+    if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    if (T > 0) {
+        if (!y || !pos || !gates || !out) return PURLIN_ERR_INVALID;
+        if (!aligned16(y) || !aligned16(pos) || !aligned16(gates) || !aligned16(out)) return PURLIN_ERR_INVALID;
+        const uint64_t ob = uint64_t(T) * H * 2, yb = ob * K;
+        if (overlaps(y, yb, out, ob)) return PURLIN_ERR_INVALID;
+    }
+    const hipError_t e = purlin::launch_unpack(T, H, K, static_cast<const uint16_t*>(y), pos, gates,
+                                               static_cast<uint16_t*>(out), dev_status,
+                                               static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
+const char* purlin_status_string(purlin_status status) {
+    switch (status) {
+        case PURLIN_OK: return "ok";
+        case PURLIN_ERR_INVALID: return "invalid argument";
+        case PURLIN_ERR_UNSUPPORTED: return "unsupported";
+        case PURLIN_ERR_NOMEM: return "out of memory or descriptor table too large";
+        case PURLIN_ERR_DEVICE: return "device error";
+    }
+    return "unknown status";
+}
+
+const char* purlin_version(void) { return "0.1.0"; }
+
+}  // extern "C"

@@ -1,0 +1,267 @@
+// Datapath executor for gfx950: each 64-wide wavefront takes one work item
+// (a slice of a chunk descriptor) and moves its bytes.
+//
+// Paper passages (Purlin, arXiv 2609.36954):
+//  - Section 3.3 / Listing 3: the datapath offers copy (move one contiguous
+//    byte range) and reduce (combine n equally sized typed sources into one
+//    destination); both share one load path and differ only in the step
+//    applied to the data once it is in registers.
+//  - Section 3.3, Eq. 2: a reduction keeps one FP32 accumulator per output
+//    element, starts it at zero and adds rank 0, 1, ..., n-1 in that order,
+//    converting each term to FP32 and the sum back to the element type once;
+//    throughput comes from many accumulators across elements, never from
+//    reassociating across ranks.
+//  - Section 3.3, Eq. 3 and Section 2.2, Eq. 1: bandwidth needs bytes in
+//    flight.  The paper stages through shared memory with asynchronous
+//    copies on its GPUs; here each lane keeps U (copy) or U*nsrc (reduce)
+//    independent 16-byte global loads in flight before consuming any, and
+//    thousands of wavefronts run at once, which is what HBM3E needs.  No
+//    LDS is involved: the data is used once, straight from registers.
+
+#include "kernels.h"
+
+namespace purlin {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kBlock = 256;
+constexpr int kWavesPerBlock = kBlock / kWave;
+
+struct ExecArgs {
+    const purlin_desc* items;
+    uint64_t n_items;
+    char* bufs[2 * PURLIN_MAX_RANKS];
+    // Sources of a REDUCE phase, resolved on the host: every item of such a
+    // phase names the same sources (bufs[src_buf + p * src_step]), so the
+    // kernel reads them at constant argument offsets instead of issuing one
+    // dependent indexed lookup per source.
+    char* srcs[PURLIN_MAX_RANKS];
+};
+
+__device__ __forceinline__ uint32_t wave_index() {
+    return __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
+}
+
+__device__ __forceinline__ uint32_t lane_index() { return threadIdx.x & (kWave - 1); }
+
+__device__ __forceinline__ u32x4 load16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+__device__ __forceinline__ void store16(char* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+// bf16 element 2m of a 32-bit word sits in its low half (little endian).
+__device__ __forceinline__ float bf16_low(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_high(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// binary32 -> bf16, round to nearest, ties to even.  Adding 0x7FFF plus the
+// lowest kept bit carries into the kept half exactly when the dropped half
+// is above one half, or equal to it with an odd kept half; a carry out of
+// the significand steps the exponent, and past the largest finite value it
+// gives the infinity encoding.  NaNs become quiet NaNs keeping sign and the
+// top payload bits.
+__device__ __forceinline__ uint32_t to_bf16(float f) {
+    const uint32_t u = __float_as_uint(f);
+    const uint32_t rounded = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+    const uint32_t quiet_nan = (u >> 16) | 0x40u;
+    return (u & 0x7FFFFFFFu) > 0x7F800000u ? quiet_nan : rounded;
+}
+
+__device__ __forceinline__ char* dst_ptr(const ExecArgs& a, const purlin_desc& d, uint32_t j) {
+    return a.bufs[d.dst_buf + j * d.dst_step] + d.dst_off;
+}
+
+// Bytes [from, to) of an item, 2 bytes per lane step (every element width
+// and offset here is a multiple of 2).
+__device__ __forceinline__ void copy_bytes2(const ExecArgs& a, const purlin_desc& d, const char* src, uint64_t from,
+                                            uint64_t to, uint32_t lane) {
+    for (uint64_t b = from + 2 * lane; b < to; b += 2 * kWave) {
+        const uint16_t v = *reinterpret_cast<const uint16_t*>(src + b);
+        for (uint32_t j = 0; j < d.ndst; ++j) *reinterpret_cast<uint16_t*>(dst_ptr(a, d, j) + b) = v;
+    }
+}
+
+template <int U>
+__global__ __launch_bounds__(kBlock) void exec_copy(ExecArgs a) {
+    const uint32_t w = wave_index();
+    if (w >= a.n_items) return;
+    const purlin_desc d = a.items[w];
+    const uint32_t lane = lane_index();
+    const char* src = a.bufs[d.src_buf] + d.src_off;
+    if (((d.src_off | d.dst_off) & 15) != 0) {
+        copy_bytes2(a, d, src, 0, d.bytes, lane);
+        return;
+    }
+    const uint64_t nvec = d.bytes >> 4;
+    uint64_t base = 0;
+    for (; base + U * kWave <= nvec; base += U * kWave) {
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = load16(src + (base + u * kWave + lane) * 16);
+        for (uint32_t j = 0; j < d.ndst; ++j) {
+            char* dst = dst_ptr(a, d, j);
+#pragma unroll
+            for (int u = 0; u < U; ++u) store16(dst + (base + u * kWave + lane) * 16, v[u]);
+        }
+    }
+    for (uint64_t i = base + lane; i < nvec; i += kWave) {
+        const u32x4 v = load16(src + i * 16);
+        for (uint32_t j = 0; j < d.ndst; ++j) store16(dst_ptr(a, d, j) + i * 16, v);
+    }
+    copy_bytes2(a, d, src, nvec * 16, d.bytes, lane);
+}
+
+// Eq. 2 on one 16-byte vector of every source: 8 bf16 or 4 fp32 elements.
+template <int NSRC, bool BF16>
+__device__ __forceinline__ u32x4 rank_order_sum(const u32x4 (&v)[NSRC]) {
+    u32x4 o;
+    if constexpr (BF16) {
+        float acc[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
+#pragma unroll
+        for (int p = 0; p < NSRC; ++p) {
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                acc[2 * m] = acc[2 * m] + bf16_low(v[p][m]);
+                acc[2 * m + 1] = acc[2 * m + 1] + bf16_high(v[p][m]);
+            }
+        }
+#pragma unroll
+        for (int m = 0; m < 4; ++m) o[m] = to_bf16(acc[2 * m]) | (to_bf16(acc[2 * m + 1]) << 16);
+    } else {
+        float acc[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) acc[m] = 0.0f;
+#pragma unroll
+        for (int p = 0; p < NSRC; ++p) {
+#pragma unroll
+            for (int m = 0; m < 4; ++m) acc[m] = acc[m] + __uint_as_float(v[p][m]);
+        }
+#pragma unroll
+        for (int m = 0; m < 4; ++m) o[m] = __float_as_uint(acc[m]);
+    }
+    return o;
+}
+
+// Element-at-a-time reduction of bytes [from, to) of an item.
+template <int NSRC, bool BF16>
+__device__ __forceinline__ void reduce_elems(const ExecArgs& a, const purlin_desc& d, const char* const (&src)[NSRC],
+                                             uint64_t from, uint64_t to, uint32_t lane) {
+    constexpr uint64_t S = BF16 ? 2 : 4;
+    for (uint64_t b = from + S * lane; b < to; b += S * kWave) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int p = 0; p < NSRC; ++p) {
+            const float x = BF16 ? __uint_as_float(uint32_t(*reinterpret_cast<const uint16_t*>(src[p] + b)) << 16)
+                                 : *reinterpret_cast<const float*>(src[p] + b);
+            acc = acc + x;
+        }
+        for (uint32_t j = 0; j < d.ndst; ++j) {
+            char* dst = dst_ptr(a, d, j) + b;
+            if constexpr (BF16)
+                *reinterpret_cast<uint16_t*>(dst) = static_cast<uint16_t>(to_bf16(acc));
+            else
+                *reinterpret_cast<float*>(dst) = acc;
+        }
+    }
+}
+
+template <int NSRC, bool BF16, int U>
+__global__ __launch_bounds__(kBlock) void exec_reduce(ExecArgs a) {
+    const uint32_t w = wave_index();
+    if (w >= a.n_items) return;
+    const purlin_desc d = a.items[w];
+    const uint32_t lane = lane_index();
+    const char* src[NSRC];
+#pragma unroll
+    for (int p = 0; p < NSRC; ++p) src[p] = a.srcs[p] + d.src_off;
+    if (((d.src_off | d.dst_off) & 15) != 0) {
+        reduce_elems<NSRC, BF16>(a, d, src, 0, d.bytes, lane);
+        return;
+    }
+    const uint64_t nvec = d.bytes >> 4;
+    uint64_t base = 0;
+    for (; base + U * kWave <= nvec; base += U * kWave) {
+        u32x4 v[U][NSRC];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int p = 0; p < NSRC; ++p) v[u][p] = load16(src[p] + (base + u * kWave + lane) * 16);
+        u32x4 o[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) o[u] = rank_order_sum<NSRC, BF16>(v[u]);
+        for (uint32_t j = 0; j < d.ndst; ++j) {
+            char* dst = dst_ptr(a, d, j);
+#pragma unroll
+            for (int u = 0; u < U; ++u) store16(dst + (base + u * kWave + lane) * 16, o[u]);
+        }
+    }
+    for (uint64_t i = base + lane; i < nvec; i += kWave) {
+        u32x4 v[NSRC];
+#pragma unroll
+        for (int p = 0; p < NSRC; ++p) v[p] = load16(src[p] + i * 16);
+        const u32x4 o = rank_order_sum<NSRC, BF16>(v);
+        for (uint32_t j = 0; j < d.ndst; ++j) store16(dst_ptr(a, d, j) + i * 16, o);
+    }
+    reduce_elems<NSRC, BF16>(a, d, src, nvec * 16, d.bytes, lane);
+}
+
+// Loads in flight per lane: U vectors for a copy, U * NSRC for a reduce.
+constexpr int kCopyUnroll = 4;
+constexpr int reduce_unroll(int nsrc) { return nsrc >= 16 ? 1 : (nsrc >= 8 ? 2 : (nsrc >= 4 ? 4 : 8)); }
+
+template <int NSRC>
+void launch_reduce(dim3 grid, hipStream_t stream, const ExecArgs& a, bool bf16) {
+    if (bf16)
+        hipLaunchKernelGGL((exec_reduce<NSRC, true, reduce_unroll(NSRC)>), grid, dim3(kBlock), 0, stream, a);
+    else
+        hipLaunchKernelGGL((exec_reduce<NSRC, false, reduce_unroll(NSRC)>), grid, dim3(kBlock), 0, stream, a);
+}
+
+}  // namespace
+
+hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
+                        uint32_t src_step, purlin_dtype dtype, void* const* bufs, int nbufs, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    ExecArgs a{};
+    a.items = items;
+    a.n_items = n;
+    for (int i = 0; i < nbufs && i < 2 * PURLIN_MAX_RANKS; ++i) a.bufs[i] = static_cast<char*>(bufs[i]);
+    if (kind == PURLIN_KIND_REDUCE) {
+        for (uint32_t p = 0; p < nsrc && p < PURLIN_MAX_RANKS; ++p) {
+            const uint64_t b = uint64_t(src_buf) + uint64_t(p) * src_step;
+            if (b >= uint64_t(nbufs)) return hipErrorInvalidValue;
+            a.srcs[p] = static_cast<char*>(bufs[b]);
+        }
+    }
+    const dim3 grid(static_cast<uint32_t>((n + kWavesPerBlock - 1) / kWavesPerBlock));
+    (void)hipGetLastError();
+    if (kind == PURLIN_KIND_COPY) {
+        hipLaunchKernelGGL(exec_copy<kCopyUnroll>, grid, dim3(kBlock), 0, stream, a);
+    } else {
+        const bool bf16 = dtype == PURLIN_BF16;
+        switch (nsrc) {
+            case 1: launch_reduce<1>(grid, stream, a, bf16); break;
+            case 2: launch_reduce<2>(grid, stream, a, bf16); break;
+            case 3: launch_reduce<3>(grid, stream, a, bf16); break;
+            case 4: launch_reduce<4>(grid, stream, a, bf16); break;
+            case 5: launch_reduce<5>(grid, stream, a, bf16); break;
+            case 6: launch_reduce<6>(grid, stream, a, bf16); break;
+            case 7: launch_reduce<7>(grid, stream, a, bf16); break;
+            case 8: launch_reduce<8>(grid, stream, a, bf16); break;
+            case 9: launch_reduce<9>(grid, stream, a, bf16); break;
+            case 10: launch_reduce<10>(grid, stream, a, bf16); break;
+            case 11: launch_reduce<11>(grid, stream, a, bf16); break;
+            case 12: launch_reduce<12>(grid, stream, a, bf16); break;
+            case 13: launch_reduce<13>(grid, stream, a, bf16); break;
+            case 14: launch_reduce<14>(grid, stream, a, bf16); break;
+            case 15: launch_reduce<15>(grid, stream, a, bf16); break;
+            case 16: launch_reduce<16>(grid, stream, a, bf16); break;
+            default: return hipErrorInvalidValue;
+        }
+    }
+    return hipGetLastError();
+}
+
+}  // namespace purlin

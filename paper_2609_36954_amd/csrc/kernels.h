@@ -1,0 +1,38 @@
+// Internal launch entry points of the HIP kernels (exec.hip, moe.hip),
+// called by the ABI glue (abi.hip) after host-side validation.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "purlin.h"
+
+namespace purlin {
+
+// Launch one phase: `n` work items starting at device pointer `items`, all
+// of consume op `kind`.  The items of a REDUCE phase all sum the same `nsrc`
+// sources bufs[src_buf + p * src_step].  `bufs` holds the 2P buffer pointers.
+hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
+                        uint32_t src_step, purlin_dtype dtype, void* const* bufs, int nbufs, hipStream_t stream);
+
+struct PackWorkspace {
+    int32_t* tile_base;  // [ntiles * E]: per-tile expert counts, then row bases
+    int32_t* lrank;      // [T * K]: rank of (t, k) among its tile's tokens of the same expert
+    int32_t* tile_err;   // [ntiles]
+};
+
+constexpr int kPackTileTokens = 64;  // one 64-bit token mask per expert and tile
+
+uint64_t pack_workspace_bytes(int T, int K, int E);
+PackWorkspace pack_workspace_carve(void* base, int T, int K, int E);
+
+hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, const int32_t* ids,
+                       uint16_t* packed, int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts,
+                       int32_t* expert_offsets, int32_t* pos, int32_t* dev_status, const PackWorkspace& ws,
+                       hipStream_t stream);
+
+hipError_t launch_unpack(int T, int H, int K, const uint16_t* y, const int32_t* pos, const float* gates,
+                         uint16_t* out, int32_t* dev_status, hipStream_t stream);
+
+}  // namespace purlin

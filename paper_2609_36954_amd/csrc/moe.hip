@@ -1,0 +1,405 @@
+// MoE dispatch (pack) and combine (unpack) for gfx950.
+//
+// Expert parallelism dispatches tokens to the ranks that own their experts
+// and combines the expert outputs (Purlin, arXiv 2609.36954: Section 2,
+// Table 2); the per-destination segments are the scatteredV layout of
+// Section 3.1.  The reduction in combine follows Eq. 2 with slots in place
+// of ranks: one FP32 accumulator per output element, started at zero, terms
+// added in ascending slot order, converted to bf16 once.
+//
+// Pack runs in three launches:
+//   1. pack_tiles: one workgroup per tile of 64 tokens.  In LDS it builds,
+//      for every expert, a 64-bit mask of the tile's tokens that chose it.
+//      The rank of (t, k) among the tile's earlier tokens of the same expert
+//      is a popcount of that mask below t; the tile's count per expert is
+//      the mask's popcount.  Deterministic: no ordering depends on atomics.
+//   2. pack_scan: one workgroup.  Exclusive prefix over tiles per expert,
+//      expert totals, exclusive prefix over experts, destination
+//      counts/offsets, and the error flag.  The per-tile counts are
+//      rewritten in place into each tile's first row per expert.
+//   3. pack_rows: one wavefront per token.  Lane k forms pos[t, k]; the wave
+//      then streams the token row once from HBM through registers and
+//      writes it to its K packed rows with 16-byte stores.
+// Unpack is one launch, one wavefront per token, slots in groups of 8 with
+// all their 16-byte row loads in flight before the FP32 accumulation.
+
+#include "kernels.h"
+
+namespace purlin {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kBlock = 256;
+constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kScanThreads = 1024;
+constexpr int kMaxExperts = 4096;
+
+__device__ __forceinline__ uint32_t wave_index() {
+    return __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
+}
+
+__device__ __forceinline__ uint32_t lane_index() { return threadIdx.x & (kWave - 1); }
+
+__device__ __forceinline__ u32x4 load16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+__device__ __forceinline__ void store16(char* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+// binary32 -> bf16, round to nearest, ties to even (see the executor for
+// the derivation); NaN -> quiet NaN with sign and top payload bits kept.
+__device__ __forceinline__ uint32_t to_bf16(float f) {
+    const uint32_t u = __float_as_uint(f);
+    const uint32_t rounded = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+    const uint32_t quiet_nan = (u >> 16) | 0x40u;
+    return (u & 0x7FFFFFFFu) > 0x7F800000u ? quiet_nan : rounded;
+}
+
+__global__ __launch_bounds__(kBlock) void pack_tiles(int T, int K, int E, const int32_t* __restrict__ ids,
+                                                     int32_t* __restrict__ tile_cnt, int32_t* __restrict__ lrank,
+                                                     int32_t* __restrict__ tile_err) {
+    extern __shared__ unsigned long long masks[];  // [E]
+    __shared__ int err;
+    const int tile = blockIdx.x;
+    const int t0 = tile * kPackTileTokens;
+    const int nt = min(kPackTileTokens, T - t0);
+    const int n = nt * K;
+    const int32_t* tids = ids + static_cast<int64_t>(t0) * K;
+
+    for (int e = threadIdx.x; e < E; e += kBlock) masks[e] = 0ull;
+    if (threadIdx.x == 0) err = 0;
+    __syncthreads();
+
+    bool bad = false;
+    for (int j = threadIdx.x; j < n; j += kBlock) {
+        const int tl = j / K;
+        const int k = j - tl * K;
+        const int e = tids[j];
+        if (e < 0 || e >= E) {
+            bad = true;
+            continue;
+        }
+        for (int k2 = 0; k2 < k; ++k2)
+            if (tids[tl * K + k2] == e) bad = true;
+        atomicOr(&masks[e], 1ull << tl);
+    }
+    if (bad) err = 1;  // every writer stores the same value
+    __syncthreads();
+
+    for (int j = threadIdx.x; j < n; j += kBlock) {
+        const int tl = j / K;
+        const int e = tids[j];
+        int r = -1;
+        if (e >= 0 && e < E) r = __popcll(masks[e] & ((1ull << tl) - 1ull));
+        lrank[static_cast<int64_t>(t0) * K + j] = r;
+    }
+    for (int e = threadIdx.x; e < E; e += kBlock) tile_cnt[static_cast<int64_t>(tile) * E + e] = __popcll(masks[e]);
+    if (threadIdx.x == 0) tile_err[tile] = err;
+}
+
+// Sum of tile counts of expert e over tiles [lo, hi), 8 loads in flight.
+__device__ __forceinline__ int sum_tiles(const int32_t* tile_cnt, int E, int e, int lo, int hi) {
+    int s = 0;
+    for (int t = lo; t < hi; t += 8) {
+        int c[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) c[i] = (t + i < hi) ? tile_cnt[static_cast<int64_t>(t + i) * E + e] : 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s += c[i];
+    }
+    return s;
+}
+
+__global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int P, int32_t* __restrict__ tile_cnt,
+                                                          const int32_t* __restrict__ tile_err,
+                                                          int32_t* __restrict__ expert_counts,
+                                                          int32_t* __restrict__ expert_offsets,
+                                                          int32_t* __restrict__ dest_counts,
+                                                          int32_t* __restrict__ dest_offsets,
+                                                          int32_t* __restrict__ dev_status) {
+    __shared__ int32_t partial[kMaxExperts];  // per work unit (expert, tile slice)
+    __shared__ int32_t total[kMaxExperts];    // per expert
+    __shared__ int32_t offs[kMaxExperts];     // per expert, exclusive prefix
+    __shared__ int32_t scan[kScanThreads];
+    const int tid = threadIdx.x;
+
+    // Work units: tpe threads per expert when E is small, each owning a
+    // contiguous slice of tiles; one unit per expert when E >= 1024.
+    const int tpe = E >= kScanThreads ? 1 : kScanThreads / E;
+    const int units = E * tpe;
+    const int span = (ntiles + tpe - 1) / tpe;
+
+    for (int u = tid; u < units; u += kScanThreads) {
+        const int e = u / tpe, q = u - e * tpe;
+        const int lo = min(ntiles, q * span), hi = min(ntiles, lo + span);
+        partial[u] = sum_tiles(tile_cnt, E, e, lo, hi);
+    }
+    __syncthreads();
+    for (int e = tid; e < E; e += kScanThreads) {
+        int s = 0;
+        for (int q = 0; q < tpe; ++q) s += partial[e * tpe + q];
+        total[e] = s;
+    }
+    __syncthreads();
+
+    // Exclusive prefix over experts: each thread sums a run of consecutive
+    // experts, a Hillis-Steele scan combines the runs.
+    const int per = (E + kScanThreads - 1) / kScanThreads;
+    int local = 0;
+    for (int i = 0; i < per; ++i) {
+        const int e = tid * per + i;
+        if (e < E) local += total[e];
+    }
+    scan[tid] = local;
+    __syncthreads();
+    for (int off = 1; off < kScanThreads; off <<= 1) {
+        const int v = tid >= off ? scan[tid - off] : 0;
+        __syncthreads();
+        scan[tid] += v;
+        __syncthreads();
+    }
+    int run = scan[tid] - local;
+    for (int i = 0; i < per; ++i) {
+        const int e = tid * per + i;
+        if (e < E) {
+            offs[e] = run;
+            expert_counts[e] = total[e];
+            if (expert_offsets) expert_offsets[e] = run;
+            run += total[e];
+        }
+    }
+    __syncthreads();
+
+    // Rewrite each tile's count into the row of its first (t, k) per expert.
+    for (int u = tid; u < units; u += kScanThreads) {
+        const int e = u / tpe, q = u - e * tpe;
+        const int lo = min(ntiles, q * span), hi = min(ntiles, lo + span);
+        int base = offs[e];
+        for (int q2 = 0; q2 < q; ++q2) base += partial[e * tpe + q2];
+        for (int t = lo; t < hi; t += 8) {
+            int c[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) c[i] = (t + i < hi) ? tile_cnt[static_cast<int64_t>(t + i) * E + e] : 0;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                if (t + i < hi) tile_cnt[static_cast<int64_t>(t + i) * E + e] = base;
+                base += c[i];
+            }
+        }
+    }
+
+    const int L = E / P;
+    for (int r = tid; r < P; r += kScanThreads) {
+        int s = 0;
+        for (int e = r * L; e < (r + 1) * L; ++e) s += total[e];
+        dest_counts[r] = s;
+        dest_offsets[r] = offs[r * L];
+    }
+
+    int any = 0;
+    for (int t = tid; t < ntiles; t += kScanThreads) any |= tile_err[t];
+    any = __syncthreads_or(any);
+    if (tid == 0 && dev_status) *dev_status = any ? 1 : 0;
+}
+
+template <int U>
+__global__ __launch_bounds__(kBlock) void pack_rows(int T, int H, int K, int E, const char* __restrict__ x,
+                                                    const int32_t* __restrict__ ids,
+                                                    const int32_t* __restrict__ tile_base,
+                                                    const int32_t* __restrict__ lrank, int32_t* __restrict__ pos,
+                                                    char* __restrict__ packed) {
+    const uint32_t t = wave_index();
+    if (t >= static_cast<uint32_t>(T)) return;
+    const uint32_t lane = lane_index();
+    const int64_t rows = static_cast<int64_t>(T) * K;
+    int p = -1;
+    if (lane < static_cast<uint32_t>(K)) {
+        const int64_t j = static_cast<int64_t>(t) * K + lane;
+        const int e = ids[j];
+        const int r = lrank[j];
+        if (e >= 0 && e < E && r >= 0) {
+            const int64_t q = static_cast<int64_t>(tile_base[static_cast<int64_t>(t / kPackTileTokens) * E + e]) + r;
+            p = (q >= 0 && q < rows) ? static_cast<int>(q) : -1;
+        }
+        pos[j] = p;
+    }
+    const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
+    const char* src = x + t * row_bytes;
+    if (row_bytes % 16 == 0) {
+        const uint64_t nvec = row_bytes / 16;
+        for (uint64_t base = 0; base < nvec; base += U * kWave) {
+            u32x4 v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint64_t i = base + u * kWave + lane;
+                if (i < nvec) v[u] = load16(src + i * 16);
+            }
+            for (int k = 0; k < K; ++k) {
+                const int pk = __builtin_amdgcn_readlane(p, k);
+                if (pk < 0) continue;
+                char* dst = packed + static_cast<uint64_t>(pk) * row_bytes;
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const uint64_t i = base + u * kWave + lane;
+                    if (i < nvec) store16(dst + i * 16, v[u]);
+                }
+            }
+        }
+    } else {
+        for (uint64_t h = lane; h < static_cast<uint64_t>(H); h += kWave) {
+            const uint16_t v = reinterpret_cast<const uint16_t*>(src)[h];
+            for (int k = 0; k < K; ++k) {
+                const int pk = __builtin_amdgcn_readlane(p, k);
+                if (pk >= 0) reinterpret_cast<uint16_t*>(packed + static_cast<uint64_t>(pk) * row_bytes)[h] = v;
+            }
+        }
+    }
+}
+
+__global__ void set_status(int32_t* status) { *status = 0; }
+
+constexpr int kSlotGroup = 8;
+
+template <int U>
+__global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, const char* __restrict__ y,
+                                                      const int32_t* __restrict__ pos,
+                                                      const float* __restrict__ gates, char* __restrict__ out,
+                                                      int32_t* __restrict__ dev_status) {
+    const uint32_t t = wave_index();
+    if (t >= static_cast<uint32_t>(T)) return;
+    const uint32_t lane = lane_index();
+    const int64_t rows = static_cast<int64_t>(T) * K;
+    int p = -1;
+    float g = 0.0f;
+    if (lane < static_cast<uint32_t>(K)) {
+        const int64_t j = static_cast<int64_t>(t) * K + lane;
+        p = pos[j];
+        g = gates[j];
+        if (p < 0 || p >= rows) {
+            p = -1;
+            if (dev_status) atomicOr(dev_status, 1);
+        }
+    }
+    const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
+    char* dst = out + t * row_bytes;
+    if (row_bytes % 16 == 0) {
+        const uint64_t nvec = row_bytes / 16;
+        for (uint64_t base = 0; base < nvec; base += U * kWave) {
+            float acc[U][8];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[u][e] = 0.0f;
+            for (int k0 = 0; k0 < K; k0 += kSlotGroup) {
+                u32x4 v[kSlotGroup][U];
+                int pk[kSlotGroup];
+#pragma unroll
+                for (int kk = 0; kk < kSlotGroup; ++kk) {
+                    pk[kk] = (k0 + kk < K) ? __builtin_amdgcn_readlane(p, k0 + kk) : -1;
+                    if (pk[kk] < 0) continue;
+                    const char* row = y + static_cast<uint64_t>(pk[kk]) * row_bytes;
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        const uint64_t i = base + u * kWave + lane;
+                        if (i < nvec) v[kk][u] = load16(row + i * 16);
+                    }
+                }
+#pragma unroll
+                for (int kk = 0; kk < kSlotGroup; ++kk) {
+                    if (pk[kk] < 0) continue;
+                    const float gk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), k0 + kk));
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+#pragma unroll
+                        for (int m = 0; m < 4; ++m) {
+                            const uint32_t wv = v[kk][u][m];
+                            acc[u][2 * m] = __fadd_rn(acc[u][2 * m], __fmul_rn(gk, __uint_as_float(wv << 16)));
+                            acc[u][2 * m + 1] =
+                                __fadd_rn(acc[u][2 * m + 1], __fmul_rn(gk, __uint_as_float(wv & 0xFFFF0000u)));
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint64_t i = base + u * kWave + lane;
+                if (i < nvec) {
+                    u32x4 o;
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) o[m] = to_bf16(acc[u][2 * m]) | (to_bf16(acc[u][2 * m + 1]) << 16);
+                    store16(dst + i * 16, o);
+                }
+            }
+        }
+    } else {
+        for (uint64_t h = lane; h < static_cast<uint64_t>(H); h += kWave) {
+            float acc = 0.0f;
+            for (int k = 0; k < K; ++k) {
+                const int pk = __builtin_amdgcn_readlane(p, k);
+                if (pk < 0) continue;
+                const float gk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), k));
+                const uint16_t hv = reinterpret_cast<const uint16_t*>(y + static_cast<uint64_t>(pk) * row_bytes)[h];
+                acc = __fadd_rn(acc, __fmul_rn(gk, __uint_as_float(uint32_t(hv) << 16)));
+            }
+            reinterpret_cast<uint16_t*>(dst)[h] = static_cast<uint16_t>(to_bf16(acc));
+        }
+    }
+}
+
+constexpr int kPackUnroll = 8;
+constexpr int kUnpackUnroll = 2;
+
+uint64_t align256(uint64_t b) { return (b + 255) & ~uint64_t(255); }
+
+}  // namespace
+
+uint64_t pack_workspace_bytes(int T, int K, int E) {
+    const uint64_t ntiles = (static_cast<uint64_t>(T) + kPackTileTokens - 1) / kPackTileTokens;
+    return align256(4 * ntiles * E) + align256(4 * static_cast<uint64_t>(T) * K) + align256(4 * ntiles);
+}
+
+PackWorkspace pack_workspace_carve(void* base, int T, int K, int E) {
+    const uint64_t ntiles = (static_cast<uint64_t>(T) + kPackTileTokens - 1) / kPackTileTokens;
+    char* p = static_cast<char*>(base);
+    PackWorkspace ws{};
+    ws.tile_base = reinterpret_cast<int32_t*>(p);
+    p += align256(4 * ntiles * E);
+    ws.lrank = reinterpret_cast<int32_t*>(p);
+    p += align256(4 * static_cast<uint64_t>(T) * K);
+    ws.tile_err = reinterpret_cast<int32_t*>(p);
+    return ws;
+}
+
+hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, const int32_t* ids, uint16_t* packed,
+                       int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts, int32_t* expert_offsets,
+                       int32_t* pos, int32_t* dev_status, const PackWorkspace& ws, hipStream_t stream) {
+    const int ntiles = (T + kPackTileTokens - 1) / kPackTileTokens;
+    (void)hipGetLastError();
+    if (ntiles > 0) {
+        hipLaunchKernelGGL(pack_tiles, dim3(ntiles), dim3(kBlock), static_cast<size_t>(E) * 8, stream, T, K, E, ids,
+                           ws.tile_base, ws.lrank, ws.tile_err);
+    }
+    hipLaunchKernelGGL(pack_scan, dim3(1), dim3(kScanThreads), 0, stream, ntiles, E, P, ws.tile_base, ws.tile_err,
+                       expert_counts, expert_offsets, dest_counts, dest_offsets, dev_status);
+    if (T > 0) {
+        const dim3 grid((T + kWavesPerBlock - 1) / kWavesPerBlock);
+        hipLaunchKernelGGL(pack_rows<kPackUnroll>, grid, dim3(kBlock), 0, stream, T, H, K, E,
+                           reinterpret_cast<const char*>(x), ids, ws.tile_base, ws.lrank, pos,
+                           reinterpret_cast<char*>(packed));
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_unpack(int T, int H, int K, const uint16_t* y, const int32_t* pos, const float* gates, uint16_t* out,
+                         int32_t* dev_status, hipStream_t stream) {
+    (void)hipGetLastError();
+    if (dev_status) hipLaunchKernelGGL(set_status, dim3(1), dim3(1), 0, stream, dev_status);
+    if (T > 0) {
+        const dim3 grid((T + kWavesPerBlock - 1) / kWavesPerBlock);
+        hipLaunchKernelGGL(unpack_rows<kUnpackUnroll>, grid, dim3(kBlock), 0, stream, T, H, K,
+                           reinterpret_cast<const char*>(y), pos, gates, reinterpret_cast<char*>(out), dev_status);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace purlin

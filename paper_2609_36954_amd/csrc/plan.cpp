@@ -1,0 +1,257 @@
+// Host orchestrator: (op, P, count, dtype, chunk) -> chunk descriptors ->
+// wavefront work items.  Pure host C++ (no HIP), so it runs and is tested
+// on machines without a GPU.
+//
+// Paper passages (Purlin, arXiv 2609.36954):
+//  - Section 3.1 / Listing 1: each collective is a consume op (copy or
+//    reduce) between an input and an output layout; AllReduce is
+//    compose<ReduceScatter, AllGather>, the AllGather consuming the
+//    ReduceScatter result in place.
+//  - Section 3.2 / Listing 2: work proceeds per chunk of a partition; a
+//    packed output is addressed dst + offset, a scattered or transposed
+//    output dst + peer * partBytes + offset; reduce consumes the chunk of
+//    every rank, copy consumes one peer's chunk.
+//  - Section 3.3, Eq. 3: throughput needs enough bytes in flight; here the
+//    policy cuts descriptors into work items so that a launch has thousands
+//    of independent wavefronts.
+
+#include "plan.h"
+
+#include <algorithm>
+#include <new>
+
+namespace purlin {
+namespace {
+
+constexpr uint64_t kMinItem = 1024;        // one 16-byte access per lane of a 64-wide wave
+constexpr uint64_t kMaxItem = 64 * 1024;   // largest automatic work item
+constexpr uint64_t kTargetItems = 4096;    // 16 wavefronts per CU on 256 CUs
+
+uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
+
+uint64_t pow2_floor(uint64_t v) {
+    uint64_t p = 1;
+    while (p <= v / 2) p <<= 1;
+    return p;
+}
+
+purlin_desc make_desc(uint32_t kind, uint32_t phase, uint32_t nsrc, uint32_t src_buf, uint32_t src_step,
+                      uint32_t ndst, uint32_t dst_buf, uint32_t dst_step, uint64_t src_off, uint64_t dst_off,
+                      uint64_t bytes, uint32_t part, uint32_t chunk) {
+    purlin_desc d{};
+    d.kind = kind;
+    d.phase = phase;
+    d.nsrc = nsrc;
+    d.src_buf = src_buf;
+    d.src_step = src_step;
+    d.ndst = ndst;
+    d.dst_buf = dst_buf;
+    d.dst_step = dst_step;
+    d.src_off = src_off;
+    d.dst_off = dst_off;
+    d.bytes = bytes;
+    d.part = part;
+    d.chunk = chunk;
+    return d;
+}
+
+// Automatic work-item size for one phase: aim at kTargetItems items, never
+// below one wave-wide 16-byte access per lane, never above kMaxItem, and
+// large enough to keep the item count under PURLIN_MAX_ITEMS.
+uint64_t auto_item_bytes(uint64_t phase_bytes) {
+    uint64_t item = pow2_floor(std::max<uint64_t>(1, phase_bytes / kTargetItems));
+    item = std::min(std::max(item, kMinItem), kMaxItem);
+    const uint64_t floor_for_cap = ceil_div(phase_bytes, PURLIN_MAX_ITEMS / 2);
+    if (item < floor_for_cap) item = ceil_div(floor_for_cap, 16) * 16;
+    return item;
+}
+
+}  // namespace
+
+purlin_status build_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype, uint64_t chunk,
+                         const purlin_policy* policy, uint32_t flags, Plan& out) {
+    if (op < PURLIN_ALLREDUCE || op > PURLIN_ALLTOALL) return PURLIN_ERR_INVALID;
+    if (dtype != PURLIN_FP32 && dtype != PURLIN_BF16) return PURLIN_ERR_INVALID;
+    if (P < 1 || P > PURLIN_MAX_RANKS) return PURLIN_ERR_INVALID;
+    if (count % static_cast<uint64_t>(P) != 0) return PURLIN_ERR_INVALID;
+    if (flags & ~PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
+    const uint64_t s = dtype == PURLIN_FP32 ? 4 : 2;
+    if (chunk < s || chunk % s != 0) return PURLIN_ERR_INVALID;
+    if (count > (uint64_t(1) << 58) / s) return PURLIN_ERR_INVALID;
+
+    purlin_policy pol{};
+    if (policy) {
+        pol = *policy;
+        if (pol.item_bytes % 16 != 0) return PURLIN_ERR_INVALID;
+        if (pol.fanout > 2 || pol.ar_mode > 2) return PURLIN_ERR_INVALID;
+        for (uint32_t r : pol.reserved)
+            if (r != 0) return PURLIN_ERR_INVALID;
+    }
+    if (pol.fanout == 0) pol.fanout = 2;
+    if (pol.ar_mode == 0) pol.ar_mode = 2;
+
+    const uint64_t M = count / P;       // elements per partition
+    const uint64_t part = M * s;        // partBytes
+    const uint64_t Cp = part ? ceil_div(part, chunk) : 0;
+
+    out = Plan{};
+    out.op = op;
+    out.P = P;
+    out.count = count;
+    out.dtype = dtype;
+    out.chunk = chunk;
+    out.flags = flags;
+    out.elem_bytes = s;
+    switch (op) {
+        case PURLIN_ALLREDUCE:
+        case PURLIN_ALLTOALL:
+            out.in_bytes = count * s;
+            out.out_bytes = count * s;
+            break;
+        case PURLIN_REDUCE_SCATTER:
+            out.in_bytes = count * s;
+            out.out_bytes = part;
+            break;
+        case PURLIN_ALLGATHER:
+            out.in_bytes = part;
+            out.out_bytes = count * s;
+            break;
+    }
+
+    // Upper bound on descriptors before allocating anything.
+    const uint64_t Pu = static_cast<uint64_t>(P);
+    if (Cp > PURLIN_MAX_ITEMS || Cp * Pu * Pu * 2 > PURLIN_MAX_ITEMS) return PURLIN_ERR_NOMEM;
+
+    const uint32_t in0 = 0, out0 = static_cast<uint32_t>(P);
+    try {
+        std::vector<purlin_desc>& D = out.descs;
+        auto for_chunks = [&](uint32_t k, auto&& emit) {
+            for (uint64_t c = 0; c < Cp; ++c) {
+                const uint64_t off = c * chunk;
+                const uint64_t len = std::min(chunk, part - off);
+                emit(static_cast<uint32_t>(c), k * part + off, off, len);
+            }
+        };
+        switch (op) {
+            case PURLIN_REDUCE_SCATTER:
+                // reduce, scattered -> packed: partition k of every input,
+                // summed in rank order, lands at out_k + offset.
+                for (uint32_t k = 0; k < Pu; ++k)
+                    for_chunks(k, [&](uint32_t c, uint64_t scat, uint64_t pk, uint64_t len) {
+                        D.push_back(make_desc(PURLIN_KIND_REDUCE, 0, P, in0, 1, 1, out0 + k, 0, scat, pk, len, k, c));
+                    });
+                break;
+            case PURLIN_ALLGATHER:
+                // copy, packed -> scattered: peer k's contribution lands at
+                // out_r + k * partBytes + offset for every consumer r.
+                for (uint32_t k = 0; k < Pu; ++k)
+                    for_chunks(k, [&](uint32_t c, uint64_t scat, uint64_t pk, uint64_t len) {
+                        if (pol.fanout == 2) {
+                            D.push_back(make_desc(PURLIN_KIND_COPY, 0, 1, in0 + k, 0, P, out0, 1, pk, scat, len, k, c));
+                        } else {
+                            for (uint32_t r = 0; r < Pu; ++r)
+                                D.push_back(make_desc(PURLIN_KIND_COPY, 0, 1, in0 + k, 0, 1, out0 + r, 0, pk, scat, len, k, c));
+                        }
+                    });
+                break;
+            case PURLIN_ALLTOALL:
+                // copy, scattered -> transposed: consumer r takes partition r
+                // of peer p and places it at out_r + p * partBytes + offset.
+                for (uint32_t r = 0; r < Pu; ++r)
+                    for (uint32_t p = 0; p < Pu; ++p)
+                        for_chunks(r, [&](uint32_t c, uint64_t scat, uint64_t pk, uint64_t len) {
+                            D.push_back(make_desc(PURLIN_KIND_COPY, 0, 1, in0 + p, 0, 1, out0 + r, 0, scat, p * part + pk, len, r, c));
+                        });
+                break;
+            case PURLIN_ALLREDUCE:
+                if (pol.ar_mode == 1) {
+                    // compose<ReduceScatter, AllGather> in place: phase 0
+                    // reduces partition k into out_k's k-th partition (the
+                    // intermediate Y_k), phase 1 copies it to every other rank.
+                    for (uint32_t k = 0; k < Pu; ++k)
+                        for_chunks(k, [&](uint32_t c, uint64_t scat, uint64_t, uint64_t len) {
+                            D.push_back(make_desc(PURLIN_KIND_REDUCE, 0, P, in0, 1, 1, out0 + k, 0, scat, scat, len, k, c));
+                        });
+                    for (uint32_t k = 0; k < Pu; ++k)
+                        for_chunks(k, [&](uint32_t c, uint64_t scat, uint64_t, uint64_t len) {
+                            if (pol.fanout == 2) {
+                                if (k > 0)
+                                    D.push_back(make_desc(PURLIN_KIND_COPY, 1, 1, out0 + k, 0, k, out0, 1, scat, scat, len, k, c));
+                                if (k + 1 < Pu)
+                                    D.push_back(make_desc(PURLIN_KIND_COPY, 1, 1, out0 + k, 0, P - 1 - k, out0 + k + 1, 1,
+                                                          scat, scat, len, k, c));
+                            } else {
+                                for (uint32_t r = 0; r < Pu; ++r)
+                                    if (r != k)
+                                        D.push_back(make_desc(PURLIN_KIND_COPY, 1, 1, out0 + k, 0, 1, out0 + r, 0, scat, scat, len, k, c));
+                            }
+                        });
+                } else {
+                    // One phase: each chunk of partition k is reduced once
+                    // and written to every rank's output.
+                    for (uint32_t k = 0; k < Pu; ++k)
+                        for_chunks(k, [&](uint32_t c, uint64_t scat, uint64_t, uint64_t len) {
+                            D.push_back(make_desc(PURLIN_KIND_REDUCE, 0, P, in0, 1, P, out0, 1, scat, scat, len, k, c));
+                        });
+                }
+                break;
+        }
+        out.policy = pol;
+
+        for (const purlin_desc& d : D) out.sched_bytes += (uint64_t(d.nsrc) + d.ndst) * d.bytes;
+
+        // Cut descriptors into work items, phase by phase.
+        uint64_t items_total = 0;
+        for (uint32_t ph = 0; ph < 2; ++ph) {
+            uint64_t phase_bytes = 0, ndesc = 0;
+            for (const purlin_desc& d : D)
+                if (d.phase == ph) phase_bytes += d.bytes, ++ndesc;
+            if (ndesc == 0) continue;
+            const uint64_t item = pol.item_bytes ? pol.item_bytes : auto_item_bytes(phase_bytes);
+            for (const purlin_desc& d : D)
+                if (d.phase == ph) items_total += ceil_div(d.bytes, item);
+            if (items_total > PURLIN_MAX_ITEMS) return PURLIN_ERR_NOMEM;
+        }
+        out.items.reserve(items_total);
+        for (uint32_t ph = 0; ph < 2; ++ph) {
+            uint64_t phase_bytes = 0;
+            bool any = false;
+            for (const purlin_desc& d : D)
+                if (d.phase == ph) phase_bytes += d.bytes, any = true;
+            if (!any) continue;
+            const uint64_t item = pol.item_bytes ? pol.item_bytes : auto_item_bytes(phase_bytes);
+            Phase& phase = out.phases[out.nphases++];
+            phase.begin = out.items.size();
+            bool first = true;
+            for (const purlin_desc& d : D) {
+                if (d.phase != ph) continue;
+                if (first) {
+                    phase.kind = d.kind;
+                    phase.nsrc = d.nsrc;
+                    phase.src_buf = d.src_buf;
+                    phase.src_step = d.src_step;
+                    first = false;
+                } else if (d.kind != phase.kind ||
+                           (d.kind == PURLIN_KIND_REDUCE &&
+                            (d.nsrc != phase.nsrc || d.src_buf != phase.src_buf || d.src_step != phase.src_step))) {
+                    return PURLIN_ERR_UNSUPPORTED;  // a phase is one kernel: one consume op, one source set
+                }
+                for (uint64_t o = 0; o < d.bytes; o += item) {
+                    purlin_desc w = d;
+                    w.src_off += o;
+                    w.dst_off += o;
+                    w.bytes = std::min(item, d.bytes - o);
+                    out.items.push_back(w);
+                }
+            }
+            phase.count = out.items.size() - phase.begin;
+        }
+    } catch (const std::bad_alloc&) {
+        out.descs.clear();
+        out.items.clear();
+        return PURLIN_ERR_NOMEM;
+    }
+    return PURLIN_OK;
+}
+
+}  // namespace purlin

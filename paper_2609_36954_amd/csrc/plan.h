@@ -1,0 +1,49 @@
+// Internal plan object shared by the planner (plan.cpp, host only) and the
+// ABI glue (abi.hip).  Not part of the public ABI.
+#pragma once
+
+#include <cstdint>
+#include <vector>
+
+#include "purlin.h"
+
+namespace purlin {
+
+// One kernel launch of a plan: every work item of a phase has the same
+// consume op and, for REDUCE, the same source count.
+struct Phase {
+    uint32_t kind = PURLIN_KIND_COPY;
+    uint32_t nsrc = 1;
+    uint32_t src_buf = 0;   // REDUCE phases: every item sums bufs[src_buf + p * src_step]
+    uint32_t src_step = 0;
+    uint64_t begin = 0;  // first work item
+    uint64_t count = 0;  // work items
+};
+
+struct Plan {
+    purlin_op op{};
+    int P = 0;
+    uint64_t count = 0;
+    purlin_dtype dtype{};
+    uint64_t chunk = 0;
+    purlin_policy policy{};  // resolved: no "auto" fields left
+    uint32_t flags = 0;
+
+    uint64_t elem_bytes = 0;
+    uint64_t in_bytes = 0;   // per rank
+    uint64_t out_bytes = 0;  // per rank
+    uint64_t sched_bytes = 0;
+
+    std::vector<purlin_desc> descs;  // chunk descriptors
+    std::vector<purlin_desc> items;  // work items (descriptors cut at item_bytes)
+    int nphases = 0;
+    Phase phases[2];
+
+    purlin_desc* d_items = nullptr;  // device copy of items (null for host-only plans)
+};
+
+// Validates the request and fills `out` (host tables only).  Pure host code.
+purlin_status build_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype, uint64_t chunk,
+                         const purlin_policy* policy, uint32_t flags, Plan& out);
+
+}  // namespace purlin

@@ -1,0 +1,301 @@
+"""Thin ctypes binding of libpurlin.so (include/purlin.h).
+
+Argument marshalling only: every step of the datapath runs in the library's
+HIP kernels.  PyTorch supplies device memory (``tensor.data_ptr()``) and the
+stream (``torch.cuda.current_stream().cuda_stream``, a hipStream_t on ROCm).
+There is no CPU fallback: if the library is missing, every call raises.
+
+The functions keep the C names (``purlin_plan``, ``purlin_exec``, ...);
+``Plan`` wraps a plan handle.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpurlin.so")
+
+PURLIN_OK = 0
+PURLIN_ERR_INVALID = 1
+PURLIN_ERR_UNSUPPORTED = 2
+PURLIN_ERR_NOMEM = 3
+PURLIN_ERR_DEVICE = 4
+
+OPS = {"allreduce": 0, "reduce_scatter": 1, "allgather": 2, "alltoall": 3}
+DTYPES = {"fp32": 0, "bf16": 1}
+ELEM_BYTES = {"fp32": 4, "bf16": 2}
+KIND_COPY = 0
+KIND_REDUCE = 1
+PLAN_HOST_ONLY = 1
+MAX_RANKS = 16
+
+# numpy view of purlin_desc (64 bytes, no padding)
+DESC_DTYPE = np.dtype(
+    [
+        ("kind", "<u4"),
+        ("phase", "<u4"),
+        ("nsrc", "<u4"),
+        ("src_buf", "<u4"),
+        ("src_step", "<u4"),
+        ("ndst", "<u4"),
+        ("dst_buf", "<u4"),
+        ("dst_step", "<u4"),
+        ("src_off", "<u8"),
+        ("dst_off", "<u8"),
+        ("bytes", "<u8"),
+        ("part", "<u4"),
+        ("chunk", "<u4"),
+    ]
+)
+assert DESC_DTYPE.itemsize == 64
+
+
+class PurlinError(RuntimeError):
+    def __init__(self, status, what=""):
+        self.status = status
+        super().__init__(f"{what}: purlin status {status} ({status_string(status)})" if what else status_string(status))
+
+
+class Policy(ctypes.Structure):
+    _fields_ = [
+        ("item_bytes", ctypes.c_uint64),
+        ("fanout", ctypes.c_uint32),
+        ("ar_mode", ctypes.c_uint32),
+        ("reserved", ctypes.c_uint32 * 4),
+    ]
+
+
+_lib = None
+_c_u64p = ctypes.POINTER(ctypes.c_uint64)
+_vp = ctypes.c_void_p
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise PurlinError(PURLIN_ERR_UNSUPPORTED, f"HIP library not built ({LIB_PATH}); run python -m paper_2609_36954_amd.build")
+    L = ctypes.CDLL(LIB_PATH)
+    i32, u32, u64 = ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64
+    L.purlin_plan.argtypes = [i32, i32, u64, i32, u64, ctypes.POINTER(_vp)]
+    L.purlin_plan_ex.argtypes = [i32, i32, u64, i32, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
+    L.purlin_plan_info.argtypes = [_vp, _c_u64p, _c_u64p, _c_u64p, _c_u64p]
+    L.purlin_plan_descriptors.argtypes = [_vp, ctypes.POINTER(_vp), _c_u64p, _c_u64p]
+    L.purlin_plan_items.argtypes = [_vp, ctypes.POINTER(_vp), _c_u64p, _c_u64p]
+    L.purlin_exec.argtypes = [_vp, ctypes.POINTER(_vp), _vp]
+    L.purlin_plan_destroy.argtypes = [_vp]
+    L.purlin_plan_destroy.restype = None
+    L.purlin_pack_workspace_size.argtypes = [i32, i32, i32, _c_u64p]
+    L.purlin_pack.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 10 + [u64, _vp]
+    L.purlin_unpack.argtypes = [i32, i32, i32] + [_vp] * 6
+    L.purlin_status_string.argtypes = [i32]
+    L.purlin_status_string.restype = ctypes.c_char_p
+    L.purlin_version.argtypes = []
+    L.purlin_version.restype = ctypes.c_char_p
+    for name in ("purlin_plan", "purlin_plan_ex", "purlin_plan_info", "purlin_plan_descriptors", "purlin_plan_items",
+                 "purlin_exec", "purlin_pack_workspace_size", "purlin_pack", "purlin_unpack"):
+        getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def status_string(status):
+    if _lib is None and not os.path.exists(LIB_PATH):
+        return f"status {status}"
+    return lib().purlin_status_string(int(status)).decode()
+
+
+purlin_status_string = status_string
+
+
+def purlin_version():
+    return lib().purlin_version().decode()
+
+
+def _check(status, what):
+    if status != PURLIN_OK:
+        raise PurlinError(status, what)
+
+
+def _stream_handle(stream):
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _require_cuda(t, name, itemsize=None):
+    if not t.is_cuda:
+        raise PurlinError(PURLIN_ERR_INVALID, f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise PurlinError(PURLIN_ERR_INVALID, f"{name} must be contiguous")
+    if itemsize is not None and t.element_size() != itemsize:
+        raise PurlinError(PURLIN_ERR_INVALID, f"{name} must have {itemsize}-byte elements")
+
+
+class Plan:
+    """A planned collective (immutable).  ``exec`` runs it on a stream."""
+
+    def __init__(self, op, P, count, dtype, chunk, policy=None, host_only=False):
+        if op not in OPS:
+            raise PurlinError(PURLIN_ERR_INVALID, f"unknown op {op!r}")
+        if dtype not in DTYPES:
+            raise PurlinError(PURLIN_ERR_INVALID, f"unknown dtype {dtype!r}")
+        self.op, self.P, self.count, self.dtype, self.chunk = op, int(P), int(count), dtype, int(chunk)
+        self.host_only = bool(host_only)
+        h = ctypes.c_void_p()
+        L = lib()
+        if policy is None and not host_only:
+            st = L.purlin_plan(OPS[op], int(P), int(count), DTYPES[dtype], int(chunk), ctypes.byref(h))
+        else:
+            pol = None
+            if policy is not None:
+                pol = policy if isinstance(policy, Policy) else Policy(**policy)
+            st = L.purlin_plan_ex(OPS[op], int(P), int(count), DTYPES[dtype], int(chunk),
+                                  ctypes.byref(pol) if pol is not None else None,
+                                  PLAN_HOST_ONLY if host_only else 0, ctypes.byref(h))
+        _check(st, "purlin_plan")
+        self._h = h
+        info = self.info()
+        self.n_desc = info["n_desc"]
+        self.in_bytes = info["in_bytes_per_rank"]
+        self.out_bytes = info["out_bytes_per_rank"]
+        self.sched_bytes = info["sched_bytes"]
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise PurlinError(PURLIN_ERR_INVALID, "plan destroyed")
+        return self._h
+
+    def info(self):
+        vals = [ctypes.c_uint64() for _ in range(4)]
+        _check(lib().purlin_plan_info(self.handle, *[ctypes.byref(v) for v in vals]), "purlin_plan_info")
+        return dict(zip(("n_desc", "in_bytes_per_rank", "out_bytes_per_rank", "sched_bytes"), (v.value for v in vals)))
+
+    def descriptors(self):
+        """Copy of the chunk descriptor table as a structured numpy array."""
+        p, n, stride = ctypes.c_void_p(), ctypes.c_uint64(), ctypes.c_uint64()
+        _check(lib().purlin_plan_descriptors(self.handle, ctypes.byref(p), ctypes.byref(n), ctypes.byref(stride)),
+               "purlin_plan_descriptors")
+        assert stride.value == DESC_DTYPE.itemsize
+        return self._copy_table(p, n.value)
+
+    def items(self):
+        """(work items as a structured array, [phase0_begin, phase1_begin, n])."""
+        p, n = ctypes.c_void_p(), ctypes.c_uint64()
+        pb = (ctypes.c_uint64 * 3)()
+        _check(lib().purlin_plan_items(self.handle, ctypes.byref(p), ctypes.byref(n), pb), "purlin_plan_items")
+        return self._copy_table(p, n.value), list(pb)
+
+    @staticmethod
+    def _copy_table(p, n):
+        if n == 0:
+            return np.zeros(0, dtype=DESC_DTYPE)
+        buf = (ctypes.c_char * (n * DESC_DTYPE.itemsize)).from_address(p.value)
+        return np.frombuffer(bytes(buf), dtype=DESC_DTYPE).copy()
+
+    def exec(self, ins, outs, stream=None):
+        """Run on device tensors ``ins`` (P inputs) and ``outs`` (P outputs)."""
+        purlin_exec(self, ins, outs, stream)
+
+    def destroy(self):
+        if getattr(self, "_h", None) is not None and _lib is not None:
+            _lib.purlin_plan_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def purlin_plan(op, P, count, dtype, chunk, policy=None, host_only=False):
+    return Plan(op, P, count, dtype, chunk, policy=policy, host_only=host_only)
+
+
+def purlin_exec(plan, ins, outs, stream=None):
+    P = plan.P
+    if len(ins) != P or len(outs) != P:
+        raise PurlinError(PURLIN_ERR_INVALID, f"need {P} inputs and {P} outputs")
+    if plan.count:
+        s = ELEM_BYTES[plan.dtype]
+        for t in ins:
+            _require_cuda(t, "input", s)
+            if t.numel() * s < plan.in_bytes:
+                raise PurlinError(PURLIN_ERR_INVALID, "input buffer too small")
+        for t in outs:
+            _require_cuda(t, "output", s)
+            if t.numel() * s < plan.out_bytes:
+                raise PurlinError(PURLIN_ERR_INVALID, "output buffer too small")
+    arr = (ctypes.c_void_p * (2 * P))(*[t.data_ptr() for t in list(ins) + list(outs)])
+    _check(lib().purlin_exec(plan.handle, arr, _stream_handle(stream) if plan.count else None), "purlin_exec")
+
+
+def purlin_pack_workspace_size(T, K, E):
+    b = ctypes.c_uint64()
+    _check(lib().purlin_pack_workspace_size(int(T), int(K), int(E), ctypes.byref(b)), "purlin_pack_workspace_size")
+    return b.value
+
+
+def purlin_pack(x, ids, E, P, out=None, workspace=None, dev_status=None, stream=None):
+    """MoE dispatch of ``x`` (bf16 [T, H]) by ``ids`` (int32 [T, K]).
+
+    Returns a dict of device tensors: packed [T*K, H], dest_counts [P],
+    dest_offsets [P], expert_counts [E], expert_offsets [E], pos [T, K].
+    ``out`` may supply preallocated tensors under the same keys.
+    """
+    import torch
+
+    T, H = x.shape
+    K = ids.shape[1]
+    if ids.shape[0] != T:
+        raise PurlinError(PURLIN_ERR_INVALID, "x and ids disagree on T")
+    _require_cuda(x, "x", 2)
+    _require_cuda(ids, "ids", 4)
+    dev = x.device
+    o = dict(out or {})
+    o.setdefault("packed", torch.empty((T * K, H), dtype=x.dtype, device=dev))
+    for name, n in (("dest_counts", P), ("dest_offsets", P), ("expert_counts", E), ("expert_offsets", E)):
+        o.setdefault(name, torch.empty(n, dtype=torch.int32, device=dev))
+    o.setdefault("pos", torch.empty((T, K), dtype=torch.int32, device=dev))
+    wsb = purlin_pack_workspace_size(T, K, E)
+    if workspace is None:
+        workspace = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+    _require_cuda(o["packed"], "packed", 2)
+    st = lib().purlin_pack(int(T), int(H), int(K), int(E), int(P), _ptr(x), _ptr(ids), _ptr(o["packed"]),
+                           _ptr(o["dest_counts"]), _ptr(o["dest_offsets"]), _ptr(o["expert_counts"]),
+                           _ptr(o["expert_offsets"]), _ptr(o["pos"]), _ptr(dev_status), _ptr(workspace),
+                           int(workspace.numel() * workspace.element_size()), _stream_handle(stream))
+    _check(st, "purlin_pack")
+    return o
+
+
+def purlin_unpack(y, pos, gates, out=None, dev_status=None, stream=None):
+    """MoE combine: bf16 [T, H] = sum_k gates[t, k] * y[pos[t, k]] in slot order."""
+    import torch
+
+    T, K = pos.shape
+    H = y.shape[1]
+    _require_cuda(y, "y", 2)
+    _require_cuda(pos, "pos", 4)
+    _require_cuda(gates, "gates", 4)
+    if gates.dtype != torch.float32:
+        raise PurlinError(PURLIN_ERR_INVALID, "gates must be float32")
+    if out is None:
+        out = torch.empty((T, H), dtype=y.dtype, device=y.device)
+    _require_cuda(out, "out", 2)
+    st = lib().purlin_unpack(int(T), int(H), int(K), _ptr(y), _ptr(pos), _ptr(gates), _ptr(out), _ptr(dev_status),
+                             _stream_handle(stream))
+    _check(st, "purlin_unpack")
+    return out

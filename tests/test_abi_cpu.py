@@ -1,0 +1,194 @@
+"""The C-ABI library on a machine without a GPU.
+
+* it loads and exports every function include/purlin.h declares;
+* argument validation returns the documented status before any HIP call
+  (plans built host-only, pack/unpack rejected on their arguments).
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_36954_amd import purlin as PL
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "purlin.h")
+
+INVALID, UNSUPPORTED, NOMEM = PL.PURLIN_ERR_INVALID, PL.PURLIN_ERR_UNSUPPORTED, PL.PURLIN_ERR_NOMEM
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"PURLIN_API\s+[\w\s\*]+?\b(purlin_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("purlin_plan", "purlin_exec", "purlin_pack", "purlin_unpack", "purlin_plan_destroy",
+                     "purlin_plan_info", "purlin_plan_descriptors", "purlin_pack_workspace_size",
+                     "purlin_status_string"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = PL.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+        assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value
+
+
+def test_status_strings():
+    assert PL.status_string(0) == "ok"
+    assert PL.status_string(1) == "invalid argument"
+    assert PL.status_string(99) == "unknown status"
+    assert PL.purlin_version()
+
+
+def _plan_status(op, P, count, dtype, chunk, policy=None, flags=PL.PLAN_HOST_ONLY):
+    h = ctypes.c_void_p()
+    pol = PL.Policy(**policy) if policy else None
+    st = PL.lib().purlin_plan_ex(op, P, count, dtype, chunk, ctypes.byref(pol) if pol else None, flags, ctypes.byref(h))
+    if h.value:
+        PL.lib().purlin_plan_destroy(h)
+    elif st == 0:
+        pytest.fail("OK status without a plan")
+    if st != 0:
+        assert not h.value, "a failed call must leave *out_plan NULL"
+    return st
+
+
+@pytest.mark.parametrize(
+    "args,want",
+    [
+        ((0, 4, 1024, 0, 64), 0),
+        ((4, 4, 1024, 0, 64), INVALID),  # unknown op
+        ((-1, 4, 1024, 0, 64), INVALID),
+        ((0, 4, 1024, 2, 64), INVALID),  # unknown dtype
+        ((0, 0, 1024, 0, 64), INVALID),  # P < 1
+        ((0, 17, 17 * 64, 0, 64), INVALID),  # P > 16
+        ((0, 16, 16 * 64, 0, 64), 0),
+        ((0, 3, 1024, 0, 64), INVALID),  # count % P
+        ((1, 4, 1024, 1, 1), INVALID),  # chunk < element size
+        ((1, 4, 1024, 1, 3), INVALID),  # chunk not a multiple of it
+        ((1, 4, 1024, 0, 6), INVALID),
+        ((1, 4, 1024, 1, 2), 0),
+        ((2, 4, 0, 1, 2), 0),  # count = 0 is valid
+        ((0, 8, 8 << 30, 1, 2), NOMEM),  # far more than 2^24 work items
+    ],
+)
+def test_plan_argument_validation(args, want):
+    assert _plan_status(*args) == want
+
+
+@pytest.mark.parametrize(
+    "policy,want",
+    [
+        (dict(item_bytes=24), INVALID),
+        (dict(item_bytes=16), 0),
+        (dict(fanout=3), INVALID),
+        (dict(ar_mode=3), INVALID),
+        (dict(reserved=(ctypes.c_uint32 * 4)(0, 1, 0, 0)), INVALID),
+        (dict(item_bytes=1 << 20, fanout=1, ar_mode=1), 0),
+    ],
+)
+def test_policy_validation(policy, want):
+    assert _plan_status(0, 4, 4096, 1, 256, policy) == want
+
+
+def test_unknown_flags_rejected():
+    assert _plan_status(0, 4, 4096, 1, 256, flags=0x80) == INVALID
+
+
+def test_null_out_plan_rejected():
+    assert PL.lib().purlin_plan_ex(0, 4, 4096, 1, 256, None, PL.PLAN_HOST_ONLY, None) == INVALID
+
+
+def test_exec_rejections_without_device():
+    L = PL.lib()
+    assert L.purlin_exec(None, None, None) == INVALID
+    plan = PL.Plan("allreduce", 2, 64, "bf16", 32, host_only=True)
+    bufs = (ctypes.c_void_p * 4)(0x1000, 0x2000, 0x3000, 0x4000)
+    assert L.purlin_exec(plan.handle, bufs, None) == INVALID  # host-only plans do not execute
+    assert L.purlin_exec(plan.handle, None, None) == INVALID
+    empty = PL.Plan("allreduce", 2, 0, "bf16", 32, host_only=True)
+    assert L.purlin_exec(empty.handle, None, None) == 0  # count = 0: a no-op
+
+
+def test_destroy_null_is_a_noop():
+    PL.lib().purlin_plan_destroy(None)
+
+
+def test_info_and_tables_reject_null():
+    L = PL.lib()
+    assert L.purlin_plan_info(None, None, None, None, None) == INVALID
+    assert L.purlin_plan_descriptors(None, None, None, None) == INVALID
+    assert L.purlin_plan_items(None, None, None, None) == INVALID
+
+
+def test_pack_workspace_size():
+    L = PL.lib()
+    b = ctypes.c_uint64()
+    assert L.purlin_pack_workspace_size(4096, 8, 256, ctypes.byref(b)) == 0
+    # 64 tiles x 256 experts + 32768 ranks + 64 flags, 4 bytes each, 256-byte aligned pieces
+    assert b.value == 65536 + 131072 + 256
+    assert L.purlin_pack_workspace_size(4096, 0, 256, ctypes.byref(b)) == INVALID
+    assert L.purlin_pack_workspace_size(4096, 65, 256, ctypes.byref(b)) == INVALID
+    assert L.purlin_pack_workspace_size(4096, 8, 4097, ctypes.byref(b)) == INVALID
+    assert L.purlin_pack_workspace_size(-1, 8, 256, ctypes.byref(b)) == INVALID
+    assert L.purlin_pack_workspace_size(1 << 28, 8, 256, ctypes.byref(b)) == INVALID
+    assert L.purlin_pack_workspace_size(4096, 8, 256, None) == INVALID
+
+
+def _pack(T=64, H=64, K=2, E=8, P=2, x=0x1000, ids=0x2000, packed=0x3000, dc=0x4000, do=0x5000, ec=0x6000, eo=None,
+          pos=0x7000, status=None, ws=0x8000, wsb=1 << 20):
+    return PL.lib().purlin_pack(T, H, K, E, P, x, ids, packed, dc, do, ec, eo, pos, status, ws, wsb, None)
+
+
+@pytest.mark.parametrize(
+    "kw",
+    [
+        dict(K=0),
+        dict(K=65),
+        dict(E=0),
+        dict(E=4097),
+        dict(E=8, P=3),  # E % P
+        dict(P=0),
+        dict(P=16, E=8),  # P > E
+        dict(T=-1),
+        dict(H=0),
+        dict(x=None),
+        dict(ids=None),
+        dict(packed=None),
+        dict(pos=None),
+        dict(dc=None),
+        dict(x=0x1008),  # misaligned
+        dict(status=0x9002),  # misaligned status word
+        dict(ws=None),
+        dict(wsb=16),  # workspace too small
+        dict(x=0x3000, packed=0x3000),  # x overlaps packed
+    ],
+)
+def test_pack_argument_validation(kw):
+    assert _pack(**kw) == INVALID
+
+
+def _unpack(T=64, H=64, K=2, y=0x100000, pos=0x2000, gates=0x3000, out=0x4000, status=None):
+    return PL.lib().purlin_unpack(T, H, K, y, pos, gates, out, status, None)
+
+
+@pytest.mark.parametrize(
+    "kw",
+    [dict(K=0), dict(K=65), dict(T=-1), dict(H=0), dict(y=None), dict(pos=None), dict(gates=None), dict(out=None),
+     dict(out=0x4004), dict(out=0x100000), dict(status=0x5001)],
+)
+def test_unpack_argument_validation(kw):
+    assert _unpack(**kw) == INVALID
+
+
+def test_python_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(PL, "_lib", None)
+    monkeypatch.setattr(PL, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(PL.PurlinError):
+        PL.lib()

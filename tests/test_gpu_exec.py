@@ -1,0 +1,243 @@
+"""GPU parity of the collective executor (purlin_plan / purlin_exec) with the oracle.
+
+Bit-exact for every op and dtype: copies are bit copies and every reduction
+follows Eq. 2 (rank order, FP32, one rounding back to bf16) on both sides.
+Outputs carry guard bands that must come back untouched.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import Guarded, assert_bits_equal, np_dtype, to_device, to_host, torch_dtype
+from paper_2609_36954_amd import purlin as PL
+from paper_2609_36954_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+S = {"fp32": 4, "bf16": 2}
+
+
+def _inputs(P, n, dtype, seed):
+    rng = np.random.default_rng(seed)
+    if dtype == "fp32":
+        return [(rng.standard_normal(n) * np.exp2(rng.integers(-20, 20, n))).astype(np.float32) for _ in range(P)]
+    return [oracle.narrow(rng.standard_normal(n).astype(np.float32)) for _ in range(P)]
+
+
+def _oracle(op, ins, dtype):
+    if op == "allgather":
+        M = len(ins[0]) // len(ins)
+        return oracle.all_gather([a[:M] for a in ins], dtype)
+    fn = {"allreduce": oracle.all_reduce, "reduce_scatter": oracle.reduce_scatter, "alltoall": oracle.all_to_all}[op]
+    return fn(ins, dtype)
+
+
+def run_plan(plan, ins_np, dtype):
+    """Upload inputs (trimmed to the plan's input size), run, return outputs."""
+    s = S[dtype]
+    ins = [to_device(a[: plan.in_bytes // s]) for a in ins_np]
+    outs = [Guarded(plan.out_bytes, torch_dtype(dtype)) for _ in range(plan.P)]
+    plan.exec(ins, [o.t for o in outs])
+    torch.cuda.synchronize()
+    for o in outs:
+        assert o.intact(), "write outside an output buffer"
+    return [to_host(o.t, np_dtype(dtype)) for o in outs]
+
+
+CASES = []
+for _op in ("allreduce", "reduce_scatter", "allgather", "alltoall"):
+    for _dt in ("fp32", "bf16"):
+        for _P, _M in ((1, 1000), (2, 16), (3, 1001), (4, 4096), (5, 777), (8, 8200), (16, 520)):
+            CASES.append((_op, _dt, _P, _M))
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "-".join(map(str, c)))
+def test_exec_matches_oracle(case):
+    op, dtype, P, M = case
+    s = S[dtype]
+    count = P * M
+    ins = _inputs(P, count, dtype, seed=P * 1000 + M)
+    want = _oracle(op, ins, dtype)
+    policies = [None]
+    if op == "allreduce":
+        policies = [None, dict(ar_mode=1, fanout=1), dict(ar_mode=1, fanout=2)]
+    elif op == "allgather":
+        policies = [None, dict(fanout=1)]
+    for chunk in (s * 64, 4096, 1 << 20):
+        for pol in policies:
+            plan = PL.Plan(op, P, count, dtype, chunk, policy=pol)
+            got = run_plan(plan, ins, dtype)
+            for r in range(P):
+                assert_bits_equal(got[r], want[r], dtype, f"{op} P={P} M={M} chunk={chunk} {pol} rank {r}")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("item_bytes", [16, 48, 1024, 65536])
+def test_result_does_not_depend_on_chunk_or_item(dtype, item_bytes):
+    P, M = 8, 3000
+    ins = _inputs(P, P * M, dtype, seed=7)
+    want = oracle.all_reduce(ins, dtype)
+    s = S[dtype]
+    for chunk in (s, 6 * s, 1000 * s, M * s):
+        for mode in (1, 2):
+            plan = PL.Plan("allreduce", P, P * M, dtype, chunk, policy=dict(item_bytes=item_bytes, ar_mode=mode))
+            got = run_plan(plan, ins, dtype)
+            for r in range(P):
+                assert_bits_equal(got[r], want[r], dtype, f"chunk={chunk} item={item_bytes} mode={mode}")
+
+
+def test_repeated_runs_are_bit_identical():
+    P, M = 8, 1 << 16
+    ins = _inputs(P, P * M, "bf16", seed=3)
+    plan = PL.Plan("allreduce", P, P * M, "bf16", 65536)
+    first = run_plan(plan, ins, "bf16")
+    for _ in range(4):
+        again = run_plan(plan, ins, "bf16")
+        for a, b in zip(first, again):
+            assert np.array_equal(a, b)
+
+
+def test_rank_order_on_device():
+    """[2**24, 1, -2**24] in rank order is 0 on the GPU too (no tree, no reassociation)."""
+    n = 3 * 64
+    ins = [np.full(n, v, np.float32) for v in (2.0**24, 1.0, -(2.0**24))]
+    for mode in (1, 2):
+        plan = PL.Plan("allreduce", 3, n, "fp32", 64, policy=dict(ar_mode=mode))
+        for out in run_plan(plan, ins, "fp32"):
+            assert np.all(out == 0.0)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_special_values(dtype):
+    """Signed zeros, denormals, infinities, NaN and overflow, against the oracle."""
+    P, n = 4, 4 * 64
+    if dtype == "fp32":
+        vals = np.array([-0.0, 2.0**-140, -(2.0**-149), np.inf, -np.inf, 3.0e38, 1.0, -1.0], np.float32)
+    else:
+        vals = np.array([0x8000, 0x0001, 0x8001, 0x7F80, 0xFF80, 0x7F7F, 0x3F80, 0xBF80], np.uint16)
+    rng = np.random.default_rng(5)
+    ins = [vals[rng.integers(0, len(vals), n)] for _ in range(P)]
+    ins[0][:8] = vals  # make sure each value shows up
+    want = oracle.all_reduce(ins, dtype)
+    plan = PL.Plan("allreduce", P, n, dtype, 128)
+    got = run_plan(plan, ins, dtype)
+    f = (lambda a: a) if dtype == "fp32" else oracle.widen
+    for g, w in zip(got, want):
+        nan_g, nan_w = np.isnan(f(g)), np.isnan(f(w))
+        assert np.array_equal(nan_g, nan_w), "NaN positions differ"
+        assert_bits_equal(g[~nan_w], w[~nan_w], dtype, "special values")
+    # all -0 sums to +0
+    zero = [np.full(n, vals[0]) for _ in range(P)]
+    for out in run_plan(plan, zero, dtype):
+        assert np.all((out.view(np.uint32) if dtype == "fp32" else out) == 0)
+
+
+def test_rejects_bad_buffers_before_enqueueing():
+    plan = PL.Plan("allreduce", 2, 1024, "bf16", 256)
+    a = torch.zeros(4096, dtype=torch.int16, device="cuda")
+    L = PL.lib()
+    base = a.data_ptr()
+
+    def call(ptrs):
+        arr = (PL.ctypes.c_void_p * 4)(*ptrs)
+        return L.purlin_exec(plan.handle, arr, None)
+
+    nb = 1024 * 2
+    assert call([base, base + nb, base + 2 * nb, base + 3 * nb]) == 0
+    torch.cuda.synchronize()
+    assert call([base + 2, base + nb, base + 2 * nb, base + 3 * nb]) == PL.PURLIN_ERR_INVALID  # misaligned
+    assert call([base, base + nb, base + nb, base + 3 * nb]) == PL.PURLIN_ERR_INVALID  # input overlaps output
+    assert call([base, base + nb, base + 2 * nb, base + 2 * nb + 16]) == PL.PURLIN_ERR_INVALID  # outputs overlap
+    assert call([base, 0, base + 2 * nb, base + 3 * nb]) == PL.PURLIN_ERR_INVALID  # null
+    assert call([base, base, base + 2 * nb, base + 3 * nb]) == 0  # inputs may alias
+    torch.cuda.synchronize()
+
+
+def test_graph_capture_replays_match_eager():
+    P, M = 8, 1 << 14
+    ins_np = _inputs(P, P * M, "bf16", seed=11)
+    plan = PL.Plan("allreduce", P, P * M, "bf16", 65536)
+    ins = [to_device(a) for a in ins_np]
+    outs = [torch.empty(P * M, dtype=torch.int16, device="cuda") for _ in range(P)]
+    plan.exec(ins, outs)
+    torch.cuda.synchronize()
+    eager = [o.clone() for o in outs]
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        for o in outs:
+            o.zero_()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            plan.exec(ins, outs, stream=side)
+    for _ in range(3):
+        for o in outs:
+            o.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for o, e in zip(outs, eager):
+            assert torch.equal(o, e)
+
+
+# ---------------------------------------------------------------------------
+# full-size configurations
+# ---------------------------------------------------------------------------
+
+
+def test_config1_allreduce_p4_fp32():
+    cfg = W.COLLECTIVE_CONFIGS[1]
+    ins = W.collective_inputs(cfg)
+    want = oracle.all_reduce(ins, cfg.dtype)
+    plan = PL.Plan(cfg.op, cfg.P, cfg.count, cfg.dtype, cfg.chunk)
+    got = run_plan(plan, ins, cfg.dtype)
+    for r in range(cfg.P):
+        assert_bits_equal(got[r], want[r], "fp32", f"config 1 rank {r}")
+
+
+def test_config2_allreduce_p8_bf16():
+    cfg = W.COLLECTIVE_CONFIGS[2]
+    ins = W.collective_inputs(cfg)
+    want = oracle.all_reduce(ins, cfg.dtype)
+    for pol in (None, dict(ar_mode=1)):
+        plan = PL.Plan(cfg.op, cfg.P, cfg.count, cfg.dtype, cfg.chunk, policy=pol)
+        got = run_plan(plan, ins, cfg.dtype)
+        for r in range(cfg.P):
+            assert_bits_equal(got[r], want[r], "bf16", f"config 2 rank {r} {pol}")
+
+
+def test_config3_reduce_scatter_then_all_gather_full_size():
+    """256 MiB per rank, P=8, bf16, chunk 1 MiB, in the launch shapes the bench times.
+
+    RS then AG must equal the AllReduce bit for bit on the whole buffer
+    (compared on the device); sampled elements are checked against the
+    oracle, which is elementwise across ranks.
+    """
+    cfg = W.COLLECTIVE_CONFIGS[3]
+    P, N = cfg.P, cfg.count
+    M = N // P
+    ins_np = W.collective_inputs(cfg)
+    ins = [to_device(a) for a in ins_np]
+    rs = PL.Plan("reduce_scatter", P, N, "bf16", cfg.chunk)
+    ag = PL.Plan("allgather", P, N, "bf16", cfg.chunk)
+    ar = PL.Plan("allreduce", P, N, "bf16", cfg.chunk)
+    rs_out = [torch.empty(M, dtype=torch.int16, device="cuda") for _ in range(P)]
+    ag_out = [torch.empty(N, dtype=torch.int16, device="cuda") for _ in range(P)]
+    rs.exec(ins, rs_out)
+    ag.exec(rs_out, ag_out)
+    torch.cuda.synchronize()
+    ar_out = [torch.empty(N, dtype=torch.int16, device="cuda") for _ in range(P)]
+    ar.exec(ins, ar_out)
+    torch.cuda.synchronize()
+    for r in range(P):
+        assert torch.equal(ag_out[r], ar_out[r]), f"RS then AG differs from AR at rank {r}"
+    del ag_out[1:], ar_out[1:]
+    rng = np.random.default_rng(33)
+    idx = np.sort(rng.choice(N, size=P * 65536, replace=False))
+    want = oracle.all_reduce([a[idx] for a in ins_np], "bf16")[0]
+    got_ar = to_host(ar_out[0], np.uint16)[idx]
+    assert_bits_equal(got_ar, want, "bf16", "config 3 AR sample")
+    rs_host = np.concatenate([to_host(t, np.uint16) for t in rs_out])
+    assert_bits_equal(rs_host[idx], want, "bf16", "config 3 RS sample")

@@ -1,0 +1,183 @@
+"""GPU parity of MoE pack (dispatch) and unpack (combine) with the oracle.
+
+Pack is integer and bit-copy work: counts, offsets, positions and rows must
+match exactly.  Combine follows the slot-order FP32 sum with separately
+rounded multiply and add on both sides: bit-exact as well.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import Guarded, assert_bits_equal, to_device, to_host
+from paper_2609_36954_amd import purlin as PL
+from paper_2609_36954_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _distinct_ids(rng, T, K, E):
+    return np.stack([rng.permutation(E)[:K] for _ in range(T)]).astype(np.int32) if T else np.zeros((0, K), np.int32)
+
+
+def run_pack(x_np, ids_np, E, P, status=True):
+    T, H = x_np.shape
+    K = ids_np.shape[1]
+    x = to_device(x_np)
+    ids = to_device(ids_np)
+    packed = Guarded(T * K * H * 2, torch.int16)
+    pos = Guarded(T * K * 4, torch.int32)
+    st = torch.full((4,), 7, dtype=torch.int32, device="cuda")
+    out = dict(packed=packed.t.view(T * K, H), pos=pos.t.view(T, K))
+    r = PL.purlin_pack(x, ids, E, P, out=out, dev_status=st if status else None)
+    torch.cuda.synchronize()
+    assert packed.intact() and pos.intact()
+    host = {k: to_host(v, np.uint16 if k == "packed" else np.int32) for k, v in r.items()}
+    host["packed"] = host["packed"].reshape(T * K, H)
+    host["pos"] = host["pos"].reshape(T, K)
+    return host, int(st[0].item())
+
+
+def check_pack(x_np, ids_np, E, P):
+    got, status = run_pack(x_np, ids_np, E, P)
+    want = oracle.pack(x_np, ids_np, E, P)
+    assert status == 0
+    for key in ("dest_counts", "dest_offsets", "expert_counts", "expert_offsets", "pos"):
+        assert np.array_equal(got[key], want[key]), key
+    assert np.array_equal(got["packed"], want["packed"])
+
+
+@pytest.mark.parametrize(
+    "T,H,K,E,P,seed",
+    [
+        (1, 8, 1, 1, 1, 0),
+        (5, 16, 2, 4, 2, 1),
+        (63, 24, 4, 16, 4, 2),
+        (64, 128, 8, 256, 8, 3),
+        (65, 7, 3, 9, 3, 4),  # H not a multiple of 8: element path
+        (200, 520, 8, 64, 8, 5),
+        (333, 1000, 6, 120, 4, 6),
+        (130, 64, 64, 64, 8, 7),  # K = 64 (every expert)
+        (97, 16, 2, 4096, 16, 8),  # E = 4096
+        (0, 64, 8, 256, 8, 9),  # no tokens
+    ],
+)
+def test_pack_matches_oracle(T, H, K, E, P, seed):
+    rng = np.random.default_rng(seed)
+    ids = _distinct_ids(rng, T, K, E)
+    x = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
+    check_pack(x, ids, E, P)
+
+
+def test_pack_zipf_routing_skewed():
+    rng = np.random.default_rng(10)
+    T, H, E, P, K = 1000, 256, 256, 8, 8
+    ids = W.zipf_topk_ids(T, E, K, 1.1, seed=10)
+    x = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
+    check_pack(x, ids, E, P)
+
+
+def test_pack_reports_bad_routing():
+    rng = np.random.default_rng(11)
+    T, H, K, E, P = 70, 16, 4, 16, 4
+    x = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
+    ids = _distinct_ids(rng, T, K, E)
+    rep = ids.copy()
+    rep[3, 2] = rep[3, 0]  # repeated id within a token
+    _, status = run_pack(x, rep, E, P)
+    assert status == 1
+    oob = ids.copy()
+    oob[66, 1] = E  # out of range
+    got, status = run_pack(x, oob, E, P)
+    assert status == 1
+    assert got["pos"][66, 1] == -1
+    _, status = run_pack(x, ids, E, P)
+    assert status == 0
+
+
+def run_unpack(y_np, pos_np, g_np, status=True):
+    T, K = pos_np.shape
+    H = y_np.shape[1]
+    out = Guarded(T * H * 2, torch.int16)
+    st = torch.full((4,), 7, dtype=torch.int32, device="cuda")
+    PL.purlin_unpack(to_device(y_np), to_device(pos_np), to_device(g_np), out=out.t.view(T, H),
+                     dev_status=st if status else None)
+    torch.cuda.synchronize()
+    assert out.intact()
+    return to_host(out.t, np.uint16).reshape(T, H), int(st[0].item())
+
+
+@pytest.mark.parametrize(
+    "T,H,K,seed",
+    [(1, 8, 1, 0), (5, 16, 2, 1), (64, 1024, 8, 2), (65, 7, 3, 3), (129, 520, 8, 4), (50, 64, 17, 5), (3, 4096, 64, 6),
+     (0, 64, 8, 7)],
+)
+def test_unpack_matches_oracle(T, H, K, seed):
+    rng = np.random.default_rng(seed)
+    y = oracle.narrow((rng.standard_normal((T * K, H)) * np.exp2(rng.integers(-10, 10, (T * K, H)))).astype(np.float32))
+    pos = rng.permutation(T * K).reshape(T, K).astype(np.int32)
+    g = rng.uniform(0, 1, (T, K)).astype(np.float32)
+    got, status = run_unpack(y, pos, g)
+    assert status == 0
+    assert_bits_equal(got, oracle.unpack(y, pos, g), "bf16", "unpack")
+
+
+def test_unpack_never_fuses_and_keeps_slot_order():
+    g0 = np.float32(-(1 + 2.0**-7 + 2.0**-23))
+    g1 = np.float32(1 + 2.0**-23)
+    v0 = oracle.narrow(np.array([1.0], np.float32))[0]
+    v1 = oracle.narrow(np.array([1 + 2.0**-7], np.float32))[0]
+    H = 64
+    y = np.array([[v0] * H, [v1] * H], np.uint16)
+    got, _ = run_unpack(y, np.array([[0, 1]], np.int32), np.array([[g0, g1]], np.float32))
+    assert np.all(got == 0)  # a fused multiply-add would give 0x3080
+    vals = oracle.narrow(np.array([2.0**24, 1.0, -(2.0**24)], np.float32))
+    y = np.repeat(vals[:, None], H, axis=1)
+    got, _ = run_unpack(y, np.array([[0, 1, 2]], np.int32), np.ones((1, 3), np.float32))
+    assert np.all(got == 0)  # slot order 0, 1, 2
+
+
+def test_unpack_reports_bad_positions():
+    rng = np.random.default_rng(12)
+    T, H, K = 9, 32, 2
+    y = rng.integers(0, 0x4000, (T * K, H)).astype(np.uint16)
+    pos = rng.permutation(T * K).reshape(T, K).astype(np.int32)
+    g = np.ones((T, K), np.float32)
+    bad = pos.copy()
+    bad[4, 1] = T * K
+    got, status = run_unpack(y, bad, g)
+    assert status == 1
+    _, status = run_unpack(y, pos, g)
+    assert status == 0
+
+
+def test_pack_then_unpack_round_trip():
+    cfg = W.MOE_CONFIG
+    T, H = 512, 256
+    ids = W.zipf_topk_ids(T, cfg.E, cfg.K, cfg.zipf_s, seed=21)
+    rng = np.random.default_rng(21)
+    x = oracle.narrow(rng.standard_normal((T, H)).astype(np.float32))
+    r = PL.purlin_pack(to_device(x), to_device(ids), cfg.E, cfg.P)
+    out = PL.purlin_unpack(r["packed"], r["pos"], torch.full((T, cfg.K), 1.0 / cfg.K, device="cuda"))
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(out, np.uint16).reshape(T, H), x)
+
+
+def test_config4_pack_and_config5_combine_full_size():
+    """4096 tokens x 7168 hidden, E=256 over P=8, top-8 Zipf(1.1); then combine."""
+    cfg = W.MOE_CONFIG
+    ids = W.zipf_topk_ids(cfg.T, cfg.E, cfg.K, cfg.zipf_s, cfg.seed_ids)
+    x = W.moe_tokens(cfg)
+    got, status = run_pack(x, ids, cfg.E, cfg.P)
+    want = oracle.pack(x, ids, cfg.E, cfg.P)
+    assert status == 0
+    for key in ("dest_counts", "dest_offsets", "expert_counts", "expert_offsets", "pos"):
+        assert np.array_equal(got[key], want[key]), key
+    assert np.array_equal(got["packed"], want["packed"])
+    del got
+    y = W.moe_expert_outputs(cfg)
+    g = W.softmax_gates(cfg.T, cfg.K, cfg.seed_gates)
+    out, status = run_unpack(y, want["pos"], g)
+    assert status == 0
+    assert_bits_equal(out, oracle.unpack(y, want["pos"], g), "bf16", "config 5 combine")

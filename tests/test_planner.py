@@ -1,0 +1,244 @@
+"""Host planner checks (CPU only: host-only plans, no device upload).
+
+* descriptor counts of the paper-shaped configurations;
+* the address rule of Listing 2 (Section 3.2): packed output at
+  dst + offset, scattered / transposed output at dst + peer*partBytes + offset;
+* every output byte written exactly once per phase, sources in bounds,
+  AllReduce's second phase reading only what its first phase wrote;
+* work items tile their descriptors exactly;
+* the CPU interpreter running the table in shuffled order reproduces the
+  oracle bit for bit, for every op, dtype, policy and ragged shape.
+"""
+
+import numpy as np
+import pytest
+
+import interp
+import oracle
+from paper_2609_36954_amd import purlin as PL
+
+S = {"fp32": 4, "bf16": 2}
+
+
+def host_plan(op, P, count, dtype, chunk, **policy):
+    return PL.Plan(op, P, count, dtype, chunk, policy=policy or None, host_only=True)
+
+
+# ---------------------------------------------------------------------------
+# descriptor counts of the configurations
+# ---------------------------------------------------------------------------
+
+COUNT_CASES = [
+    # (op, P, count, dtype, chunk, policy, reduce descs, copy descs)
+    ("allreduce", 4, 262144, "fp32", 16 * 1024, dict(ar_mode=1, fanout=1), 64, 192),
+    ("allreduce", 8, 128 * 8192, "bf16", 64 * 1024, dict(ar_mode=1, fanout=1), 32, 224),
+    ("reduce_scatter", 8, 134217728, "bf16", 1 << 20, {}, 256, 0),
+    ("allgather", 8, 134217728, "bf16", 1 << 20, dict(fanout=1), 0, 2048),
+    ("allgather", 8, 134217728, "bf16", 1 << 20, dict(fanout=2), 0, 256),
+    ("allreduce", 8, 134217728, "bf16", 1 << 20, dict(ar_mode=1, fanout=1), 256, 1792),
+    ("allreduce", 8, 134217728, "bf16", 1 << 20, dict(ar_mode=2), 256, 0),
+    ("alltoall", 8, 134217728, "bf16", 1 << 20, {}, 0, 2048),
+]
+
+
+@pytest.mark.parametrize("case", COUNT_CASES, ids=lambda c: f"{c[0]}-P{c[1]}-{c[3]}-{c[5]}")
+def test_descriptor_counts(case):
+    op, P, count, dtype, chunk, pol, n_red, n_copy = case
+    d = host_plan(op, P, count, dtype, chunk, **pol).descriptors()
+    assert int((d["kind"] == PL.KIND_REDUCE).sum()) == n_red
+    assert int((d["kind"] == PL.KIND_COPY).sum()) == n_copy
+
+
+@pytest.mark.parametrize(
+    "op,P,count,dtype,pol,want",
+    [
+        # AllReduce in two phases moves (3P-1)*N*s bytes; in one phase 2P*N*s
+        ("allreduce", 4, 262144, "fp32", dict(ar_mode=1, fanout=1), (3 * 4 - 1) * 262144 * 4),
+        ("allreduce", 8, 1 << 20, "bf16", dict(ar_mode=1, fanout=1), (3 * 8 - 1) * (1 << 20) * 2),
+        # two phases with multi-destination copies: phase 1 reads each reduced
+        # chunk once per destination run (two runs, r < k and r > k, except
+        # at the ends): (P+1)*N*s + (P-1)*N*s + (2P-2)/P*N*s
+        ("allreduce", 8, 1 << 20, "bf16", dict(ar_mode=1, fanout=2), (9 + 7) * (1 << 21) + 14 * (1 << 21) // 8),
+        ("allreduce", 8, 1 << 20, "bf16", dict(ar_mode=2), 2 * 8 * (1 << 20) * 2),
+        # ReduceScatter (P+1)*N*s; AllGather with one read per source chunk (P+1)*N*s
+        ("reduce_scatter", 8, 1 << 20, "bf16", {}, 9 * (1 << 20) * 2),
+        ("allgather", 8, 1 << 20, "bf16", dict(fanout=2), 9 * (1 << 20) * 2),
+        ("allgather", 8, 1 << 20, "bf16", dict(fanout=1), 16 * (1 << 20) * 2),
+        ("alltoall", 8, 1 << 20, "bf16", {}, 2 * 8 * (1 << 20) * 2),
+    ],
+)
+def test_scheduled_bytes(op, P, count, dtype, pol, want):
+    assert host_plan(op, P, count, dtype, 65536, **pol).sched_bytes == want
+
+
+# ---------------------------------------------------------------------------
+# structure of the table
+# ---------------------------------------------------------------------------
+
+STRUCT_CASES = [
+    ("reduce_scatter", 3, 3 * 1000, "bf16", 256, {}),
+    ("reduce_scatter", 8, 8 * 4096, "fp32", 4096, {}),
+    ("allgather", 5, 5 * 999, "bf16", 100, dict(fanout=1)),
+    ("allgather", 5, 5 * 999, "bf16", 100, dict(fanout=2)),
+    ("alltoall", 4, 4 * 777, "fp32", 64, {}),
+    ("allreduce", 4, 4 * 1000, "fp32", 160, dict(ar_mode=1, fanout=1)),
+    ("allreduce", 6, 6 * 1000, "bf16", 160, dict(ar_mode=1, fanout=2)),
+    ("allreduce", 7, 7 * 500, "bf16", 96, dict(ar_mode=2)),
+    ("allreduce", 1, 100, "bf16", 32, dict(ar_mode=1)),
+    ("allreduce", 16, 16 * 64, "bf16", 2, dict(ar_mode=1, fanout=2)),
+]
+
+
+def _intervals_cover_once(ivals, total):
+    ivals = sorted(ivals)
+    pos = 0
+    for lo, hi in ivals:
+        if lo != pos:
+            return False
+        pos = hi
+    return pos == total
+
+
+@pytest.mark.parametrize("case", STRUCT_CASES, ids=lambda c: f"{c[0]}-P{c[1]}-{c[3]}-{c[5]}")
+def test_table_structure(case):
+    op, P, count, dtype, chunk, pol = case
+    plan = host_plan(op, P, count, dtype, chunk, **pol)
+    s = S[dtype]
+    M = count // P
+    part = M * s
+    d = plan.descriptors()
+    assert plan.n_desc == len(d)
+    assert plan.sched_bytes == int(sum((int(x["nsrc"]) + int(x["ndst"])) * int(x["bytes"]) for x in d))
+
+    writes = {}  # (phase, buffer) -> list of intervals
+    for x in d:
+        ph, n = int(x["phase"]), int(x["bytes"])
+        assert n > 0 and n % s == 0
+        assert n <= chunk
+        c, k = int(x["chunk"]), int(x["part"])
+        off = c * chunk  # offset of the chunk inside its partition
+        # Listing 2 address rule
+        for j in range(int(x["ndst"])):
+            b = int(x["dst_buf"]) + j * int(x["dst_step"])
+            assert P <= b < 2 * P
+            r = b - P
+            if op == "reduce_scatter":  # packed output
+                assert int(x["dst_off"]) == off and k == r
+            elif op == "allgather":  # scattered output, peer = k
+                assert int(x["dst_off"]) == k * part + off
+            elif op == "alltoall":  # transposed output, peer = source rank
+                p = int(x["src_buf"])
+                assert int(x["dst_off"]) == p * part + off and k == r
+            else:  # allreduce: scattered output, partition k
+                assert int(x["dst_off"]) == k * part + off
+            writes.setdefault((ph, b), []).append((int(x["dst_off"]), int(x["dst_off"]) + n))
+        # sources
+        for p in range(int(x["nsrc"])):
+            b = int(x["src_buf"]) + p * int(x["src_step"])
+            lim = plan.in_bytes if b < P else plan.out_bytes
+            assert int(x["src_off"]) + n <= lim
+            if ph == 0:
+                assert b < P, "phase 0 reads inputs only"
+        if int(x["kind"]) == PL.KIND_REDUCE:
+            assert int(x["nsrc"]) == P and int(x["src_buf"]) == 0 and int(x["src_step"]) == 1
+        else:
+            assert int(x["nsrc"]) == 1
+
+    # exactly-once coverage
+    if op == "allreduce" and plan.descriptors()["phase"].max() == 1:
+        for r in range(P):
+            w0 = writes.get((0, P + r), [])
+            assert _intervals_cover_once(w0 and [(a - r * part, b - r * part) for a, b in w0], part)
+            w1 = writes.get((1, P + r), [])
+            full = sorted(w0 + w1)
+            assert _intervals_cover_once(full, plan.out_bytes)
+        # phase 1 reads out_k's partition k only (written in phase 0)
+        for x in d[d["phase"] == 1]:
+            k = int(x["src_buf"]) - P
+            assert k * part <= int(x["src_off"]) and int(x["src_off"]) + int(x["bytes"]) <= (k + 1) * part
+    else:
+        for r in range(P):
+            assert _intervals_cover_once(writes.get((0, P + r), []), plan.out_bytes)
+
+
+@pytest.mark.parametrize("case", STRUCT_CASES, ids=lambda c: f"{c[0]}-P{c[1]}-{c[3]}-{c[5]}")
+@pytest.mark.parametrize("item_bytes", [0, 16, 48, 1024])
+def test_items_tile_descriptors(case, item_bytes):
+    op, P, count, dtype, chunk, pol = case
+    plan = host_plan(op, P, count, dtype, chunk, item_bytes=item_bytes, **pol)
+    d = plan.descriptors()
+    items, pb = plan.items()
+    assert pb[0] == 0 and pb[2] == len(items) and pb[0] <= pb[1] <= pb[2]
+    assert np.all(items["phase"][: pb[1]] == 0) and np.all(items["phase"][pb[1]:] == 1)
+    if item_bytes:
+        assert int(items["bytes"].max()) <= item_bytes
+    # walk items in order; they must cut each descriptor into consecutive pieces
+    i = 0
+    for x in d:
+        covered = 0
+        while covered < int(x["bytes"]):
+            it = items[i]
+            for f in ("kind", "phase", "nsrc", "src_buf", "src_step", "ndst", "dst_buf", "dst_step", "part", "chunk"):
+                assert it[f] == x[f]
+            assert int(it["src_off"]) == int(x["src_off"]) + covered
+            assert int(it["dst_off"]) == int(x["dst_off"]) + covered
+            covered += int(it["bytes"])
+            i += 1
+        assert covered == int(x["bytes"])
+    assert i == len(items)
+    # a phase holds one consume op (one kernel per phase)
+    for lo, hi in ((pb[0], pb[1]), (pb[1], pb[2])):
+        assert len(set(items["kind"][lo:hi].tolist())) <= 1
+
+
+# ---------------------------------------------------------------------------
+# the table, run on the CPU in shuffled order, equals the oracle
+# ---------------------------------------------------------------------------
+
+
+def _inputs(P, n, dtype, seed):
+    rng = np.random.default_rng(seed)
+    if dtype == "fp32":
+        return [(rng.standard_normal(n) * np.exp2(rng.integers(-20, 20, n))).astype(np.float32) for _ in range(P)]
+    return [oracle.narrow(rng.standard_normal(n).astype(np.float32)) for _ in range(P)]
+
+
+def _oracle(op, ins, dtype):
+    if op == "allgather":
+        M = len(ins[0]) // len(ins)
+        return oracle.all_gather([a[:M] for a in ins], dtype)
+    return {"allreduce": oracle.all_reduce, "reduce_scatter": oracle.reduce_scatter, "alltoall": oracle.all_to_all}[op](
+        ins, dtype
+    )
+
+
+INTERP_CASES = []
+for _op in ("allreduce", "reduce_scatter", "allgather", "alltoall"):
+    for _dt in ("fp32", "bf16"):
+        for _P, _M in ((1, 37), (2, 16), (3, 100), (4, 256), (8, 257), (16, 9)):
+            for _chunk_elems in (1, 7, 64, 1000):
+                INTERP_CASES.append((_op, _dt, _P, _M, _chunk_elems))
+
+
+@pytest.mark.parametrize("case", INTERP_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_interpreter_matches_oracle(case):
+    op, dtype, P, M, chunk_elems = case
+    s = S[dtype]
+    count = P * M
+    ins = _inputs(P, count, dtype, seed=hash(case) % 1000)
+    want = _oracle(op, ins, dtype)
+    policies = [{}]
+    if op == "allreduce":
+        policies = [dict(ar_mode=1, fanout=1), dict(ar_mode=1, fanout=2), dict(ar_mode=2, item_bytes=32)]
+    elif op == "allgather":
+        policies = [dict(fanout=1, item_bytes=48), dict(fanout=2)]
+    for pol in policies:
+        plan = host_plan(op, P, count, dtype, chunk_elems * s, **pol)
+        items, pb = plan.items()
+        in_bytes = [np.frombuffer(a.tobytes()[: plan.in_bytes], dtype=np.uint8).copy() for a in ins]
+        outs = [np.full(plan.out_bytes, 0xA5, dtype=np.uint8) for _ in range(P)]
+        interp.run(items, pb, in_bytes + outs, dtype, seed=len(items))
+        for r in range(P):
+            got = outs[r].view(np.uint16 if dtype == "bf16" else np.uint32)
+            exp = want[r].view(np.uint16 if dtype == "bf16" else np.uint32)
+            assert np.array_equal(got, exp), (pol, r)
