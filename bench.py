@@ -41,6 +41,14 @@ if ROOT not in sys.path:
 METRIC = "datapath GB/s (read+write) and % of HBM peak; small-message latency µs"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 KERNEL_SOURCES = ["paper_2609_36954_amd/csrc/exec.hip", "paper_2609_36954_amd/csrc/moe.hip"]
+# kernel (as rocprofv3 names it, a distinctive substring) of each single-launch op
+KERNEL_OF_OP = {
+    "reduce_scatter": "exec_reduce<8, true",
+    "allgather": "exec_copy<",
+    "moe_combine": "unpack_rows<",
+}
+CALIBRATION_KERNEL = "copy"  # torch's device-to-device copy of --calibrate-copy
+CALIBRATION_BYTES = 1 << 30
 
 
 def log(*a):
@@ -79,6 +87,67 @@ def to_dev(torch, a):
     return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to("cuda")
 
 
+def _counter_means(d, counter):
+    """Mean and largest Counter_Value per kernel name over the dispatches in
+    a rocprofv3 --pmc CSV directory (…_counter_collection.csv)."""
+    import csv
+    import glob
+
+    sums = {}
+    for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for row in csv.DictReader(f):
+                if row.get("Counter_Name") != counter:
+                    continue
+                k = row["Kernel_Name"]
+                v = sums.setdefault(k, [0.0, 0, 0.0])
+                x = float(row["Counter_Value"])
+                v[0] += x
+                v[1] += 1
+                v[2] = max(v[2], x)
+    return {k: v[0] / v[1] for k, v in sums.items()}, {k: v[2] for k, v in sums.items()}
+
+
+def ingest_counters(fetch_dir, write_dir):
+    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) -> HBM bytes per launch.
+
+    Each counter is scaled by what it reads for a plain 1 GiB device copy
+    (reads 1 GiB, writes 1 GiB), run in the same process."""
+    fetch, fetch_max = _counter_means(fetch_dir, "FETCH_SIZE")
+    write, write_max = _counter_means(write_dir, "WRITE_SIZE")
+
+    def pick(table, sub, exclude=None):
+        names = [k for k in table if sub in k and (exclude is None or exclude not in k)]
+        if not names:
+            raise SystemExit(f"no kernel matching {sub!r} in the counter CSVs")
+        return max(names, key=lambda k: table[k])
+
+    # the calibration copy is the largest dispatch of the copy kernel in the run
+    cal_f = pick(fetch_max, CALIBRATION_KERNEL, exclude="purlin")
+    cal_w = pick(write_max, CALIBRATION_KERNEL, exclude="purlin")
+    f_scale = CALIBRATION_BYTES / (fetch_max[cal_f] * 1024.0)
+    w_scale = CALIBRATION_BYTES / (write_max[cal_w] * 1024.0)
+    out = {
+        "kernel_source_hash": kernel_source_hash(),
+        "calibration": {"kernel": cal_f, "bytes_read": CALIBRATION_BYTES, "bytes_written": CALIBRATION_BYTES,
+                        "fetch_KiB": fetch_max[cal_f], "write_KiB": write_max[cal_w],
+                        "fetch_scale": f_scale, "write_scale": w_scale},
+        "ops": {},
+    }
+    for op, sub in KERNEL_OF_OP.items():
+        kf, kw = pick(fetch, sub), pick(write, sub)
+        fb, wb = fetch[kf] * 1024.0 * f_scale, write[kw] * 1024.0 * w_scale
+        out["ops"][op] = {"kernel": kf, "fetch_KiB": fetch[kf], "write_KiB": write[kw],
+                          "hbm_read_bytes": round(fb), "hbm_write_bytes": round(wb),
+                          "hbm_bytes_per_launch": round(fb + wb)}
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+    return 0
+
+
 def load_traffic(src_hash):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they
     were taken on the current kernel sources; else None."""
@@ -99,7 +168,14 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--latency-sweep", action="store_true", help="also time AllReduce P=8 bf16 at 1 KiB..512 KiB per rank")
+    ap.add_argument("--no-latency", action="store_true", help="skip the graph-replayed latency measurement")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run one 1 GiB device-to-device tensor copy first (reference for HBM counter scaling)")
+    ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) into profiles/traffic.json")
     args = ap.parse_args()
+    if args.ingest_counters:
+        return ingest_counters(*args.ingest_counters)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(json.dumps({"error": "this build runs on one GPU: the P ranks are P buffers on that GPU; "
                           "--gpus above 1 is not supported"}))
@@ -129,6 +205,13 @@ def main():
     y_np = W.moe_expert_outputs(moe)
     g_np = W.softmax_gates(T, K, moe.seed_gates)
     log(f"bench: inputs ready in {time.time() - t0:.1f}s; uploading")
+
+    if args.calibrate_copy:
+        a = torch.empty(1 << 29, dtype=torch.int16, device="cuda").fill_(1)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
 
     ins = [to_dev(torch, a) for a in ins_np]
     rs_out = [torch.empty(M, dtype=torch.int16, device="cuda") for _ in range(P)]
@@ -207,7 +290,6 @@ def main():
     # dominant single-kernel op (RS, AG and combine are one launch each)
     single = ["reduce_scatter", "allgather", "moe_combine"]
     dom = max(single, key=lambda n: per_op[n]["avg_us"])
-    kernel_of = {"reduce_scatter": "exec_reduce<8, bf16>", "allgather": "exec_copy", "moe_combine": "unpack_rows"}
     achieved = per_op[dom]["bytes_min"] / (per_op[dom]["avg_us"] * 1e-6) / 1e9
     traffic = None
     tr = load_traffic(src_hash)
@@ -215,7 +297,7 @@ def main():
         traffic = tr["ops"][dom].get("hbm_bytes_per_launch")
     roofline = {
         "bound": "hbm",
-        "kernel": kernel_of[dom],
+        "kernel": KERNEL_OF_OP[dom],
         "op": dom,
         "achieved": round(achieved, 1),
         "peak": HBM_PEAK_GBS,
@@ -245,6 +327,19 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / (calls * reps)
 
+    latency = None
+    if not args.no_latency:
+        latency = measure_latency(torch, PL, W, graph_latency_us, args.latency_sweep)
+
+    # ---------------- CPU baseline: the oracle on a bounded sample ----------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_out, comb_out, P, N, M, E, K)
+    return emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, per_op, latency, plan_ms,
+                dev_name, src_hash)
+
+
+def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
     c2 = W.COLLECTIVE_CONFIGS[2]
     lat_in = [to_dev(torch, a) for a in W.collective_inputs(c2)]
     lat_out = [torch.empty(c2.count, dtype=torch.int16, device="cuda") for _ in range(c2.P)]
@@ -257,7 +352,7 @@ def main():
             "algbw_GBps": round(c2.count * 2 / (lat_us * 1e-6) / 1e9, 1),
         }
     }
-    if args.latency_sweep:
+    if sweep_sizes:
         sweep = {}
         for kib in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512):
             n = kib * 1024 // 2
@@ -267,12 +362,11 @@ def main():
             sweep[f"{kib}KiB"] = round(graph_latency_us(pl, li, lo), 2)
         latency["allreduce_p8_bf16_sweep_us"] = sweep
     del lat_in, lat_out
+    return latency
 
-    # ---------------- CPU baseline: the oracle on a bounded sample ----------------
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_out, comb_out, P, N, M, E, K)
 
+def emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, per_op, latency, plan_ms, dev_name,
+         src_hash):
     result = {
         "metric": METRIC,
         "value": round(value, 1),

@@ -117,7 +117,9 @@ typedef struct purlin_policy {
                             every other rank: the in-place compose of
                             Section 3.1), 2 = one phase (each chunk reduced
                             once and written to all P outputs)               */
-    uint32_t reserved[4];/* must be zero */
+    uint32_t load_hint;  /* global loads:  0 auto, 1 cached, 2 non-temporal */
+    uint32_t store_hint; /* global stores: 0 auto, 1 cached, 2 non-temporal */
+    uint32_t reserved[2];/* must be zero */
 } purlin_policy;
 
 #define PURLIN_PLAN_HOST_ONLY 1u /* build the tables on the host only (no device
@@ -151,8 +153,9 @@ PURLIN_API purlin_status purlin_plan(purlin_op op, int P, uint64_t count, purlin
 
 /* purlin_plan with an explicit policy (NULL = automatic) and flags
  * (0 or PURLIN_PLAN_HOST_ONLY).  PURLIN_ERR_INVALID also for a policy with
- * item_bytes not a multiple of 16, fanout > 2, ar_mode > 2 or nonzero
- * reserved fields, and for unknown flags. */
+ * item_bytes not a multiple of 16, fanout > 2, ar_mode > 2, a hint > 2 or
+ * nonzero reserved fields, and for unknown flags.  Hints change only how
+ * the caches treat the streams, never the result. */
 PURLIN_API purlin_status purlin_plan_ex(purlin_op op, int P, uint64_t count, purlin_dtype dtype,
                              uint64_t chunk_bytes, const purlin_policy* policy, uint32_t flags,
                              purlin_plan_t* out_plan);

@@ -60,7 +60,7 @@ purlin_status make_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype,
 
 bool pack_limits_ok(int T, int H, int K, int E) {
     if (T < 0 || H < 1 || K < 1 || K > 64 || E < 1 || E > 4096) return false;
-    return static_cast<int64_t>(T) * K < (int64_t(1) << 31);
+    return static_cast<int64_t>(T) * K < (int64_t(1) << 31) && purlin::moe_launch_fits(T, H);
 }
 
 }  // namespace
@@ -130,7 +130,7 @@ purlin_status purlin_exec(purlin_plan_t plan, void* const* bufs, void* stream) {
     for (int i = 0; i < p.nphases; ++i) {
         const purlin::Phase& ph = p.phases[i];
         const hipError_t e = purlin::launch_phase(p.d_items + ph.begin, ph.count, ph.kind, ph.nsrc, ph.src_buf,
-                                                  ph.src_step, p.dtype, bufs, 2 * P, s);
+                                                  ph.src_step, ph.nt_load, ph.nt_store, p.dtype, bufs, 2 * P, s);
         if (e != hipSuccess) return PURLIN_ERR_DEVICE;
     }
     return PURLIN_OK;
@@ -178,7 +178,7 @@ purlin_status purlin_pack(int T, int H, int K, int E, int P, const void* x, cons
 purlin_status purlin_unpack(int T, int H, int K, const void* y, const int32_t* pos, const float* gates, void* out,
                             int32_t* dev_status, void* stream) {
     if (T < 0 || H < 1 || K < 1 || K > 64) return PURLIN_ERR_INVALID;
-    if (static_cast<int64_t>(T) * K >= (int64_t(1) << 31)) return PURLIN_ERR_INVALID;
+    if (static_cast<int64_t>(T) * K >= (int64_t(1) << 31) || !purlin::moe_launch_fits(T, H)) return PURLIN_ERR_INVALID;
     if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
     if (T > 0) {
         if (!y || !pos || !gates || !out) return PURLIN_ERR_INVALID;

@@ -46,9 +46,23 @@ __device__ __forceinline__ uint32_t wave_index() {
 
 __device__ __forceinline__ uint32_t lane_index() { return threadIdx.x & (kWave - 1); }
 
-__device__ __forceinline__ u32x4 load16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
+// 16-byte global access; NT selects the non-temporal (streaming) form,
+// which tells the caches the line will not be reused.
+template <bool NT>
+__device__ __forceinline__ u32x4 load16(const char* p) {
+    if constexpr (NT)
+        return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    else
+        return *reinterpret_cast<const u32x4*>(p);
+}
 
-__device__ __forceinline__ void store16(char* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+template <bool NT>
+__device__ __forceinline__ void store16(char* p, u32x4 v) {
+    if constexpr (NT)
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+    else
+        *reinterpret_cast<u32x4*>(p) = v;
+}
 
 // bf16 element 2m of a 32-bit word sits in its low half (little endian).
 __device__ __forceinline__ float bf16_low(uint32_t w) { return __uint_as_float(w << 16); }
@@ -81,7 +95,7 @@ __device__ __forceinline__ void copy_bytes2(const ExecArgs& a, const purlin_desc
     }
 }
 
-template <int U>
+template <int U, bool NTL, bool NTS>
 __global__ __launch_bounds__(kBlock) void exec_copy(ExecArgs a) {
     const uint32_t w = wave_index();
     if (w >= a.n_items) return;
@@ -97,16 +111,16 @@ __global__ __launch_bounds__(kBlock) void exec_copy(ExecArgs a) {
     for (; base + U * kWave <= nvec; base += U * kWave) {
         u32x4 v[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = load16(src + (base + u * kWave + lane) * 16);
+        for (int u = 0; u < U; ++u) v[u] = load16<NTL>(src + (base + u * kWave + lane) * 16);
         for (uint32_t j = 0; j < d.ndst; ++j) {
             char* dst = dst_ptr(a, d, j);
 #pragma unroll
-            for (int u = 0; u < U; ++u) store16(dst + (base + u * kWave + lane) * 16, v[u]);
+            for (int u = 0; u < U; ++u) store16<NTS>(dst + (base + u * kWave + lane) * 16, v[u]);
         }
     }
     for (uint64_t i = base + lane; i < nvec; i += kWave) {
-        const u32x4 v = load16(src + i * 16);
-        for (uint32_t j = 0; j < d.ndst; ++j) store16(dst_ptr(a, d, j) + i * 16, v);
+        const u32x4 v = load16<NTL>(src + i * 16);
+        for (uint32_t j = 0; j < d.ndst; ++j) store16<NTS>(dst_ptr(a, d, j) + i * 16, v);
     }
     copy_bytes2(a, d, src, nvec * 16, d.bytes, lane);
 }
@@ -167,7 +181,7 @@ __device__ __forceinline__ void reduce_elems(const ExecArgs& a, const purlin_des
     }
 }
 
-template <int NSRC, bool BF16, int U>
+template <int NSRC, bool BF16, int U, bool NTL, bool NTS>
 __global__ __launch_bounds__(kBlock) void exec_reduce(ExecArgs a) {
     const uint32_t w = wave_index();
     if (w >= a.n_items) return;
@@ -187,22 +201,22 @@ __global__ __launch_bounds__(kBlock) void exec_reduce(ExecArgs a) {
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
-            for (int p = 0; p < NSRC; ++p) v[u][p] = load16(src[p] + (base + u * kWave + lane) * 16);
+            for (int p = 0; p < NSRC; ++p) v[u][p] = load16<NTL>(src[p] + (base + u * kWave + lane) * 16);
         u32x4 o[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) o[u] = rank_order_sum<NSRC, BF16>(v[u]);
         for (uint32_t j = 0; j < d.ndst; ++j) {
             char* dst = dst_ptr(a, d, j);
 #pragma unroll
-            for (int u = 0; u < U; ++u) store16(dst + (base + u * kWave + lane) * 16, o[u]);
+            for (int u = 0; u < U; ++u) store16<NTS>(dst + (base + u * kWave + lane) * 16, o[u]);
         }
     }
     for (uint64_t i = base + lane; i < nvec; i += kWave) {
         u32x4 v[NSRC];
 #pragma unroll
-        for (int p = 0; p < NSRC; ++p) v[p] = load16(src[p] + i * 16);
+        for (int p = 0; p < NSRC; ++p) v[p] = load16<NTL>(src[p] + i * 16);
         const u32x4 o = rank_order_sum<NSRC, BF16>(v);
-        for (uint32_t j = 0; j < d.ndst; ++j) store16(dst_ptr(a, d, j) + i * 16, o);
+        for (uint32_t j = 0; j < d.ndst; ++j) store16<NTS>(dst_ptr(a, d, j) + i * 16, o);
     }
     reduce_elems<NSRC, BF16>(a, d, src, nvec * 16, d.bytes, lane);
 }
@@ -211,18 +225,44 @@ __global__ __launch_bounds__(kBlock) void exec_reduce(ExecArgs a) {
 constexpr int kCopyUnroll = 4;
 constexpr int reduce_unroll(int nsrc) { return nsrc >= 16 ? 1 : (nsrc >= 8 ? 2 : (nsrc >= 4 ? 4 : 8)); }
 
-template <int NSRC>
-void launch_reduce(dim3 grid, hipStream_t stream, const ExecArgs& a, bool bf16) {
-    if (bf16)
-        hipLaunchKernelGGL((exec_reduce<NSRC, true, reduce_unroll(NSRC)>), grid, dim3(kBlock), 0, stream, a);
+template <int NSRC, bool BF16>
+void launch_reduce_hints(dim3 grid, hipStream_t stream, const ExecArgs& a, bool ntl, bool nts) {
+    constexpr int U = reduce_unroll(NSRC);
+    if (ntl && nts)
+        hipLaunchKernelGGL((exec_reduce<NSRC, BF16, U, true, true>), grid, dim3(kBlock), 0, stream, a);
+    else if (ntl)
+        hipLaunchKernelGGL((exec_reduce<NSRC, BF16, U, true, false>), grid, dim3(kBlock), 0, stream, a);
+    else if (nts)
+        hipLaunchKernelGGL((exec_reduce<NSRC, BF16, U, false, true>), grid, dim3(kBlock), 0, stream, a);
     else
-        hipLaunchKernelGGL((exec_reduce<NSRC, false, reduce_unroll(NSRC)>), grid, dim3(kBlock), 0, stream, a);
+        hipLaunchKernelGGL((exec_reduce<NSRC, BF16, U, false, false>), grid, dim3(kBlock), 0, stream, a);
+}
+
+template <int NSRC>
+void launch_reduce(dim3 grid, hipStream_t stream, const ExecArgs& a, bool bf16, bool ntl, bool nts) {
+    if (bf16)
+        launch_reduce_hints<NSRC, true>(grid, stream, a, ntl, nts);
+    else
+        launch_reduce_hints<NSRC, false>(grid, stream, a, ntl, nts);
+}
+
+void launch_copy(dim3 grid, hipStream_t stream, const ExecArgs& a, bool ntl, bool nts) {
+    constexpr int U = kCopyUnroll;
+    if (ntl && nts)
+        hipLaunchKernelGGL((exec_copy<U, true, true>), grid, dim3(kBlock), 0, stream, a);
+    else if (ntl)
+        hipLaunchKernelGGL((exec_copy<U, true, false>), grid, dim3(kBlock), 0, stream, a);
+    else if (nts)
+        hipLaunchKernelGGL((exec_copy<U, false, true>), grid, dim3(kBlock), 0, stream, a);
+    else
+        hipLaunchKernelGGL((exec_copy<U, false, false>), grid, dim3(kBlock), 0, stream, a);
 }
 
 }  // namespace
 
 hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
-                        uint32_t src_step, purlin_dtype dtype, void* const* bufs, int nbufs, hipStream_t stream) {
+                        uint32_t src_step, bool nt_load, bool nt_store, purlin_dtype dtype, void* const* bufs,
+                        int nbufs, hipStream_t stream) {
     if (n == 0) return hipSuccess;
     ExecArgs a{};
     a.items = items;
@@ -238,26 +278,17 @@ hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uin
     const dim3 grid(static_cast<uint32_t>((n + kWavesPerBlock - 1) / kWavesPerBlock));
     (void)hipGetLastError();
     if (kind == PURLIN_KIND_COPY) {
-        hipLaunchKernelGGL(exec_copy<kCopyUnroll>, grid, dim3(kBlock), 0, stream, a);
+        launch_copy(grid, stream, a, nt_load, nt_store);
     } else {
         const bool bf16 = dtype == PURLIN_BF16;
         switch (nsrc) {
-            case 1: launch_reduce<1>(grid, stream, a, bf16); break;
-            case 2: launch_reduce<2>(grid, stream, a, bf16); break;
-            case 3: launch_reduce<3>(grid, stream, a, bf16); break;
-            case 4: launch_reduce<4>(grid, stream, a, bf16); break;
-            case 5: launch_reduce<5>(grid, stream, a, bf16); break;
-            case 6: launch_reduce<6>(grid, stream, a, bf16); break;
-            case 7: launch_reduce<7>(grid, stream, a, bf16); break;
-            case 8: launch_reduce<8>(grid, stream, a, bf16); break;
-            case 9: launch_reduce<9>(grid, stream, a, bf16); break;
-            case 10: launch_reduce<10>(grid, stream, a, bf16); break;
-            case 11: launch_reduce<11>(grid, stream, a, bf16); break;
-            case 12: launch_reduce<12>(grid, stream, a, bf16); break;
-            case 13: launch_reduce<13>(grid, stream, a, bf16); break;
-            case 14: launch_reduce<14>(grid, stream, a, bf16); break;
-            case 15: launch_reduce<15>(grid, stream, a, bf16); break;
-            case 16: launch_reduce<16>(grid, stream, a, bf16); break;
+#define PURLIN_REDUCE_CASE(n) \
+    case n: launch_reduce<n>(grid, stream, a, bf16, nt_load, nt_store); break;
+            PURLIN_REDUCE_CASE(1) PURLIN_REDUCE_CASE(2) PURLIN_REDUCE_CASE(3) PURLIN_REDUCE_CASE(4)
+            PURLIN_REDUCE_CASE(5) PURLIN_REDUCE_CASE(6) PURLIN_REDUCE_CASE(7) PURLIN_REDUCE_CASE(8)
+            PURLIN_REDUCE_CASE(9) PURLIN_REDUCE_CASE(10) PURLIN_REDUCE_CASE(11) PURLIN_REDUCE_CASE(12)
+            PURLIN_REDUCE_CASE(13) PURLIN_REDUCE_CASE(14) PURLIN_REDUCE_CASE(15) PURLIN_REDUCE_CASE(16)
+#undef PURLIN_REDUCE_CASE
             default: return hipErrorInvalidValue;
         }
     }

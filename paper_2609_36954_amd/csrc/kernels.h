@@ -13,8 +13,10 @@ namespace purlin {
 // Launch one phase: `n` work items starting at device pointer `items`, all
 // of consume op `kind`.  The items of a REDUCE phase all sum the same `nsrc`
 // sources bufs[src_buf + p * src_step].  `bufs` holds the 2P buffer pointers.
+// nt_load / nt_store select non-temporal global loads / stores.
 hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
-                        uint32_t src_step, purlin_dtype dtype, void* const* bufs, int nbufs, hipStream_t stream);
+                        uint32_t src_step, bool nt_load, bool nt_store, purlin_dtype dtype, void* const* bufs,
+                        int nbufs, hipStream_t stream);
 
 struct PackWorkspace {
     int32_t* tile_base;  // [ntiles * E]: per-tile expert counts, then row bases
@@ -25,6 +27,7 @@ struct PackWorkspace {
 constexpr int kPackTileTokens = 64;  // one 64-bit token mask per expert and tile
 
 uint64_t pack_workspace_bytes(int T, int K, int E);
+bool moe_launch_fits(int T, int H);  // the pack/unpack grids for T tokens of H elements are launchable
 PackWorkspace pack_workspace_carve(void* base, int T, int K, int E);
 
 hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, const int32_t* ids,

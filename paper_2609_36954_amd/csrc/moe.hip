@@ -25,6 +25,8 @@
 
 #include "kernels.h"
 
+#include <algorithm>
+
 namespace purlin {
 namespace {
 
@@ -42,9 +44,21 @@ __device__ __forceinline__ uint32_t wave_index() {
 
 __device__ __forceinline__ uint32_t lane_index() { return threadIdx.x & (kWave - 1); }
 
-__device__ __forceinline__ u32x4 load16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
+template <bool NT>
+__device__ __forceinline__ u32x4 load16(const char* p) {
+    if constexpr (NT)
+        return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    else
+        return *reinterpret_cast<const u32x4*>(p);
+}
 
-__device__ __forceinline__ void store16(char* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+template <bool NT>
+__device__ __forceinline__ void store16(char* p, u32x4 v) {
+    if constexpr (NT)
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+    else
+        *reinterpret_cast<u32x4*>(p) = v;
+}
 
 // binary32 -> bf16, round to nearest, ties to even (see the executor for
 // the derivation); NaN -> quiet NaN with sign and top payload bits kept.
@@ -202,14 +216,20 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
     if (tid == 0 && dev_status) *dev_status = any ? 1 : 0;
 }
 
-template <int U>
-__global__ __launch_bounds__(kBlock) void pack_rows(int T, int H, int K, int E, const char* __restrict__ x,
+// One wavefront per (token, column slice): a slice is U * 64 16-byte
+// vectors of the row, so each lane holds U vectors of it.  Every slice's
+// wave forms the token's K positions (lane k forms pos[t, k]); the wave of
+// slice 0 also stores them.
+template <int U, bool NTL, bool NTS>
+__global__ __launch_bounds__(kBlock) void pack_rows(int T, int H, int K, int E, int slices, const char* __restrict__ x,
                                                     const int32_t* __restrict__ ids,
                                                     const int32_t* __restrict__ tile_base,
                                                     const int32_t* __restrict__ lrank, int32_t* __restrict__ pos,
                                                     char* __restrict__ packed) {
-    const uint32_t t = wave_index();
+    const uint32_t w = wave_index();
+    const uint32_t t = w / slices;
     if (t >= static_cast<uint32_t>(T)) return;
+    const uint32_t slice = w - t * slices;
     const uint32_t lane = lane_index();
     const int64_t rows = static_cast<int64_t>(T) * K;
     int p = -1;
@@ -221,31 +241,31 @@ __global__ __launch_bounds__(kBlock) void pack_rows(int T, int H, int K, int E, 
             const int64_t q = static_cast<int64_t>(tile_base[static_cast<int64_t>(t / kPackTileTokens) * E + e]) + r;
             p = (q >= 0 && q < rows) ? static_cast<int>(q) : -1;
         }
-        pos[j] = p;
+        if (slice == 0) pos[j] = p;
     }
     const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
     const char* src = x + t * row_bytes;
     if (row_bytes % 16 == 0) {
         const uint64_t nvec = row_bytes / 16;
-        for (uint64_t base = 0; base < nvec; base += U * kWave) {
-            u32x4 v[U];
+        const uint64_t base = static_cast<uint64_t>(slice) * U * kWave;
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint64_t i = base + u * kWave + lane;
+            if (i < nvec) v[u] = load16<NTL>(src + i * 16);
+        }
+        for (int k = 0; k < K; ++k) {
+            const int pk = __builtin_amdgcn_readlane(p, k);
+            if (pk < 0) continue;
+            char* dst = packed + static_cast<uint64_t>(pk) * row_bytes;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const uint64_t i = base + u * kWave + lane;
-                if (i < nvec) v[u] = load16(src + i * 16);
-            }
-            for (int k = 0; k < K; ++k) {
-                const int pk = __builtin_amdgcn_readlane(p, k);
-                if (pk < 0) continue;
-                char* dst = packed + static_cast<uint64_t>(pk) * row_bytes;
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const uint64_t i = base + u * kWave + lane;
-                    if (i < nvec) store16(dst + i * 16, v[u]);
-                }
+                if (i < nvec) store16<NTS>(dst + i * 16, v[u]);
             }
         }
     } else {
+        // rows not a multiple of 16 bytes: one slice per token, 2 bytes per lane step
         for (uint64_t h = lane; h < static_cast<uint64_t>(H); h += kWave) {
             const uint16_t v = reinterpret_cast<const uint16_t*>(src)[h];
             for (int k = 0; k < K; ++k) {
@@ -260,13 +280,16 @@ __global__ void set_status(int32_t* status) { *status = 0; }
 
 constexpr int kSlotGroup = 8;
 
-template <int U>
-__global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, const char* __restrict__ y,
+// One wavefront per (token, column slice) of the output row.
+template <int U, bool NTL, bool NTS>
+__global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, int slices, const char* __restrict__ y,
                                                       const int32_t* __restrict__ pos,
                                                       const float* __restrict__ gates, char* __restrict__ out,
                                                       int32_t* __restrict__ dev_status) {
-    const uint32_t t = wave_index();
+    const uint32_t w = wave_index();
+    const uint32_t t = w / slices;
     if (t >= static_cast<uint32_t>(T)) return;
+    const uint32_t slice = w - t * slices;
     const uint32_t lane = lane_index();
     const int64_t rows = static_cast<int64_t>(T) * K;
     int p = -1;
@@ -277,58 +300,57 @@ __global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, const
         g = gates[j];
         if (p < 0 || p >= rows) {
             p = -1;
-            if (dev_status) atomicOr(dev_status, 1);
+            if (dev_status && slice == 0) atomicOr(dev_status, 1);
         }
     }
     const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
     char* dst = out + t * row_bytes;
     if (row_bytes % 16 == 0) {
         const uint64_t nvec = row_bytes / 16;
-        for (uint64_t base = 0; base < nvec; base += U * kWave) {
-            float acc[U][8];
+        const uint64_t base = static_cast<uint64_t>(slice) * U * kWave;
+        float acc[U][8];
 #pragma unroll
-            for (int u = 0; u < U; ++u)
+        for (int u = 0; u < U; ++u)
 #pragma unroll
-                for (int e = 0; e < 8; ++e) acc[u][e] = 0.0f;
-            for (int k0 = 0; k0 < K; k0 += kSlotGroup) {
-                u32x4 v[kSlotGroup][U];
-                int pk[kSlotGroup];
+            for (int e = 0; e < 8; ++e) acc[u][e] = 0.0f;
+        for (int k0 = 0; k0 < K; k0 += kSlotGroup) {
+            u32x4 v[kSlotGroup][U];
+            int pk[kSlotGroup];
 #pragma unroll
-                for (int kk = 0; kk < kSlotGroup; ++kk) {
-                    pk[kk] = (k0 + kk < K) ? __builtin_amdgcn_readlane(p, k0 + kk) : -1;
-                    if (pk[kk] < 0) continue;
-                    const char* row = y + static_cast<uint64_t>(pk[kk]) * row_bytes;
+            for (int kk = 0; kk < kSlotGroup; ++kk) {
+                pk[kk] = (k0 + kk < K) ? __builtin_amdgcn_readlane(p, k0 + kk) : -1;
+                if (pk[kk] < 0) continue;
+                const char* row = y + static_cast<uint64_t>(pk[kk]) * row_bytes;
 #pragma unroll
-                    for (int u = 0; u < U; ++u) {
-                        const uint64_t i = base + u * kWave + lane;
-                        if (i < nvec) v[kk][u] = load16(row + i * 16);
-                    }
-                }
-#pragma unroll
-                for (int kk = 0; kk < kSlotGroup; ++kk) {
-                    if (pk[kk] < 0) continue;
-                    const float gk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), k0 + kk));
-#pragma unroll
-                    for (int u = 0; u < U; ++u) {
-#pragma unroll
-                        for (int m = 0; m < 4; ++m) {
-                            const uint32_t wv = v[kk][u][m];
-                            acc[u][2 * m] = __fadd_rn(acc[u][2 * m], __fmul_rn(gk, __uint_as_float(wv << 16)));
-                            acc[u][2 * m + 1] =
-                                __fadd_rn(acc[u][2 * m + 1], __fmul_rn(gk, __uint_as_float(wv & 0xFFFF0000u)));
-                        }
-                    }
+                for (int u = 0; u < U; ++u) {
+                    const uint64_t i = base + u * kWave + lane;
+                    if (i < nvec) v[kk][u] = load16<NTL>(row + i * 16);
                 }
             }
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const uint64_t i = base + u * kWave + lane;
-                if (i < nvec) {
-                    u32x4 o;
+            for (int kk = 0; kk < kSlotGroup; ++kk) {
+                if (pk[kk] < 0) continue;
+                const float gk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), k0 + kk));
 #pragma unroll
-                    for (int m = 0; m < 4; ++m) o[m] = to_bf16(acc[u][2 * m]) | (to_bf16(acc[u][2 * m + 1]) << 16);
-                    store16(dst + i * 16, o);
+                for (int u = 0; u < U; ++u) {
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) {
+                        const uint32_t wv = v[kk][u][m];
+                        acc[u][2 * m] = __fadd_rn(acc[u][2 * m], __fmul_rn(gk, __uint_as_float(wv << 16)));
+                        acc[u][2 * m + 1] =
+                            __fadd_rn(acc[u][2 * m + 1], __fmul_rn(gk, __uint_as_float(wv & 0xFFFF0000u)));
+                    }
                 }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint64_t i = base + u * kWave + lane;
+            if (i < nvec) {
+                u32x4 o;
+#pragma unroll
+                for (int m = 0; m < 4; ++m) o[m] = to_bf16(acc[u][2 * m]) | (to_bf16(acc[u][2 * m + 1]) << 16);
+                store16<NTS>(dst + i * 16, o);
             }
         }
     } else {
@@ -346,12 +368,33 @@ __global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, const
     }
 }
 
+// Launch shapes and cache hints, measured on MI355X: the packed rows and
+// the expert outputs are streams far larger than the last-level cache.
 constexpr int kPackUnroll = 8;
-constexpr int kUnpackUnroll = 2;
+constexpr bool kPackNtLoad = false;
+constexpr bool kPackNtStore = true;
+constexpr int kUnpackUnroll = 1;
+constexpr bool kUnpackNtLoad = true;
+constexpr bool kUnpackNtStore = true;
+
+// Column slices per token: U * 64 vectors each; rows that are not a
+// multiple of 16 bytes are handled by one wave per token.
+int row_slices(int H, int U) {
+    const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
+    if (row_bytes % 16 != 0) return 1;
+    const uint64_t nvec = row_bytes / 16, per = static_cast<uint64_t>(U) * kWave;
+    return static_cast<int>((nvec + per - 1) / per);
+}
 
 uint64_t align256(uint64_t b) { return (b + 255) & ~uint64_t(255); }
 
 }  // namespace
+
+bool moe_launch_fits(int T, int H) {
+    // one wave per (token, slice); wave ids are 32-bit
+    const uint64_t waves = static_cast<uint64_t>(T) * std::max(row_slices(H, kPackUnroll), row_slices(H, kUnpackUnroll));
+    return waves < (uint64_t(1) << 31);
+}
 
 uint64_t pack_workspace_bytes(int T, int K, int E) {
     const uint64_t ntiles = (static_cast<uint64_t>(T) + kPackTileTokens - 1) / kPackTileTokens;
@@ -382,9 +425,11 @@ hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, con
     hipLaunchKernelGGL(pack_scan, dim3(1), dim3(kScanThreads), 0, stream, ntiles, E, P, ws.tile_base, ws.tile_err,
                        expert_counts, expert_offsets, dest_counts, dest_offsets, dev_status);
     if (T > 0) {
-        const dim3 grid((T + kWavesPerBlock - 1) / kWavesPerBlock);
-        hipLaunchKernelGGL(pack_rows<kPackUnroll>, grid, dim3(kBlock), 0, stream, T, H, K, E,
-                           reinterpret_cast<const char*>(x), ids, ws.tile_base, ws.lrank, pos,
+        const int slices = row_slices(H, kPackUnroll);
+        const uint64_t waves = static_cast<uint64_t>(T) * slices;
+        const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
+        hipLaunchKernelGGL((pack_rows<kPackUnroll, kPackNtLoad, kPackNtStore>), grid, dim3(kBlock), 0, stream, T, H,
+                           K, E, slices, reinterpret_cast<const char*>(x), ids, ws.tile_base, ws.lrank, pos,
                            reinterpret_cast<char*>(packed));
     }
     return hipGetLastError();
@@ -395,9 +440,12 @@ hipError_t launch_unpack(int T, int H, int K, const uint16_t* y, const int32_t* 
     (void)hipGetLastError();
     if (dev_status) hipLaunchKernelGGL(set_status, dim3(1), dim3(1), 0, stream, dev_status);
     if (T > 0) {
-        const dim3 grid((T + kWavesPerBlock - 1) / kWavesPerBlock);
-        hipLaunchKernelGGL(unpack_rows<kUnpackUnroll>, grid, dim3(kBlock), 0, stream, T, H, K,
-                           reinterpret_cast<const char*>(y), pos, gates, reinterpret_cast<char*>(out), dev_status);
+        const int slices = row_slices(H, kUnpackUnroll);
+        const uint64_t waves = static_cast<uint64_t>(T) * slices;
+        const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
+        hipLaunchKernelGGL((unpack_rows<kUnpackUnroll, kUnpackNtLoad, kUnpackNtStore>), grid, dim3(kBlock), 0, stream,
+                           T, H, K, slices, reinterpret_cast<const char*>(y), pos, gates, reinterpret_cast<char*>(out),
+                           dev_status);
     }
     return hipGetLastError();
 }

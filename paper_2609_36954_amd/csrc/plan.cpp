@@ -26,6 +26,7 @@ namespace {
 constexpr uint64_t kMinItem = 1024;        // one 16-byte access per lane of a 64-wide wave
 constexpr uint64_t kMaxItem = 64 * 1024;   // largest automatic work item
 constexpr uint64_t kTargetItems = 4096;    // 16 wavefronts per CU on 256 CUs
+constexpr uint64_t kStreamingBytes = 512ull << 20;  // twice the last-level cache
 
 uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
 
@@ -55,11 +56,31 @@ purlin_desc make_desc(uint32_t kind, uint32_t phase, uint32_t nsrc, uint32_t src
     return d;
 }
 
-// Automatic work-item size for one phase: aim at kTargetItems items, never
-// below one wave-wide 16-byte access per lane, never above kMaxItem, and
-// large enough to keep the item count under PURLIN_MAX_ITEMS.
-uint64_t auto_item_bytes(uint64_t phase_bytes) {
-    uint64_t item = pow2_floor(std::max<uint64_t>(1, phase_bytes / kTargetItems));
+// Automatic work-item size for one phase.
+//  - Phases that stream more than the last-level cache holds: a wave's
+//    share is sized by the bytes it moves.  Measured on MI355X (256 MiB
+//    per rank, P = 8): a reduce item reading ~32 KiB (4 KiB of output from
+//    each of 8 sources), a multi-destination copy item writing ~256 KiB
+//    (32 KiB to each of 8 destinations) and a one-to-one copy item of 4 KiB
+//    run fastest; larger items leave too few wavefronts, smaller ones pay
+//    per-item overhead.
+//  - Smaller phases (latency regime): aim at kTargetItems items of at
+//    least one wave-wide 16-byte access per lane.
+// Never above kMaxItem, and large enough to keep the item count under
+// PURLIN_MAX_ITEMS.
+uint64_t auto_item_bytes(uint64_t phase_bytes, uint64_t traffic, uint32_t kind, uint32_t nsrc, uint32_t ndst) {
+    uint64_t item;
+    if (traffic >= kStreamingBytes) {
+        if (kind == PURLIN_KIND_REDUCE)
+            item = pow2_floor(std::max<uint64_t>(1, (32 * 1024) / std::max<uint32_t>(1, nsrc)));
+        else if (ndst > 1)
+            item = std::min<uint64_t>(32 * 1024, pow2_floor(std::max<uint64_t>(1, (256 * 1024) / ndst)));
+        else
+            item = 4096;  // one-to-one copies: many small items (AllToAll measured best at 4 KiB)
+        item = std::max<uint64_t>(item, 2048);
+    } else {
+        item = pow2_floor(std::max<uint64_t>(1, phase_bytes / kTargetItems));
+    }
     item = std::min(std::max(item, kMinItem), kMaxItem);
     const uint64_t floor_for_cap = ceil_div(phase_bytes, PURLIN_MAX_ITEMS / 2);
     if (item < floor_for_cap) item = ceil_div(floor_for_cap, 16) * 16;
@@ -84,15 +105,26 @@ purlin_status build_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype
         pol = *policy;
         if (pol.item_bytes % 16 != 0) return PURLIN_ERR_INVALID;
         if (pol.fanout > 2 || pol.ar_mode > 2) return PURLIN_ERR_INVALID;
+        if (pol.load_hint > 2 || pol.store_hint > 2) return PURLIN_ERR_INVALID;
         for (uint32_t r : pol.reserved)
             if (r != 0) return PURLIN_ERR_INVALID;
     }
-    if (pol.fanout == 0) pol.fanout = 2;
-    if (pol.ar_mode == 0) pol.ar_mode = 2;
-
     const uint64_t M = count / P;       // elements per partition
     const uint64_t part = M * s;        // partBytes
     const uint64_t Cp = part ? ceil_div(part, chunk) : 0;
+
+    if (pol.fanout == 0) pol.fanout = 2;
+    if (pol.ar_mode == 0) {
+        // AllReduce: in the latency regime one launch that reduces each chunk
+        // once and writes it to all P outputs wins (no second launch).  When
+        // the traffic streams from HBM, the two-phase compose wins although
+        // it schedules more bytes: phase 0 leaves the N*s reduced bytes in the
+        // last-level cache and phase 1's copies read them back from there,
+        // while each wave streams one direction at a time (measured on
+        // MI355X at 256 MiB per rank, P = 8).
+        const uint64_t one_phase_traffic = 2 * uint64_t(P) * count * s;
+        pol.ar_mode = one_phase_traffic >= kStreamingBytes ? 1 : 2;
+    }
 
     out = Plan{};
     out.op = op;
@@ -200,26 +232,35 @@ purlin_status build_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype
 
         for (const purlin_desc& d : D) out.sched_bytes += (uint64_t(d.nsrc) + d.ndst) * d.bytes;
 
+        // Per-phase shape: bytes of the descriptors, bytes moved, fan-in/out.
+        struct PhaseShape {
+            uint64_t bytes = 0, traffic = 0, ndesc = 0;
+            uint32_t kind = 0, nsrc = 0, ndst = 0;
+            uint64_t item = 0;
+        } shape[2];
+        for (const purlin_desc& d : D) {
+            PhaseShape& sh = shape[d.phase];
+            sh.bytes += d.bytes;
+            sh.traffic += (uint64_t(d.nsrc) + d.ndst) * d.bytes;
+            sh.kind = d.kind;
+            sh.nsrc = std::max(sh.nsrc, d.nsrc);
+            sh.ndst = std::max(sh.ndst, d.ndst);
+            ++sh.ndesc;
+        }
         // Cut descriptors into work items, phase by phase.
         uint64_t items_total = 0;
         for (uint32_t ph = 0; ph < 2; ++ph) {
-            uint64_t phase_bytes = 0, ndesc = 0;
+            PhaseShape& sh = shape[ph];
+            if (sh.ndesc == 0) continue;
+            sh.item = pol.item_bytes ? pol.item_bytes : auto_item_bytes(sh.bytes, sh.traffic, sh.kind, sh.nsrc, sh.ndst);
             for (const purlin_desc& d : D)
-                if (d.phase == ph) phase_bytes += d.bytes, ++ndesc;
-            if (ndesc == 0) continue;
-            const uint64_t item = pol.item_bytes ? pol.item_bytes : auto_item_bytes(phase_bytes);
-            for (const purlin_desc& d : D)
-                if (d.phase == ph) items_total += ceil_div(d.bytes, item);
+                if (d.phase == ph) items_total += ceil_div(d.bytes, sh.item);
             if (items_total > PURLIN_MAX_ITEMS) return PURLIN_ERR_NOMEM;
         }
         out.items.reserve(items_total);
         for (uint32_t ph = 0; ph < 2; ++ph) {
-            uint64_t phase_bytes = 0;
-            bool any = false;
-            for (const purlin_desc& d : D)
-                if (d.phase == ph) phase_bytes += d.bytes, any = true;
-            if (!any) continue;
-            const uint64_t item = pol.item_bytes ? pol.item_bytes : auto_item_bytes(phase_bytes);
+            if (shape[ph].ndesc == 0) continue;
+            const uint64_t item = shape[ph].item;
             Phase& phase = out.phases[out.nphases++];
             phase.begin = out.items.size();
             bool first = true;
@@ -245,6 +286,30 @@ purlin_status build_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype
                 }
             }
             phase.count = out.items.size() - phase.begin;
+            // Cache hints.  A stream that is touched once and is much larger
+            // than the 256 MB last-level cache gains from non-temporal
+            // accesses; which side gains was measured on MI355X: reads for
+            // many-to-one (reduce), writes for one-to-many (multi-destination
+            // copy), both for one-to-one copies.  Phases whose traffic fits
+            // the cache keep cached accesses so repeated calls hit it.
+            uint64_t traffic = 0, max_ndst = 0;
+            for (uint64_t i = phase.begin; i < out.items.size(); ++i) {
+                traffic += (uint64_t(out.items[i].nsrc) + out.items[i].ndst) * out.items[i].bytes;
+                max_ndst = std::max<uint64_t>(max_ndst, out.items[i].ndst);
+            }
+            const bool streaming = traffic >= kStreamingBytes;
+            bool auto_nt_load = false, auto_nt_store = false;
+            if (streaming) {
+                if (phase.kind == PURLIN_KIND_REDUCE) {
+                    auto_nt_load = true;
+                } else if (max_ndst > 1) {
+                    auto_nt_store = true;
+                } else {
+                    auto_nt_load = auto_nt_store = true;
+                }
+            }
+            phase.nt_load = pol.load_hint ? pol.load_hint == 2 : auto_nt_load;
+            phase.nt_store = pol.store_hint ? pol.store_hint == 2 : auto_nt_store;
         }
     } catch (const std::bad_alloc&) {
         out.descs.clear();

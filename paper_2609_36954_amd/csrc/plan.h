@@ -16,6 +16,8 @@ struct Phase {
     uint32_t nsrc = 1;
     uint32_t src_buf = 0;   // REDUCE phases: every item sums bufs[src_buf + p * src_step]
     uint32_t src_step = 0;
+    bool nt_load = false;   // non-temporal (streaming) global loads
+    bool nt_store = false;  // non-temporal (streaming) global stores
     uint64_t begin = 0;  // first work item
     uint64_t count = 0;  // work items
 };

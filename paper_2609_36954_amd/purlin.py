@@ -63,7 +63,9 @@ class Policy(ctypes.Structure):
         ("item_bytes", ctypes.c_uint64),
         ("fanout", ctypes.c_uint32),
         ("ar_mode", ctypes.c_uint32),
-        ("reserved", ctypes.c_uint32 * 4),
+        ("load_hint", ctypes.c_uint32),  # 0 auto, 1 cached, 2 non-temporal
+        ("store_hint", ctypes.c_uint32),
+        ("reserved", ctypes.c_uint32 * 2),
     ]
 
 

@@ -89,7 +89,10 @@ def test_plan_argument_validation(args, want):
         (dict(item_bytes=16), 0),
         (dict(fanout=3), INVALID),
         (dict(ar_mode=3), INVALID),
-        (dict(reserved=(ctypes.c_uint32 * 4)(0, 1, 0, 0)), INVALID),
+        (dict(reserved=(ctypes.c_uint32 * 2)(0, 1)), INVALID),
+        (dict(load_hint=3), INVALID),
+        (dict(store_hint=3), INVALID),
+        (dict(load_hint=2, store_hint=1), 0),
         (dict(item_bytes=1 << 20, fanout=1, ar_mode=1), 0),
     ],
 )
