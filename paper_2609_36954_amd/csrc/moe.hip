@@ -73,14 +73,16 @@ __global__ __launch_bounds__(kBlock) void pack_tiles(int T, int K, int E, const 
                                                      int32_t* __restrict__ tile_cnt, int32_t* __restrict__ lrank,
                                                      int32_t* __restrict__ tile_err) {
     extern __shared__ unsigned long long masks[];  // [E]
+    __shared__ int32_t tids[kPackTileTokens * 64];  // the tile's ids (K <= 64)
     __shared__ int err;
     const int tile = blockIdx.x;
     const int t0 = tile * kPackTileTokens;
     const int nt = min(kPackTileTokens, T - t0);
     const int n = nt * K;
-    const int32_t* tids = ids + static_cast<int64_t>(t0) * K;
+    const int32_t* gids = ids + static_cast<int64_t>(t0) * K;
 
     for (int e = threadIdx.x; e < E; e += kBlock) masks[e] = 0ull;
+    for (int j = threadIdx.x; j < n; j += kBlock) tids[j] = gids[j];
     if (threadIdx.x == 0) err = 0;
     __syncthreads();
 
@@ -111,18 +113,8 @@ __global__ __launch_bounds__(kBlock) void pack_tiles(int T, int K, int E, const 
     if (threadIdx.x == 0) tile_err[tile] = err;
 }
 
-// Sum of tile counts of expert e over tiles [lo, hi), 8 loads in flight.
-__device__ __forceinline__ int sum_tiles(const int32_t* tile_cnt, int E, int e, int lo, int hi) {
-    int s = 0;
-    for (int t = lo; t < hi; t += 8) {
-        int c[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) c[i] = (t + i < hi) ? tile_cnt[static_cast<int64_t>(t + i) * E + e] : 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) s += c[i];
-    }
-    return s;
-}
+// Tile counts of one work unit kept in registers between the two passes.
+constexpr int kScanBatch = 16;
 
 __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int P, int32_t* __restrict__ tile_cnt,
                                                           const int32_t* __restrict__ tile_err,
@@ -137,22 +129,36 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
     __shared__ int32_t scan[kScanThreads];
     const int tid = threadIdx.x;
 
+    // error flags first, so their loads overlap the count loads
+    int any = 0;
+    for (int t = tid; t < ntiles; t += kScanThreads) any |= tile_err[t];
+
     // Work units: tpe threads per expert when E is small, each owning a
-    // contiguous slice of tiles; one unit per expert when E >= 1024.
+    // contiguous slice of tiles; one unit per expert when E >= 1024.  A
+    // unit whose slice fits kScanBatch keeps its counts in registers.
     const int tpe = E >= kScanThreads ? 1 : kScanThreads / E;
     const int units = E * tpe;
     const int span = (ntiles + tpe - 1) / tpe;
+    const bool in_regs = span <= kScanBatch && units <= kScanThreads;
 
+    int c[kScanBatch];
     for (int u = tid; u < units; u += kScanThreads) {
         const int e = u / tpe, q = u - e * tpe;
         const int lo = min(ntiles, q * span), hi = min(ntiles, lo + span);
-        partial[u] = sum_tiles(tile_cnt, E, e, lo, hi);
+        int sum = 0;
+        for (int t = lo; t < hi; t += kScanBatch) {
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i) c[i] = (t + i < hi) ? tile_cnt[static_cast<int64_t>(t + i) * E + e] : 0;
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i) sum += c[i];
+        }
+        partial[u] = sum;
     }
     __syncthreads();
     for (int e = tid; e < E; e += kScanThreads) {
-        int s = 0;
-        for (int q = 0; q < tpe; ++q) s += partial[e * tpe + q];
-        total[e] = s;
+        int sum = 0;
+        for (int q = 0; q < tpe; ++q) sum += partial[e * tpe + q];
+        total[e] = sum;
     }
     __syncthreads();
 
@@ -190,12 +196,14 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
         const int lo = min(ntiles, q * span), hi = min(ntiles, lo + span);
         int base = offs[e];
         for (int q2 = 0; q2 < q; ++q2) base += partial[e * tpe + q2];
-        for (int t = lo; t < hi; t += 8) {
-            int c[8];
+        for (int t = lo; t < hi; t += kScanBatch) {
+            if (!in_regs) {
 #pragma unroll
-            for (int i = 0; i < 8; ++i) c[i] = (t + i < hi) ? tile_cnt[static_cast<int64_t>(t + i) * E + e] : 0;
+                for (int i = 0; i < kScanBatch; ++i)
+                    c[i] = (t + i < hi) ? tile_cnt[static_cast<int64_t>(t + i) * E + e] : 0;
+            }
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
+            for (int i = 0; i < kScanBatch; ++i) {
                 if (t + i < hi) tile_cnt[static_cast<int64_t>(t + i) * E + e] = base;
                 base += c[i];
             }
@@ -204,14 +212,12 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
 
     const int L = E / P;
     for (int r = tid; r < P; r += kScanThreads) {
-        int s = 0;
-        for (int e = r * L; e < (r + 1) * L; ++e) s += total[e];
-        dest_counts[r] = s;
+        int sum = 0;
+        for (int e = r * L; e < (r + 1) * L; ++e) sum += total[e];
+        dest_counts[r] = sum;
         dest_offsets[r] = offs[r * L];
     }
 
-    int any = 0;
-    for (int t = tid; t < ntiles; t += kScanThreads) any |= tile_err[t];
     any = __syncthreads_or(any);
     if (tid == 0 && dev_status) *dev_status = any ? 1 : 0;
 }
