@@ -410,7 +410,7 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
         return t.contiguous().view(torch.uint8).cpu().numpy().view(dt)
 
     log("bench: cpu baseline (oracle on a sample)")
-    frac = 16  # 1/16 of each partition of the collectives
+    frac = 2  # half of each partition of the collectives
     m = M // frac
     ok = True
     t_total, bytes_total = 0.0, 0
@@ -430,16 +430,21 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
     for r in (0, P - 1):
         got = np.concatenate([down(ag_out[r][k * M:k * M + m], np.uint16) for k in range(P)])
         ok &= bool(np.array_equal(got, ag_want[r]))
-    # MoE pack and combine on the first 512 tokens (positions for the combine
-    # come from the oracle's own pack of the full routing)
-    Ts = 512
+    # MoE pack and combine of all 4096 tokens
+    T = ids_np.shape[0]
+    Ts = T
     H = x_np.shape[1]
     t = time.perf_counter()
-    oracle.pack(x_np[:Ts], ids_np[:Ts], E, P)
+    pw = oracle.pack(x_np, ids_np, E, P)
     t_total += time.perf_counter() - t
-    bytes_total += pack_bytes(Ts, H, K, E, P)
-    pos_want = oracle.pack(np.zeros((ids_np.shape[0], 1), np.uint16), ids_np, E, P)["pos"]
+    bytes_total += pack_bytes(T, H, K, E, P)
+    pos_want = pw["pos"]
     ok &= bool(np.array_equal(down(pack_out["pos"], np.int32).reshape(-1, K), pos_want))
+    for key in ("dest_counts", "dest_offsets", "expert_counts", "expert_offsets"):
+        ok &= bool(np.array_equal(down(pack_out[key], np.int32), pw[key]))
+    rows = np.random.default_rng(0).choice(T * K, 256, replace=False)
+    ok &= bool(np.array_equal(down(pack_out["packed"], np.uint16).reshape(T * K, H)[rows], pw["packed"][rows]))
+    del pw
     t = time.perf_counter()
     cw = oracle.unpack(y_np, pos_want[:Ts], g_np[:Ts])
     t_total += time.perf_counter() - t
@@ -455,7 +460,7 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
         "cores": 1,
         "kind": "oracle",
         "sample": f"ReduceScatter+AllGather on 1/{frac} of each 32 MiB partition (P=8, bf16); "
-                  f"MoE pack and combine of the first {Ts} of 4096 tokens",
+                  f"MoE pack and combine of all {T} tokens",
         "seconds": round(t_total, 3),
         "host_cores_available": cores,
         "cpu": platform.processor() or platform.machine(),

@@ -13,6 +13,7 @@ Contents
 ``collectives``  AllGather, ReduceScatter, AllReduce, AllToAll over P ranks
                  (Section 2.1 "Stable communication semantics"; layouts of
                  Section 3.1; rank-order reduction of Eq. 2, Section 3.3).
+``rooted``       Broadcast, Scatter, Gather, Reduce (Appendix A).
 ``moe``          MoE dispatch ``pack`` and combine ``unpack`` (the paper names
                  them only as the expert-parallel use of AllToAll, Table 2;
                  their contract is written out in ``moe``'s docstrings).
@@ -30,6 +31,7 @@ example, closed forms, special cases); none is "parity unpinned".
 from .bf16 import narrow, widen
 from .collectives import all_gather, all_reduce, all_to_all, reduce_scatter
 from .moe import pack, unpack
+from .rooted import broadcast, gather, reduce, scatter
 
 __all__ = [
     "narrow",
@@ -40,4 +42,8 @@ __all__ = [
     "reduce_scatter",
     "pack",
     "unpack",
+    "broadcast",
+    "gather",
+    "reduce",
+    "scatter",
 ]

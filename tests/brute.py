@@ -137,3 +137,26 @@ def unpack(y, pos, gates):
             row.append(bf16_narrow(acc))
         out.append(row)
     return out
+
+
+def broadcast(ins, root):
+    return [list(ins[root]) for _ in range(len(ins))]
+
+
+def scatter(ins, root):
+    P = len(ins)
+    M = len(ins[root]) // P
+    return [[ins[root][r * M + i] for i in range(M)] for r in range(P)]
+
+
+def gather(ins, root):
+    P = len(ins)
+    out = [None] * P
+    out[root] = [ins[p][i] for p in range(P) for i in range(len(ins[p]))]
+    return out
+
+
+def reduce(ins, root, dtype):
+    out = [None] * len(ins)
+    out[root] = rank_order_reduce([list(a) for a in ins], dtype)
+    return out
