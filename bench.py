@@ -169,6 +169,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--latency-sweep", action="store_true", help="also time AllReduce P=8 bf16 at 1 KiB..512 KiB per rank")
     ap.add_argument("--no-latency", action="store_true", help="skip the graph-replayed latency measurement")
+    ap.add_argument("--no-extra", action="store_true", help="skip timing the other collectives (outside the step)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device-to-device tensor copy first (reference for HBM counter scaling)")
     ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -327,6 +328,11 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / (calls * reps)
 
+    # ---------------- the other collectives at the same shape (not in the step) ----------------
+    extra = None
+    if not args.no_extra:
+        extra = measure_extra_ops(torch, PL, ins, rs_out, ag_out, P, N, s)
+
     latency = None
     if not args.no_latency:
         latency = measure_latency(torch, PL, W, graph_latency_us, args.latency_sweep)
@@ -336,7 +342,40 @@ def main():
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_out, comb_out, P, N, M, E, K)
     return emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, per_op, latency, plan_ms,
-                dev_name, src_hash)
+                dev_name, src_hash, extra)
+
+
+def measure_extra_ops(torch, PL, ins, rs_out, ag_out, P, N, s, reps=5):
+    """AllReduce, AllToAll and the rooted collectives at 256 MiB/rank, P=8,
+    bf16, chunk 1 MiB: event-timed on the current stream, outside the step."""
+    root = 0
+    cases = [
+        ("allreduce", PL.Plan("allreduce", P, N, "bf16", 1 << 20), ins, ag_out, 2 * P * N * s),
+        ("alltoall", PL.Plan("alltoall", P, N, "bf16", 1 << 20), ins, ag_out, 2 * P * N * s),
+        ("broadcast", PL.Plan("broadcast", P, N, "bf16", 1 << 20, root=root),
+         [ins[root]] + [None] * (P - 1), ag_out, N * s + P * N * s),
+        ("reduce", PL.Plan("reduce", P, N, "bf16", 1 << 20, root=root), ins,
+         [ag_out[root]] + [None] * (P - 1), P * N * s + N * s),
+        ("scatter", PL.Plan("scatter", P, N, "bf16", 1 << 20, root=root),
+         [ins[root]] + [None] * (P - 1), rs_out, 2 * N * s),
+        ("gather", PL.Plan("gather", P, N, "bf16", 1 << 20, root=root), rs_out,
+         [ag_out[root]] + [None] * (P - 1), 2 * N * s),
+    ]
+    out = {}
+    for name, plan, i, o, bmin in cases:
+        plan.exec(i, o)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            plan.exec(i, o)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        out[name] = {"avg_us": round(us, 2), "bytes_min": int(bmin), "bytes_sched": int(plan.sched_bytes),
+                     "GBps_min": round(bmin / (us * 1e-6) / 1e9, 1),
+                     "frac_of_hbm_peak": round(bmin / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+    return out
 
 
 def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
@@ -366,7 +405,7 @@ def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
 
 
 def emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, per_op, latency, plan_ms, dev_name,
-         src_hash):
+         src_hash, extra):
     result = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -393,6 +432,7 @@ def emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, 
         "cpu_baseline": cpu,
         "ops": per_op,
         "latency_us": latency,
+        "other_ops_256MiB_per_rank": extra,
         "plan_ms": round(plan_ms, 3),
         "device": dev_name,
         "kernel_source_hash": src_hash,

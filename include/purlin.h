@@ -58,12 +58,22 @@ typedef enum purlin_status {
  *   ALLREDUCE      reduce, scattered -> scattered  (compose<RS, AG>)
  *   REDUCE_SCATTER reduce, scattered -> packed
  *   ALLGATHER      copy,   packed    -> scattered
- *   ALLTOALL       copy,   scattered -> transposed                       */
+ *   ALLTOALL       copy,   scattered -> transposed
+ * Rooted collectives (Appendix A), planned with purlin_plan_rooted:
+ *   BROADCAST      the root's input to every rank   (compose<scatter, AG>)
+ *   REDUCE         every rank's input reduced at the root
+ *                                                   (compose<RS, gather>)
+ *   SCATTER        copy, scattered -> packed, only the root produces
+ *   GATHER         copy, packed -> scattered, only the root consumes      */
 typedef enum purlin_op {
     PURLIN_ALLREDUCE = 0,
     PURLIN_REDUCE_SCATTER = 1,
     PURLIN_ALLGATHER = 2,
-    PURLIN_ALLTOALL = 3
+    PURLIN_ALLTOALL = 3,
+    PURLIN_BROADCAST = 4,
+    PURLIN_REDUCE = 5,
+    PURLIN_SCATTER = 6,
+    PURLIN_GATHER = 7
 } purlin_op;
 
 typedef enum purlin_dtype { PURLIN_FP32 = 0, PURLIN_BF16 = 1 } purlin_dtype;
@@ -131,7 +141,8 @@ typedef struct purlin_policy {
 
 typedef struct purlin_plan_s* purlin_plan_t;
 
-/* Build a plan for `op` over P ranks (1..16) of `count` elements per rank
+/* Build a plan for a non-rooted `op` (ALLREDUCE, REDUCE_SCATTER, ALLGATHER,
+ * ALLTOALL) over P ranks (1..16) of `count` elements per rank
  * on the scattered side (the paper's message-size convention, Section 5
  * "Microbenchmark methodology"):
  *     ALLREDUCE      in: count      out: count        elements per rank
@@ -151,6 +162,21 @@ typedef struct purlin_plan_s* purlin_plan_t;
 PURLIN_API purlin_status purlin_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype,
                           uint64_t chunk_bytes, purlin_plan_t* out_plan);
 
+/* A rooted collective (Appendix A) with root rank `root` (0 <= root < P).
+ * `count` is the root-side scattered size N (a multiple of P):
+ *     BROADCAST  in: N (root only)      out: N       on every rank
+ *     REDUCE     in: N on every rank    out: N       (root only)
+ *     SCATTER    in: N (root only)      out: N / P   on every rank
+ *     GATHER     in: N / P on every rank out: N      (root only)
+ * Buffers a rank does not use (the inputs of non-roots for BROADCAST and
+ * SCATTER, the outputs of non-roots for REDUCE and GATHER) are ignored by
+ * purlin_exec and may be NULL.  Policy, flags and errors as for
+ * purlin_plan_ex; PURLIN_ERR_INVALID also for a root out of range or a
+ * non-rooted op. */
+PURLIN_API purlin_status purlin_plan_rooted(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype,
+                                            uint64_t chunk_bytes, const purlin_policy* policy, uint32_t flags,
+                                            purlin_plan_t* out_plan);
+
 /* purlin_plan with an explicit policy (NULL = automatic) and flags
  * (0 or PURLIN_PLAN_HOST_ONLY).  PURLIN_ERR_INVALID also for a policy with
  * item_bytes not a multiple of 16, fanout > 2, ar_mode > 2, a hint > 2 or
@@ -162,8 +188,8 @@ PURLIN_API purlin_status purlin_plan_ex(purlin_op op, int P, uint64_t count, pur
 
 /* Sizes of a plan (any output pointer may be NULL):
  *   n_desc             chunk descriptors;
- *   in_bytes_per_rank  bytes each bufs[p], p < P, must hold;
- *   out_bytes_per_rank bytes each bufs[P + r] must hold;
+ *   in_bytes_per_rank  bytes each used bufs[p], p < P, must hold;
+ *   out_bytes_per_rank bytes each used bufs[P + r] must hold;
  *   sched_bytes        bytes the schedule reads plus writes,
  *                      sum over descriptors of (nsrc + ndst) * bytes. */
 PURLIN_API purlin_status purlin_plan_info(purlin_plan_t plan, uint64_t* n_desc, uint64_t* in_bytes_per_rank,
@@ -182,7 +208,8 @@ PURLIN_API purlin_status purlin_plan_items(purlin_plan_t plan, const purlin_desc
                                 uint64_t phase_begin[3]);
 
 /* Run the plan: bufs[] holds 2P device pointers, in_0..in_{P-1} then
- * out_0..out_{P-1}, sized per purlin_plan_info.  Each phase is one kernel
+ * out_0..out_{P-1}, sized per purlin_plan_info (entries a rooted plan does
+ * not use are ignored).  Each phase is one kernel
  * launch on `stream`; no host-device copy, no allocation, no
  * synchronisation (graph-capturable).  Errors (nothing enqueued):
  * PURLIN_ERR_INVALID for a NULL or host-only plan, NULL bufs, a NULL or

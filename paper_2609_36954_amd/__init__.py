@@ -19,6 +19,7 @@ from .purlin import (  # noqa: F401
     purlin_pack,
     purlin_pack_workspace_size,
     purlin_plan,
+    purlin_plan_rooted,
     purlin_status_string,
     purlin_unpack,
     purlin_version,

@@ -24,7 +24,7 @@ bool overlaps(const void* a, uint64_t na, const void* b, uint64_t nb) {
     return x < y + nb && y < x + na;
 }
 
-purlin_status make_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype, uint64_t chunk,
+purlin_status make_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,
                         const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan) {
     if (!out_plan) return PURLIN_ERR_INVALID;
     *out_plan = nullptr;
@@ -32,7 +32,7 @@ purlin_status make_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype,
     if (!h) return PURLIN_ERR_NOMEM;
     purlin_status st;
     try {
-        st = purlin::build_plan(op, P, count, dtype, chunk, policy, flags, h->plan);
+        st = purlin::build_plan(op, P, root, count, dtype, chunk, policy, flags, h->plan);
     } catch (...) {
         st = PURLIN_ERR_NOMEM;
     }
@@ -69,12 +69,22 @@ extern "C" {
 
 purlin_status purlin_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype, uint64_t chunk_bytes,
                           purlin_plan_t* out_plan) {
-    return make_plan(op, P, count, dtype, chunk_bytes, nullptr, 0, out_plan);
+    return make_plan(op, P, -1, count, dtype, chunk_bytes, nullptr, 0, out_plan);
 }
 
 purlin_status purlin_plan_ex(purlin_op op, int P, uint64_t count, purlin_dtype dtype, uint64_t chunk_bytes,
                              const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan) {
-    return make_plan(op, P, count, dtype, chunk_bytes, policy, flags, out_plan);
+    return make_plan(op, P, -1, count, dtype, chunk_bytes, policy, flags, out_plan);
+}
+
+purlin_status purlin_plan_rooted(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype,
+                                 uint64_t chunk_bytes, const purlin_policy* policy, uint32_t flags,
+                                 purlin_plan_t* out_plan) {
+    if (op < PURLIN_BROADCAST || op > PURLIN_GATHER) {
+        if (out_plan) *out_plan = nullptr;
+        return PURLIN_ERR_INVALID;
+    }
+    return make_plan(op, P, root, count, dtype, chunk_bytes, policy, flags, out_plan);
 }
 
 purlin_status purlin_plan_info(purlin_plan_t plan, uint64_t* n_desc, uint64_t* in_bytes_per_rank,
@@ -117,14 +127,17 @@ purlin_status purlin_exec(purlin_plan_t plan, void* const* bufs, void* stream) {
     if (p.flags & PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
     if (!bufs) return PURLIN_ERR_INVALID;
     const int P = p.P;
+    auto used = [&](int i) { return i < P ? ((p.in_mask >> i) & 1u) : ((p.out_mask >> (i - P)) & 1u); };
     for (int i = 0; i < 2 * P; ++i)
-        if (!bufs[i] || !aligned16(bufs[i])) return PURLIN_ERR_INVALID;
+        if (used(i) && (!bufs[i] || !aligned16(bufs[i]))) return PURLIN_ERR_INVALID;
     for (int i = 0; i < P; ++i)
         for (int r = 0; r < P; ++r)
-            if (overlaps(bufs[i], p.in_bytes, bufs[P + r], p.out_bytes)) return PURLIN_ERR_INVALID;
+            if (used(i) && used(P + r) && overlaps(bufs[i], p.in_bytes, bufs[P + r], p.out_bytes))
+                return PURLIN_ERR_INVALID;
     for (int r = 0; r < P; ++r)
         for (int q = r + 1; q < P; ++q)
-            if (overlaps(bufs[P + r], p.out_bytes, bufs[P + q], p.out_bytes)) return PURLIN_ERR_INVALID;
+            if (used(P + r) && used(P + q) && overlaps(bufs[P + r], p.out_bytes, bufs[P + q], p.out_bytes))
+                return PURLIN_ERR_INVALID;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     for (int i = 0; i < p.nphases; ++i) {

@@ -89,11 +89,13 @@ uint64_t auto_item_bytes(uint64_t phase_bytes, uint64_t traffic, uint32_t kind, 
 
 }  // namespace
 
-purlin_status build_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype, uint64_t chunk,
+purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,
                          const purlin_policy* policy, uint32_t flags, Plan& out) {
-    if (op < PURLIN_ALLREDUCE || op > PURLIN_ALLTOALL) return PURLIN_ERR_INVALID;
+    if (op < PURLIN_ALLREDUCE || op > PURLIN_GATHER) return PURLIN_ERR_INVALID;
+    const bool rooted = op >= PURLIN_BROADCAST;
     if (dtype != PURLIN_FP32 && dtype != PURLIN_BF16) return PURLIN_ERR_INVALID;
     if (P < 1 || P > PURLIN_MAX_RANKS) return PURLIN_ERR_INVALID;
+    if (rooted ? (root < 0 || root >= P) : root != -1) return PURLIN_ERR_INVALID;
     if (count % static_cast<uint64_t>(P) != 0) return PURLIN_ERR_INVALID;
     if (flags & ~PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
     const uint64_t s = dtype == PURLIN_FP32 ? 4 : 2;
@@ -134,21 +136,32 @@ purlin_status build_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype
     out.chunk = chunk;
     out.flags = flags;
     out.elem_bytes = s;
+    out.root = rooted ? root : -1;
+    const uint32_t all = (P >= 32) ? 0xFFFFFFFFu : ((1u << P) - 1u);
+    const uint32_t root_bit = rooted ? (1u << root) : 0u;
+    out.in_mask = all;
+    out.out_mask = all;
     switch (op) {
         case PURLIN_ALLREDUCE:
         case PURLIN_ALLTOALL:
+        case PURLIN_BROADCAST:
+        case PURLIN_REDUCE:
             out.in_bytes = count * s;
             out.out_bytes = count * s;
             break;
         case PURLIN_REDUCE_SCATTER:
+        case PURLIN_SCATTER:
             out.in_bytes = count * s;
             out.out_bytes = part;
             break;
         case PURLIN_ALLGATHER:
+        case PURLIN_GATHER:
             out.in_bytes = part;
             out.out_bytes = count * s;
             break;
     }
+    if (op == PURLIN_BROADCAST || op == PURLIN_SCATTER) out.in_mask = root_bit;
+    if (op == PURLIN_REDUCE || op == PURLIN_GATHER) out.out_mask = root_bit;
 
     // Upper bound on descriptors before allocating anything.
     const uint64_t Pu = static_cast<uint64_t>(P);
@@ -194,6 +207,40 @@ purlin_status build_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype
                         for_chunks(r, [&](uint32_t c, uint64_t scat, uint64_t pk, uint64_t len) {
                             D.push_back(make_desc(PURLIN_KIND_COPY, 0, 1, in0 + p, 0, 1, out0 + r, 0, scat, p * part + pk, len, r, c));
                         });
+                break;
+            case PURLIN_BROADCAST:
+                // compose<scatter, allGather> with the intermediate in
+                // registers: each chunk of the root's partition k is read
+                // once and written to every rank's partition k.
+                for (uint32_t k = 0; k < Pu; ++k)
+                    for_chunks(k, [&](uint32_t c, uint64_t scat, uint64_t, uint64_t len) {
+                        D.push_back(make_desc(PURLIN_KIND_COPY, 0, 1, in0 + root, 0, P, out0, 1, scat, scat, len, k, c));
+                    });
+                break;
+            case PURLIN_SCATTER:
+                // copy, scattered -> packed: partition k of the root's input
+                // lands at out_k + offset.
+                for (uint32_t k = 0; k < Pu; ++k)
+                    for_chunks(k, [&](uint32_t c, uint64_t scat, uint64_t pk, uint64_t len) {
+                        D.push_back(make_desc(PURLIN_KIND_COPY, 0, 1, in0 + root, 0, 1, out0 + k, 0, scat, pk, len, k, c));
+                    });
+                break;
+            case PURLIN_GATHER:
+                // copy, packed -> scattered: rank p's contribution lands at
+                // out_root + p * partBytes + offset.
+                for (uint32_t p = 0; p < Pu; ++p)
+                    for_chunks(p, [&](uint32_t c, uint64_t scat, uint64_t pk, uint64_t len) {
+                        D.push_back(make_desc(PURLIN_KIND_COPY, 0, 1, in0 + p, 0, 1, out0 + root, 0, pk, scat, len, p, c));
+                    });
+                break;
+            case PURLIN_REDUCE:
+                // compose<reduceScatter, gather> with the intermediate in
+                // registers: partition k of every input, summed in rank
+                // order, lands at out_root + k * partBytes + offset.
+                for (uint32_t k = 0; k < Pu; ++k)
+                    for_chunks(k, [&](uint32_t c, uint64_t scat, uint64_t, uint64_t len) {
+                        D.push_back(make_desc(PURLIN_KIND_REDUCE, 0, P, in0, 1, 1, out0 + root, 0, scat, scat, len, k, c));
+                    });
                 break;
             case PURLIN_ALLREDUCE:
                 if (pol.ar_mode == 1) {

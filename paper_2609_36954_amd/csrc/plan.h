@@ -31,6 +31,9 @@ struct Plan {
     purlin_policy policy{};  // resolved: no "auto" fields left
     uint32_t flags = 0;
 
+    int root = -1;           // rooted collectives only
+    uint32_t in_mask = 0;    // bit p: input p is read
+    uint32_t out_mask = 0;   // bit r: output r is written
     uint64_t elem_bytes = 0;
     uint64_t in_bytes = 0;   // per rank
     uint64_t out_bytes = 0;  // per rank
@@ -45,7 +48,8 @@ struct Plan {
 };
 
 // Validates the request and fills `out` (host tables only).  Pure host code.
-purlin_status build_plan(purlin_op op, int P, uint64_t count, purlin_dtype dtype, uint64_t chunk,
+// `root` is -1 for the non-rooted collectives and a rank for the rooted ones.
+purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,
                          const purlin_policy* policy, uint32_t flags, Plan& out);
 
 }  // namespace purlin

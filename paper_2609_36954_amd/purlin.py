@@ -23,7 +23,9 @@ PURLIN_ERR_UNSUPPORTED = 2
 PURLIN_ERR_NOMEM = 3
 PURLIN_ERR_DEVICE = 4
 
-OPS = {"allreduce": 0, "reduce_scatter": 1, "allgather": 2, "alltoall": 3}
+OPS = {"allreduce": 0, "reduce_scatter": 1, "allgather": 2, "alltoall": 3,
+       "broadcast": 4, "reduce": 5, "scatter": 6, "gather": 7}
+ROOTED = ("broadcast", "reduce", "scatter", "gather")
 DTYPES = {"fp32": 0, "bf16": 1}
 ELEM_BYTES = {"fp32": 4, "bf16": 2}
 KIND_COPY = 0
@@ -85,6 +87,7 @@ def lib():
     i32, u32, u64 = ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64
     L.purlin_plan.argtypes = [i32, i32, u64, i32, u64, ctypes.POINTER(_vp)]
     L.purlin_plan_ex.argtypes = [i32, i32, u64, i32, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
+    L.purlin_plan_rooted.argtypes = [i32, i32, i32, u64, i32, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
     L.purlin_plan_info.argtypes = [_vp, _c_u64p, _c_u64p, _c_u64p, _c_u64p]
     L.purlin_plan_descriptors.argtypes = [_vp, ctypes.POINTER(_vp), _c_u64p, _c_u64p]
     L.purlin_plan_items.argtypes = [_vp, ctypes.POINTER(_vp), _c_u64p, _c_u64p]
@@ -98,7 +101,7 @@ def lib():
     L.purlin_status_string.restype = ctypes.c_char_p
     L.purlin_version.argtypes = []
     L.purlin_version.restype = ctypes.c_char_p
-    for name in ("purlin_plan", "purlin_plan_ex", "purlin_plan_info", "purlin_plan_descriptors", "purlin_plan_items",
+    for name in ("purlin_plan", "purlin_plan_ex", "purlin_plan_rooted", "purlin_plan_info", "purlin_plan_descriptors", "purlin_plan_items",
                  "purlin_exec", "purlin_pack_workspace_size", "purlin_pack", "purlin_unpack"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -147,16 +150,26 @@ def _require_cuda(t, name, itemsize=None):
 class Plan:
     """A planned collective (immutable).  ``exec`` runs it on a stream."""
 
-    def __init__(self, op, P, count, dtype, chunk, policy=None, host_only=False):
+    def __init__(self, op, P, count, dtype, chunk, policy=None, host_only=False, root=None):
         if op not in OPS:
             raise PurlinError(PURLIN_ERR_INVALID, f"unknown op {op!r}")
         if dtype not in DTYPES:
             raise PurlinError(PURLIN_ERR_INVALID, f"unknown dtype {dtype!r}")
+        if (op in ROOTED) != (root is not None):
+            raise PurlinError(PURLIN_ERR_INVALID, f"{op} {'needs' if op in ROOTED else 'takes no'} root")
         self.op, self.P, self.count, self.dtype, self.chunk = op, int(P), int(count), dtype, int(chunk)
+        self.root = root
         self.host_only = bool(host_only)
         h = ctypes.c_void_p()
         L = lib()
-        if policy is None and not host_only:
+        if root is not None:
+            pol = None
+            if policy is not None:
+                pol = policy if isinstance(policy, Policy) else Policy(**policy)
+            st = L.purlin_plan_rooted(OPS[op], int(P), int(root), int(count), DTYPES[dtype], int(chunk),
+                                      ctypes.byref(pol) if pol is not None else None,
+                                      PLAN_HOST_ONLY if host_only else 0, ctypes.byref(h))
+        elif policy is None and not host_only:
             st = L.purlin_plan(OPS[op], int(P), int(count), DTYPES[dtype], int(chunk), ctypes.byref(h))
         else:
             pol = None
@@ -226,21 +239,44 @@ def purlin_plan(op, P, count, dtype, chunk, policy=None, host_only=False):
     return Plan(op, P, count, dtype, chunk, policy=policy, host_only=host_only)
 
 
+def purlin_plan_rooted(op, P, root, count, dtype, chunk, policy=None, host_only=False):
+    return Plan(op, P, count, dtype, chunk, policy=policy, host_only=host_only, root=root)
+
+
+def used_buffers(plan):
+    """(inputs used, outputs used) as lists of booleans, rank order."""
+    P, op, root = plan.P, plan.op, plan.root
+    ins = [True] * P
+    outs = [True] * P
+    if op in ("broadcast", "scatter"):
+        ins = [r == root for r in range(P)]
+    if op in ("reduce", "gather"):
+        outs = [r == root for r in range(P)]
+    return ins, outs
+
+
 def purlin_exec(plan, ins, outs, stream=None):
+    """``ins``/``outs``: P device tensors each; for a rooted plan, entries of
+    buffers it does not use may be None."""
     P = plan.P
     if len(ins) != P or len(outs) != P:
         raise PurlinError(PURLIN_ERR_INVALID, f"need {P} inputs and {P} outputs")
+    use_in, use_out = used_buffers(plan)
     if plan.count:
         s = ELEM_BYTES[plan.dtype]
-        for t in ins:
+        for t, u in zip(ins, use_in):
+            if not u:
+                continue
             _require_cuda(t, "input", s)
             if t.numel() * s < plan.in_bytes:
                 raise PurlinError(PURLIN_ERR_INVALID, "input buffer too small")
-        for t in outs:
+        for t, u in zip(outs, use_out):
+            if not u:
+                continue
             _require_cuda(t, "output", s)
             if t.numel() * s < plan.out_bytes:
                 raise PurlinError(PURLIN_ERR_INVALID, "output buffer too small")
-    arr = (ctypes.c_void_p * (2 * P))(*[t.data_ptr() for t in list(ins) + list(outs)])
+    arr = (ctypes.c_void_p * (2 * P))(*[(t.data_ptr() if t is not None else 0) for t in list(ins) + list(outs)])
     _check(lib().purlin_exec(plan.handle, arr, _stream_handle(stream) if plan.count else None), "purlin_exec")
 
 

@@ -100,6 +100,33 @@ def test_policy_validation(policy, want):
     assert _plan_status(0, 4, 4096, 1, 256, policy) == want
 
 
+def _rooted_status(op, P, root, count=4096, dtype=1, chunk=256):
+    h = ctypes.c_void_p()
+    st = PL.lib().purlin_plan_rooted(op, P, root, count, dtype, chunk, None, PL.PLAN_HOST_ONLY, ctypes.byref(h))
+    if h.value:
+        PL.lib().purlin_plan_destroy(h)
+    return st
+
+
+@pytest.mark.parametrize(
+    "op,P,root,want",
+    [
+        (4, 4, 0, 0), (5, 4, 3, 0), (6, 4, 1, 0), (7, 4, 2, 0),  # broadcast, reduce, scatter, gather
+        (4, 4, 4, INVALID), (5, 4, -1, INVALID),  # root out of range
+        (0, 4, 0, INVALID), (3, 4, 0, INVALID),  # non-rooted ops through the rooted entry
+        (8, 4, 0, INVALID),  # unknown op
+        (6, 3, 0, INVALID),  # count % P (4096 % 3)
+    ],
+)
+def test_rooted_plan_validation(op, P, root, want):
+    assert _rooted_status(op, P, root) == want
+
+
+def test_rooted_ops_need_the_rooted_entry():
+    assert _plan_status(4, 4, 4096, 1, 256) == INVALID
+    assert _plan_status(7, 4, 4096, 1, 256) == INVALID
+
+
 def test_unknown_flags_rejected():
     assert _plan_status(0, 4, 4096, 1, 256, flags=0x80) == INVALID
 

@@ -242,3 +242,66 @@ def test_interpreter_matches_oracle(case):
             got = outs[r].view(np.uint16 if dtype == "bf16" else np.uint32)
             exp = want[r].view(np.uint16 if dtype == "bf16" else np.uint32)
             assert np.array_equal(got, exp), (pol, r)
+
+
+# ---------------------------------------------------------------------------
+# rooted collectives (Appendix A)
+# ---------------------------------------------------------------------------
+
+ROOTED_CASES = []
+for _op in ("broadcast", "reduce", "scatter", "gather"):
+    for _dt in ("fp32", "bf16"):
+        for _P, _M in ((1, 9), (2, 16), (3, 100), (8, 257)):
+            for _chunk_elems in (1, 64, 1000):
+                ROOTED_CASES.append((_op, _dt, _P, _M, _chunk_elems))
+
+
+@pytest.mark.parametrize("case", ROOTED_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_rooted_interpreter_matches_oracle(case):
+    op, dtype, P, M, chunk_elems = case
+    s = S[dtype]
+    count = P * M
+    ins = _inputs(P, count, dtype, seed=hash(case) % 1000)
+    for root in sorted({0, P - 1, P // 2}):
+        if op == "gather":
+            want = oracle.gather([a[:M] for a in ins], root, dtype)
+        else:
+            want = getattr(oracle, op)(ins, root, dtype)
+        plan = PL.Plan(op, P, count, dtype, chunk_elems * s, host_only=True, root=root)
+        use_in, use_out = PL.used_buffers(plan)
+        items, pb = plan.items()
+        # buffers a rooted plan does not use are poisoned: reading them would show
+        in_bytes = [np.frombuffer(a.tobytes()[: plan.in_bytes], dtype=np.uint8).copy() if u
+                    else np.full(plan.in_bytes, 0xEE, np.uint8) for a, u in zip(ins, use_in)]
+        outs = [np.full(plan.out_bytes, 0xA5, dtype=np.uint8) for _ in range(P)]
+        interp.run(items, pb, in_bytes + outs, dtype, seed=len(items))
+        for r in range(P):
+            if not use_out[r]:
+                assert want[r] is None
+                assert np.all(outs[r] == 0xA5), "a buffer the plan does not use was written"
+                continue
+            got = outs[r].view(np.uint16 if dtype == "bf16" else np.uint32)
+            exp = want[r].view(np.uint16 if dtype == "bf16" else np.uint32)
+            assert np.array_equal(got, exp), (op, root, r)
+
+
+@pytest.mark.parametrize("op", ["broadcast", "reduce", "scatter", "gather"])
+def test_rooted_tables_touch_only_used_buffers(op):
+    P, M = 6, 1000
+    for root in range(P):
+        plan = host_plan_rooted(op, P, P * M, "bf16", 256, root)
+        use_in, use_out = PL.used_buffers(plan)
+        d = plan.descriptors()
+        for x in d:
+            for p in range(int(x["nsrc"])):
+                b = int(x["src_buf"]) + p * int(x["src_step"])
+                assert b < P and use_in[b]
+            for j in range(int(x["ndst"])):
+                b = int(x["dst_buf"]) + j * int(x["dst_step"]) - P
+                assert 0 <= b < P and use_out[b]
+        expected = {"broadcast": P * 8, "reduce": P * 8, "scatter": P * 8, "gather": P * 8}[op]
+        assert len(d) == expected  # one descriptor per (partition, chunk): 2000 B / 256 B = 8 chunks
+
+
+def host_plan_rooted(op, P, count, dtype, chunk, root, **policy):
+    return PL.Plan(op, P, count, dtype, chunk, policy=policy or None, host_only=True, root=root)
