@@ -328,6 +328,12 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / (calls * reps)
 
+    # ---------------- CPU baseline: the oracle on a bounded sample ----------------
+    # (first: it compares the step's own outputs, which the later measurements overwrite)
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_out, comb_out, P, N, M, E, K)
+
     # ---------------- the other collectives at the same shape (not in the step) ----------------
     extra = None
     if not args.no_extra:
@@ -336,11 +342,6 @@ def main():
     latency = None
     if not args.no_latency:
         latency = measure_latency(torch, PL, W, graph_latency_us, args.latency_sweep)
-
-    # ---------------- CPU baseline: the oracle on a bounded sample ----------------
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_out, comb_out, P, N, M, E, K)
     return emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, per_op, latency, plan_ms,
                 dev_name, src_hash, extra)
 

@@ -126,7 +126,11 @@ typedef struct purlin_policy {
                             into out_k's partition k, then copies of it to
                             every other rank: the in-place compose of
                             Section 3.1), 2 = one phase (each chunk reduced
-                            once and written to all P outputs)               */
+                            once and written to all P outputs), 3 = the two
+                            phases of 1 in one launch: a chunk's copies start
+                            when its reduction has finished (per-chunk
+                            counters with epochs, Section 3.2 and 4.2; such a
+                            plan must not run concurrently with itself)     */
     uint32_t load_hint;  /* global loads:  0 auto, 1 cached, 2 non-temporal */
     uint32_t store_hint; /* global stores: 0 auto, 1 cached, 2 non-temporal */
     uint32_t reserved[2];/* must be zero */
@@ -179,7 +183,7 @@ PURLIN_API purlin_status purlin_plan_rooted(purlin_op op, int P, int root, uint6
 
 /* purlin_plan with an explicit policy (NULL = automatic) and flags
  * (0 or PURLIN_PLAN_HOST_ONLY).  PURLIN_ERR_INVALID also for a policy with
- * item_bytes not a multiple of 16, fanout > 2, ar_mode > 2, a hint > 2 or
+ * item_bytes not a multiple of 16, fanout > 2, ar_mode > 3, a hint > 2 or
  * nonzero reserved fields, and for unknown flags.  Hints change only how
  * the caches treat the streams, never the result. */
 PURLIN_API purlin_status purlin_plan_ex(purlin_op op, int P, uint64_t count, purlin_dtype dtype,
@@ -219,6 +223,12 @@ PURLIN_API purlin_status purlin_plan_items(purlin_plan_t plan, const purlin_desc
  * ignores bufs.  A plan is immutable: concurrent execs on different
  * streams with distinct buffers are safe. */
 PURLIN_API purlin_status purlin_exec(purlin_plan_t plan, void* const* bufs, void* stream);
+
+/* Device error word of a plan (0 = none).  Only single-launch AllReduce
+ * plans (ar_mode 3) can set it: a copy that waited longer than a fixed bound
+ * for its chunk gives up and sets it, so a launch always completes.
+ * Synchronous: waits for the device to finish the plan's queued work. */
+PURLIN_API purlin_status purlin_plan_device_error(purlin_plan_t plan, uint32_t* error);
 
 /* Free a plan (NULL-safe).  Does not synchronise: the caller keeps the plan
  * alive until work queued with it has finished. */

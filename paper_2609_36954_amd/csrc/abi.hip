@@ -24,6 +24,10 @@ bool overlaps(const void* a, uint64_t na, const void* b, uint64_t nb) {
     return x < y + nb && y < x + na;
 }
 
+size_t fused_state_bytes(const purlin::Plan& p) {
+    return sizeof(purlin::FusedState) + sizeof(uint64_t) * p.chunks_per_part * static_cast<uint64_t>(p.P);
+}
+
 purlin_status make_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,
                         const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan) {
     if (!out_plan) return PURLIN_ERR_INVALID;
@@ -52,6 +56,21 @@ purlin_status make_plan(purlin_op op, int P, int root, uint64_t count, purlin_dt
             (void)hipFree(pl.d_items);
             delete h;
             return PURLIN_ERR_DEVICE;
+        }
+        if (pl.fused) {
+            const size_t sb = fused_state_bytes(pl);
+            if (hipMalloc(&pl.d_state, sb) != hipSuccess) {
+                pl.d_state = nullptr;
+                (void)hipFree(pl.d_items);
+                delete h;
+                return PURLIN_ERR_NOMEM;
+            }
+            if (hipMemset(pl.d_state, 0, sb) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+                (void)hipFree(pl.d_state);
+                (void)hipFree(pl.d_items);
+                delete h;
+                return PURLIN_ERR_DEVICE;
+            }
         }
     }
     *out_plan = h;
@@ -140,6 +159,16 @@ purlin_status purlin_exec(purlin_plan_t plan, void* const* bufs, void* stream) {
                 return PURLIN_ERR_INVALID;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (p.fused) {
+        auto* state = static_cast<purlin::FusedState*>(p.d_state);
+        auto* ready = reinterpret_cast<uint64_t*>(state + 1);
+        const uint64_t n = p.items.size();
+        const uint64_t n_reduce = p.phases[0].count;
+        const hipError_t e = purlin::launch_fused_allreduce(
+            p.d_items, n, n_reduce, p.phases[0].nsrc, p.dtype, p.phases[0].nt_load, bufs, 2 * P, state, ready,
+            p.part_bytes, p.chunk, p.reduce_item_bytes, p.chunks_per_part, s);
+        return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+    }
     for (int i = 0; i < p.nphases; ++i) {
         const purlin::Phase& ph = p.phases[i];
         const hipError_t e = purlin::launch_phase(p.d_items + ph.begin, ph.count, ph.kind, ph.nsrc, ph.src_buf,
@@ -149,9 +178,21 @@ purlin_status purlin_exec(purlin_plan_t plan, void* const* bufs, void* stream) {
     return PURLIN_OK;
 }
 
+purlin_status purlin_plan_device_error(purlin_plan_t plan, uint32_t* error) {
+    if (!plan || !error) return PURLIN_ERR_INVALID;
+    *error = 0;
+    if (!plan->plan.d_state) return PURLIN_OK;
+    if (hipDeviceSynchronize() != hipSuccess) return PURLIN_ERR_DEVICE;
+    const auto* state = static_cast<const purlin::FusedState*>(plan->plan.d_state);
+    if (hipMemcpy(error, &state->error, sizeof(uint32_t), hipMemcpyDeviceToHost) != hipSuccess)
+        return PURLIN_ERR_DEVICE;
+    return PURLIN_OK;
+}
+
 void purlin_plan_destroy(purlin_plan_t plan) {
     if (!plan) return;
     if (plan->plan.d_items) (void)hipFree(plan->plan.d_items);
+    if (plan->plan.d_state) (void)hipFree(plan->plan.d_state);
     delete plan;
 }
 

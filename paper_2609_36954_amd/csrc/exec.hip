@@ -40,6 +40,10 @@ struct ExecArgs {
     char* srcs[PURLIN_MAX_RANKS];
 };
 
+// Loads in flight per lane: U vectors for a copy, U * NSRC for a reduce.
+constexpr int kCopyUnroll = 4;
+constexpr int reduce_unroll(int nsrc) { return nsrc >= 16 ? 1 : (nsrc >= 8 ? 2 : (nsrc >= 4 ? 4 : 8)); }
+
 __device__ __forceinline__ uint32_t wave_index() {
     return __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
 }
@@ -95,12 +99,9 @@ __device__ __forceinline__ void copy_bytes2(const ExecArgs& a, const purlin_desc
     }
 }
 
+// One COPY work item, executed by the whole wave.
 template <int U, bool NTL, bool NTS>
-__global__ __launch_bounds__(kBlock) void exec_copy(ExecArgs a) {
-    const uint32_t w = wave_index();
-    if (w >= a.n_items) return;
-    const purlin_desc d = a.items[w];
-    const uint32_t lane = lane_index();
+__device__ __forceinline__ void run_copy(const ExecArgs& a, const purlin_desc& d, uint32_t lane) {
     const char* src = a.bufs[d.src_buf] + d.src_off;
     if (((d.src_off | d.dst_off) & 15) != 0) {
         copy_bytes2(a, d, src, 0, d.bytes, lane);
@@ -123,6 +124,14 @@ __global__ __launch_bounds__(kBlock) void exec_copy(ExecArgs a) {
         for (uint32_t j = 0; j < d.ndst; ++j) store16<NTS>(dst_ptr(a, d, j) + i * 16, v);
     }
     copy_bytes2(a, d, src, nvec * 16, d.bytes, lane);
+}
+
+template <int U, bool NTL, bool NTS>
+__global__ __launch_bounds__(kBlock) void exec_copy(ExecArgs a) {
+    const uint32_t w = wave_index();
+    if (w >= a.n_items) return;
+    const purlin_desc d = a.items[w];
+    run_copy<U, NTL, NTS>(a, d, lane_index());
 }
 
 // Eq. 2 on one 16-byte vector of every source: 8 bf16 or 4 fp32 elements.
@@ -181,12 +190,9 @@ __device__ __forceinline__ void reduce_elems(const ExecArgs& a, const purlin_des
     }
 }
 
+// One REDUCE work item, executed by the whole wave.
 template <int NSRC, bool BF16, int U, bool NTL, bool NTS>
-__global__ __launch_bounds__(kBlock) void exec_reduce(ExecArgs a) {
-    const uint32_t w = wave_index();
-    if (w >= a.n_items) return;
-    const purlin_desc d = a.items[w];
-    const uint32_t lane = lane_index();
+__device__ __forceinline__ void run_reduce(const ExecArgs& a, const purlin_desc& d, uint32_t lane) {
     const char* src[NSRC];
 #pragma unroll
     for (int p = 0; p < NSRC; ++p) src[p] = a.srcs[p] + d.src_off;
@@ -221,9 +227,100 @@ __global__ __launch_bounds__(kBlock) void exec_reduce(ExecArgs a) {
     reduce_elems<NSRC, BF16>(a, d, src, nvec * 16, d.bytes, lane);
 }
 
-// Loads in flight per lane: U vectors for a copy, U * NSRC for a reduce.
-constexpr int kCopyUnroll = 4;
-constexpr int reduce_unroll(int nsrc) { return nsrc >= 16 ? 1 : (nsrc >= 8 ? 2 : (nsrc >= 4 ? 4 : 8)); }
+template <int NSRC, bool BF16, int U, bool NTL, bool NTS>
+__global__ __launch_bounds__(kBlock) void exec_reduce(ExecArgs a) {
+    const uint32_t w = wave_index();
+    if (w >= a.n_items) return;
+    const purlin_desc d = a.items[w];
+    run_reduce<NSRC, BF16, U, NTL, NTS>(a, d, lane_index());
+}
+
+// ---------------------------------------------------------------------------
+// Single-launch AllReduce: compose<ReduceScatter, AllGather> with the gather
+// of each chunk released by the completion of that chunk's reduction
+// (Algorithm 1's reduce and gather roles, notify and consume of Section 3.2)
+// inside one launch.  All ranks share one address space, so there is no
+// staging; the notification is a per-chunk counter of finished reduce items.
+//
+// * Items are claimed in table order through an atomic counter: every
+//   reduce item precedes every copy item, so a copy item is only ever
+//   claimed after all reduce items have been claimed by running waves, and
+//   reduce items never wait.  Every wait therefore ends.
+// * Counters are never reset (the epochs of Section 4.2): chunk (k, c) is
+//   ready in launch e when its counter reaches (e + 1) * (its reduce
+//   items).  The last wave to finish resets the claim and done counters and
+//   advances the epoch for the next launch on the stream.
+// * Waits are bounded: a wave that waits longer than kSpinLimit sleeps
+//   records an error in the state block and gives up its item, so the
+//   launch always drains.
+struct FusedArgs {
+    FusedState* state;
+    uint64_t* ready;         // [P * chunks_per_part] finished reduce items, cumulative
+    uint64_t n_reduce;       // items [0, n_reduce) reduce, the rest copy
+    uint64_t part_bytes;     // partition bytes
+    uint64_t chunk_bytes;
+    uint64_t item_bytes;     // cut size of the reduce items
+    uint64_t chunks_per_part;
+};
+
+constexpr uint32_t kSpinLimit = 1u << 24;
+
+__device__ __forceinline__ uint64_t reduce_items_of_chunk(const FusedArgs& f, uint32_t c) {
+    const uint64_t off = uint64_t(c) * f.chunk_bytes;
+    const uint64_t len = min(f.chunk_bytes, f.part_bytes - off);
+    return (len + f.item_bytes - 1) / f.item_bytes;
+}
+
+template <int NSRC, bool BF16, bool STREAM>
+__global__ __launch_bounds__(kBlock) void exec_fused_allreduce(ExecArgs a, FusedArgs f) {
+    const uint32_t w = wave_index();
+    if (w >= a.n_items) return;  // exactly n_items waves claim
+    const uint32_t lane = lane_index();
+    FusedState* st = f.state;
+    const uint64_t epoch = __hip_atomic_load(&st->epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t claimed = 0;
+    if (lane == 0) claimed = __hip_atomic_fetch_add(&st->claim, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t i = __builtin_amdgcn_readfirstlane(claimed);
+    if (i < a.n_items) {
+        const purlin_desc d = a.items[i];
+        uint64_t* ready = f.ready + uint64_t(d.part) * f.chunks_per_part + d.chunk;
+        if (i < f.n_reduce) {
+            run_reduce<NSRC, BF16, reduce_unroll(NSRC), STREAM, false>(a, d, lane);
+            // release: this wave's stores are visible device-wide before the count
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            if (lane == 0) __hip_atomic_fetch_add(ready, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            const uint64_t target = (epoch + 1) * reduce_items_of_chunk(f, d.chunk);
+            uint32_t spins = 0;
+            bool ok = true;
+            while (__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
+                       __hip_atomic_load(ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target))) {
+                if (++spins > kSpinLimit) {
+                    ok = false;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(2);
+            }
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            if (ok) {
+                run_copy<kCopyUnroll, false, STREAM>(a, d, lane);
+            } else if (lane == 0) {
+                __hip_atomic_store(&st->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+    }
+    // the last wave of the launch resets the claim counters, then advances the epoch
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    if (lane == 0) {
+        const uint32_t prev = __hip_atomic_fetch_add(&st->done, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        if (prev + 1 == a.n_items) {
+            __hip_atomic_store(&st->claim, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&st->done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_fetch_add(&st->epoch, 1ull, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
 
 template <int NSRC, bool BF16>
 void launch_reduce_hints(dim3 grid, hipStream_t stream, const ExecArgs& a, bool ntl, bool nts) {
@@ -258,7 +355,50 @@ void launch_copy(dim3 grid, hipStream_t stream, const ExecArgs& a, bool ntl, boo
         hipLaunchKernelGGL((exec_copy<U, false, false>), grid, dim3(kBlock), 0, stream, a);
 }
 
+template <int NSRC>
+void launch_fused_n(dim3 grid, hipStream_t stream, const ExecArgs& a, const FusedArgs& f, bool bf16, bool stream_hint) {
+    if (bf16) {
+        if (stream_hint)
+            hipLaunchKernelGGL((exec_fused_allreduce<NSRC, true, true>), grid, dim3(kBlock), 0, stream, a, f);
+        else
+            hipLaunchKernelGGL((exec_fused_allreduce<NSRC, true, false>), grid, dim3(kBlock), 0, stream, a, f);
+    } else {
+        if (stream_hint)
+            hipLaunchKernelGGL((exec_fused_allreduce<NSRC, false, true>), grid, dim3(kBlock), 0, stream, a, f);
+        else
+            hipLaunchKernelGGL((exec_fused_allreduce<NSRC, false, false>), grid, dim3(kBlock), 0, stream, a, f);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_fused_allreduce(const purlin_desc* items, uint64_t n, uint64_t n_reduce, uint32_t nsrc,
+                                  purlin_dtype dtype, bool streaming, void* const* bufs, int nbufs, FusedState* state,
+                                  uint64_t* ready, uint64_t part_bytes, uint64_t chunk_bytes, uint64_t item_bytes,
+                                  uint64_t chunks_per_part, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    if (n >= (uint64_t(1) << 32)) return hipErrorInvalidValue;
+    ExecArgs a{};
+    a.items = items;
+    a.n_items = n;
+    for (int i = 0; i < nbufs && i < 2 * PURLIN_MAX_RANKS; ++i) a.bufs[i] = static_cast<char*>(bufs[i]);
+    for (uint32_t p = 0; p < nsrc && p < PURLIN_MAX_RANKS; ++p) a.srcs[p] = static_cast<char*>(bufs[p]);
+    FusedArgs f{state, ready, n_reduce, part_bytes, chunk_bytes, item_bytes, chunks_per_part};
+    const dim3 grid(static_cast<uint32_t>((n + kWavesPerBlock - 1) / kWavesPerBlock));
+    const bool bf16 = dtype == PURLIN_BF16;
+    (void)hipGetLastError();
+    switch (nsrc) {
+#define PURLIN_FUSED_CASE(k) \
+    case k: launch_fused_n<k>(grid, stream, a, f, bf16, streaming); break;
+        PURLIN_FUSED_CASE(1) PURLIN_FUSED_CASE(2) PURLIN_FUSED_CASE(3) PURLIN_FUSED_CASE(4)
+        PURLIN_FUSED_CASE(5) PURLIN_FUSED_CASE(6) PURLIN_FUSED_CASE(7) PURLIN_FUSED_CASE(8)
+        PURLIN_FUSED_CASE(9) PURLIN_FUSED_CASE(10) PURLIN_FUSED_CASE(11) PURLIN_FUSED_CASE(12)
+        PURLIN_FUSED_CASE(13) PURLIN_FUSED_CASE(14) PURLIN_FUSED_CASE(15) PURLIN_FUSED_CASE(16)
+#undef PURLIN_FUSED_CASE
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
 
 hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
                         uint32_t src_step, bool nt_load, bool nt_store, purlin_dtype dtype, void* const* bufs,

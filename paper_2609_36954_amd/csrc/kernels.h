@@ -18,6 +18,22 @@ hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uin
                         uint32_t src_step, bool nt_load, bool nt_store, purlin_dtype dtype, void* const* bufs,
                         int nbufs, hipStream_t stream);
 
+// Device state of a single-launch AllReduce plan (zeroed at plan creation).
+struct FusedState {
+    uint32_t claim;   // next work item to claim in the current launch
+    uint32_t done;    // waves of the current launch that have finished
+    uint64_t epoch;   // launches completed
+    uint32_t error;   // set if a wait gave up (bounded spin)
+    uint32_t pad[3];
+};
+
+// One launch for a whole AllReduce: items [0, n_reduce) reduce partition k
+// into out_k, the rest copy it to the other ranks once its chunk is done.
+hipError_t launch_fused_allreduce(const purlin_desc* items, uint64_t n, uint64_t n_reduce, uint32_t nsrc,
+                                  purlin_dtype dtype, bool streaming, void* const* bufs, int nbufs, FusedState* state,
+                                  uint64_t* ready, uint64_t part_bytes, uint64_t chunk_bytes, uint64_t item_bytes,
+                                  uint64_t chunks_per_part, hipStream_t stream);
+
 struct PackWorkspace {
     int32_t* tile_base;  // [ntiles * E]: per-tile expert counts, then row bases
     int32_t* lrank;      // [T * K]: rank of (t, k) among its tile's tokens of the same expert

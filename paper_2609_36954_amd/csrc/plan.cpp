@@ -106,7 +106,7 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
     if (policy) {
         pol = *policy;
         if (pol.item_bytes % 16 != 0) return PURLIN_ERR_INVALID;
-        if (pol.fanout > 2 || pol.ar_mode > 2) return PURLIN_ERR_INVALID;
+        if (pol.fanout > 2 || pol.ar_mode > 3) return PURLIN_ERR_INVALID;
         if (pol.load_hint > 2 || pol.store_hint > 2) return PURLIN_ERR_INVALID;
         for (uint32_t r : pol.reserved)
             if (r != 0) return PURLIN_ERR_INVALID;
@@ -243,7 +243,7 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
                     });
                 break;
             case PURLIN_ALLREDUCE:
-                if (pol.ar_mode == 1) {
+                if (pol.ar_mode == 1 || pol.ar_mode == 3) {
                     // compose<ReduceScatter, AllGather> in place: phase 0
                     // reduces partition k into out_k's k-th partition (the
                     // intermediate Y_k), phase 1 copies it to every other rank.
@@ -276,6 +276,9 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
                 break;
         }
         out.policy = pol;
+        out.part_bytes = part;
+        out.chunks_per_part = Cp;
+        out.fused = op == PURLIN_ALLREDUCE && pol.ar_mode == 3 && P > 1;
 
         for (const purlin_desc& d : D) out.sched_bytes += (uint64_t(d.nsrc) + d.ndst) * d.bytes;
 
@@ -305,6 +308,7 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
             if (items_total > PURLIN_MAX_ITEMS) return PURLIN_ERR_NOMEM;
         }
         out.items.reserve(items_total);
+        out.reduce_item_bytes = shape[0].item;
         for (uint32_t ph = 0; ph < 2; ++ph) {
             if (shape[ph].ndesc == 0) continue;
             const uint64_t item = shape[ph].item;

@@ -44,7 +44,14 @@ struct Plan {
     int nphases = 0;
     Phase phases[2];
 
+    // Single-launch AllReduce (ar_mode 3): one launch over all items.
+    bool fused = false;
+    uint64_t part_bytes = 0;
+    uint64_t chunks_per_part = 0;
+    uint64_t reduce_item_bytes = 0;  // cut size of the reduce items
+
     purlin_desc* d_items = nullptr;  // device copy of items (null for host-only plans)
+    void* d_state = nullptr;         // fused plans: FusedState followed by the per-chunk counters
 };
 
 // Validates the request and fills `out` (host tables only).  Pure host code.

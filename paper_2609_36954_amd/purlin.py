@@ -92,6 +92,8 @@ def lib():
     L.purlin_plan_descriptors.argtypes = [_vp, ctypes.POINTER(_vp), _c_u64p, _c_u64p]
     L.purlin_plan_items.argtypes = [_vp, ctypes.POINTER(_vp), _c_u64p, _c_u64p]
     L.purlin_exec.argtypes = [_vp, ctypes.POINTER(_vp), _vp]
+    L.purlin_plan_device_error.argtypes = [_vp, ctypes.POINTER(ctypes.c_uint32)]
+    L.purlin_plan_device_error.restype = ctypes.c_int
     L.purlin_plan_destroy.argtypes = [_vp]
     L.purlin_plan_destroy.restype = None
     L.purlin_pack_workspace_size.argtypes = [i32, i32, i32, _c_u64p]
@@ -218,6 +220,12 @@ class Plan:
             return np.zeros(0, dtype=DESC_DTYPE)
         buf = (ctypes.c_char * (n * DESC_DTYPE.itemsize)).from_address(p.value)
         return np.frombuffer(bytes(buf), dtype=DESC_DTYPE).copy()
+
+    def device_error(self):
+        """Device error word (single-launch AllReduce plans); synchronises."""
+        e = ctypes.c_uint32()
+        _check(lib().purlin_plan_device_error(self.handle, ctypes.byref(e)), "purlin_plan_device_error")
+        return e.value
 
     def exec(self, ins, outs, stream=None):
         """Run on device tensors ``ins`` (P inputs) and ``outs`` (P outputs)."""

@@ -88,7 +88,8 @@ def test_plan_argument_validation(args, want):
         (dict(item_bytes=24), INVALID),
         (dict(item_bytes=16), 0),
         (dict(fanout=3), INVALID),
-        (dict(ar_mode=3), INVALID),
+        (dict(ar_mode=4), INVALID),
+        (dict(ar_mode=3), 0),
         (dict(reserved=(ctypes.c_uint32 * 2)(0, 1)), INVALID),
         (dict(load_hint=3), INVALID),
         (dict(store_hint=3), INVALID),
@@ -152,6 +153,7 @@ def test_destroy_null_is_a_noop():
 
 def test_info_and_tables_reject_null():
     L = PL.lib()
+    assert L.purlin_plan_device_error(None, None) == INVALID
     assert L.purlin_plan_info(None, None, None, None, None) == INVALID
     assert L.purlin_plan_descriptors(None, None, None, None) == INVALID
     assert L.purlin_plan_items(None, None, None, None) == INVALID

@@ -241,3 +241,69 @@ def test_config3_reduce_scatter_then_all_gather_full_size():
     assert_bits_equal(got_ar, want, "bf16", "config 3 AR sample")
     rs_host = np.concatenate([to_host(t, np.uint16) for t in rs_out])
     assert_bits_equal(rs_host[idx], want, "bf16", "config 3 RS sample")
+
+
+# ---------------------------------------------------------------------------
+# single-launch AllReduce (ar_mode 3): per-chunk counters with epochs
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("P,M", [(2, 16), (3, 1001), (8, 8200), (16, 520)])
+def test_fused_allreduce_matches_oracle(dtype, P, M):
+    s = S[dtype]
+    ins = _inputs(P, P * M, dtype, seed=900 + P)
+    want = oracle.all_reduce(ins, dtype)
+    for chunk in (s * 64, 4096, 1 << 20):
+        for pol in (dict(ar_mode=3), dict(ar_mode=3, fanout=1, item_bytes=256)):
+            plan = PL.Plan("allreduce", P, P * M, dtype, chunk, policy=pol)
+            for rep in range(3):  # the epoch advances on every launch
+                got = run_plan(plan, ins, dtype)
+                for r in range(P):
+                    assert_bits_equal(got[r], want[r], dtype, f"fused P={P} M={M} chunk={chunk} {pol} rep={rep}")
+            assert plan.device_error() == 0
+
+
+def test_fused_allreduce_graph_replays():
+    P, M = 8, 1 << 14
+    ins_np = _inputs(P, P * M, "bf16", seed=12)
+    want = oracle.all_reduce(ins_np, "bf16")
+    plan = PL.Plan("allreduce", P, P * M, "bf16", 65536, policy=dict(ar_mode=3))
+    ins = [to_device(a) for a in ins_np]
+    outs = [torch.empty(P * M, dtype=torch.int16, device="cuda") for _ in range(P)]
+    plan.exec(ins, outs)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            for _ in range(4):
+                plan.exec(ins, outs, stream=side)
+    for _ in range(3):
+        for o in outs:
+            o.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for r in range(P):
+            assert_bits_equal(to_host(outs[r], np.uint16), want[r], "bf16", "fused AR graph replay")
+    assert plan.device_error() == 0
+
+
+def test_fused_allreduce_full_size_equals_two_launches():
+    cfg = W.COLLECTIVE_CONFIGS[3]
+    P, N = cfg.P, cfg.count
+    ins = [to_device(a) for a in W.collective_inputs(cfg)]
+    fused = PL.Plan("allreduce", P, N, "bf16", cfg.chunk, policy=dict(ar_mode=3))
+    two = PL.Plan("allreduce", P, N, "bf16", cfg.chunk, policy=dict(ar_mode=1))
+    a = [torch.empty(N, dtype=torch.int16, device="cuda") for _ in range(P)]
+    fused.exec(ins, a)
+    fused.exec(ins, a)
+    torch.cuda.synchronize()
+    b = [torch.empty(N, dtype=torch.int16, device="cuda") for _ in range(P)]
+    two.exec(ins, b)
+    torch.cuda.synchronize()
+    for r in range(P):
+        assert torch.equal(a[r], b[r])
+    assert fused.device_error() == 0

@@ -305,3 +305,52 @@ def test_rooted_tables_touch_only_used_buffers(op):
 
 def host_plan_rooted(op, P, count, dtype, chunk, root, **policy):
     return PL.Plan(op, P, count, dtype, chunk, policy=policy or None, host_only=True, root=root)
+
+
+# ---------------------------------------------------------------------------
+# single-launch AllReduce (ar_mode 3): the claim order is a valid schedule
+# ---------------------------------------------------------------------------
+
+FUSED_CASES = [(P, M, dt, ce, it) for P in (2, 3, 8, 16) for M in (16, 1000, 4099)
+               for dt in ("fp32", "bf16") for ce in (1, 100, 4096) for it in (0, 32)]
+
+
+@pytest.mark.parametrize("case", FUSED_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_fused_allreduce_claim_order(case):
+    """Waves claim items in table order.  Every copy item must find all
+    reduce items of its chunk already claimed (they never wait), the number
+    of reduce items per chunk must be what the kernel computes from
+    (partBytes, chunk, item size), and running the items in claim order
+    must reproduce the oracle."""
+    P, M, dtype, chunk_elems, item = case
+    s = S[dtype]
+    chunk = chunk_elems * s
+    plan = host_plan("allreduce", P, P * M, dtype, chunk, ar_mode=3, fanout=2, item_bytes=item)
+    items, pb = plan.items()
+    part = M * s
+    reduce_item = int(items["bytes"][: pb[1]].max())  # the reduce items' cut size (the last of a chunk may be shorter)
+    if item:
+        assert reduce_item <= item
+    claimed = {}
+    for i, it in enumerate(items):
+        key = (int(it["part"]), int(it["chunk"]))
+        if it["kind"] == PL.KIND_REDUCE:
+            assert i < pb[1]
+            claimed[key] = claimed.get(key, 0) + 1
+        else:
+            assert i >= pb[1]
+            off = int(it["chunk"]) * chunk
+            length = min(chunk, part - off)
+            cut = item if item else None
+            if cut:
+                assert claimed.get(key, 0) == -(-length // cut), "copy claimed before its chunk's reductions"
+            else:
+                assert claimed.get(key, 0) >= 1
+    ins = _inputs(P, P * M, dtype, seed=P + M)
+    want = oracle.all_reduce(ins, dtype)
+    bufs = [np.frombuffer(a.tobytes(), np.uint8).copy() for a in ins] + [np.zeros(plan.out_bytes, np.uint8) for _ in range(P)]
+    for it in items:  # claim order
+        interp.apply_item(it, bufs, dtype)
+    for r in range(P):
+        got = bufs[P + r].view(np.uint16 if dtype == "bf16" else np.uint32)
+        assert np.array_equal(got, want[r].view(got.dtype))
