@@ -14,6 +14,7 @@ Contents
                  (Section 2.1 "Stable communication semantics"; layouts of
                  Section 3.1; rank-order reduction of Eq. 2, Section 3.3).
 ``rooted``       Broadcast, Scatter, Gather, Reduce (Appendix A).
+``vcollectives`` AllGatherV, ReduceScatterV, AllToAllV (sizes at run time).
 ``moe``          MoE dispatch ``pack`` and combine ``unpack`` (the paper names
                  them only as the expert-parallel use of AllToAll, Table 2;
                  their contract is written out in ``moe``'s docstrings).
@@ -32,6 +33,7 @@ from .bf16 import narrow, widen
 from .collectives import all_gather, all_reduce, all_to_all, reduce_scatter
 from .moe import pack, unpack
 from .rooted import broadcast, gather, reduce, scatter
+from .vcollectives import all_gather_v, all_to_all_v, reduce_scatter_v
 
 __all__ = [
     "narrow",
@@ -46,4 +48,7 @@ __all__ = [
     "gather",
     "reduce",
     "scatter",
+    "all_gather_v",
+    "all_to_all_v",
+    "reduce_scatter_v",
 ]

@@ -172,3 +172,37 @@ def moe_expert_outputs(cfg=MOE_CONFIG, rows=None, H=None):
     H = cfg.H if H is None else H
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(cfg.seed_y)))
     return normal_bf16(rng, rows * H).reshape(rows, H)
+
+
+def zipf_split(total_bytes, W=8, s=0.125, min_unit=128):
+    """Partition sizes in bytes for the variable-size collectives (Eq. 4,
+    Appendix C.4 of the paper): units of u = max(min_unit, T / (8 W)) bytes,
+    rank r gets floor(x_r) units with x_r = (T/u) (r+1)^-s / sum_k (k+1)^-s,
+    and the leftover units go, one each, to the largest fractional parts of
+    x_r, ties to the lower rank.  Exact for the power-of-two totals the paper
+    uses (T a multiple of u)."""
+    u = max(min_unit, total_bytes // (8 * W))
+    units = total_bytes // u
+    w = [(r + 1) ** (-s) for r in range(W)]
+    tot = sum(w)
+    x = [units * wr / tot for wr in w]
+    base = [int(xr // 1) for xr in x]
+    left = units - sum(base)
+    order = sorted(range(W), key=lambda r: (-(x[r] - base[r]), r))
+    for r in order[:left]:
+        base[r] += 1
+    return [u * b for b in base]
+
+
+def rotate_right(v, k):
+    """v rotated right by k positions: out[i] = v[(i - k) mod len(v)]."""
+    n = len(v)
+    return [v[(i - k) % n] for i in range(n)]
+
+
+def alltoallv_counts(split):
+    """AllToAllV sizes of Appendix C.4: rank p sends its split rotated right by
+    (p + 1) mod W positions, so every rank sends and receives the total.
+    Returns counts[p][r] = what rank p sends to rank r."""
+    W = len(split)
+    return [rotate_right(split, (p + 1) % W) for p in range(W)]

@@ -160,3 +160,33 @@ def reduce(ins, root, dtype):
     out = [None] * len(ins)
     out[root] = rank_order_reduce([list(a) for a in ins], dtype)
     return out
+
+
+def all_gather_v(ins, counts):
+    out = []
+    for p in range(len(ins)):
+        for i in range(counts[p]):
+            out.append(ins[p][i])
+    return [list(out) for _ in ins]
+
+
+def reduce_scatter_v(ins, counts, dtype):
+    outs = []
+    off = 0
+    for r in range(len(ins)):
+        cols = [list(a[off:off + counts[r]]) for a in ins]
+        outs.append(rank_order_reduce(cols, dtype) if counts[r] else [])
+        off += counts[r]
+    return outs
+
+
+def all_to_all_v(ins, counts):
+    P = len(ins)
+    outs = []
+    for r in range(P):
+        o = []
+        for p in range(P):
+            start = sum(counts[p][:r])
+            o.extend(ins[p][start:start + counts[p][r]])
+        outs.append(o)
+    return outs
