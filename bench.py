@@ -347,8 +347,9 @@ def main():
 
 
 def measure_extra_ops(torch, PL, ins, rs_out, ag_out, P, N, s, reps=5):
-    """AllReduce, AllToAll and the rooted collectives at 256 MiB/rank, P=8,
-    bf16, chunk 1 MiB: event-timed on the current stream, outside the step."""
+    """AllReduce, AllToAll, the rooted and the variable-size collectives at
+    256 MiB/rank, P=8, bf16, chunk 1 MiB: event-timed on the current stream,
+    outside the step."""
     root = 0
     cases = [
         ("allreduce", PL.Plan("allreduce", P, N, "bf16", 1 << 20), ins, ag_out, 2 * P * N * s),
@@ -362,14 +363,35 @@ def measure_extra_ops(torch, PL, ins, rs_out, ag_out, P, N, s, reps=5):
         ("gather", PL.Plan("gather", P, N, "bf16", 1 << 20, root=root), rs_out,
          [ag_out[root]] + [None] * (P - 1), 2 * N * s),
     ]
+    # variable-size collectives with the Appendix C.4 split of T = 256 MiB per rank
+    from paper_2609_36954_amd import workloads as W
+
+    split = [b // s for b in W.zipf_split(N * s)]
+    dev_split = torch.tensor(split, dtype=torch.int32, device="cuda")
+    dev_a2av = torch.tensor([x for row in W.alltoallv_counts(split) for x in row], dtype=torch.int32, device="cuda")
+    vcases = [
+        ("allgatherv_zipf", PL.Plan("allgatherv", P, N, "bf16", 1 << 20, unit=1), ins, ag_out, dev_split,
+         (P + 1) * N * s),
+        ("reduce_scatterv_zipf", PL.Plan("reduce_scatterv", P, N, "bf16", 1 << 20, unit=1), ins, ag_out, dev_split,
+         (P + 1) * N * s),
+        ("alltoallv_zipf", PL.Plan("alltoallv", P, N, "bf16", 1 << 20, unit=1), ins, ag_out, dev_a2av,
+         2 * P * N * s),
+    ]
     out = {}
+    for name, plan, i, o, counts, bmin in vcases:
+        cases.append((name, plan, i, o, bmin))
+        plan._bench_counts = counts
     for name, plan, i, o, bmin in cases:
-        plan.exec(i, o)
+        if plan.unit is not None:
+            run = (lambda plan=plan, i=i, o=o: plan.exec_v(i, o, plan._bench_counts))
+        else:
+            run = (lambda plan=plan, i=i, o=o: plan.exec(i, o))
+        run()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for _ in range(reps):
-            plan.exec(i, o)
+            run()
         e1.record()
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) * 1e3 / reps

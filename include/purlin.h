@@ -73,7 +73,12 @@ typedef enum purlin_op {
     PURLIN_BROADCAST = 4,
     PURLIN_REDUCE = 5,
     PURLIN_SCATTER = 6,
-    PURLIN_GATHER = 7
+    PURLIN_GATHER = 7,
+    /* Variable-size collectives (Section 3.1: the V layouts take partition
+     * sizes at run time), planned with purlin_plan_v, run with purlin_exec_v */
+    PURLIN_ALLGATHERV = 8,      /* copy,   packedV    -> scatteredV  */
+    PURLIN_REDUCE_SCATTERV = 9, /* reduce, scatteredV -> packedV     */
+    PURLIN_ALLTOALLV = 10       /* copy,   scatteredV -> transposedV */
 } purlin_op;
 
 typedef enum purlin_dtype { PURLIN_FP32 = 0, PURLIN_BF16 = 1 } purlin_dtype;
@@ -180,6 +185,36 @@ PURLIN_API purlin_status purlin_plan(purlin_op op, int P, uint64_t count, purlin
 PURLIN_API purlin_status purlin_plan_rooted(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype,
                                             uint64_t chunk_bytes, const purlin_policy* policy, uint32_t flags,
                                             purlin_plan_t* out_plan);
+
+/* A variable-size collective over P ranks whose buffers each hold
+ * `capacity` elements (in and out).  The sizes are not part of the plan:
+ * purlin_exec_v reads them from device memory at run time, so they may be
+ * produced by an earlier kernel on the stream (e.g. purlin_pack's
+ * dest_counts) and the call can be captured in a graph.  Counts are in units
+ * of `unit` elements (1 <= unit <= 2^31).  `chunk_bytes` cuts the virtual
+ * index space into chunks, as for the fixed-size plans.  Policy, flags and
+ * errors as for purlin_plan_ex; PURLIN_ERR_INVALID also for a non-V op or a
+ * bad unit.  `capacity` need not be a multiple of P. */
+PURLIN_API purlin_status purlin_plan_v(purlin_op op, int P, uint64_t capacity, purlin_dtype dtype,
+                                       uint64_t chunk_bytes, uint64_t unit, const purlin_policy* policy,
+                                       uint32_t flags, purlin_plan_t* out_plan);
+
+/* Run a variable-size plan.  `counts` is device memory (int32):
+ *   ALLGATHERV      counts[p], p < P: elements rank p contributes; every
+ *                   out_r receives them in rank order,
+ *                   out_r[off_p + i] = in_p[i], off_p = sum(counts[0..p)).
+ *   REDUCE_SCATTERV counts[r]: partition sizes of every input; out_r[i] =
+ *                   rank-order sum (Eq. 2) of in_p[off_r + i], i < counts[r].
+ *   ALLTOALLV       counts[p*P + r]: elements rank p sends to rank r; in_p
+ *                   holds them in destination order, out_r receives them in
+ *                   source order.
+ * Each count (times unit) must be >= 0 and every input and output total
+ * must fit the capacity; otherwise the call writes nothing and, if
+ * `dev_status` (device int32, optional) is given, sets it to 1 (else 0).
+ * Host-side errors as for purlin_exec, plus PURLIN_ERR_INVALID for a
+ * non-V plan or NULL counts.  purlin_exec rejects V plans. */
+PURLIN_API purlin_status purlin_exec_v(purlin_plan_t plan, void* const* bufs, const int32_t* counts,
+                                       int32_t* dev_status, void* stream);
 
 /* purlin_plan with an explicit policy (NULL = automatic) and flags
  * (0 or PURLIN_PLAN_HOST_ONLY).  PURLIN_ERR_INVALID also for a policy with

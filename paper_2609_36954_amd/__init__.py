@@ -16,10 +16,12 @@ from .purlin import (  # noqa: F401
     PurlinError,
     lib,
     purlin_exec,
+    purlin_exec_v,
     purlin_pack,
     purlin_pack_workspace_size,
     purlin_plan,
     purlin_plan_rooted,
+    purlin_plan_v,
     purlin_status_string,
     purlin_unpack,
     purlin_version,

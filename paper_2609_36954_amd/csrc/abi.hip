@@ -29,14 +29,15 @@ size_t fused_state_bytes(const purlin::Plan& p) {
 }
 
 purlin_status make_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,
-                        const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan) {
+                        const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan, uint64_t v_unit = 0) {
     if (!out_plan) return PURLIN_ERR_INVALID;
     *out_plan = nullptr;
     purlin_plan_s* h = new (std::nothrow) purlin_plan_s;
     if (!h) return PURLIN_ERR_NOMEM;
     purlin_status st;
     try {
-        st = purlin::build_plan(op, P, root, count, dtype, chunk, policy, flags, h->plan);
+        st = v_unit ? purlin::build_plan_v(op, P, count, dtype, chunk, v_unit, policy, flags, h->plan)
+                    : purlin::build_plan(op, P, root, count, dtype, chunk, policy, flags, h->plan);
     } catch (...) {
         st = PURLIN_ERR_NOMEM;
     }
@@ -82,6 +83,26 @@ bool pack_limits_ok(int T, int H, int K, int E) {
     return static_cast<int64_t>(T) * K < (int64_t(1) << 31) && purlin::moe_launch_fits(T, H);
 }
 
+// Host-side checks shared by purlin_exec and purlin_exec_v: non-null,
+// aligned, no input/output or output/output overlap among used buffers.
+purlin_status check_buffers(const purlin::Plan& p, void* const* bufs) {
+    if (p.flags & PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
+    if (!bufs) return PURLIN_ERR_INVALID;
+    const int P = p.P;
+    auto used = [&](int i) { return i < P ? ((p.in_mask >> i) & 1u) : ((p.out_mask >> (i - P)) & 1u); };
+    for (int i = 0; i < 2 * P; ++i)
+        if (used(i) && (!bufs[i] || !aligned16(bufs[i]))) return PURLIN_ERR_INVALID;
+    for (int i = 0; i < P; ++i)
+        for (int r = 0; r < P; ++r)
+            if (used(i) && used(P + r) && overlaps(bufs[i], p.in_bytes, bufs[P + r], p.out_bytes))
+                return PURLIN_ERR_INVALID;
+    for (int r = 0; r < P; ++r)
+        for (int q = r + 1; q < P; ++q)
+            if (used(P + r) && used(P + q) && overlaps(bufs[P + r], p.out_bytes, bufs[P + q], p.out_bytes))
+                return PURLIN_ERR_INVALID;
+    return PURLIN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -104,6 +125,15 @@ purlin_status purlin_plan_rooted(purlin_op op, int P, int root, uint64_t count, 
         return PURLIN_ERR_INVALID;
     }
     return make_plan(op, P, root, count, dtype, chunk_bytes, policy, flags, out_plan);
+}
+
+purlin_status purlin_plan_v(purlin_op op, int P, uint64_t capacity, purlin_dtype dtype, uint64_t chunk_bytes,
+                            uint64_t unit, const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan) {
+    if (unit == 0) {
+        if (out_plan) *out_plan = nullptr;
+        return PURLIN_ERR_INVALID;
+    }
+    return make_plan(op, P, -1, capacity, dtype, chunk_bytes, policy, flags, out_plan, unit);
 }
 
 purlin_status purlin_plan_info(purlin_plan_t plan, uint64_t* n_desc, uint64_t* in_bytes_per_rank,
@@ -139,24 +169,30 @@ purlin_status purlin_plan_items(purlin_plan_t plan, const purlin_desc** items, u
     return PURLIN_OK;
 }
 
+purlin_status purlin_exec_v(purlin_plan_t plan, void* const* bufs, const int32_t* counts, int32_t* dev_status,
+                            void* stream) {
+    if (!plan) return PURLIN_ERR_INVALID;
+    const purlin::Plan& p = plan->plan;
+    if (!p.vop) return PURLIN_ERR_INVALID;
+    if (p.items.empty()) return PURLIN_OK;
+    if (!counts || (reinterpret_cast<uintptr_t>(counts) & 3u)) return PURLIN_ERR_INVALID;
+    if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    const purlin_status st = check_buffers(p, bufs);
+    if (st != PURLIN_OK) return st;
+    const purlin::Phase& ph = p.phases[0];
+    const hipError_t e = purlin::launch_v(p.op, p.d_items, ph.count, p.P, p.dtype, ph.nt_load || ph.nt_store, bufs,
+                                          counts, dev_status, p.capacity, p.unit, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
 purlin_status purlin_exec(purlin_plan_t plan, void* const* bufs, void* stream) {
     if (!plan) return PURLIN_ERR_INVALID;
     const purlin::Plan& p = plan->plan;
+    if (p.vop) return PURLIN_ERR_INVALID;  // sizes come with purlin_exec_v
     if (p.count == 0) return PURLIN_OK;
-    if (p.flags & PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
-    if (!bufs) return PURLIN_ERR_INVALID;
+    const purlin_status st = check_buffers(p, bufs);
+    if (st != PURLIN_OK) return st;
     const int P = p.P;
-    auto used = [&](int i) { return i < P ? ((p.in_mask >> i) & 1u) : ((p.out_mask >> (i - P)) & 1u); };
-    for (int i = 0; i < 2 * P; ++i)
-        if (used(i) && (!bufs[i] || !aligned16(bufs[i]))) return PURLIN_ERR_INVALID;
-    for (int i = 0; i < P; ++i)
-        for (int r = 0; r < P; ++r)
-            if (used(i) && used(P + r) && overlaps(bufs[i], p.in_bytes, bufs[P + r], p.out_bytes))
-                return PURLIN_ERR_INVALID;
-    for (int r = 0; r < P; ++r)
-        for (int q = r + 1; q < P; ++q)
-            if (used(P + r) && used(P + q) && overlaps(bufs[P + r], p.out_bytes, bufs[P + q], p.out_bytes))
-                return PURLIN_ERR_INVALID;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (p.fused) {

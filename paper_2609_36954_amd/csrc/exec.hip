@@ -355,6 +355,173 @@ void launch_copy(dim3 grid, hipStream_t stream, const ExecArgs& a, bool ntl, boo
         hipLaunchKernelGGL((exec_copy<U, false, false>), grid, dim3(kBlock), 0, stream, a);
 }
 
+// ---------------------------------------------------------------------------
+// Variable-size collectives (the V layouts of Section 3.1): partition sizes
+// are read from device memory at run time.  The work items cover a fixed
+// virtual index space sized by the plan's capacity; each wave maps its range
+// onto (source, destination, offset) from prefix sums over at most 16
+// counts (P x P for AllToAllV), which every wave forms in registers.  Sizes
+// that are negative or exceed the capacity make every wave skip the call
+// (all waves reach the same verdict); wave 0 reports it.
+// ---------------------------------------------------------------------------
+struct VArgs {
+    const int32_t* counts;  // P (AllGatherV, ReduceScatterV) or P*P row-major (AllToAllV)
+    int32_t* status;        // optional: 0, or 1 for invalid sizes
+    uint64_t capacity;      // elements every buffer holds
+    uint64_t unit;          // elements per count
+    uint32_t P;
+    uint32_t elem_bytes;
+};
+
+__device__ __forceinline__ int64_t readlane64(int64_t v, int lane) {
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(v), lane);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(static_cast<uint64_t>(v) >> 32), lane);
+    return static_cast<int64_t>((uint64_t(hi) << 32) | lo);
+}
+
+// Lane p < P holds count p (elements); returns whether every count is >= 0
+// and their sum fits the capacity.
+__device__ __forceinline__ bool load_counts(const VArgs& v, uint32_t lane, int64_t& c) {
+    c = 0;
+    if (lane < v.P) c = static_cast<int64_t>(v.counts[lane]) * static_cast<int64_t>(v.unit);
+    const int64_t cap = static_cast<int64_t>(v.capacity);
+    bool ok = true;
+    int64_t total = 0;  // each term is checked against the capacity first, so this cannot overflow
+    for (uint32_t p = 0; p < v.P; ++p) {
+        const int64_t cp = readlane64(c, p);
+        const bool fits = cp >= 0 && cp <= cap;
+        ok = ok && fits;
+        total += fits ? cp : 0;
+    }
+    return ok && total <= cap;
+}
+
+__device__ __forceinline__ void report(const VArgs& v, uint32_t w, uint32_t lane, bool ok) {
+    if (w == 0 && lane == 0 && v.status) *v.status = ok ? 0 : 1;
+}
+
+template <bool STREAM>
+__global__ __launch_bounds__(kBlock) void exec_allgatherv(ExecArgs a, VArgs v) {
+    const uint32_t w = wave_index();
+    if (w >= a.n_items) return;
+    const uint32_t lane = lane_index();
+    int64_t c;
+    const bool ok = load_counts(v, lane, c);
+    report(v, w, lane, ok);
+    if (!ok) return;
+    const purlin_desc d = a.items[w];
+    const uint64_t s = v.elem_bytes;
+    const int64_t lo_v = static_cast<int64_t>(d.src_off / s), hi_v = lo_v + static_cast<int64_t>(d.bytes / s);
+    int64_t off = 0;
+    for (uint32_t p = 0; p < v.P; ++p) {
+        const int64_t cp = readlane64(c, p);
+        const int64_t x = max(lo_v, off), y = min(hi_v, off + cp);
+        if (x < y) {
+            purlin_desc sub = d;
+            sub.src_buf = p;
+            sub.ndst = v.P;
+            sub.dst_buf = v.P;
+            sub.dst_step = 1;
+            sub.src_off = uint64_t(x - off) * s;
+            sub.dst_off = uint64_t(x) * s;
+            sub.bytes = uint64_t(y - x) * s;
+            run_copy<kCopyUnroll, false, STREAM>(a, sub, lane);
+        }
+        off += cp;
+    }
+}
+
+template <int NSRC, bool BF16, bool STREAM>
+__global__ __launch_bounds__(kBlock) void exec_reducescatterv(ExecArgs a, VArgs v) {
+    const uint32_t w = wave_index();
+    if (w >= a.n_items) return;
+    const uint32_t lane = lane_index();
+    int64_t c;
+    const bool ok = load_counts(v, lane, c);
+    report(v, w, lane, ok);
+    if (!ok) return;
+    const purlin_desc d = a.items[w];
+    const uint64_t s = v.elem_bytes;
+    const int64_t lo_v = static_cast<int64_t>(d.src_off / s), hi_v = lo_v + static_cast<int64_t>(d.bytes / s);
+    int64_t off = 0;
+    for (uint32_t r = 0; r < v.P; ++r) {
+        const int64_t cr = readlane64(c, r);
+        const int64_t x = max(lo_v, off), y = min(hi_v, off + cr);
+        if (x < y) {
+            purlin_desc sub = d;
+            sub.ndst = 1;
+            sub.dst_buf = v.P + r;
+            sub.dst_step = 0;
+            sub.src_off = uint64_t(x) * s;
+            sub.dst_off = uint64_t(x - off) * s;
+            sub.bytes = uint64_t(y - x) * s;
+            run_reduce<NSRC, BF16, reduce_unroll(NSRC), STREAM, false>(a, sub, lane);
+        }
+        off += cr;
+    }
+}
+
+// AllToAllV: item d covers bytes [src_off, src_off + bytes) of destination
+// d.part's output.  counts[p * P + r] = elements rank p sends to rank r.
+template <bool STREAM>
+__global__ __launch_bounds__(kBlock) void exec_alltoallv(ExecArgs a, VArgs v) {
+    const uint32_t w = wave_index();
+    if (w >= a.n_items) return;
+    const uint32_t lane = lane_index();
+    const purlin_desc d = a.items[w];
+    const uint32_t r = d.part;
+    const int64_t unit = static_cast<int64_t>(v.unit);
+    // lane p: its row's total (send size), the offset of partition r in it,
+    // and the size of partition r
+    const int64_t cap = static_cast<int64_t>(v.capacity);
+    int64_t row_total = 0, send_off = 0, c = 0;
+    bool ok = true;
+    if (lane < v.P) {
+        for (uint32_t q = 0; q < v.P; ++q) {
+            int64_t x = static_cast<int64_t>(v.counts[uint64_t(lane) * v.P + q]) * unit;
+            if (x < 0 || x > cap) {  // checked before any sum, so sums cannot overflow
+                ok = false;
+                x = 0;
+            }
+            if (q < r) send_off += x;
+            if (q == r) c = x;
+            row_total += x;
+        }
+        ok = ok && row_total <= cap;
+    }
+    // every column (receive size) must fit too; all waves check all columns
+    for (uint32_t q = 0; q < v.P; ++q) {
+        int64_t x = 0;
+        if (lane < v.P) x = static_cast<int64_t>(v.counts[uint64_t(lane) * v.P + q]) * unit;
+        if (x < 0 || x > cap) x = 0;  // already reported through ok
+        int64_t col = 0;
+        for (uint32_t p = 0; p < v.P; ++p) col += readlane64(x, p);
+        ok = ok && col <= cap;
+    }
+    const bool all_ok = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(__all(ok)));
+    report(v, w, lane, all_ok);
+    if (!all_ok) return;
+    const uint64_t s = v.elem_bytes;
+    const int64_t lo_v = static_cast<int64_t>(d.src_off / s), hi_v = lo_v + static_cast<int64_t>(d.bytes / s);
+    int64_t recv = 0;
+    for (uint32_t p = 0; p < v.P; ++p) {
+        const int64_t cp = readlane64(c, p), sp = readlane64(send_off, p);
+        const int64_t x = max(lo_v, recv), y = min(hi_v, recv + cp);
+        if (x < y) {
+            purlin_desc sub = d;
+            sub.src_buf = p;
+            sub.ndst = 1;
+            sub.dst_buf = v.P + r;
+            sub.dst_step = 0;
+            sub.src_off = uint64_t(sp + (x - recv)) * s;
+            sub.dst_off = uint64_t(x) * s;
+            sub.bytes = uint64_t(y - x) * s;
+            run_copy<kCopyUnroll, STREAM, STREAM>(a, sub, lane);
+        }
+        recv += cp;
+    }
+}
+
 template <int NSRC>
 void launch_fused_n(dim3 grid, hipStream_t stream, const ExecArgs& a, const FusedArgs& f, bool bf16, bool stream_hint) {
     if (bf16) {
@@ -396,6 +563,55 @@ hipError_t launch_fused_allreduce(const purlin_desc* items, uint64_t n, uint64_t
         PURLIN_FUSED_CASE(13) PURLIN_FUSED_CASE(14) PURLIN_FUSED_CASE(15) PURLIN_FUSED_CASE(16)
 #undef PURLIN_FUSED_CASE
         default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_v(purlin_op op, const purlin_desc* items, uint64_t n, int P, purlin_dtype dtype, bool streaming,
+                    void* const* bufs, const int32_t* counts, int32_t* status, uint64_t capacity, uint64_t unit,
+                    hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    ExecArgs a{};
+    a.items = items;
+    a.n_items = n;
+    for (int i = 0; i < 2 * P && i < 2 * PURLIN_MAX_RANKS; ++i) a.bufs[i] = static_cast<char*>(bufs[i]);
+    for (int p = 0; p < P && p < PURLIN_MAX_RANKS; ++p) a.srcs[p] = static_cast<char*>(bufs[p]);
+    VArgs v{counts, status, capacity, unit, static_cast<uint32_t>(P), dtype == PURLIN_FP32 ? 4u : 2u};
+    const dim3 grid(static_cast<uint32_t>((n + kWavesPerBlock - 1) / kWavesPerBlock));
+    const bool bf16 = dtype == PURLIN_BF16;
+    (void)hipGetLastError();
+    if (op == PURLIN_ALLGATHERV) {
+        if (streaming)
+            hipLaunchKernelGGL((exec_allgatherv<true>), grid, dim3(kBlock), 0, stream, a, v);
+        else
+            hipLaunchKernelGGL((exec_allgatherv<false>), grid, dim3(kBlock), 0, stream, a, v);
+    } else if (op == PURLIN_ALLTOALLV) {
+        if (streaming)
+            hipLaunchKernelGGL((exec_alltoallv<true>), grid, dim3(kBlock), 0, stream, a, v);
+        else
+            hipLaunchKernelGGL((exec_alltoallv<false>), grid, dim3(kBlock), 0, stream, a, v);
+    } else if (op == PURLIN_REDUCE_SCATTERV) {
+        switch (P) {
+#define PURLIN_RSV_CASE(k)                                                                                      \
+    case k:                                                                                                     \
+        if (bf16 && streaming)                                                                                  \
+            hipLaunchKernelGGL((exec_reducescatterv<k, true, true>), grid, dim3(kBlock), 0, stream, a, v);     \
+        else if (bf16)                                                                                          \
+            hipLaunchKernelGGL((exec_reducescatterv<k, true, false>), grid, dim3(kBlock), 0, stream, a, v);    \
+        else if (streaming)                                                                                     \
+            hipLaunchKernelGGL((exec_reducescatterv<k, false, true>), grid, dim3(kBlock), 0, stream, a, v);    \
+        else                                                                                                    \
+            hipLaunchKernelGGL((exec_reducescatterv<k, false, false>), grid, dim3(kBlock), 0, stream, a, v);   \
+        break;
+            PURLIN_RSV_CASE(1) PURLIN_RSV_CASE(2) PURLIN_RSV_CASE(3) PURLIN_RSV_CASE(4)
+            PURLIN_RSV_CASE(5) PURLIN_RSV_CASE(6) PURLIN_RSV_CASE(7) PURLIN_RSV_CASE(8)
+            PURLIN_RSV_CASE(9) PURLIN_RSV_CASE(10) PURLIN_RSV_CASE(11) PURLIN_RSV_CASE(12)
+            PURLIN_RSV_CASE(13) PURLIN_RSV_CASE(14) PURLIN_RSV_CASE(15) PURLIN_RSV_CASE(16)
+#undef PURLIN_RSV_CASE
+            default: return hipErrorInvalidValue;
+        }
+    } else {
+        return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }

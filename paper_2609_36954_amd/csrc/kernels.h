@@ -34,6 +34,13 @@ hipError_t launch_fused_allreduce(const purlin_desc* items, uint64_t n, uint64_t
                                   uint64_t* ready, uint64_t part_bytes, uint64_t chunk_bytes, uint64_t item_bytes,
                                   uint64_t chunks_per_part, hipStream_t stream);
 
+// Variable-size collectives: one launch; sizes read from device `counts`
+// (int32, in units of `unit` elements).  `status` (optional) receives 0 or
+// 1 (invalid sizes: the call then writes nothing).
+hipError_t launch_v(purlin_op op, const purlin_desc* items, uint64_t n, int P, purlin_dtype dtype, bool streaming,
+                    void* const* bufs, const int32_t* counts, int32_t* status, uint64_t capacity, uint64_t unit,
+                    hipStream_t stream);
+
 struct PackWorkspace {
     int32_t* tile_base;  // [ntiles * E]: per-tile expert counts, then row bases
     int32_t* lrank;      // [T * K]: rank of (t, k) among its tile's tokens of the same expert

@@ -87,6 +87,23 @@ uint64_t auto_item_bytes(uint64_t phase_bytes, uint64_t traffic, uint32_t kind, 
     return item;
 }
 
+bool parse_policy(const purlin_policy* policy, purlin_policy& pol) {
+    pol = purlin_policy{};
+    if (!policy) return true;
+    pol = *policy;
+    if (pol.item_bytes % 16 != 0) return false;
+    if (pol.fanout > 2 || pol.ar_mode > 3) return false;
+    if (pol.load_hint > 2 || pol.store_hint > 2) return false;
+    for (uint32_t r : pol.reserved)
+        if (r != 0) return false;
+    return true;
+}
+
+// Cuts out.descs into work items phase by phase, records the launches and
+// resolves the cache hints.  Returns PURLIN_ERR_NOMEM past PURLIN_MAX_ITEMS
+// or PURLIN_ERR_UNSUPPORTED if a phase mixes consume ops or source sets.
+purlin_status cut_items(Plan& out, const purlin_policy& pol);
+
 }  // namespace
 
 purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,
@@ -103,14 +120,7 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
     if (count > (uint64_t(1) << 58) / s) return PURLIN_ERR_INVALID;
 
     purlin_policy pol{};
-    if (policy) {
-        pol = *policy;
-        if (pol.item_bytes % 16 != 0) return PURLIN_ERR_INVALID;
-        if (pol.fanout > 2 || pol.ar_mode > 3) return PURLIN_ERR_INVALID;
-        if (pol.load_hint > 2 || pol.store_hint > 2) return PURLIN_ERR_INVALID;
-        for (uint32_t r : pol.reserved)
-            if (r != 0) return PURLIN_ERR_INVALID;
-    }
+    if (!parse_policy(policy, pol)) return PURLIN_ERR_INVALID;
     const uint64_t M = count / P;       // elements per partition
     const uint64_t part = M * s;        // partBytes
     const uint64_t Cp = part ? ceil_div(part, chunk) : 0;
@@ -159,6 +169,8 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
             out.in_bytes = part;
             out.out_bytes = count * s;
             break;
+        default:
+            return PURLIN_ERR_INVALID;  // variable-size ops go through build_plan_v
     }
     if (op == PURLIN_BROADCAST || op == PURLIN_SCATTER) out.in_mask = root_bit;
     if (op == PURLIN_REDUCE || op == PURLIN_GATHER) out.out_mask = root_bit;
@@ -274,94 +286,169 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
                         });
                 }
                 break;
+            default:
+                return PURLIN_ERR_INVALID;
         }
         out.policy = pol;
         out.part_bytes = part;
         out.chunks_per_part = Cp;
         out.fused = op == PURLIN_ALLREDUCE && pol.ar_mode == 3 && P > 1;
 
-        for (const purlin_desc& d : D) out.sched_bytes += (uint64_t(d.nsrc) + d.ndst) * d.bytes;
+        const purlin_status st = cut_items(out, pol);
+        if (st != PURLIN_OK) return st;
+    } catch (const std::bad_alloc&) {
+        out.descs.clear();
+        out.items.clear();
+        return PURLIN_ERR_NOMEM;
+    }
+    return PURLIN_OK;
+}
 
-        // Per-phase shape: bytes of the descriptors, bytes moved, fan-in/out.
-        struct PhaseShape {
-            uint64_t bytes = 0, traffic = 0, ndesc = 0;
-            uint32_t kind = 0, nsrc = 0, ndst = 0;
-            uint64_t item = 0;
-        } shape[2];
-        for (const purlin_desc& d : D) {
-            PhaseShape& sh = shape[d.phase];
-            sh.bytes += d.bytes;
-            sh.traffic += (uint64_t(d.nsrc) + d.ndst) * d.bytes;
-            sh.kind = d.kind;
-            sh.nsrc = std::max(sh.nsrc, d.nsrc);
-            sh.ndst = std::max(sh.ndst, d.ndst);
-            ++sh.ndesc;
-        }
-        // Cut descriptors into work items, phase by phase.
-        uint64_t items_total = 0;
-        for (uint32_t ph = 0; ph < 2; ++ph) {
-            PhaseShape& sh = shape[ph];
-            if (sh.ndesc == 0) continue;
-            sh.item = pol.item_bytes ? pol.item_bytes : auto_item_bytes(sh.bytes, sh.traffic, sh.kind, sh.nsrc, sh.ndst);
-            for (const purlin_desc& d : D)
-                if (d.phase == ph) items_total += ceil_div(d.bytes, sh.item);
-            if (items_total > PURLIN_MAX_ITEMS) return PURLIN_ERR_NOMEM;
-        }
-        out.items.reserve(items_total);
-        out.reduce_item_bytes = shape[0].item;
-        for (uint32_t ph = 0; ph < 2; ++ph) {
-            if (shape[ph].ndesc == 0) continue;
-            const uint64_t item = shape[ph].item;
-            Phase& phase = out.phases[out.nphases++];
-            phase.begin = out.items.size();
-            bool first = true;
-            for (const purlin_desc& d : D) {
-                if (d.phase != ph) continue;
-                if (first) {
-                    phase.kind = d.kind;
-                    phase.nsrc = d.nsrc;
-                    phase.src_buf = d.src_buf;
-                    phase.src_step = d.src_step;
-                    first = false;
-                } else if (d.kind != phase.kind ||
-                           (d.kind == PURLIN_KIND_REDUCE &&
-                            (d.nsrc != phase.nsrc || d.src_buf != phase.src_buf || d.src_step != phase.src_step))) {
-                    return PURLIN_ERR_UNSUPPORTED;  // a phase is one kernel: one consume op, one source set
-                }
-                for (uint64_t o = 0; o < d.bytes; o += item) {
-                    purlin_desc w = d;
-                    w.src_off += o;
-                    w.dst_off += o;
-                    w.bytes = std::min(item, d.bytes - o);
-                    out.items.push_back(w);
-                }
+namespace {
+
+purlin_status cut_items(Plan& out, const purlin_policy& pol) {
+    for (const purlin_desc& d : out.descs) out.sched_bytes += (uint64_t(d.nsrc) + d.ndst) * d.bytes;
+
+    // Per-phase shape: bytes of the descriptors, bytes moved, fan-in/out.
+    struct PhaseShape {
+        uint64_t bytes = 0, traffic = 0, ndesc = 0;
+        uint32_t kind = 0, nsrc = 0, ndst = 0;
+        uint64_t item = 0;
+    } shape[2];
+    for (const purlin_desc& d : out.descs) {
+        PhaseShape& sh = shape[d.phase];
+        sh.bytes += d.bytes;
+        sh.traffic += (uint64_t(d.nsrc) + d.ndst) * d.bytes;
+        sh.kind = d.kind;
+        sh.nsrc = std::max(sh.nsrc, d.nsrc);
+        sh.ndst = std::max(sh.ndst, d.ndst);
+        ++sh.ndesc;
+    }
+    // Cut descriptors into work items, phase by phase.
+    uint64_t items_total = 0;
+    for (uint32_t ph = 0; ph < 2; ++ph) {
+        PhaseShape& sh = shape[ph];
+        if (sh.ndesc == 0) continue;
+        sh.item = pol.item_bytes ? pol.item_bytes : auto_item_bytes(sh.bytes, sh.traffic, sh.kind, sh.nsrc, sh.ndst);
+        for (const purlin_desc& d : out.descs)
+            if (d.phase == ph) items_total += ceil_div(d.bytes, sh.item);
+        if (items_total > PURLIN_MAX_ITEMS) return PURLIN_ERR_NOMEM;
+    }
+    out.items.reserve(items_total);
+    out.reduce_item_bytes = shape[0].item;
+    for (uint32_t ph = 0; ph < 2; ++ph) {
+        if (shape[ph].ndesc == 0) continue;
+        const uint64_t item = shape[ph].item;
+        Phase& phase = out.phases[out.nphases++];
+        phase.begin = out.items.size();
+        bool first = true;
+        for (const purlin_desc& d : out.descs) {
+            if (d.phase != ph) continue;
+            if (first) {
+                phase.kind = d.kind;
+                phase.nsrc = d.nsrc;
+                phase.src_buf = d.src_buf;
+                phase.src_step = d.src_step;
+                first = false;
+            } else if (d.kind != phase.kind ||
+                       (d.kind == PURLIN_KIND_REDUCE &&
+                        (d.nsrc != phase.nsrc || d.src_buf != phase.src_buf || d.src_step != phase.src_step))) {
+                return PURLIN_ERR_UNSUPPORTED;  // a phase is one kernel: one consume op, one source set
             }
-            phase.count = out.items.size() - phase.begin;
-            // Cache hints.  A stream that is touched once and is much larger
-            // than the 256 MB last-level cache gains from non-temporal
-            // accesses; which side gains was measured on MI355X: reads for
-            // many-to-one (reduce), writes for one-to-many (multi-destination
-            // copy), both for one-to-one copies.  Phases whose traffic fits
-            // the cache keep cached accesses so repeated calls hit it.
-            uint64_t traffic = 0, max_ndst = 0;
-            for (uint64_t i = phase.begin; i < out.items.size(); ++i) {
-                traffic += (uint64_t(out.items[i].nsrc) + out.items[i].ndst) * out.items[i].bytes;
-                max_ndst = std::max<uint64_t>(max_ndst, out.items[i].ndst);
+            for (uint64_t o = 0; o < d.bytes; o += item) {
+                purlin_desc w = d;
+                w.src_off += o;
+                w.dst_off += o;
+                w.bytes = std::min(item, d.bytes - o);
+                out.items.push_back(w);
             }
-            const bool streaming = traffic >= kStreamingBytes;
-            bool auto_nt_load = false, auto_nt_store = false;
-            if (streaming) {
-                if (phase.kind == PURLIN_KIND_REDUCE) {
-                    auto_nt_load = true;
-                } else if (max_ndst > 1) {
-                    auto_nt_store = true;
-                } else {
-                    auto_nt_load = auto_nt_store = true;
-                }
-            }
-            phase.nt_load = pol.load_hint ? pol.load_hint == 2 : auto_nt_load;
-            phase.nt_store = pol.store_hint ? pol.store_hint == 2 : auto_nt_store;
         }
+        phase.count = out.items.size() - phase.begin;
+        // Cache hints.  A stream that is touched once and is much larger
+        // than the 256 MB last-level cache gains from non-temporal
+        // accesses; which side gains was measured on MI355X: reads for
+        // many-to-one (reduce), writes for one-to-many (multi-destination
+        // copy), both for one-to-one copies.  Phases whose traffic fits
+        // the cache keep cached accesses so repeated calls hit it.
+        uint64_t traffic = 0, max_ndst = 0;
+        for (uint64_t i = phase.begin; i < out.items.size(); ++i) {
+            traffic += (uint64_t(out.items[i].nsrc) + out.items[i].ndst) * out.items[i].bytes;
+            max_ndst = std::max<uint64_t>(max_ndst, out.items[i].ndst);
+        }
+        const bool streaming = traffic >= kStreamingBytes;
+        bool auto_nt_load = false, auto_nt_store = false;
+        if (streaming) {
+            if (phase.kind == PURLIN_KIND_REDUCE) {
+                auto_nt_load = true;
+            } else if (max_ndst > 1) {
+                auto_nt_store = true;
+            } else {
+                auto_nt_load = auto_nt_store = true;
+            }
+        }
+        phase.nt_load = pol.load_hint ? pol.load_hint == 2 : auto_nt_load;
+        phase.nt_store = pol.store_hint ? pol.store_hint == 2 : auto_nt_store;
+    }
+    return PURLIN_OK;
+}
+
+}  // namespace
+
+purlin_status build_plan_v(purlin_op op, int P, uint64_t capacity, purlin_dtype dtype, uint64_t chunk, uint64_t unit,
+                           const purlin_policy* policy, uint32_t flags, Plan& out) {
+    if (op != PURLIN_ALLGATHERV && op != PURLIN_REDUCE_SCATTERV && op != PURLIN_ALLTOALLV) return PURLIN_ERR_INVALID;
+    if (dtype != PURLIN_FP32 && dtype != PURLIN_BF16) return PURLIN_ERR_INVALID;
+    if (P < 1 || P > PURLIN_MAX_RANKS) return PURLIN_ERR_INVALID;
+    if (flags & ~PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
+    const uint64_t s = dtype == PURLIN_FP32 ? 4 : 2;
+    if (chunk < s || chunk % s != 0) return PURLIN_ERR_INVALID;
+    if (capacity > (uint64_t(1) << 58) / s) return PURLIN_ERR_INVALID;
+    if (unit < 1 || unit > (uint64_t(1) << 31)) return PURLIN_ERR_INVALID;
+    purlin_policy pol{};
+    if (!parse_policy(policy, pol)) return PURLIN_ERR_INVALID;
+
+    out = Plan{};
+    out.op = op;
+    out.P = P;
+    out.count = capacity;
+    out.dtype = dtype;
+    out.chunk = chunk;
+    out.flags = flags;
+    out.elem_bytes = s;
+    out.vop = true;
+    out.capacity = capacity;
+    out.unit = unit;
+    out.in_bytes = capacity * s;
+    out.out_bytes = capacity * s;
+    out.in_mask = out.out_mask = (1u << P) - 1u;
+    if (pol.fanout == 0) pol.fanout = 2;
+    if (pol.ar_mode == 0) pol.ar_mode = 2;
+
+    // The virtual index space: the gathered output (ALLGATHERV), the
+    // partitioned input (REDUCE_SCATTERV), or each destination's output
+    // (ALLTOALLV), cut into chunks; one descriptor per chunk.
+    const uint64_t vbytes = capacity * s;
+    const uint64_t Cv = vbytes ? ceil_div(vbytes, chunk) : 0;
+    const uint64_t spaces = op == PURLIN_ALLTOALLV ? uint64_t(P) : 1;
+    if (Cv > PURLIN_MAX_ITEMS || Cv * spaces > PURLIN_MAX_ITEMS) return PURLIN_ERR_NOMEM;
+    const uint32_t out0 = static_cast<uint32_t>(P);
+    try {
+        for (uint32_t r = 0; r < spaces; ++r)
+            for (uint64_t c = 0; c < Cv; ++c) {
+                const uint64_t off = c * chunk, len = std::min(chunk, vbytes - off);
+                if (op == PURLIN_ALLGATHERV)
+                    out.descs.push_back(make_desc(PURLIN_KIND_COPY, 0, 1, 0, 0, P, out0, 1, off, off, len, 0,
+                                                  static_cast<uint32_t>(c)));
+                else if (op == PURLIN_REDUCE_SCATTERV)
+                    out.descs.push_back(make_desc(PURLIN_KIND_REDUCE, 0, P, 0, 1, 1, out0, 0, off, off, len, 0,
+                                                  static_cast<uint32_t>(c)));
+                else
+                    out.descs.push_back(make_desc(PURLIN_KIND_COPY, 0, 1, 0, 0, 1, out0 + r, 0, off, off, len, r,
+                                                  static_cast<uint32_t>(c)));
+            }
+        out.policy = pol;
+        const purlin_status st = cut_items(out, pol);
+        if (st != PURLIN_OK) return st;
     } catch (const std::bad_alloc&) {
         out.descs.clear();
         out.items.clear();

@@ -44,6 +44,11 @@ struct Plan {
     int nphases = 0;
     Phase phases[2];
 
+    // Variable-size collectives: capacity in elements, counts' unit.
+    bool vop = false;
+    uint64_t capacity = 0;
+    uint64_t unit = 1;
+
     // Single-launch AllReduce (ar_mode 3): one launch over all items.
     bool fused = false;
     uint64_t part_bytes = 0;
@@ -55,6 +60,12 @@ struct Plan {
 };
 
 // Validates the request and fills `out` (host tables only).  Pure host code.
+// Variable-size collectives (ALLGATHERV, REDUCE_SCATTERV, ALLTOALLV): the
+// table covers a virtual index space of `capacity` elements (per destination
+// for ALLTOALLV); sizes are applied on the device.
+purlin_status build_plan_v(purlin_op op, int P, uint64_t capacity, purlin_dtype dtype, uint64_t chunk, uint64_t unit,
+                           const purlin_policy* policy, uint32_t flags, Plan& out);
+
 // `root` is -1 for the non-rooted collectives and a rank for the rooted ones.
 purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,
                          const purlin_policy* policy, uint32_t flags, Plan& out);

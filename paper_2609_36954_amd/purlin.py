@@ -26,6 +26,8 @@ PURLIN_ERR_DEVICE = 4
 OPS = {"allreduce": 0, "reduce_scatter": 1, "allgather": 2, "alltoall": 3,
        "broadcast": 4, "reduce": 5, "scatter": 6, "gather": 7}
 ROOTED = ("broadcast", "reduce", "scatter", "gather")
+OPS.update({"allgatherv": 8, "reduce_scatterv": 9, "alltoallv": 10})
+VOPS = ("allgatherv", "reduce_scatterv", "alltoallv")
 DTYPES = {"fp32": 0, "bf16": 1}
 ELEM_BYTES = {"fp32": 4, "bf16": 2}
 KIND_COPY = 0
@@ -88,6 +90,8 @@ def lib():
     L.purlin_plan.argtypes = [i32, i32, u64, i32, u64, ctypes.POINTER(_vp)]
     L.purlin_plan_ex.argtypes = [i32, i32, u64, i32, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
     L.purlin_plan_rooted.argtypes = [i32, i32, i32, u64, i32, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
+    L.purlin_plan_v.argtypes = [i32, i32, u64, i32, u64, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
+    L.purlin_exec_v.argtypes = [_vp, ctypes.POINTER(_vp), _vp, _vp, _vp]
     L.purlin_plan_info.argtypes = [_vp, _c_u64p, _c_u64p, _c_u64p, _c_u64p]
     L.purlin_plan_descriptors.argtypes = [_vp, ctypes.POINTER(_vp), _c_u64p, _c_u64p]
     L.purlin_plan_items.argtypes = [_vp, ctypes.POINTER(_vp), _c_u64p, _c_u64p]
@@ -103,7 +107,8 @@ def lib():
     L.purlin_status_string.restype = ctypes.c_char_p
     L.purlin_version.argtypes = []
     L.purlin_version.restype = ctypes.c_char_p
-    for name in ("purlin_plan", "purlin_plan_ex", "purlin_plan_rooted", "purlin_plan_info", "purlin_plan_descriptors", "purlin_plan_items",
+    for name in ("purlin_plan", "purlin_plan_ex", "purlin_plan_rooted", "purlin_plan_v", "purlin_exec_v",
+                 "purlin_plan_info", "purlin_plan_descriptors", "purlin_plan_items",
                  "purlin_exec", "purlin_pack_workspace_size", "purlin_pack", "purlin_unpack"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -152,7 +157,7 @@ def _require_cuda(t, name, itemsize=None):
 class Plan:
     """A planned collective (immutable).  ``exec`` runs it on a stream."""
 
-    def __init__(self, op, P, count, dtype, chunk, policy=None, host_only=False, root=None):
+    def __init__(self, op, P, count, dtype, chunk, policy=None, host_only=False, root=None, unit=None):
         if op not in OPS:
             raise PurlinError(PURLIN_ERR_INVALID, f"unknown op {op!r}")
         if dtype not in DTYPES:
@@ -161,10 +166,20 @@ class Plan:
             raise PurlinError(PURLIN_ERR_INVALID, f"{op} {'needs' if op in ROOTED else 'takes no'} root")
         self.op, self.P, self.count, self.dtype, self.chunk = op, int(P), int(count), dtype, int(chunk)
         self.root = root
+        self.unit = unit
         self.host_only = bool(host_only)
+        if (op in VOPS) != (unit is not None):
+            raise PurlinError(PURLIN_ERR_INVALID, f"{op} {'needs' if op in VOPS else 'takes no'} unit")
         h = ctypes.c_void_p()
         L = lib()
-        if root is not None:
+        if unit is not None:
+            pol = None
+            if policy is not None:
+                pol = policy if isinstance(policy, Policy) else Policy(**policy)
+            st = L.purlin_plan_v(OPS[op], int(P), int(count), DTYPES[dtype], int(chunk), int(unit),
+                                 ctypes.byref(pol) if pol is not None else None,
+                                 PLAN_HOST_ONLY if host_only else 0, ctypes.byref(h))
+        elif root is not None:
             pol = None
             if policy is not None:
                 pol = policy if isinstance(policy, Policy) else Policy(**policy)
@@ -231,6 +246,10 @@ class Plan:
         """Run on device tensors ``ins`` (P inputs) and ``outs`` (P outputs)."""
         purlin_exec(self, ins, outs, stream)
 
+    def exec_v(self, ins, outs, counts, dev_status=None, stream=None):
+        """Run a variable-size plan; ``counts`` is a device int32 tensor."""
+        purlin_exec_v(self, ins, outs, counts, dev_status, stream)
+
     def destroy(self):
         if getattr(self, "_h", None) is not None and _lib is not None:
             _lib.purlin_plan_destroy(self._h)
@@ -261,6 +280,38 @@ def used_buffers(plan):
     if op in ("reduce", "gather"):
         outs = [r == root for r in range(P)]
     return ins, outs
+
+
+def purlin_plan_v(op, P, capacity, dtype, chunk, unit=1, policy=None, host_only=False):
+    return Plan(op, P, capacity, dtype, chunk, policy=policy, host_only=host_only, unit=unit)
+
+
+def _buffer_array(plan, ins, outs):
+    P = plan.P
+    if len(ins) != P or len(outs) != P:
+        raise PurlinError(PURLIN_ERR_INVALID, f"need {P} inputs and {P} outputs")
+    use_in, use_out = used_buffers(plan)
+    s = ELEM_BYTES[plan.dtype]
+    for t, u in zip(ins, use_in):
+        if u:
+            _require_cuda(t, "input", s)
+            if t.numel() * s < plan.in_bytes:
+                raise PurlinError(PURLIN_ERR_INVALID, "input buffer too small")
+    for t, u in zip(outs, use_out):
+        if u:
+            _require_cuda(t, "output", s)
+            if t.numel() * s < plan.out_bytes:
+                raise PurlinError(PURLIN_ERR_INVALID, "output buffer too small")
+    return (ctypes.c_void_p * (2 * P))(*[(t.data_ptr() if t is not None else 0) for t in list(ins) + list(outs)])
+
+
+def purlin_exec_v(plan, ins, outs, counts, dev_status=None, stream=None):
+    """Variable-size collective; ``counts``: device int32 tensor (P, or P*P
+    row-major for alltoallv), in units of the plan's ``unit`` elements."""
+    _require_cuda(counts, "counts", 4)
+    arr = _buffer_array(plan, ins, outs)
+    _check(lib().purlin_exec_v(plan.handle, arr, _ptr(counts), _ptr(dev_status), _stream_handle(stream)),
+           "purlin_exec_v")
 
 
 def purlin_exec(plan, ins, outs, stream=None):

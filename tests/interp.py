@@ -43,3 +43,54 @@ def run(items, phase_begin, bufs, dtype, seed=0):
         order = rng.permutation(np.arange(lo, hi))
         for i in order:
             apply_item(items[i], bufs, dtype)
+
+
+def run_v(items, bufs, counts, op, P, unit, dtype, capacity):
+    """The variable-size mapping on the CPU: every item covers a range of the
+    virtual index space; the sizes decide which source / destination and
+    offset each element belongs to.  Returns False (writing nothing) for
+    sizes the device would reject."""
+    s = 2 if dtype == "bf16" else 4
+    c = [int(x) * unit for x in counts]
+    if op == "alltoallv":
+        m = [c[p * P:(p + 1) * P] for p in range(P)]
+        if any(x < 0 or x > capacity for x in c):
+            return False
+        if any(sum(row) > capacity for row in m) or any(sum(m[p][r] for p in range(P)) > capacity for r in range(P)):
+            return False
+    elif any(x < 0 or x > capacity for x in c) or sum(c) > capacity:
+        return False
+    for it in items:
+        lo, hi = int(it["src_off"]) // s, (int(it["src_off"]) + int(it["bytes"])) // s
+        if op == "allgatherv":
+            off = 0
+            for p in range(P):
+                x, y = max(lo, off), min(hi, off + c[p])
+                if x < y:
+                    data = bufs[p][(x - off) * s:(y - off) * s].copy()
+                    for r in range(P):
+                        bufs[P + r][x * s:y * s] = data
+                off += c[p]
+        elif op == "reduce_scatterv":
+            off = 0
+            for r in range(P):
+                x, y = max(lo, off), min(hi, off + c[r])
+                if x < y:
+                    acc = np.zeros(y - x, np.float32)
+                    for p in range(P):
+                        v = _typed(bufs[p], x * s, (y - x) * s, dtype)
+                        acc = np.add(acc, widen(v) if dtype == "bf16" else v, dtype=np.float32)
+                    out = narrow(acc) if dtype == "bf16" else acc
+                    bufs[P + r][(x - off) * s:(y - off) * s] = out.view(np.uint8)
+                off += c[r]
+        else:
+            r = int(it["part"])
+            recv = 0
+            for p in range(P):
+                send = sum(m[p][:r])
+                x, y = max(lo, recv), min(hi, recv + m[p][r])
+                if x < y:
+                    a0 = send + (x - recv)
+                    bufs[P + r][x * s:y * s] = bufs[p][a0 * s:(a0 + y - x) * s]
+                recv += m[p][r]
+    return True
