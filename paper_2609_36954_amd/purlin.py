@@ -309,6 +309,9 @@ def purlin_exec_v(plan, ins, outs, counts, dev_status=None, stream=None):
     """Variable-size collective; ``counts``: device int32 tensor (P, or P*P
     row-major for alltoallv), in units of the plan's ``unit`` elements."""
     _require_cuda(counts, "counts", 4)
+    need = plan.P * plan.P if plan.op == "alltoallv" else plan.P
+    if counts.numel() < need:
+        raise PurlinError(PURLIN_ERR_INVALID, f"{plan.op} needs {need} counts")
     arr = _buffer_array(plan, ins, outs)
     _check(lib().purlin_exec_v(plan.handle, arr, _ptr(counts), _ptr(dev_status), _stream_handle(stream)),
            "purlin_exec_v")
