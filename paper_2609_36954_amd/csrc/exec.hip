@@ -462,41 +462,41 @@ __global__ __launch_bounds__(kBlock) void exec_reducescatterv(ExecArgs a, VArgs 
 }
 
 // AllToAllV: item d covers bytes [src_off, src_off + bytes) of destination
-// d.part's output.  counts[p * P + r] = elements rank p sends to rank r.
+// d.part's output.  counts[p * P + r] = elements rank p sends to rank r.  The
+// P x P sizes are staged once per workgroup in LDS; lane p then forms rank
+// p's row total and the offset of partition r in its row, lane q its
+// column total (what rank q receives).
 template <bool STREAM>
 __global__ __launch_bounds__(kBlock) void exec_alltoallv(ExecArgs a, VArgs v) {
+    __shared__ int64_t m[PURLIN_MAX_RANKS * PURLIN_MAX_RANKS];
+    const uint32_t P = v.P;
+    const int64_t unit = static_cast<int64_t>(v.unit);
+    for (uint32_t i = threadIdx.x; i < P * P; i += kBlock) m[i] = static_cast<int64_t>(v.counts[i]) * unit;
+    __syncthreads();
     const uint32_t w = wave_index();
     if (w >= a.n_items) return;
     const uint32_t lane = lane_index();
     const purlin_desc d = a.items[w];
     const uint32_t r = d.part;
-    const int64_t unit = static_cast<int64_t>(v.unit);
-    // lane p: its row's total (send size), the offset of partition r in it,
-    // and the size of partition r
     const int64_t cap = static_cast<int64_t>(v.capacity);
-    int64_t row_total = 0, send_off = 0, c = 0;
+    int64_t send_off = 0, c = 0;
     bool ok = true;
-    if (lane < v.P) {
-        for (uint32_t q = 0; q < v.P; ++q) {
-            int64_t x = static_cast<int64_t>(v.counts[uint64_t(lane) * v.P + q]) * unit;
-            if (x < 0 || x > cap) {  // checked before any sum, so sums cannot overflow
+    if (lane < P) {
+        int64_t row = 0, col = 0;  // each term is checked against the capacity first: no overflow
+        for (uint32_t q = 0; q < P; ++q) {
+            int64_t x = m[lane * P + q];
+            if (x < 0 || x > cap) {
                 ok = false;
                 x = 0;
             }
             if (q < r) send_off += x;
             if (q == r) c = x;
-            row_total += x;
+            row += x;
+            int64_t y = m[q * P + lane];
+            if (y < 0 || y > cap) y = 0;  // reported by lane q's row
+            col += y;
         }
-        ok = ok && row_total <= cap;
-    }
-    // every column (receive size) must fit too; all waves check all columns
-    for (uint32_t q = 0; q < v.P; ++q) {
-        int64_t x = 0;
-        if (lane < v.P) x = static_cast<int64_t>(v.counts[uint64_t(lane) * v.P + q]) * unit;
-        if (x < 0 || x > cap) x = 0;  // already reported through ok
-        int64_t col = 0;
-        for (uint32_t p = 0; p < v.P; ++p) col += readlane64(x, p);
-        ok = ok && col <= cap;
+        ok = ok && row <= cap && col <= cap;
     }
     const bool all_ok = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(__all(ok)));
     report(v, w, lane, all_ok);
@@ -504,14 +504,14 @@ __global__ __launch_bounds__(kBlock) void exec_alltoallv(ExecArgs a, VArgs v) {
     const uint64_t s = v.elem_bytes;
     const int64_t lo_v = static_cast<int64_t>(d.src_off / s), hi_v = lo_v + static_cast<int64_t>(d.bytes / s);
     int64_t recv = 0;
-    for (uint32_t p = 0; p < v.P; ++p) {
+    for (uint32_t p = 0; p < P; ++p) {
         const int64_t cp = readlane64(c, p), sp = readlane64(send_off, p);
         const int64_t x = max(lo_v, recv), y = min(hi_v, recv + cp);
         if (x < y) {
             purlin_desc sub = d;
             sub.src_buf = p;
             sub.ndst = 1;
-            sub.dst_buf = v.P + r;
+            sub.dst_buf = P + r;
             sub.dst_step = 0;
             sub.src_off = uint64_t(sp + (x - recv)) * s;
             sub.dst_off = uint64_t(x) * s;
