@@ -307,3 +307,32 @@ def test_fused_allreduce_full_size_equals_two_launches():
     for r in range(P):
         assert torch.equal(a[r], b[r])
     assert fused.device_error() == 0
+
+
+def test_offsets_beyond_4GiB_per_rank():
+    """P = 2 AllReduce of 5 GiB per rank: byte offsets above 2^32 in every
+    buffer.  Inputs are drawn on the device with a seeded torch generator;
+    sampled elements are checked against the oracle, and RS then AG must equal
+    the AllReduce bit for bit."""
+    P, N = 2, (5 << 30) // 2
+    g = torch.Generator(device="cuda").manual_seed(55)
+    ins = [torch.randn(N, device="cuda", generator=g).to(torch.bfloat16).view(torch.int16) for _ in range(P)]
+    ar = PL.Plan("allreduce", P, N, "bf16", 1 << 20)
+    outs = [torch.empty(N, dtype=torch.int16, device="cuda") for _ in range(P)]
+    ar.exec(ins, outs)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(56)
+    idx = np.sort(np.concatenate([rng.integers(0, N, 65536), np.arange(N - 4096, N)]))
+    idx_t = torch.from_numpy(idx).to("cuda")
+    sample = [to_host(t[idx_t], np.uint16) for t in ins]
+    want = oracle.all_reduce([s[: len(s) // P * P] for s in sample], "bf16")[0]
+    assert_bits_equal(to_host(outs[0][idx_t], np.uint16)[: len(want)], want, "bf16", "AR beyond 4 GiB")
+    assert torch.equal(outs[0], outs[1])
+    rs = PL.Plan("reduce_scatter", P, N, "bf16", 1 << 20)
+    rs_out = [torch.empty(N // P, dtype=torch.int16, device="cuda") for _ in range(P)]
+    rs.exec(ins, rs_out)
+    del ins
+    ag = PL.Plan("allgather", P, N, "bf16", 1 << 20)
+    ag.exec(rs_out, [outs[1], torch.empty(N, dtype=torch.int16, device="cuda")])
+    torch.cuda.synchronize()
+    assert torch.equal(outs[1], outs[0])
