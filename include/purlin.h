@@ -144,6 +144,12 @@ typedef struct purlin_policy {
 #define PURLIN_PLAN_HOST_ONLY 1u /* build the tables on the host only (no device
                                     upload); such a plan can be inspected but
                                     not executed */
+#define PURLIN_PLAN_COUNTS_TRANSPOSED 2u /* ALLTOALLV only: read the P x P
+                                    sizes column-major, counts[r*P + p] =
+                                    what rank p sends to rank r.  The reverse
+                                    exchange of an expert-parallel dispatch
+                                    (the combine, Table 2) then reuses the
+                                    dispatch's counts as they are. */
 
 #define PURLIN_MAX_RANKS 16
 #define PURLIN_MAX_ITEMS (1ull << 24)
@@ -186,18 +192,21 @@ PURLIN_API purlin_status purlin_plan_rooted(purlin_op op, int P, int root, uint6
                                             uint64_t chunk_bytes, const purlin_policy* policy, uint32_t flags,
                                             purlin_plan_t* out_plan);
 
-/* A variable-size collective over P ranks whose buffers each hold
- * `capacity` elements (in and out).  The sizes are not part of the plan:
- * purlin_exec_v reads them from device memory at run time, so they may be
- * produced by an earlier kernel on the stream (e.g. purlin_pack's
- * dest_counts) and the call can be captured in a graph.  Counts are in units
- * of `unit` elements (1 <= unit <= 2^31).  `chunk_bytes` cuts the virtual
- * index space into chunks, as for the fixed-size plans.  Policy, flags and
- * errors as for purlin_plan_ex; PURLIN_ERR_INVALID also for a non-V op or a
- * bad unit.  `capacity` need not be a multiple of P. */
-PURLIN_API purlin_status purlin_plan_v(purlin_op op, int P, uint64_t capacity, purlin_dtype dtype,
-                                       uint64_t chunk_bytes, uint64_t unit, const purlin_policy* policy,
-                                       uint32_t flags, purlin_plan_t* out_plan);
+/* A variable-size collective over P ranks: every input buffer holds
+ * `in_capacity` elements and every output buffer `out_capacity`.  The sizes
+ * are not part of the plan: purlin_exec_v reads them from device memory at
+ * run time, so they may be produced by an earlier kernel on the stream (e.g.
+ * purlin_pack's dest_counts, with unit = the row length) and the call can be
+ * captured in a graph.  Counts are in units of `unit` elements
+ * (1 <= unit <= 2^31).  `chunk_bytes` cuts the virtual index space (the
+ * gathered output, the partitioned input, or each destination's output)
+ * into chunks, as for the fixed-size plans.  Policy and errors as for
+ * purlin_plan_ex; flags: PURLIN_PLAN_HOST_ONLY, and for ALLTOALLV
+ * PURLIN_PLAN_COUNTS_TRANSPOSED.  PURLIN_ERR_INVALID also for a non-V op, a
+ * bad unit or a flag the op does not take. */
+PURLIN_API purlin_status purlin_plan_v(purlin_op op, int P, uint64_t in_capacity, uint64_t out_capacity,
+                                       purlin_dtype dtype, uint64_t chunk_bytes, uint64_t unit,
+                                       const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan);
 
 /* Run a variable-size plan.  `counts` is device memory (int32):
  *   ALLGATHERV      counts[p], p < P: elements rank p contributes; every
@@ -205,11 +214,13 @@ PURLIN_API purlin_status purlin_plan_v(purlin_op op, int P, uint64_t capacity, p
  *                   out_r[off_p + i] = in_p[i], off_p = sum(counts[0..p)).
  *   REDUCE_SCATTERV counts[r]: partition sizes of every input; out_r[i] =
  *                   rank-order sum (Eq. 2) of in_p[off_r + i], i < counts[r].
- *   ALLTOALLV       counts[p*P + r]: elements rank p sends to rank r; in_p
- *                   holds them in destination order, out_r receives them in
- *                   source order.
- * Each count (times unit) must be >= 0 and every input and output total
- * must fit the capacity; otherwise the call writes nothing and, if
+ *   ALLTOALLV       counts[p*P + r]: elements rank p sends to rank r
+ *                   (counts[r*P + p] with PURLIN_PLAN_COUNTS_TRANSPOSED);
+ *                   in_p holds them in destination order, out_r receives
+ *                   them in source order.
+ * Each count (times unit) must be >= 0, every input's part must fit
+ * in_capacity and every output's part out_capacity; otherwise the call
+ * writes nothing and, if
  * `dev_status` (device int32, optional) is given, sets it to 1 (else 0).
  * Host-side errors as for purlin_exec, plus PURLIN_ERR_INVALID for a
  * non-V plan or NULL counts.  purlin_exec rejects V plans. */

@@ -29,14 +29,15 @@ size_t fused_state_bytes(const purlin::Plan& p) {
 }
 
 purlin_status make_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,
-                        const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan, uint64_t v_unit = 0) {
+                        const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan, uint64_t v_unit = 0,
+                        uint64_t v_out_capacity = 0) {
     if (!out_plan) return PURLIN_ERR_INVALID;
     *out_plan = nullptr;
     purlin_plan_s* h = new (std::nothrow) purlin_plan_s;
     if (!h) return PURLIN_ERR_NOMEM;
     purlin_status st;
     try {
-        st = v_unit ? purlin::build_plan_v(op, P, count, dtype, chunk, v_unit, policy, flags, h->plan)
+        st = v_unit ? purlin::build_plan_v(op, P, count, v_out_capacity, dtype, chunk, v_unit, policy, flags, h->plan)
                     : purlin::build_plan(op, P, root, count, dtype, chunk, policy, flags, h->plan);
     } catch (...) {
         st = PURLIN_ERR_NOMEM;
@@ -127,13 +128,14 @@ purlin_status purlin_plan_rooted(purlin_op op, int P, int root, uint64_t count, 
     return make_plan(op, P, root, count, dtype, chunk_bytes, policy, flags, out_plan);
 }
 
-purlin_status purlin_plan_v(purlin_op op, int P, uint64_t capacity, purlin_dtype dtype, uint64_t chunk_bytes,
-                            uint64_t unit, const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan) {
+purlin_status purlin_plan_v(purlin_op op, int P, uint64_t in_capacity, uint64_t out_capacity, purlin_dtype dtype,
+                            uint64_t chunk_bytes, uint64_t unit, const purlin_policy* policy, uint32_t flags,
+                            purlin_plan_t* out_plan) {
     if (unit == 0) {
         if (out_plan) *out_plan = nullptr;
         return PURLIN_ERR_INVALID;
     }
-    return make_plan(op, P, -1, capacity, dtype, chunk_bytes, policy, flags, out_plan, unit);
+    return make_plan(op, P, -1, in_capacity, dtype, chunk_bytes, policy, flags, out_plan, unit, out_capacity);
 }
 
 purlin_status purlin_plan_info(purlin_plan_t plan, uint64_t* n_desc, uint64_t* in_bytes_per_rank,
@@ -180,8 +182,10 @@ purlin_status purlin_exec_v(purlin_plan_t plan, void* const* bufs, const int32_t
     const purlin_status st = check_buffers(p, bufs);
     if (st != PURLIN_OK) return st;
     const purlin::Phase& ph = p.phases[0];
-    const hipError_t e = purlin::launch_v(p.op, p.d_items, ph.count, p.P, p.dtype, ph.nt_load || ph.nt_store, bufs,
-                                          counts, dev_status, p.capacity, p.unit, static_cast<hipStream_t>(stream));
+    const hipError_t e =
+        purlin::launch_v(p.op, p.d_items, ph.count, p.P, p.dtype, ph.nt_load || ph.nt_store, bufs, counts,
+                         (p.flags & PURLIN_PLAN_COUNTS_TRANSPOSED) != 0, dev_status, p.in_capacity, p.out_capacity,
+                         p.unit, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
 }
 

@@ -367,10 +367,12 @@ void launch_copy(dim3 grid, hipStream_t stream, const ExecArgs& a, bool ntl, boo
 struct VArgs {
     const int32_t* counts;  // P (AllGatherV, ReduceScatterV) or P*P row-major (AllToAllV)
     int32_t* status;        // optional: 0, or 1 for invalid sizes
-    uint64_t capacity;      // elements every buffer holds
+    uint64_t in_cap;        // elements every input holds
+    uint64_t out_cap;       // elements every output holds
     uint64_t unit;          // elements per count
     uint32_t P;
     uint32_t elem_bytes;
+    uint32_t transposed;  // AllToAllV: counts are column-major
 };
 
 __device__ __forceinline__ int64_t readlane64(int64_t v, int lane) {
@@ -380,20 +382,20 @@ __device__ __forceinline__ int64_t readlane64(int64_t v, int lane) {
 }
 
 // Lane p < P holds count p (elements); returns whether every count is >= 0
-// and their sum fits the capacity.
-__device__ __forceinline__ bool load_counts(const VArgs& v, uint32_t lane, int64_t& c) {
+// and fits `part_cap`, and their sum fits `total_cap`.
+__device__ __forceinline__ bool load_counts(const VArgs& v, uint32_t lane, int64_t part_cap, int64_t total_cap,
+                                            int64_t& c) {
     c = 0;
     if (lane < v.P) c = static_cast<int64_t>(v.counts[lane]) * static_cast<int64_t>(v.unit);
-    const int64_t cap = static_cast<int64_t>(v.capacity);
     bool ok = true;
-    int64_t total = 0;  // each term is checked against the capacity first, so this cannot overflow
+    int64_t total = 0;  // each term is checked against a capacity first, so this cannot overflow
     for (uint32_t p = 0; p < v.P; ++p) {
         const int64_t cp = readlane64(c, p);
-        const bool fits = cp >= 0 && cp <= cap;
+        const bool fits = cp >= 0 && cp <= part_cap;
         ok = ok && fits;
         total += fits ? cp : 0;
     }
-    return ok && total <= cap;
+    return ok && total <= total_cap;
 }
 
 __device__ __forceinline__ void report(const VArgs& v, uint32_t w, uint32_t lane, bool ok) {
@@ -406,7 +408,7 @@ __global__ __launch_bounds__(kBlock) void exec_allgatherv(ExecArgs a, VArgs v) {
     if (w >= a.n_items) return;
     const uint32_t lane = lane_index();
     int64_t c;
-    const bool ok = load_counts(v, lane, c);
+    const bool ok = load_counts(v, lane, static_cast<int64_t>(v.in_cap), static_cast<int64_t>(v.out_cap), c);
     report(v, w, lane, ok);
     if (!ok) return;
     const purlin_desc d = a.items[w];
@@ -437,7 +439,7 @@ __global__ __launch_bounds__(kBlock) void exec_reducescatterv(ExecArgs a, VArgs 
     if (w >= a.n_items) return;
     const uint32_t lane = lane_index();
     int64_t c;
-    const bool ok = load_counts(v, lane, c);
+    const bool ok = load_counts(v, lane, static_cast<int64_t>(v.out_cap), static_cast<int64_t>(v.in_cap), c);
     report(v, w, lane, ok);
     if (!ok) return;
     const purlin_desc d = a.items[w];
@@ -462,27 +464,32 @@ __global__ __launch_bounds__(kBlock) void exec_reducescatterv(ExecArgs a, VArgs 
 }
 
 // AllToAllV: item d covers bytes [src_off, src_off + bytes) of destination
-// d.part's output.  counts[p * P + r] = elements rank p sends to rank r.  The
-// P x P sizes are staged once per workgroup in LDS; lane p then forms rank
-// p's row total and the offset of partition r in its row, lane q its
-// column total (what rank q receives).
+// d.part's output.  counts[p * P + r] = elements rank p sends to rank r
+// (counts[r * P + p] when transposed).  The P x P sizes are staged once per
+// workgroup in LDS, row-major; lane p then forms rank p's row total and the
+// offset of partition r in its row, lane q its column total (what rank q
+// receives).
 template <bool STREAM>
 __global__ __launch_bounds__(kBlock) void exec_alltoallv(ExecArgs a, VArgs v) {
     __shared__ int64_t m[PURLIN_MAX_RANKS * PURLIN_MAX_RANKS];
     const uint32_t P = v.P;
     const int64_t unit = static_cast<int64_t>(v.unit);
-    for (uint32_t i = threadIdx.x; i < P * P; i += kBlock) m[i] = static_cast<int64_t>(v.counts[i]) * unit;
+    for (uint32_t i = threadIdx.x; i < P * P; i += kBlock) {
+        const uint32_t src = v.transposed ? (i % P) * P + i / P : i;
+        m[i] = static_cast<int64_t>(v.counts[src]) * unit;
+    }
     __syncthreads();
     const uint32_t w = wave_index();
     if (w >= a.n_items) return;
     const uint32_t lane = lane_index();
     const purlin_desc d = a.items[w];
     const uint32_t r = d.part;
-    const int64_t cap = static_cast<int64_t>(v.capacity);
+    const int64_t in_cap = static_cast<int64_t>(v.in_cap), out_cap = static_cast<int64_t>(v.out_cap);
+    const int64_t cap = max(in_cap, out_cap);
     int64_t send_off = 0, c = 0;
     bool ok = true;
     if (lane < P) {
-        int64_t row = 0, col = 0;  // each term is checked against the capacity first: no overflow
+        int64_t row = 0, col = 0;  // each term is checked against a capacity first: no overflow
         for (uint32_t q = 0; q < P; ++q) {
             int64_t x = m[lane * P + q];
             if (x < 0 || x > cap) {
@@ -496,7 +503,7 @@ __global__ __launch_bounds__(kBlock) void exec_alltoallv(ExecArgs a, VArgs v) {
             if (y < 0 || y > cap) y = 0;  // reported by lane q's row
             col += y;
         }
-        ok = ok && row <= cap && col <= cap;
+        ok = ok && row <= in_cap && col <= out_cap;
     }
     const bool all_ok = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(__all(ok)));
     report(v, w, lane, all_ok);
@@ -568,15 +575,16 @@ hipError_t launch_fused_allreduce(const purlin_desc* items, uint64_t n, uint64_t
 }
 
 hipError_t launch_v(purlin_op op, const purlin_desc* items, uint64_t n, int P, purlin_dtype dtype, bool streaming,
-                    void* const* bufs, const int32_t* counts, int32_t* status, uint64_t capacity, uint64_t unit,
-                    hipStream_t stream) {
+                    void* const* bufs, const int32_t* counts, bool counts_transposed, int32_t* status,
+                    uint64_t in_capacity, uint64_t out_capacity, uint64_t unit, hipStream_t stream) {
     if (n == 0) return hipSuccess;
     ExecArgs a{};
     a.items = items;
     a.n_items = n;
     for (int i = 0; i < 2 * P && i < 2 * PURLIN_MAX_RANKS; ++i) a.bufs[i] = static_cast<char*>(bufs[i]);
     for (int p = 0; p < P && p < PURLIN_MAX_RANKS; ++p) a.srcs[p] = static_cast<char*>(bufs[p]);
-    VArgs v{counts, status, capacity, unit, static_cast<uint32_t>(P), dtype == PURLIN_FP32 ? 4u : 2u};
+    VArgs v{counts, status, in_capacity, out_capacity, unit, static_cast<uint32_t>(P), dtype == PURLIN_FP32 ? 4u : 2u,
+            counts_transposed ? 1u : 0u};
     const dim3 grid(static_cast<uint32_t>((n + kWavesPerBlock - 1) / kWavesPerBlock));
     const bool bf16 = dtype == PURLIN_BF16;
     (void)hipGetLastError();

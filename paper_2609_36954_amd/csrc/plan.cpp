@@ -394,15 +394,16 @@ purlin_status cut_items(Plan& out, const purlin_policy& pol) {
 
 }  // namespace
 
-purlin_status build_plan_v(purlin_op op, int P, uint64_t capacity, purlin_dtype dtype, uint64_t chunk, uint64_t unit,
-                           const purlin_policy* policy, uint32_t flags, Plan& out) {
+purlin_status build_plan_v(purlin_op op, int P, uint64_t in_capacity, uint64_t out_capacity, purlin_dtype dtype,
+                           uint64_t chunk, uint64_t unit, const purlin_policy* policy, uint32_t flags, Plan& out) {
     if (op != PURLIN_ALLGATHERV && op != PURLIN_REDUCE_SCATTERV && op != PURLIN_ALLTOALLV) return PURLIN_ERR_INVALID;
     if (dtype != PURLIN_FP32 && dtype != PURLIN_BF16) return PURLIN_ERR_INVALID;
     if (P < 1 || P > PURLIN_MAX_RANKS) return PURLIN_ERR_INVALID;
-    if (flags & ~PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
+    const uint32_t allowed = PURLIN_PLAN_HOST_ONLY | (op == PURLIN_ALLTOALLV ? PURLIN_PLAN_COUNTS_TRANSPOSED : 0u);
+    if (flags & ~allowed) return PURLIN_ERR_INVALID;
     const uint64_t s = dtype == PURLIN_FP32 ? 4 : 2;
     if (chunk < s || chunk % s != 0) return PURLIN_ERR_INVALID;
-    if (capacity > (uint64_t(1) << 58) / s) return PURLIN_ERR_INVALID;
+    if (in_capacity > (uint64_t(1) << 58) / s || out_capacity > (uint64_t(1) << 58) / s) return PURLIN_ERR_INVALID;
     if (unit < 1 || unit > (uint64_t(1) << 31)) return PURLIN_ERR_INVALID;
     purlin_policy pol{};
     if (!parse_policy(policy, pol)) return PURLIN_ERR_INVALID;
@@ -410,16 +411,18 @@ purlin_status build_plan_v(purlin_op op, int P, uint64_t capacity, purlin_dtype 
     out = Plan{};
     out.op = op;
     out.P = P;
-    out.count = capacity;
+    const uint64_t space = op == PURLIN_REDUCE_SCATTERV ? in_capacity : out_capacity;
+    out.count = space;
     out.dtype = dtype;
     out.chunk = chunk;
     out.flags = flags;
     out.elem_bytes = s;
     out.vop = true;
-    out.capacity = capacity;
+    out.in_capacity = in_capacity;
+    out.out_capacity = out_capacity;
     out.unit = unit;
-    out.in_bytes = capacity * s;
-    out.out_bytes = capacity * s;
+    out.in_bytes = in_capacity * s;
+    out.out_bytes = out_capacity * s;
     out.in_mask = out.out_mask = (1u << P) - 1u;
     if (pol.fanout == 0) pol.fanout = 2;
     if (pol.ar_mode == 0) pol.ar_mode = 2;
@@ -427,7 +430,7 @@ purlin_status build_plan_v(purlin_op op, int P, uint64_t capacity, purlin_dtype 
     // The virtual index space: the gathered output (ALLGATHERV), the
     // partitioned input (REDUCE_SCATTERV), or each destination's output
     // (ALLTOALLV), cut into chunks; one descriptor per chunk.
-    const uint64_t vbytes = capacity * s;
+    const uint64_t vbytes = space * s;
     const uint64_t Cv = vbytes ? ceil_div(vbytes, chunk) : 0;
     const uint64_t spaces = op == PURLIN_ALLTOALLV ? uint64_t(P) : 1;
     if (Cv > PURLIN_MAX_ITEMS || Cv * spaces > PURLIN_MAX_ITEMS) return PURLIN_ERR_NOMEM;

@@ -44,9 +44,10 @@ struct Plan {
     int nphases = 0;
     Phase phases[2];
 
-    // Variable-size collectives: capacity in elements, counts' unit.
+    // Variable-size collectives: capacities in elements, counts' unit.
     bool vop = false;
-    uint64_t capacity = 0;
+    uint64_t in_capacity = 0;
+    uint64_t out_capacity = 0;
     uint64_t unit = 1;
 
     // Single-launch AllReduce (ar_mode 3): one launch over all items.
@@ -61,10 +62,11 @@ struct Plan {
 
 // Validates the request and fills `out` (host tables only).  Pure host code.
 // Variable-size collectives (ALLGATHERV, REDUCE_SCATTERV, ALLTOALLV): the
-// table covers a virtual index space of `capacity` elements (per destination
-// for ALLTOALLV); sizes are applied on the device.
-purlin_status build_plan_v(purlin_op op, int P, uint64_t capacity, purlin_dtype dtype, uint64_t chunk, uint64_t unit,
-                           const purlin_policy* policy, uint32_t flags, Plan& out);
+// table covers a virtual index space: the gathered output (out_capacity),
+// the partitioned input (in_capacity) or each destination's output
+// (out_capacity); sizes are applied on the device.
+purlin_status build_plan_v(purlin_op op, int P, uint64_t in_capacity, uint64_t out_capacity, purlin_dtype dtype,
+                           uint64_t chunk, uint64_t unit, const purlin_policy* policy, uint32_t flags, Plan& out);
 
 // `root` is -1 for the non-rooted collectives and a rank for the rooted ones.
 purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,

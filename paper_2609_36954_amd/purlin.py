@@ -33,6 +33,7 @@ ELEM_BYTES = {"fp32": 4, "bf16": 2}
 KIND_COPY = 0
 KIND_REDUCE = 1
 PLAN_HOST_ONLY = 1
+PLAN_COUNTS_TRANSPOSED = 2
 MAX_RANKS = 16
 
 # numpy view of purlin_desc (64 bytes, no padding)
@@ -90,7 +91,7 @@ def lib():
     L.purlin_plan.argtypes = [i32, i32, u64, i32, u64, ctypes.POINTER(_vp)]
     L.purlin_plan_ex.argtypes = [i32, i32, u64, i32, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
     L.purlin_plan_rooted.argtypes = [i32, i32, i32, u64, i32, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
-    L.purlin_plan_v.argtypes = [i32, i32, u64, i32, u64, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
+    L.purlin_plan_v.argtypes = [i32, i32, u64, u64, i32, u64, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
     L.purlin_exec_v.argtypes = [_vp, ctypes.POINTER(_vp), _vp, _vp, _vp]
     L.purlin_plan_info.argtypes = [_vp, _c_u64p, _c_u64p, _c_u64p, _c_u64p]
     L.purlin_plan_descriptors.argtypes = [_vp, ctypes.POINTER(_vp), _c_u64p, _c_u64p]
@@ -157,7 +158,8 @@ def _require_cuda(t, name, itemsize=None):
 class Plan:
     """A planned collective (immutable).  ``exec`` runs it on a stream."""
 
-    def __init__(self, op, P, count, dtype, chunk, policy=None, host_only=False, root=None, unit=None):
+    def __init__(self, op, P, count, dtype, chunk, policy=None, host_only=False, root=None, unit=None,
+                 out_capacity=None, counts_transposed=False):
         if op not in OPS:
             raise PurlinError(PURLIN_ERR_INVALID, f"unknown op {op!r}")
         if dtype not in DTYPES:
@@ -176,9 +178,10 @@ class Plan:
             pol = None
             if policy is not None:
                 pol = policy if isinstance(policy, Policy) else Policy(**policy)
-            st = L.purlin_plan_v(OPS[op], int(P), int(count), DTYPES[dtype], int(chunk), int(unit),
-                                 ctypes.byref(pol) if pol is not None else None,
-                                 PLAN_HOST_ONLY if host_only else 0, ctypes.byref(h))
+            out_cap = int(count) if out_capacity is None else int(out_capacity)
+            flags = (PLAN_HOST_ONLY if host_only else 0) | (PLAN_COUNTS_TRANSPOSED if counts_transposed else 0)
+            st = L.purlin_plan_v(OPS[op], int(P), int(count), out_cap, DTYPES[dtype], int(chunk), int(unit),
+                                 ctypes.byref(pol) if pol is not None else None, flags, ctypes.byref(h))
         elif root is not None:
             pol = None
             if policy is not None:
@@ -282,8 +285,13 @@ def used_buffers(plan):
     return ins, outs
 
 
-def purlin_plan_v(op, P, capacity, dtype, chunk, unit=1, policy=None, host_only=False):
-    return Plan(op, P, capacity, dtype, chunk, policy=policy, host_only=host_only, unit=unit)
+def purlin_plan_v(op, P, in_capacity, dtype, chunk, unit=1, out_capacity=None, policy=None, host_only=False,
+                  counts_transposed=False):
+    """Variable-size plan; ``in_capacity``/``out_capacity`` in elements
+    (``out_capacity`` defaults to ``in_capacity``).  ``counts_transposed``
+    (alltoallv): the P x P sizes are read column-major."""
+    return Plan(op, P, in_capacity, dtype, chunk, policy=policy, host_only=host_only, unit=unit,
+                out_capacity=out_capacity, counts_transposed=counts_transposed)
 
 
 def _buffer_array(plan, ins, outs):

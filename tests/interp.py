@@ -45,20 +45,26 @@ def run(items, phase_begin, bufs, dtype, seed=0):
             apply_item(items[i], bufs, dtype)
 
 
-def run_v(items, bufs, counts, op, P, unit, dtype, capacity):
+def run_v(items, bufs, counts, op, P, unit, dtype, capacity, out_capacity=None, transposed=False):
     """The variable-size mapping on the CPU: every item covers a range of the
     virtual index space; the sizes decide which source / destination and
     offset each element belongs to.  Returns False (writing nothing) for
     sizes the device would reject."""
     s = 2 if dtype == "bf16" else 4
+    in_cap, out_cap = capacity, capacity if out_capacity is None else out_capacity
     c = [int(x) * unit for x in counts]
+    if op == "alltoallv" and transposed:
+        c = [c[(i % P) * P + i // P] for i in range(P * P)]
     if op == "alltoallv":
         m = [c[p * P:(p + 1) * P] for p in range(P)]
-        if any(x < 0 or x > capacity for x in c):
+        if any(x < 0 or x > max(in_cap, out_cap) for x in c):
             return False
-        if any(sum(row) > capacity for row in m) or any(sum(m[p][r] for p in range(P)) > capacity for r in range(P)):
+        if any(sum(row) > in_cap for row in m) or any(sum(m[p][r] for p in range(P)) > out_cap for r in range(P)):
             return False
-    elif any(x < 0 or x > capacity for x in c) or sum(c) > capacity:
+    elif op == "allgatherv":
+        if any(x < 0 or x > in_cap for x in c) or sum(c) > out_cap:
+            return False
+    elif any(x < 0 or x > out_cap for x in c) or sum(c) > in_cap:
         return False
     for it in items:
         lo, hi = int(it["src_off"]) // s, (int(it["src_off"]) + int(it["bytes"])) // s

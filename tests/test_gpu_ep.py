@@ -1,0 +1,291 @@
+"""Expert-parallel dispatch and combine over P simulated ranks on one GPU
+(Table 2: expert parallelism moves tokens to their experts and the expert
+outputs back with AllToAll(V)).
+
+Rank p packs its tokens (purlin_pack); the rows travel by an AllToAllV
+whose P x P sizes are the packs' dest_counts, read from device memory with
+unit = H; each expert rank r marks the rows it received with an exact,
+rank-specific bit flip (a stand-in for the expert computation, which is not
+part of the path); the reverse AllToAllV, reading the same counts
+column-major, brings the rows home in pack order; purlin_unpack combines
+them.  Expected values come from the oracle (pack, AllToAllV, unpack), or at
+full size from the combine's definition on sampled tokens.
+
+Also here: the variable-size collectives with input and output capacities
+that differ, and the column-major counts of AllToAllV.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import CANARY, Guarded, assert_bits_equal, to_device, to_host
+from paper_2609_36954_amd import purlin as PL
+from paper_2609_36954_amd import workloads as W
+from test_planner_v import _inputs, _oracle_v
+
+pytestmark = pytest.mark.gpu
+
+
+def _rank_inputs(P, T, H, K, E, seed, s=1.1):
+    rngs = W.rank_rngs(seed, P)
+    xs = [W.normal_bf16(rngs[p], T * H).reshape(T, H) for p in range(P)]
+    ids = [W.zipf_topk_ids(T, E, K, s, seed * 1000 + p) for p in range(P)]
+    gates = [W.softmax_gates(T, K, seed * 1000 + 500 + p) for p in range(P)]
+    return xs, ids, gates
+
+
+class EPStep:
+    """Device buffers and plans for one dispatch / combine over P ranks."""
+
+    def __init__(self, P, T, H, K, E, chunk=1 << 20):
+        self.P, self.T, self.H, self.K, self.E = P, T, H, K, E
+        rows_in, rows_out = T * K, P * T * K
+        self.fwd = PL.purlin_plan_v("alltoallv", P, rows_in * H, "bf16", chunk, unit=H, out_capacity=rows_out * H)
+        self.bwd = PL.purlin_plan_v("alltoallv", P, rows_out * H, "bf16", chunk, unit=H, out_capacity=rows_in * H,
+                                    counts_transposed=True)
+        dev = "cuda"
+        # Row p of `counts` is rank p's dest_counts (written in place by its pack
+        # when the row is 16-byte aligned, else copied there).
+        self.counts = torch.zeros((P, P), dtype=torch.int32, device=dev)
+        self.direct = (P * 4) % 16 == 0
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.packs = [dict(packed=torch.empty((rows_in, H), dtype=torch.int16, device=dev),
+                           dest_counts=self.counts[p] if self.direct else torch.empty(P, **i32),
+                           dest_offsets=torch.empty(P, **i32), expert_counts=torch.empty(E, **i32),
+                           expert_offsets=torch.empty(E, **i32), pos=torch.empty((T, K), **i32))
+                      for p in range(P)]
+        self.workspace = torch.empty(max(PL.purlin_pack_workspace_size(T, K, E), 16), dtype=torch.uint8, device=dev)
+        self.recv = [torch.empty(rows_out * H, dtype=torch.int16, device=dev) for _ in range(P)]
+        self.back = [torch.empty(rows_in * H, dtype=torch.int16, device=dev) for _ in range(P)]
+        self.status = torch.zeros(P + 2, dtype=torch.int32, device=dev)
+
+    def dispatch(self, xs, ids):
+        P = self.P
+        for p in range(P):
+            PL.purlin_pack(xs[p], ids[p], self.E, P, out=self.packs[p], workspace=self.workspace,
+                           dev_status=self.status[p:p + 1])
+            if not self.direct:
+                self.counts[p].copy_(self.packs[p]["dest_counts"])
+        self.fwd.exec_v([pk["packed"].view(-1) for pk in self.packs], self.recv, self.counts.view(-1),
+                        dev_status=self.status[P:P + 1])
+
+    def combine(self, gates, outs):
+        P = self.P
+        self.bwd.exec_v(self.recv, self.back, self.counts.view(-1), dev_status=self.status[P + 1:P + 2])
+        for p in range(P):
+            PL.purlin_unpack(self.back[p].view(self.T * self.K, self.H), self.packs[p]["pos"], gates[p], out=outs[p])
+
+
+def _mark(recv_rows, r):
+    """The stand-in expert of rank r: flip the low bits of every bf16 word by r + 1."""
+    recv_rows.bitwise_xor_(r + 1)
+
+
+def _dest_of_rows(dest_counts):
+    return np.repeat(np.arange(len(dest_counts)), dest_counts)
+
+
+@pytest.mark.parametrize("P,T,H,K,E", [
+    (1, 33, 40, 2, 4),
+    (2, 50, 24, 2, 8),
+    (3, 70, 7, 3, 9),  # row of 14 bytes: unaligned row offsets
+    (4, 64, 136, 4, 16),
+    (8, 200, 520, 8, 64),
+    (8, 128, 1024, 8, 256),
+])
+def test_ep_dispatch_combine_matches_oracle(P, T, H, K, E):
+    xs_np, ids_np, gates_np = _rank_inputs(P, T, H, K, E, seed=P * 100 + H)
+    ep = EPStep(P, T, H, K, E, chunk=4096)
+    xs = [to_device(x) for x in xs_np]
+    ids = [to_device(i) for i in ids_np]
+    gates = [to_device(g) for g in gates_np]
+    ep.dispatch(xs, ids)
+    torch.cuda.synchronize()
+    packs = [oracle.pack(xs_np[p], ids_np[p], E, P) for p in range(P)]
+    m = [[int(c) for c in packs[p]["dest_counts"]] for p in range(P)]
+    assert np.array_equal(to_host(ep.counts, np.int32).reshape(P, P), np.array(m))
+    want_recv = oracle.all_to_all_v([pk["packed"].reshape(-1) for pk in packs],
+                                    [[c * H for c in row] for row in m], "bf16")
+    for r in range(P):
+        got = to_host(ep.recv[r], np.uint16)[: want_recv[r].size]
+        assert_bits_equal(got, want_recv[r], "bf16", f"dispatch: rank {r} received")
+        rows_r = sum(m[p][r] for p in range(P))
+        _mark(ep.recv[r][: rows_r * H], r)
+    outs = [Guarded(T * H * 2, torch.int16) for _ in range(P)]
+    ep.combine(gates, [o.t.view(T, H) for o in outs])
+    torch.cuda.synchronize()
+    assert not ep.status.any().item()
+    for p in range(P):
+        mark = (_dest_of_rows(packs[p]["dest_counts"]) + 1).astype(np.uint16)
+        y = packs[p]["packed"] ^ mark[:, None]
+        assert np.array_equal(to_host(ep.back[p], np.uint16).reshape(T * K, H), y), f"combine exchange, rank {p}"
+        want = oracle.unpack(y, packs[p]["pos"], gates_np[p])
+        assert outs[p].intact()
+        assert_bits_equal(to_host(outs[p].t, np.uint16).reshape(T, H), want, "bf16", f"combined output, rank {p}")
+
+
+def test_ep_dispatch_combine_full_size_p8():
+    """T = 4096 tokens per rank, H = 7168, E = 256, K = 8 (Zipf(1.1) routing)
+    on P = 8 ranks.  Checked by properties over every row and by the
+    combine's definition on sampled tokens."""
+    P, T, H, K, E = 8, 4096, 7168, 8, 256
+    xs_np, ids_np, gates_np = _rank_inputs(P, T, H, K, E, seed=4)
+    ep = EPStep(P, T, H, K, E)
+    xs = [to_device(x) for x in xs_np]
+    ids = [to_device(i) for i in ids_np]
+    gates = [to_device(g) for g in gates_np]
+    ep.dispatch(xs, ids)
+    torch.cuda.synchronize()
+    m = to_host(ep.counts, np.int32).reshape(P, P)
+    for p in range(P):  # sizes and positions from the oracle's pack (of 8 columns: they do not depend on H)
+        meta = oracle.pack(xs_np[p][:, :8], ids_np[p], E, P)
+        assert np.array_equal(m[p], meta["dest_counts"]), f"dest_counts of rank {p}"
+        assert np.array_equal(to_host(ep.packs[p]["pos"], np.int32).reshape(T, K), meta["pos"]), f"pos of rank {p}"
+    # Every received row is the token row it names: rank p's packed rows sent to r.
+    for r in range(P):
+        pieces = []
+        for p in range(P):
+            start = int(m[p, :r].sum())
+            pieces.append(ep.packs[p]["packed"][start:start + m[p, r]])
+        rows_r = int(m[:, r].sum())
+        got = ep.recv[r][: rows_r * H].view(rows_r, H)
+        assert torch.equal(got, torch.cat(pieces)), f"dispatch: rank {r}"
+        _mark(got, r)
+    outs = [torch.empty((T, H), dtype=torch.int16, device="cuda") for _ in range(P)]
+    ep.combine(gates, outs)
+    torch.cuda.synchronize()
+    assert not ep.status.any().item()
+    rng = np.random.default_rng(44)
+    for p in range(P):
+        dest = torch.from_numpy(_dest_of_rows(m[p]).astype(np.int16)).to("cuda")
+        back = ep.back[p].view(T * K, H)
+        assert torch.equal(back ^ (dest[:, None] + 1), ep.packs[p]["packed"]), f"combine exchange, rank {p}"
+        # Sampled tokens: out[t] = sum_k gate[t, k] * expert_r(x[t]) in slot order,
+        # expert_r(row) = row ^ (r + 1) with r the rank owning expert ids[t, k].
+        ts = np.sort(rng.choice(T, 64, replace=False))
+        rows = np.repeat(xs_np[p][ts], K, axis=0)
+        owner = (ids_np[p][ts].reshape(-1) // (E // P) + 1).astype(np.uint16)
+        y = rows ^ owner[:, None]
+        want = oracle.unpack(y, np.arange(len(ts) * K, dtype=np.int32).reshape(len(ts), K), gates_np[p][ts])
+        got = to_host(outs[p], np.uint16).reshape(T, H)[ts]
+        assert_bits_equal(got, want, "bf16", f"combined output sample, rank {p}")
+
+
+def test_ep_round_trip_in_one_graph():
+    """Dispatch and combine captured once, replayed with different routing:
+    the sizes are read on the device each time."""
+    P, T, H, K, E = 8, 96, 256, 4, 32
+    ep = EPStep(P, T, H, K, E, chunk=8192)
+    xs = [torch.empty((T, H), dtype=torch.int16, device="cuda") for _ in range(P)]
+    ids = [torch.empty((T, K), dtype=torch.int32, device="cuda") for _ in range(P)]
+    gates = [torch.empty((T, K), dtype=torch.float32, device="cuda") for _ in range(P)]
+    outs = [torch.empty((T, H), dtype=torch.int16, device="cuda") for _ in range(P)]
+
+    def load(seed):
+        xs_np, ids_np, gates_np = _rank_inputs(P, T, H, K, E, seed=seed)
+        for p in range(P):
+            xs[p].copy_(to_device(xs_np[p]))
+            ids[p].copy_(to_device(ids_np[p]))
+            gates[p].copy_(to_device(gates_np[p]))
+        return xs_np, ids_np, gates_np
+
+    load(1)
+    ep.dispatch(xs, ids)
+    ep.combine(gates, outs)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            ep.dispatch(xs, ids)
+            ep.combine(gates, outs)
+    for rep, seed in enumerate((2, 3, 4)):
+        xs_np, ids_np, gates_np = load(seed)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for p in range(P):
+            pk = oracle.pack(xs_np[p], ids_np[p], E, P)
+            want = oracle.unpack(pk["packed"], pk["pos"], gates_np[p])  # identity experts
+            assert_bits_equal(to_host(outs[p], np.uint16).reshape(T, H), want, "bf16", f"replay {rep} rank {p}")
+
+
+ASYM = [("allgatherv", 1500, 9000), ("reduce_scatterv", 9000, 1500), ("alltoallv", 3000, 9000),
+        ("alltoallv", 9000, 3000)]
+
+
+@pytest.mark.parametrize("op,in_cap,out_cap", ASYM)
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_v_separate_capacities(op, in_cap, out_cap, dtype):
+    P, s = 6, 4 if dtype == "fp32" else 2
+    rng = np.random.default_rng(in_cap + out_cap + s)
+    if op == "allgatherv":
+        counts = [int(x) for x in rng.integers(0, in_cap + 1, P)]
+        counts[2] = in_cap
+    elif op == "reduce_scatterv":
+        counts = [int(x) for x in rng.integers(0, out_cap + 1, P)]
+        counts[3] = out_cap
+    else:
+        mm = np.zeros((P, P), np.int64)
+        for p in range(P):
+            for r in range(P):
+                room = min(in_cap - mm[p].sum(), out_cap - mm[:, r].sum())
+                mm[p, r] = rng.integers(0, room + 1) if r < P - 1 else room
+        counts = [int(x) for x in mm.reshape(-1)]
+    ins_np = _inputs(P, in_cap, dtype, seed=9)
+    want = _oracle_v(op, ins_np, counts, P, dtype, 1)
+    plan = PL.purlin_plan_v(op, P, in_cap, dtype, 512, unit=1, out_capacity=out_cap)
+    outs = [Guarded(out_cap * s, torch.float32 if dtype == "fp32" else torch.int16) for _ in range(P)]
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    plan.exec_v([to_device(a) for a in ins_np], [o.t for o in outs], to_device(np.asarray(counts, np.int32)),
+                dev_status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    for r in range(P):
+        assert outs[r].intact()
+        got = to_host(outs[r].t, np.uint16 if dtype == "bf16" else np.float32)
+        n = len(want[r])
+        assert_bits_equal(got[:n], want[r], dtype, f"{op} rank {r}")
+        assert np.all(got[n:].view(np.uint8) == CANARY)
+
+
+@pytest.mark.parametrize("op,in_cap,out_cap,counts", [
+    ("allgatherv", 10, 100, [11, 0]),
+    ("allgatherv", 100, 10, [6, 5]),
+    ("reduce_scatterv", 10, 100, [6, 5]),
+    ("reduce_scatterv", 100, 10, [11, 0]),
+    ("alltoallv", 10, 100, [6, 5, 0, 0]),
+    ("alltoallv", 100, 10, [6, 0, 5, 0]),
+])
+def test_v_sizes_beyond_either_capacity_write_nothing(op, in_cap, out_cap, counts):
+    plan = PL.purlin_plan_v(op, 2, in_cap, "fp32", 64, unit=1, out_capacity=out_cap)
+    ins = [to_device(np.arange(in_cap, dtype=np.float32)) for _ in range(2)]
+    outs = [Guarded(out_cap * 4, torch.float32) for _ in range(2)]
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    plan.exec_v(ins, [o.t for o in outs], to_device(np.asarray(counts, np.int32)), dev_status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 1
+    for o in outs:
+        assert o.intact() and bool(torch.all(o.t.view(torch.uint8) == CANARY).item())
+
+
+@pytest.mark.parametrize("P", [2, 5, 16])
+def test_alltoallv_counts_transposed(P):
+    cap = 4000
+    rng = np.random.default_rng(P + 1)
+    mm = rng.integers(0, cap // P + 1, (P, P))
+    ins_np = _inputs(P, cap, "bf16", seed=P)
+    want = oracle.all_to_all_v(ins_np, mm.tolist(), "bf16")
+    plan = PL.purlin_plan_v("alltoallv", P, cap, "bf16", 1024, unit=1, counts_transposed=True)
+    outs = [Guarded(cap * 2, torch.int16) for _ in range(P)]
+    plan.exec_v([to_device(a) for a in ins_np], [o.t for o in outs],
+                to_device(np.ascontiguousarray(mm.T).astype(np.int32).reshape(-1)))
+    torch.cuda.synchronize()
+    for r in range(P):
+        assert outs[r].intact()
+        got = to_host(outs[r].t, np.uint16)
+        assert_bits_equal(got[: len(want[r])], want[r], "bf16", f"rank {r}")
+        assert np.all(got[len(want[r]):].view(np.uint8) == CANARY)

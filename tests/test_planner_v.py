@@ -100,7 +100,7 @@ def test_v_plan_tables():
 
 def _plan_v_status(op, P, cap, dtype=1, chunk=256, unit=1, flags=PL.PLAN_HOST_ONLY):
     h = ctypes.c_void_p()
-    st = PL.lib().purlin_plan_v(op, P, cap, dtype, chunk, unit, None, flags, ctypes.byref(h))
+    st = PL.lib().purlin_plan_v(op, P, cap, cap, dtype, chunk, unit, None, flags, ctypes.byref(h))
     if h.value:
         PL.lib().purlin_plan_destroy(h)
     return st
@@ -127,3 +127,116 @@ def test_exec_v_and_exec_reject_the_other_kind():
     assert L.purlin_exec_v(f.handle, bufs, 0x5000, None, None) == INVALID
     assert L.purlin_exec_v(v.handle, bufs, None, None, None) == INVALID  # no counts
     assert L.purlin_exec_v(v.handle, bufs, 0x5002, None, None) == INVALID  # misaligned counts
+
+
+ASYM = [("allgatherv", 150, 1000), ("reduce_scatterv", 1000, 150), ("alltoallv", 400, 900), ("alltoallv", 900, 400)]
+
+
+@pytest.mark.parametrize("op,in_cap,out_cap", ASYM)
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_v_mapping_with_separate_capacities(op, in_cap, out_cap, dtype):
+    """Inputs and outputs of different sizes (e.g. expert-parallel dispatch:
+    T*K rows sent, up to P*T*K received)."""
+    P, s = 6, S[dtype]
+    rng = np.random.default_rng(len(op) + in_cap)
+    if op == "allgatherv":
+        counts = [int(x) for x in rng.integers(0, in_cap + 1, P)]
+        counts[-1] = in_cap  # a full input
+    elif op == "reduce_scatterv":
+        counts = [int(x) for x in rng.integers(0, out_cap + 1, P)]
+        counts[0] = out_cap
+    else:
+        m = np.zeros((P, P), np.int64)
+        for p in range(P):  # row sums <= in_cap, column sums <= out_cap
+            for r in range(P):
+                room = min(in_cap - m[p].sum(), out_cap - m[:, r].sum())
+                m[p, r] = rng.integers(0, room + 1) if r < P - 1 else room
+        counts = [int(x) for x in m.reshape(-1)]
+    ins = _inputs(P, in_cap, dtype, seed=7)
+    want = _oracle_v(op, ins, counts, P, dtype, 1)
+    plan = PL.purlin_plan_v(op, P, in_cap, dtype, 64 * s, unit=1, out_capacity=out_cap, host_only=True)
+    assert plan.in_bytes == in_cap * s and plan.out_bytes == out_cap * s
+    items, _ = plan.items()
+    bufs = [np.frombuffer(a.tobytes(), np.uint8).copy() for a in ins] + \
+           [np.full(out_cap * s, 0xA5, np.uint8) for _ in range(P)]
+    assert interp.run_v(items, bufs, counts, op, P, 1, dtype, in_cap, out_cap)
+    for r in range(P):
+        n = len(want[r])
+        got = bufs[P + r][: n * s].view(np.uint16 if dtype == "bf16" else np.uint32)
+        assert np.array_equal(got, want[r].view(got.dtype)), (op, r)
+        assert np.all(bufs[P + r][n * s:] == 0xA5)
+
+
+@pytest.mark.parametrize("op,in_cap,out_cap,counts", [
+    ("allgatherv", 10, 100, [11, 0]),  # one input overflows its buffer
+    ("allgatherv", 100, 10, [6, 5]),  # the gathered total overflows
+    ("reduce_scatterv", 10, 100, [6, 5]),  # the partitioned total overflows the input
+    ("reduce_scatterv", 100, 10, [11, 0]),  # one output overflows
+    ("alltoallv", 10, 100, [6, 5, 0, 0]),  # a send row overflows the input
+    ("alltoallv", 100, 10, [6, 0, 5, 0]),  # a receive column overflows the output
+])
+def test_v_rejects_sizes_beyond_either_capacity(op, in_cap, out_cap, counts):
+    plan = PL.purlin_plan_v(op, 2, in_cap, "fp32", 64, unit=1, out_capacity=out_cap, host_only=True)
+    items, _ = plan.items()
+    bufs = [np.zeros(in_cap * 4, np.uint8) for _ in range(2)] + [np.zeros(out_cap * 4, np.uint8) for _ in range(2)]
+    assert not interp.run_v(items, bufs, counts, op, 2, 1, "fp32", in_cap, out_cap)
+
+
+@pytest.mark.parametrize("op,flags,want", [
+    (10, 3, 0), (8, 3, INVALID), (9, 3, INVALID), (10, 5, INVALID)])
+def test_plan_v_counts_transposed_flag(op, flags, want):
+    assert _plan_v_status(op, 4, 1000, flags=flags) == want
+
+
+@pytest.mark.parametrize("P", [1, 3, 8])
+def test_alltoallv_transposed_counts(P):
+    """Column-major sizes give the same exchange as the row-major matrix."""
+    rng = np.random.default_rng(P)
+    cap = 500
+    m = rng.integers(0, cap // P + 1, (P, P))
+    ins = _inputs(P, cap, "bf16", seed=P)
+    want = oracle.all_to_all_v(ins, m.tolist(), "bf16")
+    plan = PL.purlin_plan_v("alltoallv", P, cap, "bf16", 128, unit=1, host_only=True, counts_transposed=True)
+    items, _ = plan.items()
+    bufs = [np.frombuffer(a.tobytes(), np.uint8).copy() for a in ins] + \
+           [np.full(cap * 2, 0xA5, np.uint8) for _ in range(P)]
+    assert interp.run_v(items, bufs, m.T.reshape(-1).tolist(), "alltoallv", P, 1, "bf16", cap, transposed=True)
+    for r in range(P):
+        n = len(want[r])
+        assert np.array_equal(bufs[P + r][: n * 2].view(np.uint16), want[r])
+        assert np.all(bufs[P + r][n * 2:] == 0xA5)
+
+
+def test_expert_parallel_round_trip_mapping():
+    """Dispatch (pack, then AllToAllV of rows with the packs' dest_counts)
+    and combine (the reverse AllToAllV with the same counts read
+    column-major, then unpack) on the CPU: the reverse exchange restores
+    every rank's packed order, so with identity experts the combine equals
+    unpack(pack) of each rank (Table 2: EP dispatch / combine)."""
+    P, T, H, K, E = 4, 40, 6, 3, 8
+    rng = np.random.default_rng(11)
+    xs = [oracle.narrow(rng.standard_normal((T, H)).astype(np.float32)) for _ in range(P)]
+    ids = [np.stack([rng.permutation(E)[:K] for _ in range(T)]).astype(np.int32) for _ in range(P)]
+    gates = [rng.random((T, K)).astype(np.float32) for _ in range(P)]
+    packs = [oracle.pack(xs[p], ids[p], E, P) for p in range(P)]
+    counts = [int(x) for p in range(P) for x in packs[p]["dest_counts"]]  # row p = rank p's dest_counts
+    in_cap, out_cap = T * K * H, P * T * K * H
+    fwd = PL.purlin_plan_v("alltoallv", P, in_cap, "bf16", 64, unit=H, out_capacity=out_cap, host_only=True)
+    bwd = PL.purlin_plan_v("alltoallv", P, out_cap, "bf16", 64, unit=H, out_capacity=in_cap, host_only=True,
+                           counts_transposed=True)
+    bufs = [np.frombuffer(packs[p]["packed"].tobytes(), np.uint8).copy() for p in range(P)] + \
+           [np.zeros(out_cap * 2, np.uint8) for _ in range(P)]
+    assert interp.run_v(fwd.items()[0], bufs, counts, "alltoallv", P, H, "bf16", in_cap, out_cap)
+    recv = bufs[P:]
+    want_recv = oracle.all_to_all_v([pk["packed"].reshape(-1) for pk in packs],
+                                    [[c * H for c in counts[p * P:(p + 1) * P]] for p in range(P)], "bf16")
+    for r in range(P):
+        assert np.array_equal(recv[r][: want_recv[r].size * 2].view(np.uint16), want_recv[r])
+    bufs2 = recv + [np.zeros(in_cap * 2, np.uint8) for _ in range(P)]
+    assert interp.run_v(bwd.items()[0], bufs2, counts, "alltoallv", P, H, "bf16", out_cap, in_cap, transposed=True)
+    for p in range(P):
+        back = bufs2[P + p].view(np.uint16).reshape(T * K, H)
+        assert np.array_equal(back, packs[p]["packed"])
+        want = oracle.unpack(packs[p]["packed"], packs[p]["pos"], gates[p])
+        got = oracle.unpack(back, packs[p]["pos"], gates[p])
+        assert np.array_equal(got, want)
