@@ -198,9 +198,14 @@ PURLIN_API purlin_status purlin_plan_rooted(purlin_op op, int P, int root, uint6
  * run time, so they may be produced by an earlier kernel on the stream (e.g.
  * purlin_pack's dest_counts, with unit = the row length) and the call can be
  * captured in a graph.  Counts are in units of `unit` elements
- * (1 <= unit <= 2^31).  `chunk_bytes` cuts the virtual index space (the
- * gathered output, the partitioned input, or each destination's output)
- * into chunks, as for the fixed-size plans.  Policy and errors as for
+ * (1 <= unit <= 2^31).  `chunk_bytes` cuts a virtual index space into
+ * chunks, as for the fixed-size plans: the gathered output (ALLGATHERV,
+ * out_capacity), the partitioned input (REDUCE_SCATTERV, in_capacity), or
+ * for ALLTOALLV each destination's output (descriptor part = r, dst_buf =
+ * out_r) or, when in_capacity < out_capacity, each source's input (part =
+ * p, src_buf = in_p, dst_step = 1: the sizes pick the output).  Covering the
+ * smaller side keeps a receive buffer sized for the worst case (P*T*K rows
+ * of an expert-parallel dispatch) from adding idle work items.  Policy and errors as for
  * purlin_plan_ex; flags: PURLIN_PLAN_HOST_ONLY, and for ALLTOALLV
  * PURLIN_PLAN_COUNTS_TRANSPOSED.  PURLIN_ERR_INVALID also for a non-V op, a
  * bad unit or a flag the op does not take. */

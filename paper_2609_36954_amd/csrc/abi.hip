@@ -184,7 +184,8 @@ purlin_status purlin_exec_v(purlin_plan_t plan, void* const* bufs, const int32_t
     const purlin::Phase& ph = p.phases[0];
     const hipError_t e =
         purlin::launch_v(p.op, p.d_items, ph.count, p.P, p.dtype, ph.nt_load || ph.nt_store, bufs, counts,
-                         (p.flags & PURLIN_PLAN_COUNTS_TRANSPOSED) != 0, dev_status, p.in_capacity, p.out_capacity,
+                         (p.flags & PURLIN_PLAN_COUNTS_TRANSPOSED) != 0, p.v_src_major, dev_status, p.in_capacity,
+                         p.out_capacity,
                          p.unit, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
 }

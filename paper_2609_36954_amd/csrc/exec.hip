@@ -373,6 +373,7 @@ struct VArgs {
     uint32_t P;
     uint32_t elem_bytes;
     uint32_t transposed;  // AllToAllV: counts are column-major
+    uint32_t src_major;   // AllToAllV: items cover each source's input
 };
 
 __device__ __forceinline__ int64_t readlane64(int64_t v, int lane) {
@@ -463,12 +464,15 @@ __global__ __launch_bounds__(kBlock) void exec_reducescatterv(ExecArgs a, VArgs 
     }
 }
 
-// AllToAllV: item d covers bytes [src_off, src_off + bytes) of destination
-// d.part's output.  counts[p * P + r] = elements rank p sends to rank r
-// (counts[r * P + p] when transposed).  The P x P sizes are staged once per
-// workgroup in LDS, row-major; lane p then forms rank p's row total and the
-// offset of partition r in its row, lane q its column total (what rank q
-// receives).
+// AllToAllV.  counts[p * P + r] = elements rank p sends to rank r
+// (counts[r * P + p] when transposed).  Item d covers bytes [src_off,
+// src_off + bytes) of a virtual space: destination d.part's output, whose
+// pieces come from the sources in rank order, or (source-major) source
+// d.part's input, whose pieces go to the destinations in rank order.  The
+// P x P sizes are staged once per workgroup in LDS, row-major; lane q then
+// checks row q (what q sends) and column q (what q receives) and forms, for
+// piece q of the item's space, its length and where it starts on the other
+// side.
 template <bool STREAM>
 __global__ __launch_bounds__(kBlock) void exec_alltoallv(ExecArgs a, VArgs v) {
     __shared__ int64_t m[PURLIN_MAX_RANKS * PURLIN_MAX_RANKS];
@@ -483,25 +487,31 @@ __global__ __launch_bounds__(kBlock) void exec_alltoallv(ExecArgs a, VArgs v) {
     if (w >= a.n_items) return;
     const uint32_t lane = lane_index();
     const purlin_desc d = a.items[w];
-    const uint32_t r = d.part;
+    const uint32_t k = d.part;
+    const bool src_major = v.src_major != 0;
     const int64_t in_cap = static_cast<int64_t>(v.in_cap), out_cap = static_cast<int64_t>(v.out_cap);
     const int64_t cap = max(in_cap, out_cap);
-    int64_t send_off = 0, c = 0;
+    // Piece `lane` of the space: destination-major, source lane's part for k
+    // (m[lane][k]) starting at sum_{j<k} m[lane][j] in in_lane; source-major,
+    // k's part for destination lane (m[k][lane]) landing at sum_{j<k}
+    // m[j][lane] in out_lane.
+    int64_t other = 0, c = 0;
     bool ok = true;
     if (lane < P) {
         int64_t row = 0, col = 0;  // each term is checked against a capacity first: no overflow
-        for (uint32_t q = 0; q < P; ++q) {
-            int64_t x = m[lane * P + q];
+        for (uint32_t j = 0; j < P; ++j) {
+            int64_t x = m[lane * P + j];
             if (x < 0 || x > cap) {
                 ok = false;
                 x = 0;
             }
-            if (q < r) send_off += x;
-            if (q == r) c = x;
             row += x;
-            int64_t y = m[q * P + lane];
-            if (y < 0 || y > cap) y = 0;  // reported by lane q's row
+            int64_t y = m[j * P + lane];
+            if (y < 0 || y > cap) y = 0;  // reported by lane j's row
             col += y;
+            const int64_t e = src_major ? y : x;
+            if (j < k) other += e;
+            if (j == k) c = e;
         }
         ok = ok && row <= in_cap && col <= out_cap;
     }
@@ -510,22 +520,29 @@ __global__ __launch_bounds__(kBlock) void exec_alltoallv(ExecArgs a, VArgs v) {
     if (!all_ok) return;
     const uint64_t s = v.elem_bytes;
     const int64_t lo_v = static_cast<int64_t>(d.src_off / s), hi_v = lo_v + static_cast<int64_t>(d.bytes / s);
-    int64_t recv = 0;
-    for (uint32_t p = 0; p < P; ++p) {
-        const int64_t cp = readlane64(c, p), sp = readlane64(send_off, p);
-        const int64_t x = max(lo_v, recv), y = min(hi_v, recv + cp);
+    int64_t base = 0;
+    for (uint32_t q = 0; q < P; ++q) {
+        const int64_t cq = readlane64(c, q), oq = readlane64(other, q);
+        const int64_t x = max(lo_v, base), y = min(hi_v, base + cq);
         if (x < y) {
             purlin_desc sub = d;
-            sub.src_buf = p;
             sub.ndst = 1;
-            sub.dst_buf = P + r;
             sub.dst_step = 0;
-            sub.src_off = uint64_t(sp + (x - recv)) * s;
-            sub.dst_off = uint64_t(x) * s;
+            if (src_major) {
+                sub.src_buf = k;
+                sub.dst_buf = P + q;
+                sub.src_off = uint64_t(x) * s;
+                sub.dst_off = uint64_t(oq + (x - base)) * s;
+            } else {
+                sub.src_buf = q;
+                sub.dst_buf = P + k;
+                sub.src_off = uint64_t(oq + (x - base)) * s;
+                sub.dst_off = uint64_t(x) * s;
+            }
             sub.bytes = uint64_t(y - x) * s;
             run_copy<kCopyUnroll, STREAM, STREAM>(a, sub, lane);
         }
-        recv += cp;
+        base += cq;
     }
 }
 
@@ -575,8 +592,8 @@ hipError_t launch_fused_allreduce(const purlin_desc* items, uint64_t n, uint64_t
 }
 
 hipError_t launch_v(purlin_op op, const purlin_desc* items, uint64_t n, int P, purlin_dtype dtype, bool streaming,
-                    void* const* bufs, const int32_t* counts, bool counts_transposed, int32_t* status,
-                    uint64_t in_capacity, uint64_t out_capacity, uint64_t unit, hipStream_t stream) {
+                    void* const* bufs, const int32_t* counts, bool counts_transposed, bool source_major,
+                    int32_t* status, uint64_t in_capacity, uint64_t out_capacity, uint64_t unit, hipStream_t stream) {
     if (n == 0) return hipSuccess;
     ExecArgs a{};
     a.items = items;
@@ -584,7 +601,7 @@ hipError_t launch_v(purlin_op op, const purlin_desc* items, uint64_t n, int P, p
     for (int i = 0; i < 2 * P && i < 2 * PURLIN_MAX_RANKS; ++i) a.bufs[i] = static_cast<char*>(bufs[i]);
     for (int p = 0; p < P && p < PURLIN_MAX_RANKS; ++p) a.srcs[p] = static_cast<char*>(bufs[p]);
     VArgs v{counts, status, in_capacity, out_capacity, unit, static_cast<uint32_t>(P), dtype == PURLIN_FP32 ? 4u : 2u,
-            counts_transposed ? 1u : 0u};
+            counts_transposed ? 1u : 0u, source_major ? 1u : 0u};
     const dim3 grid(static_cast<uint32_t>((n + kWavesPerBlock - 1) / kWavesPerBlock));
     const bool bf16 = dtype == PURLIN_BF16;
     (void)hipGetLastError();

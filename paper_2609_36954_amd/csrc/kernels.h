@@ -38,8 +38,8 @@ hipError_t launch_fused_allreduce(const purlin_desc* items, uint64_t n, uint64_t
 // (int32, in units of `unit` elements).  `status` (optional) receives 0 or
 // 1 (invalid sizes: the call then writes nothing).
 hipError_t launch_v(purlin_op op, const purlin_desc* items, uint64_t n, int P, purlin_dtype dtype, bool streaming,
-                    void* const* bufs, const int32_t* counts, bool counts_transposed, int32_t* status,
-                    uint64_t in_capacity, uint64_t out_capacity, uint64_t unit, hipStream_t stream);
+                    void* const* bufs, const int32_t* counts, bool counts_transposed, bool source_major,
+                    int32_t* status, uint64_t in_capacity, uint64_t out_capacity, uint64_t unit, hipStream_t stream);
 
 struct PackWorkspace {
     int32_t* tile_base;  // [ntiles * E]: per-tile expert counts, then row bases

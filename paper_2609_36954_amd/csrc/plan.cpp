@@ -411,7 +411,11 @@ purlin_status build_plan_v(purlin_op op, int P, uint64_t in_capacity, uint64_t o
     out = Plan{};
     out.op = op;
     out.P = P;
-    const uint64_t space = op == PURLIN_REDUCE_SCATTERV ? in_capacity : out_capacity;
+    // ALLTOALLV covers the side whose buffers are smaller: a receive buffer
+    // sized for the worst case (every rank sending everything to one rank)
+    // then adds no idle work items.
+    const bool src_major = op == PURLIN_ALLTOALLV && in_capacity < out_capacity;
+    const uint64_t space = (op == PURLIN_REDUCE_SCATTERV || src_major) ? in_capacity : out_capacity;
     out.count = space;
     out.dtype = dtype;
     out.chunk = chunk;
@@ -420,6 +424,7 @@ purlin_status build_plan_v(purlin_op op, int P, uint64_t in_capacity, uint64_t o
     out.vop = true;
     out.in_capacity = in_capacity;
     out.out_capacity = out_capacity;
+    out.v_src_major = src_major;
     out.unit = unit;
     out.in_bytes = in_capacity * s;
     out.out_bytes = out_capacity * s;
@@ -429,7 +434,8 @@ purlin_status build_plan_v(purlin_op op, int P, uint64_t in_capacity, uint64_t o
 
     // The virtual index space: the gathered output (ALLGATHERV), the
     // partitioned input (REDUCE_SCATTERV), or each destination's output
-    // (ALLTOALLV), cut into chunks; one descriptor per chunk.
+    // (ALLTOALLV; each source's input when source-major), cut into chunks;
+    // one descriptor per chunk.
     const uint64_t vbytes = space * s;
     const uint64_t Cv = vbytes ? ceil_div(vbytes, chunk) : 0;
     const uint64_t spaces = op == PURLIN_ALLTOALLV ? uint64_t(P) : 1;
@@ -445,7 +451,10 @@ purlin_status build_plan_v(purlin_op op, int P, uint64_t in_capacity, uint64_t o
                 else if (op == PURLIN_REDUCE_SCATTERV)
                     out.descs.push_back(make_desc(PURLIN_KIND_REDUCE, 0, P, 0, 1, 1, out0, 0, off, off, len, 0,
                                                   static_cast<uint32_t>(c)));
-                else
+                else if (src_major)  // source r's input; the sizes pick the output
+                    out.descs.push_back(make_desc(PURLIN_KIND_COPY, 0, 1, r, 0, 1, out0, 1, off, off, len, r,
+                                                  static_cast<uint32_t>(c)));
+                else  // destination r's output; the sizes pick the input
                     out.descs.push_back(make_desc(PURLIN_KIND_COPY, 0, 1, 0, 0, 1, out0 + r, 0, off, off, len, r,
                                                   static_cast<uint32_t>(c)));
             }

@@ -49,6 +49,7 @@ struct Plan {
     uint64_t in_capacity = 0;
     uint64_t out_capacity = 0;
     uint64_t unit = 1;
+    bool v_src_major = false;  // ALLTOALLV: descriptors cover each source's input
 
     // Single-launch AllReduce (ar_mode 3): one launch over all items.
     bool fused = false;

@@ -89,7 +89,17 @@ def run_v(items, bufs, counts, op, P, unit, dtype, capacity, out_capacity=None, 
                     out = narrow(acc) if dtype == "bf16" else acc
                     bufs[P + r][(x - off) * s:(y - off) * s] = out.view(np.uint8)
                 off += c[r]
-        else:
+        elif int(it["dst_step"]) == 1:  # source-major: the item covers source `part`'s input
+            p = int(it["part"])
+            send = 0
+            for r in range(P):
+                recv = sum(m[q][r] for q in range(p))
+                x, y = max(lo, send), min(hi, send + m[p][r])
+                if x < y:
+                    b0 = recv + (x - send)
+                    bufs[P + r][b0 * s:(b0 + y - x) * s] = bufs[p][x * s:y * s]
+                send += m[p][r]
+        else:  # destination-major: the item covers destination `part`'s output
             r = int(it["part"])
             recv = 0
             for p in range(P):

@@ -240,3 +240,17 @@ def test_expert_parallel_round_trip_mapping():
         want = oracle.unpack(packs[p]["packed"], packs[p]["pos"], gates[p])
         got = oracle.unpack(back, packs[p]["pos"], gates[p])
         assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("in_cap,out_cap,src_major", [(100, 800, True), (800, 100, False), (300, 300, False)])
+def test_alltoallv_covers_the_smaller_side(in_cap, out_cap, src_major):
+    P, chunk = 4, 64
+    plan = PL.purlin_plan_v("alltoallv", P, in_cap, "fp32", chunk, unit=1, out_capacity=out_cap, host_only=True)
+    d = plan.descriptors()
+    space = min(in_cap, out_cap) * 4
+    assert len(d) == P * -(-space // chunk)
+    assert sorted(set(d["part"].tolist())) == list(range(P))
+    if src_major:
+        assert np.array_equal(d["src_buf"], d["part"]) and np.all(d["dst_step"] == 1) and np.all(d["dst_buf"] == P)
+    else:
+        assert np.array_equal(d["dst_buf"], d["part"] + P) and np.all(d["dst_step"] == 0)
