@@ -50,6 +50,12 @@ __device__ __forceinline__ uint32_t wave_index() {
 
 __device__ __forceinline__ uint32_t lane_index() { return threadIdx.x & (kWave - 1); }
 
+__device__ __forceinline__ int64_t readlane64(int64_t v, int lane) {
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(v), lane);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(static_cast<uint64_t>(v) >> 32), lane);
+    return static_cast<int64_t>((uint64_t(hi) << 32) | lo);
+}
+
 // 16-byte global access; NT selects the non-temporal (streaming) form,
 // which tells the caches the line will not be reused.
 template <bool NT>
@@ -242,17 +248,20 @@ __global__ __launch_bounds__(kBlock) void exec_reduce(ExecArgs a) {
 // inside one launch.  All ranks share one address space, so there is no
 // staging; the notification is a per-chunk counter of finished reduce items.
 //
-// * Items are claimed in table order through an atomic counter: every
+// * Items are claimed in table order through a ticket counter: every
 //   reduce item precedes every copy item, so a copy item is only ever
 //   claimed after all reduce items have been claimed by running waves, and
 //   reduce items never wait.  Every wait therefore ends.
-// * Counters are never reset (the epochs of Section 4.2): chunk (k, c) is
-//   ready in launch e when its counter reaches (e + 1) * (its reduce
-//   items).  The last wave to finish resets the claim and done counters and
-//   advances the epoch for the next launch on the stream.
+// * Nothing is ever reset (the epochs of Section 4.2).  Each launch has
+//   exactly n waves and each claims one ticket, and launches of a plan are
+//   ordered on its stream, so launch e's tickets are [e*n, (e+1)*n): the
+//   ticket gives both the epoch and the item.  Chunk (k, c) is ready in
+//   launch e when its cumulative counter reaches (e + 1) * (its reduce
+//   items).  No wave does any work after its item, so only the release of
+//   a finished reduction and the acquire before a copy touch the caches.
 // * Waits are bounded: a wave that waits longer than kSpinLimit sleeps
 //   records an error in the state block and gives up its item, so the
-//   launch always drains.
+//   launch always drains (and the epochs stay consistent).
 struct FusedArgs {
     FusedState* state;
     uint64_t* ready;         // [P * chunks_per_part] finished reduce items, cumulative
@@ -277,11 +286,12 @@ __global__ __launch_bounds__(kBlock) void exec_fused_allreduce(ExecArgs a, Fused
     if (w >= a.n_items) return;  // exactly n_items waves claim
     const uint32_t lane = lane_index();
     FusedState* st = f.state;
-    const uint64_t epoch = __hip_atomic_load(&st->epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    uint32_t claimed = 0;
-    if (lane == 0) claimed = __hip_atomic_fetch_add(&st->claim, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint32_t i = __builtin_amdgcn_readfirstlane(claimed);
-    if (i < a.n_items) {
+    uint64_t ticket = 0;
+    if (lane == 0) ticket = __hip_atomic_fetch_add(&st->tickets, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    ticket = static_cast<uint64_t>(readlane64(static_cast<int64_t>(ticket), 0));
+    const uint64_t epoch = ticket / a.n_items;
+    const uint64_t i = ticket - epoch * a.n_items;
+    {
         const purlin_desc d = a.items[i];
         uint64_t* ready = f.ready + uint64_t(d.part) * f.chunks_per_part + d.chunk;
         if (i < f.n_reduce) {
@@ -307,16 +317,6 @@ __global__ __launch_bounds__(kBlock) void exec_fused_allreduce(ExecArgs a, Fused
             } else if (lane == 0) {
                 __hip_atomic_store(&st->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
-        }
-    }
-    // the last wave of the launch resets the claim counters, then advances the epoch
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    if (lane == 0) {
-        const uint32_t prev = __hip_atomic_fetch_add(&st->done, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        if (prev + 1 == a.n_items) {
-            __hip_atomic_store(&st->claim, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&st->done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_fetch_add(&st->epoch, 1ull, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 }
@@ -375,12 +375,6 @@ struct VArgs {
     uint32_t transposed;  // AllToAllV: counts are column-major
     uint32_t src_major;   // AllToAllV: items cover each source's input
 };
-
-__device__ __forceinline__ int64_t readlane64(int64_t v, int lane) {
-    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(v), lane);
-    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(static_cast<uint64_t>(v) >> 32), lane);
-    return static_cast<int64_t>((uint64_t(hi) << 32) | lo);
-}
 
 // Lane p < P holds count p (elements); returns whether every count is >= 0
 // and fits `part_cap`, and their sum fits `total_cap`.

@@ -20,11 +20,9 @@ hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uin
 
 // Device state of a single-launch AllReduce plan (zeroed at plan creation).
 struct FusedState {
-    uint32_t claim;   // next work item to claim in the current launch
-    uint32_t done;    // waves of the current launch that have finished
-    uint64_t epoch;   // launches completed
-    uint32_t error;   // set if a wait gave up (bounded spin)
-    uint32_t pad[3];
+    uint64_t tickets;  // items claimed over all launches: launch e's waves take [e*n, (e+1)*n)
+    uint32_t error;    // set if a wait gave up (bounded spin)
+    uint32_t pad[5];
 };
 
 // One launch for a whole AllReduce: items [0, n_reduce) reduce partition k
