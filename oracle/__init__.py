@@ -18,6 +18,8 @@ Contents
 ``moe``          MoE dispatch ``pack`` and combine ``unpack`` (the paper names
                  them only as the expert-parallel use of AllToAll, Table 2;
                  their contract is written out in ``moe``'s docstrings).
+``moe_dedup``    De-duplicated dispatch ``pack_dedup`` (one row per token and
+                 destination rank) and its combine ``unpack_dedup``.
 
 Representation: fp32 data is ``numpy.float32``; bf16 data is its 16-bit
 encoding held in ``numpy.uint16``.  Floating-point arithmetic is numpy
@@ -25,13 +27,14 @@ float32 ufuncs, which round every operation to binary32 (round to nearest,
 ties to even, denormals kept) and never contract a multiply and an add.
 
 Parity status: every function has independent pins in
-``tests/test_oracle_pins.py`` (brute force, the paper's worked layout
+``tests/test_oracle_pins*.py`` (brute force, the paper's worked layout
 example, closed forms, special cases); none is "parity unpinned".
 """
 
 from .bf16 import narrow, widen
 from .collectives import all_gather, all_reduce, all_to_all, reduce_scatter
 from .moe import pack, unpack
+from .moe_dedup import pack_dedup, unpack_dedup
 from .rooted import broadcast, gather, reduce, scatter
 from .vcollectives import all_gather_v, all_to_all_v, reduce_scatter_v
 
@@ -44,6 +47,8 @@ __all__ = [
     "reduce_scatter",
     "pack",
     "unpack",
+    "pack_dedup",
+    "unpack_dedup",
     "broadcast",
     "gather",
     "reduce",
