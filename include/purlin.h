@@ -339,6 +339,59 @@ PURLIN_API purlin_status purlin_pack(int T, int H, int K, int E, int P, const vo
 PURLIN_API purlin_status purlin_unpack(int T, int H, int K, const void* y, const int32_t* pos,
                             const float* gates, void* out, int32_t* dev_status, void* stream);
 
+/* Workspace bytes purlin_pack_dedup needs for T tokens over P ranks. */
+PURLIN_API purlin_status purlin_pack_dedup_workspace_size(int T, int P, uint64_t* bytes);
+
+/* De-duplicated MoE dispatch: one row per (token, destination rank) instead
+ * of one per (token, slot).  A token whose K experts live on fewer than K
+ * ranks is sent once to each of them (expert parallelism's dispatch, Section
+ * 2, Table 2; the paper does not cover de-duplication, this is the
+ * library's contract).  With L = E / P and dests(t) = {ids[t,k] / L}:
+ *   dest_counts[r]  = #{t : r in dests(t)}
+ *   dest_offsets[r] = sum of dest_counts[0..r)
+ *   row_of[t, r]    = dest_offsets[r] + #{t' < t : r in dests(t')} if r in
+ *                     dests(t), else -1
+ *   packed[row_of[t, r], :] = x[t, :]                          (bit copy)
+ * so rows are grouped by destination rank, then token.
+ *   x        bf16 [T, H] device, row-major
+ *   ids      int32 [T, K] device; each id in [0, E), distinct within a token
+ *   packed   bf16 [T*min(K, P), H] device (output; the first
+ *            sum(dest_counts) rows are written)
+ *   dest_counts, dest_offsets  int32 [P] device (output)
+ *   row_of   int32 [T, P] device (output)
+ *   dev_status int32 device (optional: NULL): set to 0, or to 1 when an id
+ *            is out of range or repeated within a token; out-of-range ids
+ *            are then ignored, and no row is written outside packed.
+ *   workspace >= purlin_pack_dedup_workspace_size bytes of device memory,
+ *            owned by the caller; its contents on entry do not matter.
+ * Limits: T >= 0, H >= 1, 1 <= K <= 64, 1 <= E <= 4096, 1 <= P <= 16,
+ * P <= E, E % P == 0, T*K < 2^31.  Errors: PURLIN_ERR_INVALID (limits, NULL
+ * or misaligned pointer, small workspace, x overlapping packed),
+ * PURLIN_ERR_DEVICE. */
+PURLIN_API purlin_status purlin_pack_dedup(int T, int H, int K, int E, int P, const void* x, const int32_t* ids,
+                                           void* packed, int32_t* dest_counts, int32_t* dest_offsets,
+                                           int32_t* row_of, int32_t* dev_status, void* workspace,
+                                           uint64_t workspace_bytes, void* stream);
+
+/* Combine of the de-duplicated dispatch: y holds one partial output per
+ * (token, rank) in purlin_pack_dedup's layout (each rank has applied its
+ * experts and their gates), and
+ *   acc = +0.0f;
+ *   for r = 0 .. P-1 with row_of[t, r] >= 0:  acc = acc + widen(y[row_of[t, r], h]);
+ *   out[t, h] = narrow(acc)
+ * binary32 adds in rank order (Eq. 2).
+ *   y      bf16 [rows, H] device
+ *   row_of int32 [T, P] device, each -1 or in [0, rows)
+ *   out    bf16 [T, H] device (output)
+ *   dev_status int32 device (optional: NULL): set to 0, or to 1 if some
+ *          entry is neither -1 nor in [0, rows) (it then contributes
+ *          nothing).
+ * Limits: T >= 0, H >= 1, 1 <= P <= 16, 0 <= rows < 2^31.  Errors:
+ * PURLIN_ERR_INVALID (limits, NULL or misaligned pointer, y overlapping
+ * out), PURLIN_ERR_DEVICE. */
+PURLIN_API purlin_status purlin_unpack_dedup(int T, int H, int P, int64_t rows, const void* y,
+                                             const int32_t* row_of, void* out, int32_t* dev_status, void* stream);
+
 /* Static text for a status code ("unknown status" for others). */
 PURLIN_API const char* purlin_status_string(purlin_status status);
 

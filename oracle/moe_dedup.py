@@ -107,7 +107,8 @@ def unpack_dedup(y, row_of):
     T, P = row_of.shape
     H = y.shape[1]
     acc = np.zeros((T, H), dtype=np.float32)  # +0.0
-    for r in range(P):  # rank order
-        sel = row_of[:, r] >= 0
-        acc[sel] = np.add(acc[sel], widen(y[row_of[sel, r]]), dtype=np.float32)
+    with np.errstate(over="ignore", invalid="ignore"):  # IEEE overflow to inf, inf - inf = NaN
+        for r in range(P):  # rank order
+            sel = row_of[:, r] >= 0
+            acc[sel] = np.add(acc[sel], widen(y[row_of[sel, r]]), dtype=np.float32)
     return narrow(acc)

@@ -2,6 +2,7 @@
 // validation (always complete before anything is enqueued), plan lifetime,
 // and the launches.  Status codes only: no exception crosses the ABI.
 
+#include <algorithm>
 #include <cstdint>
 #include <new>
 
@@ -267,6 +268,51 @@ purlin_status purlin_pack(int T, int H, int K, int E, int P, const void* x, cons
                                              static_cast<uint16_t*>(packed), dest_counts, dest_offsets,
                                              expert_counts, expert_offsets, pos, dev_status, ws,
                                              static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
+purlin_status purlin_pack_dedup_workspace_size(int T, int P, uint64_t* bytes) {
+    if (!bytes || T < 0 || P < 1 || P > PURLIN_MAX_RANKS) return PURLIN_ERR_INVALID;
+    *bytes = purlin::pack_dedup_workspace_bytes(T, P);
+    return PURLIN_OK;
+}
+
+purlin_status purlin_pack_dedup(int T, int H, int K, int E, int P, const void* x, const int32_t* ids, void* packed,
+                                int32_t* dest_counts, int32_t* dest_offsets, int32_t* row_of, int32_t* dev_status,
+                                void* workspace, uint64_t workspace_bytes, void* stream) {
+    if (!pack_limits_ok(T, H, K, E)) return PURLIN_ERR_INVALID;
+    if (P < 1 || P > PURLIN_MAX_RANKS || P > E || E % P != 0) return PURLIN_ERR_INVALID;
+    if (!dest_counts || !dest_offsets || !aligned16(dest_counts) || !aligned16(dest_offsets)) return PURLIN_ERR_INVALID;
+    if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    const uint64_t need = purlin::pack_dedup_workspace_bytes(T, P);
+    if (workspace_bytes < need || (need && (!workspace || !aligned16(workspace)))) return PURLIN_ERR_INVALID;
+    if (T > 0) {
+        if (!x || !ids || !packed || !row_of) return PURLIN_ERR_INVALID;
+        if (!aligned16(x) || !aligned16(ids) || !aligned16(packed) || !aligned16(row_of)) return PURLIN_ERR_INVALID;
+        const uint64_t xb = uint64_t(T) * H * 2, pb = xb * static_cast<uint64_t>(std::min(K, P));
+        if (overlaps(x, xb, packed, pb)) return PURLIN_ERR_INVALID;
+    }
+    const hipError_t e = purlin::launch_pack_dedup(T, H, K, E, P, static_cast<const uint16_t*>(x), ids,
+                                                   static_cast<uint16_t*>(packed), dest_counts, dest_offsets, row_of,
+                                                   dev_status, workspace, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
+purlin_status purlin_unpack_dedup(int T, int H, int P, int64_t rows, const void* y, const int32_t* row_of, void* out,
+                                  int32_t* dev_status, void* stream) {
+    if (T < 0 || H < 1 || P < 1 || P > PURLIN_MAX_RANKS) return PURLIN_ERR_INVALID;
+    if (rows < 0 || rows >= (int64_t(1) << 31) || !purlin::moe_launch_fits(T, H)) return PURLIN_ERR_INVALID;
+    if (static_cast<int64_t>(T) * P >= (int64_t(1) << 31)) return PURLIN_ERR_INVALID;
+    if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    if (T > 0) {
+        if (!row_of || !out || (rows > 0 && !y)) return PURLIN_ERR_INVALID;
+        if (!aligned16(row_of) || !aligned16(out) || (y && !aligned16(y))) return PURLIN_ERR_INVALID;
+        const uint64_t ob = uint64_t(T) * H * 2, yb = uint64_t(rows) * H * 2;
+        if (rows > 0 && overlaps(y, yb, out, ob)) return PURLIN_ERR_INVALID;
+    }
+    const hipError_t e = purlin::launch_unpack_dedup(T, H, P, rows, static_cast<const uint16_t*>(y), row_of,
+                                                     static_cast<uint16_t*>(out), dev_status,
+                                                     static_cast<hipStream_t>(stream));
     return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
 }
 

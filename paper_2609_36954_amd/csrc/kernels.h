@@ -59,4 +59,16 @@ hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, con
 hipError_t launch_unpack(int T, int H, int K, const uint16_t* y, const int32_t* pos, const float* gates,
                          uint16_t* out, int32_t* dev_status, hipStream_t stream);
 
+// De-duplicated dispatch: one row per (token, destination rank).  The
+// workspace holds per-tile destination counts (then bases), each token's
+// rank among its tile's tokens per destination, and per-tile error flags.
+uint64_t pack_dedup_workspace_bytes(int T, int P);
+
+hipError_t launch_pack_dedup(int T, int H, int K, int E, int P, const uint16_t* x, const int32_t* ids,
+                             uint16_t* packed, int32_t* dest_counts, int32_t* dest_offsets, int32_t* row_of,
+                             int32_t* dev_status, void* workspace, hipStream_t stream);
+
+hipError_t launch_unpack_dedup(int T, int H, int P, int64_t rows, const uint16_t* y, const int32_t* row_of,
+                               uint16_t* out, int32_t* dev_status, hipStream_t stream);
+
 }  // namespace purlin

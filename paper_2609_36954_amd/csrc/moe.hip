@@ -22,6 +22,11 @@
 //      writes it to its K packed rows with 16-byte stores.
 // Unpack is one launch, one wavefront per token, slots in groups of 8 with
 // all their 16-byte row loads in flight before the FP32 accumulation.
+//
+// The de-duplicated variants (one row per token and destination rank) use
+// the same structure with destinations in place of experts: pack_dedup is
+// dedup_tiles, dedup_scan, dedup_rows; unpack_dedup is unpack_rows without
+// gates, summing a token's rows in rank order.
 
 #include "kernels.h"
 
@@ -37,6 +42,7 @@ constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kScanThreads = 1024;
 constexpr int kMaxExperts = 4096;
+constexpr int kMaxDedupRanks = 16;
 
 __device__ __forceinline__ uint32_t wave_index() {
     return __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
@@ -222,6 +228,45 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
     if (tid == 0 && dev_status) *dev_status = any ? 1 : 0;
 }
 
+// Stream one column slice of a token row (U * 64 16-byte vectors, U per
+// lane) through registers into every slot whose row index lane j < nslots
+// holds in `row` (-1 = no row): the row is read once from HBM.  Rows that
+// are not a multiple of 16 bytes take one slice per token, 2 bytes per lane
+// step.
+template <int U, bool NTL, bool NTS>
+__device__ __forceinline__ void copy_row_to_slots(const char* src, char* packed, uint64_t row_bytes, uint32_t slice,
+                                                  int row, int nslots, uint32_t lane) {
+    if (row_bytes % 16 == 0) {
+        const uint64_t nvec = row_bytes / 16;
+        const uint64_t base = static_cast<uint64_t>(slice) * U * kWave;
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint64_t i = base + u * kWave + lane;
+            if (i < nvec) v[u] = load16<NTL>(src + i * 16);
+        }
+        for (int j = 0; j < nslots; ++j) {
+            const int pj = __builtin_amdgcn_readlane(row, j);
+            if (pj < 0) continue;
+            char* dst = packed + static_cast<uint64_t>(pj) * row_bytes;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint64_t i = base + u * kWave + lane;
+                if (i < nvec) store16<NTS>(dst + i * 16, v[u]);
+            }
+        }
+    } else {
+        const uint64_t H = row_bytes / 2;
+        for (uint64_t h = lane; h < H; h += kWave) {
+            const uint16_t v = reinterpret_cast<const uint16_t*>(src)[h];
+            for (int j = 0; j < nslots; ++j) {
+                const int pj = __builtin_amdgcn_readlane(row, j);
+                if (pj >= 0) reinterpret_cast<uint16_t*>(packed + static_cast<uint64_t>(pj) * row_bytes)[h] = v;
+            }
+        }
+    }
+}
+
 // One wavefront per (token, column slice): a slice is U * 64 16-byte
 // vectors of the row, so each lane holds U vectors of it.  Every slice's
 // wave forms the token's K positions (lane k forms pos[t, k]); the wave of
@@ -250,46 +295,126 @@ __global__ __launch_bounds__(kBlock) void pack_rows(int T, int H, int K, int E, 
         if (slice == 0) pos[j] = p;
     }
     const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
-    const char* src = x + t * row_bytes;
-    if (row_bytes % 16 == 0) {
-        const uint64_t nvec = row_bytes / 16;
-        const uint64_t base = static_cast<uint64_t>(slice) * U * kWave;
-        u32x4 v[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint64_t i = base + u * kWave + lane;
-            if (i < nvec) v[u] = load16<NTL>(src + i * 16);
-        }
+    copy_row_to_slots<U, NTL, NTS>(x + t * row_bytes, packed, row_bytes, slice, p, K, lane);
+}
+
+// ---------------------------------------------------------------------------
+// De-duplicated dispatch: one row per (token, destination rank).
+//   1. dedup_tiles: one wavefront per tile of 64 tokens, lane = token.  A
+//      lane forms its token's destination mask (bit r: some expert of the
+//      token lives on rank r) and checks the ids; per destination a ballot
+//      gives the tile's count and each token's rank among the tile's tokens
+//      bound there (popcount below the lane).
+//   2. dedup_scan: one workgroup; wave r scans destination r's tile counts
+//      in tile order with cross-lane prefix sums, rewriting them into tile
+//      bases; then destination counts and offsets, and the error flag.
+//   3. dedup_rows: one wavefront per (token, column slice); lane r < P forms
+//      row_of[t, r], and the row is streamed once into each of its rows.
+__global__ __launch_bounds__(kWave) void dedup_tiles(int T, int K, int E, int P, const int32_t* __restrict__ ids,
+                                                     int32_t* __restrict__ tile_cnt, int32_t* __restrict__ lrank,
+                                                     int32_t* __restrict__ tile_err) {
+    const int tile = blockIdx.x;
+    const uint32_t lane = threadIdx.x;
+    const int64_t t = static_cast<int64_t>(tile) * kWave + lane;
+    const bool valid = t < T;
+    const int L = E / P;
+    uint32_t mask = 0;
+    bool bad = false;
+    if (valid) {
+        const int32_t* row = ids + t * K;
         for (int k = 0; k < K; ++k) {
-            const int pk = __builtin_amdgcn_readlane(p, k);
-            if (pk < 0) continue;
-            char* dst = packed + static_cast<uint64_t>(pk) * row_bytes;
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const uint64_t i = base + u * kWave + lane;
-                if (i < nvec) store16<NTS>(dst + i * 16, v[u]);
+            const int e = row[k];
+            if (e < 0 || e >= E) {
+                bad = true;
+                continue;
             }
-        }
-    } else {
-        // rows not a multiple of 16 bytes: one slice per token, 2 bytes per lane step
-        for (uint64_t h = lane; h < static_cast<uint64_t>(H); h += kWave) {
-            const uint16_t v = reinterpret_cast<const uint16_t*>(src)[h];
-            for (int k = 0; k < K; ++k) {
-                const int pk = __builtin_amdgcn_readlane(p, k);
-                if (pk >= 0) reinterpret_cast<uint16_t*>(packed + static_cast<uint64_t>(pk) * row_bytes)[h] = v;
-            }
+            for (int k2 = 0; k2 < k; ++k2)
+                if (row[k2] == e) bad = true;
+            mask |= 1u << (e / L);
         }
     }
+    const uint64_t below = (uint64_t(1) << lane) - 1u;
+    for (int r = 0; r < P; ++r) {
+        const bool has = valid && ((mask >> r) & 1u);
+        const uint64_t b = __ballot(has);
+        if (lane == 0) tile_cnt[static_cast<int64_t>(tile) * P + r] = __popcll(b);
+        if (valid) lrank[t * P + r] = has ? __popcll(b & below) : -1;
+    }
+    const uint64_t eb = __ballot(bad);
+    if (lane == 0) tile_err[tile] = eb != 0 ? 1 : 0;
+}
+
+__global__ __launch_bounds__(kScanThreads) void dedup_scan(int ntiles, int P, int32_t* __restrict__ tile_cnt,
+                                                           const int32_t* __restrict__ tile_err,
+                                                           int32_t* __restrict__ dest_counts,
+                                                           int32_t* __restrict__ dest_offsets,
+                                                           int32_t* __restrict__ dev_status) {
+    __shared__ int32_t totals[kMaxDedupRanks];
+    const uint32_t wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
+    int any = 0;
+    for (int t = threadIdx.x; t < ntiles; t += kScanThreads) any |= tile_err[t];
+    if (wave < static_cast<uint32_t>(P)) {
+        const int r = static_cast<int>(wave);
+        int carry = 0;
+        for (int t0 = 0; t0 < ntiles; t0 += kWave) {
+            const int t = t0 + static_cast<int>(lane);
+            const int c = t < ntiles ? tile_cnt[static_cast<int64_t>(t) * P + r] : 0;
+            int v = c;  // inclusive prefix over the 64 lanes
+            for (int off = 1; off < kWave; off <<= 1) {
+                const int u = __shfl_up(v, off);
+                if (lane >= static_cast<uint32_t>(off)) v += u;
+            }
+            if (t < ntiles) tile_cnt[static_cast<int64_t>(t) * P + r] = carry + v - c;
+            carry += __shfl(v, kWave - 1);
+        }
+        if (lane == 0) totals[r] = carry;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int run = 0;
+        for (int r = 0; r < P; ++r) {
+            dest_counts[r] = totals[r];
+            dest_offsets[r] = run;
+            run += totals[r];
+        }
+    }
+    any = __syncthreads_or(any);
+    if (threadIdx.x == 0 && dev_status) *dev_status = any ? 1 : 0;
+}
+
+template <int U, bool NTL, bool NTS>
+__global__ __launch_bounds__(kBlock) void dedup_rows(int T, int H, int P, int slices, const char* __restrict__ x,
+                                                     const int32_t* __restrict__ tile_base,
+                                                     const int32_t* __restrict__ lrank,
+                                                     const int32_t* __restrict__ dest_offsets,
+                                                     int32_t* __restrict__ row_of, char* __restrict__ packed) {
+    const uint32_t w = wave_index();
+    const uint32_t t = w / slices;
+    if (t >= static_cast<uint32_t>(T)) return;
+    const uint32_t slice = w - t * slices;
+    const uint32_t lane = lane_index();
+    int row = -1;
+    if (lane < static_cast<uint32_t>(P)) {
+        const int64_t j = static_cast<int64_t>(t) * P + lane;
+        const int lr = lrank[j];
+        if (lr >= 0) row = dest_offsets[lane] + tile_base[static_cast<int64_t>(t / kWave) * P + lane] + lr;
+        if (slice == 0) row_of[j] = row;
+    }
+    const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
+    copy_row_to_slots<U, NTL, NTS>(x + t * row_bytes, packed, row_bytes, slice, row, P, lane);
 }
 
 __global__ void set_status(int32_t* status) { *status = 0; }
 
 constexpr int kSlotGroup = 8;
 
-// One wavefront per (token, column slice) of the output row.
-template <int U, bool NTL, bool NTS>
-__global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, int slices, const char* __restrict__ y,
-                                                      const int32_t* __restrict__ pos,
+// One wavefront per (token, column slice) of the output row.  GATED: the
+// combine of one row per (t, k), acc (+)= g[t, k] (x) row; otherwise the
+// de-duplicated combine of one row per (t, rank), acc (+)= row, where a
+// slot of -1 means "no row".  Slots name rows in [0, rows).
+template <int U, bool NTL, bool NTS, bool GATED>
+__global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, int slices, int64_t rows,
+                                                      const char* __restrict__ y, const int32_t* __restrict__ pos,
                                                       const float* __restrict__ gates, char* __restrict__ out,
                                                       int32_t* __restrict__ dev_status) {
     const uint32_t w = wave_index();
@@ -297,17 +422,17 @@ __global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, int s
     if (t >= static_cast<uint32_t>(T)) return;
     const uint32_t slice = w - t * slices;
     const uint32_t lane = lane_index();
-    const int64_t rows = static_cast<int64_t>(T) * K;
     int p = -1;
-    float g = 0.0f;
+    float g = 1.0f;
     if (lane < static_cast<uint32_t>(K)) {
         const int64_t j = static_cast<int64_t>(t) * K + lane;
         p = pos[j];
-        g = gates[j];
-        if (p < 0 || p >= rows) {
-            p = -1;
+        if constexpr (GATED) g = gates[j];
+        const bool absent = !GATED && p == -1;
+        if (!absent && (p < 0 || p >= rows)) {
             if (dev_status && slice == 0) atomicOr(dev_status, 1);
         }
+        if (p < 0 || p >= rows) p = -1;
     }
     const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
     char* dst = out + t * row_bytes;
@@ -342,9 +467,14 @@ __global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, int s
 #pragma unroll
                     for (int m = 0; m < 4; ++m) {
                         const uint32_t wv = v[kk][u][m];
-                        acc[u][2 * m] = __fadd_rn(acc[u][2 * m], __fmul_rn(gk, __uint_as_float(wv << 16)));
-                        acc[u][2 * m + 1] =
-                            __fadd_rn(acc[u][2 * m + 1], __fmul_rn(gk, __uint_as_float(wv & 0xFFFF0000u)));
+                        const float lo = __uint_as_float(wv << 16), hi = __uint_as_float(wv & 0xFFFF0000u);
+                        if constexpr (GATED) {
+                            acc[u][2 * m] = __fadd_rn(acc[u][2 * m], __fmul_rn(gk, lo));
+                            acc[u][2 * m + 1] = __fadd_rn(acc[u][2 * m + 1], __fmul_rn(gk, hi));
+                        } else {
+                            acc[u][2 * m] = __fadd_rn(acc[u][2 * m], lo);
+                            acc[u][2 * m + 1] = __fadd_rn(acc[u][2 * m + 1], hi);
+                        }
                     }
                 }
             }
@@ -367,7 +497,8 @@ __global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, int s
                 if (pk < 0) continue;
                 const float gk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), k));
                 const uint16_t hv = reinterpret_cast<const uint16_t*>(y + static_cast<uint64_t>(pk) * row_bytes)[h];
-                acc = __fadd_rn(acc, __fmul_rn(gk, __uint_as_float(uint32_t(hv) << 16)));
+                const float v = __uint_as_float(uint32_t(hv) << 16);
+                acc = __fadd_rn(acc, GATED ? __fmul_rn(gk, v) : v);
             }
             reinterpret_cast<uint16_t*>(dst)[h] = static_cast<uint16_t>(to_bf16(acc));
         }
@@ -449,9 +580,55 @@ hipError_t launch_unpack(int T, int H, int K, const uint16_t* y, const int32_t* 
         const int slices = row_slices(H, kUnpackUnroll);
         const uint64_t waves = static_cast<uint64_t>(T) * slices;
         const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
-        hipLaunchKernelGGL((unpack_rows<kUnpackUnroll, kUnpackNtLoad, kUnpackNtStore>), grid, dim3(kBlock), 0, stream,
-                           T, H, K, slices, reinterpret_cast<const char*>(y), pos, gates, reinterpret_cast<char*>(out),
-                           dev_status);
+        hipLaunchKernelGGL((unpack_rows<kUnpackUnroll, kUnpackNtLoad, kUnpackNtStore, true>), grid, dim3(kBlock), 0,
+                           stream, T, H, K, slices, static_cast<int64_t>(T) * K, reinterpret_cast<const char*>(y), pos,
+                           gates, reinterpret_cast<char*>(out), dev_status);
+    }
+    return hipGetLastError();
+}
+
+uint64_t pack_dedup_workspace_bytes(int T, int P) {
+    const uint64_t ntiles = (static_cast<uint64_t>(T) + kWave - 1) / kWave;
+    return align256(4 * ntiles * P) + align256(4 * static_cast<uint64_t>(T) * P) + align256(4 * ntiles);
+}
+
+hipError_t launch_pack_dedup(int T, int H, int K, int E, int P, const uint16_t* x, const int32_t* ids,
+                             uint16_t* packed, int32_t* dest_counts, int32_t* dest_offsets, int32_t* row_of,
+                             int32_t* dev_status, void* workspace, hipStream_t stream) {
+    const int ntiles = (T + kWave - 1) / kWave;
+    char* ws = static_cast<char*>(workspace);
+    int32_t* tile_base = reinterpret_cast<int32_t*>(ws);
+    int32_t* lrank = reinterpret_cast<int32_t*>(ws + align256(4 * static_cast<uint64_t>(ntiles) * P));
+    int32_t* tile_err = reinterpret_cast<int32_t*>(ws + align256(4 * static_cast<uint64_t>(ntiles) * P) +
+                                                   align256(4 * static_cast<uint64_t>(T) * P));
+    (void)hipGetLastError();
+    if (ntiles > 0)
+        hipLaunchKernelGGL(dedup_tiles, dim3(ntiles), dim3(kWave), 0, stream, T, K, E, P, ids, tile_base, lrank,
+                           tile_err);
+    hipLaunchKernelGGL(dedup_scan, dim3(1), dim3(kScanThreads), 0, stream, ntiles, P, tile_base, tile_err, dest_counts,
+                       dest_offsets, dev_status);
+    if (T > 0) {
+        const int slices = row_slices(H, kPackUnroll);
+        const uint64_t waves = static_cast<uint64_t>(T) * slices;
+        const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
+        hipLaunchKernelGGL((dedup_rows<kPackUnroll, kPackNtLoad, kPackNtStore>), grid, dim3(kBlock), 0, stream, T, H,
+                           P, slices, reinterpret_cast<const char*>(x), tile_base, lrank, dest_offsets, row_of,
+                           reinterpret_cast<char*>(packed));
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_unpack_dedup(int T, int H, int P, int64_t rows, const uint16_t* y, const int32_t* row_of,
+                               uint16_t* out, int32_t* dev_status, hipStream_t stream) {
+    (void)hipGetLastError();
+    if (dev_status) hipLaunchKernelGGL(set_status, dim3(1), dim3(1), 0, stream, dev_status);
+    if (T > 0) {
+        const int slices = row_slices(H, kUnpackUnroll);
+        const uint64_t waves = static_cast<uint64_t>(T) * slices;
+        const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
+        hipLaunchKernelGGL((unpack_rows<kUnpackUnroll, kUnpackNtLoad, kUnpackNtStore, false>), grid, dim3(kBlock), 0,
+                           stream, T, H, P, slices, rows, reinterpret_cast<const char*>(y), row_of, nullptr,
+                           reinterpret_cast<char*>(out), dev_status);
     }
     return hipGetLastError();
 }

@@ -104,13 +104,17 @@ def lib():
     L.purlin_pack_workspace_size.argtypes = [i32, i32, i32, _c_u64p]
     L.purlin_pack.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 10 + [u64, _vp]
     L.purlin_unpack.argtypes = [i32, i32, i32] + [_vp] * 6
+    L.purlin_pack_dedup_workspace_size.argtypes = [i32, i32, _c_u64p]
+    L.purlin_pack_dedup.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 8 + [u64, _vp]
+    L.purlin_unpack_dedup.argtypes = [i32, i32, i32, ctypes.c_int64] + [_vp] * 5
     L.purlin_status_string.argtypes = [i32]
     L.purlin_status_string.restype = ctypes.c_char_p
     L.purlin_version.argtypes = []
     L.purlin_version.restype = ctypes.c_char_p
     for name in ("purlin_plan", "purlin_plan_ex", "purlin_plan_rooted", "purlin_plan_v", "purlin_exec_v",
                  "purlin_plan_info", "purlin_plan_descriptors", "purlin_plan_items",
-                 "purlin_exec", "purlin_pack_workspace_size", "purlin_pack", "purlin_unpack"):
+                 "purlin_exec", "purlin_pack_workspace_size", "purlin_pack", "purlin_unpack",
+                 "purlin_pack_dedup_workspace_size", "purlin_pack_dedup", "purlin_unpack_dedup"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -406,4 +410,68 @@ def purlin_unpack(y, pos, gates, out=None, dev_status=None, stream=None):
     st = lib().purlin_unpack(int(T), int(H), int(K), _ptr(y), _ptr(pos), _ptr(gates), _ptr(out), _ptr(dev_status),
                              _stream_handle(stream))
     _check(st, "purlin_unpack")
+    return out
+
+
+def purlin_pack_dedup_workspace_size(T, P):
+    b = ctypes.c_uint64()
+    _check(lib().purlin_pack_dedup_workspace_size(int(T), int(P), ctypes.byref(b)),
+           "purlin_pack_dedup_workspace_size")
+    return b.value
+
+
+def purlin_pack_dedup(x, ids, E, P, out=None, workspace=None, dev_status=None, stream=None):
+    """De-duplicated MoE dispatch of ``x`` (bf16 [T, H]) by ``ids`` (int32
+    [T, K]): one row per (token, destination rank).
+
+    Returns a dict of device tensors: packed [T*min(K, P), H] (the first
+    sum(dest_counts) rows written), dest_counts [P], dest_offsets [P],
+    row_of [T, P].  ``out`` may supply preallocated tensors under the same
+    keys.
+    """
+    import torch
+
+    T, H = x.shape
+    K = ids.shape[1]
+    if ids.shape[0] != T:
+        raise PurlinError(PURLIN_ERR_INVALID, "x and ids disagree on T")
+    _require_cuda(x, "x", 2)
+    _require_cuda(ids, "ids", 4)
+    dev = x.device
+    o = dict(out or {})
+    o.setdefault("packed", torch.empty((T * min(K, P), H), dtype=x.dtype, device=dev))
+    for name in ("dest_counts", "dest_offsets"):
+        o.setdefault(name, torch.empty(P, dtype=torch.int32, device=dev))
+    o.setdefault("row_of", torch.empty((T, P), dtype=torch.int32, device=dev))
+    _require_cuda(o["packed"], "packed", 2)
+    if o["packed"].numel() < T * min(K, P) * H:
+        raise PurlinError(PURLIN_ERR_INVALID, "packed holds fewer than T*min(K, P) rows")
+    if o["row_of"].numel() < T * P:
+        raise PurlinError(PURLIN_ERR_INVALID, "row_of holds fewer than T*P entries")
+    wsb = purlin_pack_dedup_workspace_size(T, P)
+    if workspace is None:
+        workspace = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+    st = lib().purlin_pack_dedup(int(T), int(H), int(K), int(E), int(P), _ptr(x), _ptr(ids), _ptr(o["packed"]),
+                                 _ptr(o["dest_counts"]), _ptr(o["dest_offsets"]), _ptr(o["row_of"]),
+                                 _ptr(dev_status), _ptr(workspace), int(workspace.numel() * workspace.element_size()),
+                                 _stream_handle(stream))
+    _check(st, "purlin_pack_dedup")
+    return o
+
+
+def purlin_unpack_dedup(y, row_of, out=None, dev_status=None, stream=None):
+    """Combine of the de-duplicated dispatch: bf16 [T, H] = sum over ranks r
+    (ascending) of y[row_of[t, r]], skipping -1 entries."""
+    import torch
+
+    T, P = row_of.shape
+    rows, H = y.shape
+    _require_cuda(y, "y", 2)
+    _require_cuda(row_of, "row_of", 4)
+    if out is None:
+        out = torch.empty((T, H), dtype=y.dtype, device=y.device)
+    _require_cuda(out, "out", 2)
+    st = lib().purlin_unpack_dedup(int(T), int(H), int(P), int(rows), _ptr(y), _ptr(row_of), _ptr(out),
+                                   _ptr(dev_status), _stream_handle(stream))
+    _check(st, "purlin_unpack_dedup")
     return out

@@ -219,6 +219,52 @@ def test_unpack_argument_validation(kw):
     assert _unpack(**kw) == INVALID
 
 
+def test_pack_dedup_workspace_size():
+    L = PL.lib()
+    b = ctypes.c_uint64()
+    assert L.purlin_pack_dedup_workspace_size(4096, 8, ctypes.byref(b)) == 0
+    # 64 tiles x 8 ranks + 4096 x 8 ranks + 64 flags, 4 bytes each, 256-byte aligned pieces
+    assert b.value == 2048 + 131072 + 256
+    assert L.purlin_pack_dedup_workspace_size(0, 8, ctypes.byref(b)) == 0 and b.value == 0
+    for T, P in ((4096, 0), (4096, 17), (-1, 8)):
+        assert L.purlin_pack_dedup_workspace_size(T, P, ctypes.byref(b)) == INVALID
+    assert L.purlin_pack_dedup_workspace_size(4096, 8, None) == INVALID
+
+
+def _pack_dedup(T=64, H=64, K=2, E=8, P=2, x=0x1000, ids=0x2000, packed=0x300000, dc=0x4000, do=0x5000,
+                row_of=0x7000, status=None, ws=0x8000, wsb=1 << 20):
+    return PL.lib().purlin_pack_dedup(T, H, K, E, P, x, ids, packed, dc, do, row_of, status, ws, wsb, None)
+
+
+@pytest.mark.parametrize(
+    "kw",
+    [
+        dict(K=0), dict(K=65), dict(E=0), dict(E=4097), dict(E=8, P=3), dict(P=0), dict(P=16, E=8),
+        dict(P=17, E=34),  # more ranks than the destination masks hold
+        dict(T=-1), dict(H=0), dict(x=None), dict(ids=None), dict(packed=None), dict(row_of=None), dict(dc=None),
+        dict(do=None), dict(x=0x1008), dict(row_of=0x7004), dict(status=0x9002), dict(ws=None), dict(wsb=16),
+        dict(x=0x300000),  # x overlaps packed
+        dict(packed=0x1000 + 64 * 64 * 2 - 16),  # packed (T*min(K,P) rows) overlaps x's last row
+    ],
+)
+def test_pack_dedup_argument_validation(kw):
+    assert _pack_dedup(**kw) == INVALID
+
+
+def _unpack_dedup(T=64, H=64, P=4, rows=100, y=0x100000, row_of=0x2000, out=0x4000, status=None):
+    return PL.lib().purlin_unpack_dedup(T, H, P, rows, y, row_of, out, status, None)
+
+
+@pytest.mark.parametrize(
+    "kw",
+    [dict(P=0), dict(P=17), dict(T=-1), dict(H=0), dict(rows=-1), dict(rows=1 << 31), dict(y=None),
+     dict(row_of=None), dict(out=None), dict(out=0x4004), dict(y=0x100008), dict(out=0x100000 + 64 * 2 * 99),
+     dict(status=0x5001)],
+)
+def test_unpack_dedup_argument_validation(kw):
+    assert _unpack_dedup(**kw) == INVALID
+
+
 def test_python_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(PL, "_lib", None)
     monkeypatch.setattr(PL, "LIB_PATH", str(tmp_path / "missing.so"))
