@@ -403,60 +403,11 @@ def measure_extra_ops(torch, PL, ins, rs_out, ag_out, P, N, s, reps=5):
     return out
 
 
-def measure_ep(torch, PL, W, P, T, H, E, K, reps=5):
-    """Expert-parallel dispatch and combine of P ranks with T tokens each
-    (Table 2): dispatch = P packs, then the AllToAllV of the packed rows with
-    the packs' dest_counts (read on the device, unit = H); combine = the
-    reverse AllToAllV (same counts, column-major), then P unpacks.  Receive
-    buffers hold the worst case, P*T*K rows.  Routing: Zipf(1.1) top-K per
-    rank, seeded per rank.  Event-timed on the current stream."""
-    rows_in, rows_out = T * K, P * T * K
-    i32 = dict(dtype=torch.int32, device="cuda")
-    counts = torch.zeros((P, P), **i32)
-    xs, ids, gates, packs = [], [], [], []
-    rngs = W.rank_rngs(4040, P)
-    for p in range(P):
-        xs.append(to_dev(torch, W.normal_bf16(rngs[p], T * H).reshape(T, H)))
-        ids.append(torch.from_numpy(W.zipf_topk_ids(T, E, K, 1.1, 4000 + p)).to("cuda"))
-        gates.append(torch.from_numpy(W.softmax_gates(T, K, 5000 + p)).to("cuda"))
-        packs.append(dict(packed=torch.empty((rows_in, H), dtype=torch.int16, device="cuda"), dest_counts=counts[p],
-                          dest_offsets=torch.empty(P, **i32), expert_counts=torch.empty(E, **i32),
-                          expert_offsets=torch.empty(E, **i32), pos=torch.empty((T, K), **i32)))
-    ws = torch.empty(max(PL.purlin_pack_workspace_size(T, K, E), 16), dtype=torch.uint8, device="cuda")
-    recv = [torch.empty(rows_out * H, dtype=torch.int16, device="cuda") for _ in range(P)]
-    back = [torch.empty(rows_in * H, dtype=torch.int16, device="cuda") for _ in range(P)]
-    outs = [torch.empty((T, H), dtype=torch.int16, device="cuda") for _ in range(P)]
-    fwd = PL.purlin_plan_v("alltoallv", P, rows_in * H, "bf16", 1 << 20, unit=H, out_capacity=rows_out * H)
-    bwd = PL.purlin_plan_v("alltoallv", P, rows_out * H, "bf16", 1 << 20, unit=H, out_capacity=rows_in * H,
-                           counts_transposed=True)
-    flat = counts.view(-1)
-
-    def pack_all():
-        for p in range(P):
-            PL.purlin_pack(xs[p], ids[p], E, P, out=packs[p], workspace=ws)
-
-    def dispatch_a2a():
-        fwd.exec_v([pk["packed"].view(-1) for pk in packs], recv, flat)
-
-    def combine_a2a():
-        bwd.exec_v(recv, back, flat)
-
-    def unpack_all():
-        for p in range(P):
-            PL.purlin_unpack(back[p].view(rows_in, H), packs[p]["pos"], gates[p], out=outs[p])
-
-    stages = [("pack", pack_all), ("dispatch_alltoallv", dispatch_a2a), ("combine_alltoallv", combine_a2a),
-              ("unpack", unpack_all)]
+def _time_stages(torch, stages, bmin, reps):
+    """Event-time each stage (a callable) of a sequence, averaged over reps."""
     for _, f in stages:
         f()
     torch.cuda.synchronize()
-    row = H * 2
-    bmin = {
-        "pack": P * (T * row + rows_in * row + 2 * rows_in * 4),
-        "dispatch_alltoallv": P * 2 * rows_in * row,
-        "combine_alltoallv": P * 2 * rows_in * row,
-        "unpack": P * (rows_in * row + T * row + 2 * rows_in * 4),
-    }
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
     tot = [0.0] * len(stages)
     for _ in range(reps):
@@ -473,16 +424,94 @@ def measure_ep(torch, PL, W, P, T, H, E, K, reps=5):
         out[name] = {"avg_us": round(us, 2), "bytes_min": int(bmin[name]),
                      "GBps_min": round(bmin[name] / (us * 1e-6) / 1e9, 1),
                      "frac_of_hbm_peak": round(bmin[name] / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
-    m = counts.cpu().numpy()
     total_us = sum(v["avg_us"] for v in out.values())
     total_b = sum(bmin.values())
     out["round_trip"] = {"avg_us": round(total_us, 2), "bytes_min": int(total_b),
                          "GBps_min": round(total_b / (total_us * 1e-6) / 1e9, 1),
                          "frac_of_hbm_peak": round(total_b / (total_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
-    out["workload"] = {"P": P, "T_per_rank": T, "H": H, "E": E, "K": K, "routing": "Zipf(1.1) top-K",
-                       "rows_received_per_rank": [int(x) for x in m.sum(axis=0)]}
-    del xs, ids, gates, packs, recv, back, outs, ws
     return out
+
+
+def measure_ep(torch, PL, W, P, T, H, E, K, reps=5):
+    """Expert-parallel dispatch and combine of P ranks with T tokens each
+    (Table 2): dispatch = P packs, then the AllToAllV of the packed rows with
+    the packs' dest_counts (read on the device, unit = H); combine = the
+    reverse AllToAllV (same counts, column-major), then P unpacks.  Receive
+    buffers hold the worst case.  Routing: Zipf(1.1) top-K per rank, seeded
+    per rank.  Two variants: one row per (token, slot), and de-duplicated
+    (one row per token and destination rank; its combine sums the ranks'
+    partial rows).  Event-timed on the current stream."""
+    i32 = dict(dtype=torch.int32, device="cuda")
+    row = H * 2
+    xs, ids, gates = [], [], []
+    rngs = W.rank_rngs(4040, P)
+    for p in range(P):
+        xs.append(to_dev(torch, W.normal_bf16(rngs[p], T * H).reshape(T, H)))
+        ids.append(torch.from_numpy(W.zipf_topk_ids(T, E, K, 1.1, 4000 + p)).to("cuda"))
+        gates.append(torch.from_numpy(W.softmax_gates(T, K, 5000 + p)).to("cuda"))
+    result = {}
+    for variant in ("per_slot", "dedup"):
+        dedup = variant == "dedup"
+        rows_in = T * (min(K, P) if dedup else K)
+        rows_out = P * rows_in
+        counts = torch.zeros((P, P), **i32)
+        if dedup:
+            packs = [dict(packed=torch.empty((rows_in, H), dtype=torch.int16, device="cuda"), dest_counts=counts[p],
+                          dest_offsets=torch.empty(P, **i32), row_of=torch.empty((T, P), **i32)) for p in range(P)]
+            ws = torch.empty(max(PL.purlin_pack_dedup_workspace_size(T, P), 16), dtype=torch.uint8, device="cuda")
+        else:
+            packs = [dict(packed=torch.empty((rows_in, H), dtype=torch.int16, device="cuda"), dest_counts=counts[p],
+                          dest_offsets=torch.empty(P, **i32), expert_counts=torch.empty(E, **i32),
+                          expert_offsets=torch.empty(E, **i32), pos=torch.empty((T, K), **i32)) for p in range(P)]
+            ws = torch.empty(max(PL.purlin_pack_workspace_size(T, K, E), 16), dtype=torch.uint8, device="cuda")
+        recv = [torch.empty(rows_out * H, dtype=torch.int16, device="cuda") for _ in range(P)]
+        back = [torch.empty(rows_in * H, dtype=torch.int16, device="cuda") for _ in range(P)]
+        outs = [torch.empty((T, H), dtype=torch.int16, device="cuda") for _ in range(P)]
+        fwd = PL.purlin_plan_v("alltoallv", P, rows_in * H, "bf16", 1 << 20, unit=H, out_capacity=rows_out * H)
+        bwd = PL.purlin_plan_v("alltoallv", P, rows_out * H, "bf16", 1 << 20, unit=H, out_capacity=rows_in * H,
+                               counts_transposed=True)
+        flat = counts.view(-1)
+
+        def pack_all(dedup=dedup, packs=packs, ws=ws):
+            for p in range(P):
+                if dedup:
+                    PL.purlin_pack_dedup(xs[p], ids[p], E, P, out=packs[p], workspace=ws)
+                else:
+                    PL.purlin_pack(xs[p], ids[p], E, P, out=packs[p], workspace=ws)
+
+        def unpack_all(dedup=dedup, packs=packs, back=back, outs=outs, rows_in=rows_in):
+            for p in range(P):
+                if dedup:
+                    PL.purlin_unpack_dedup(back[p].view(rows_in, H), packs[p]["row_of"], out=outs[p])
+                else:
+                    PL.purlin_unpack(back[p].view(rows_in, H), packs[p]["pos"], gates[p], out=outs[p])
+
+        stages = [("pack", pack_all),
+                  ("dispatch_alltoallv", lambda fwd=fwd, packs=packs, recv=recv, flat=flat:
+                   fwd.exec_v([pk["packed"].view(-1) for pk in packs], recv, flat)),
+                  ("combine_alltoallv", lambda bwd=bwd, recv=recv, back=back, flat=flat: bwd.exec_v(recv, back, flat)),
+                  ("unpack", unpack_all)]
+        pack_all()
+        torch.cuda.synchronize()
+        m = counts.cpu().numpy()
+        sent = m.sum(axis=1)  # rows each rank sends (= receives back)
+        meta = P * T * K * 4 + (P * T * P * 4 if dedup else P * T * K * 4)  # ids + row_of / pos
+        bmin = {
+            "pack": P * T * row + int(sent.sum()) * row + meta,
+            "dispatch_alltoallv": 2 * int(sent.sum()) * row,
+            "combine_alltoallv": 2 * int(sent.sum()) * row,
+            "unpack": int(sent.sum()) * row + P * T * row + (P * T * P * 4 if dedup else 2 * P * T * K * 4),
+        }
+        r = _time_stages(torch, stages, bmin, reps)
+        r["rows_sent_per_rank"] = [int(v) for v in sent]
+        r["rows_received_per_rank"] = [int(v) for v in m.sum(axis=0)]
+        result[variant] = r
+        del packs, recv, back, outs, ws
+    result["workload"] = {"P": P, "T_per_rank": T, "H": H, "E": E, "K": K, "routing": "Zipf(1.1) top-K"}
+    result["dedup_speedup"] = round(result["per_slot"]["round_trip"]["avg_us"] /
+                                    result["dedup"]["round_trip"]["avg_us"], 3)
+    del xs, ids, gates
+    return result
 
 
 def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
