@@ -177,17 +177,23 @@ purlin_status purlin_exec_v(purlin_plan_t plan, void* const* bufs, const int32_t
     if (!plan) return PURLIN_ERR_INVALID;
     const purlin::Plan& p = plan->plan;
     if (!p.vop) return PURLIN_ERR_INVALID;
-    if (p.items.empty()) return PURLIN_OK;
+    if (p.flags & PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
     if (!counts || (reinterpret_cast<uintptr_t>(counts) & 3u)) return PURLIN_ERR_INVALID;
     if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
-    const purlin_status st = check_buffers(p, bufs);
-    if (st != PURLIN_OK) return st;
+    if (p.items.empty()) {
+        // zero capacity: no buffer is touched (bufs is ignored), but the sizes
+        // are still checked on the device when a status word is given
+        if (!dev_status) return PURLIN_OK;
+    } else {
+        const purlin_status st = check_buffers(p, bufs);
+        if (st != PURLIN_OK) return st;
+    }
     const purlin::Phase& ph = p.phases[0];
     const hipError_t e =
         purlin::launch_v(p.op, p.d_items, ph.count, p.P, p.dtype, ph.nt_load || ph.nt_store, bufs, counts,
                          (p.flags & PURLIN_PLAN_COUNTS_TRANSPOSED) != 0, p.v_src_major, dev_status, p.in_capacity,
-                         p.out_capacity,
-                         p.unit, static_cast<hipStream_t>(stream));
+                         p.out_capacity, p.unit, p.chunk, p.reduce_item_bytes ? p.reduce_item_bytes : p.chunk,
+                         p.op == PURLIN_ALLTOALLV ? static_cast<uint32_t>(p.P) : 1u, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
 }
 

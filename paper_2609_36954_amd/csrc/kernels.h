@@ -34,10 +34,12 @@ hipError_t launch_fused_allreduce(const purlin_desc* items, uint64_t n, uint64_t
 
 // Variable-size collectives: one launch; sizes read from device `counts`
 // (int32, in units of `unit` elements).  `status` (optional) receives 0 or
-// 1 (invalid sizes: the call then writes nothing).
+// 1 (invalid sizes: the call then writes nothing).  The n items form
+// `spaces` equal spaces, each a run of chunks cut at item_bytes.
 hipError_t launch_v(purlin_op op, const purlin_desc* items, uint64_t n, int P, purlin_dtype dtype, bool streaming,
                     void* const* bufs, const int32_t* counts, bool counts_transposed, bool source_major,
-                    int32_t* status, uint64_t in_capacity, uint64_t out_capacity, uint64_t unit, hipStream_t stream);
+                    int32_t* status, uint64_t in_capacity, uint64_t out_capacity, uint64_t unit, uint64_t chunk,
+                    uint64_t item_bytes, uint32_t spaces, hipStream_t stream);
 
 struct PackWorkspace {
     int32_t* tile_base;  // [ntiles * E]: per-tile expert counts, then row bases

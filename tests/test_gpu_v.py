@@ -144,3 +144,33 @@ def test_v_zipf_split_at_256MiB_per_rank():
             start = sum(m[p][:r])
             pieces.append(ins[p][start:start + m[p][r]])
         assert torch.equal(out2[r], torch.cat(pieces)), f"AllToAllV rank {r}"
+
+
+@pytest.mark.parametrize("op", ["allgatherv", "reduce_scatterv", "alltoallv"])
+def test_v_zero_capacity_still_checks_sizes(op):
+    P = 4
+    plan = PL.Plan(op, P, 0, "bf16", 256, unit=1)
+    n = P * P if op == "alltoallv" else P
+    empty = [torch.empty(0, dtype=torch.int16, device="cuda") for _ in range(P)]
+    for counts, want in (([0] * n, 0), ([0] * (n - 1) + [1], 1)):
+        st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+        plan.exec_v(empty, empty, to_device(np.asarray(counts, np.int32)), dev_status=st)
+        torch.cuda.synchronize()
+        assert int(st.item()) == want
+
+
+@pytest.mark.parametrize("op", ["allgatherv", "reduce_scatterv", "alltoallv"])
+def test_v_small_sizes_in_a_large_capacity(op):
+    """Most items lie beyond the run-time sizes (the waves skip them)."""
+    P, cap = 8, 1 << 20
+    rng = np.random.default_rng(len(op))
+    n = P * P if op == "alltoallv" else P
+    counts = [int(x) for x in rng.integers(0, 3000, n)]
+    ins = _inputs(P, cap, "bf16", seed=11)
+    want = _oracle_v(op, ins, counts, P, "bf16", 1)
+    plan = PL.Plan(op, P, cap, "bf16", 4096, unit=1)
+    got, status = run_v(plan, ins, counts, "bf16")
+    assert status == 0
+    for r in range(P):
+        assert_bits_equal(got[r][: len(want[r])], want[r], "bf16", f"{op} rank {r}")
+        assert np.all(got[r][len(want[r]):].view(np.uint8) == CANARY)

@@ -254,3 +254,45 @@ def test_alltoallv_covers_the_smaller_side(in_cap, out_cap, src_major):
         assert np.array_equal(d["src_buf"], d["part"]) and np.all(d["dst_step"] == 1) and np.all(d["dst_buf"] == P)
     else:
         assert np.array_equal(d["dst_buf"], d["part"] + P) and np.all(d["dst_step"] == 0)
+
+
+def _item_layout_ok(d, spaces, chunk, item_bytes):
+    """Item j of every space starts at (j // per_chunk) * chunk + (j % per_chunk) * item."""
+    n = len(d)
+    assert n % spaces == 0
+    per_space = n // spaces
+    per_chunk = -(-chunk // item_bytes)
+    for k in range(spaces):
+        seg = d[k * per_space:(k + 1) * per_space]
+        assert np.all(seg["part"] == (k if spaces > 1 else 0))
+        j = np.arange(per_space)
+        assert np.array_equal(seg["src_off"], (j // per_chunk) * chunk + (j % per_chunk) * item_bytes)
+    return per_space, per_chunk
+
+
+def _active(extent, chunk, item_bytes, per_chunk, per_space):
+    """The kernels' closed form: items of a space that start below `extent` bytes."""
+    if extent == 0:
+        return 0
+    o = extent - 1
+    return min(per_space, (o // chunk) * per_chunk + (o % chunk) // item_bytes + 1)
+
+
+@pytest.mark.parametrize("op", ["allgatherv", "reduce_scatterv", "alltoallv"])
+@pytest.mark.parametrize("cap,chunk_e,item", [(1000, 64, 0), (999, 7, 16), (4096, 1000, 48), (5, 1000, 0),
+                                              (12345, 256, 128)])
+def test_v_items_follow_the_closed_form_the_kernels_use(op, cap, chunk_e, item):
+    """The V kernels enumerate only the items below the run-time extent by
+    arithmetic on (chunk, item); this pins the table layout that relies on."""
+    P, s = 4, 2
+    plan = PL.Plan(op, P, cap, "bf16", chunk_e * s, policy=dict(item_bytes=item) if item else None, host_only=True,
+                   unit=1)
+    items, _ = plan.items()
+    spaces = P if op == "alltoallv" else 1
+    item_bytes = int(items["bytes"].max())
+    per_space, per_chunk = _item_layout_ok(items, spaces, chunk_e * s, item_bytes)
+    for extent in sorted({0, 1, s, chunk_e * s - s, chunk_e * s, chunk_e * s + s, cap * s // 2, cap * s - s, cap * s}):
+        if extent < 0 or extent > cap * s:
+            continue
+        want = int(np.sum(items["src_off"][:per_space] < extent))
+        assert _active(extent, chunk_e * s, item_bytes, per_chunk, per_space) == want, extent
