@@ -132,7 +132,7 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
     __shared__ int32_t partial[kMaxExperts];  // per work unit (expert, tile slice)
     __shared__ int32_t total[kMaxExperts];    // per expert
     __shared__ int32_t offs[kMaxExperts];     // per expert, exclusive prefix
-    __shared__ int32_t scan[kScanThreads];
+    __shared__ int32_t scan[kScanThreads / kWave];  // wave totals
     const int tid = threadIdx.x;
 
     // error flags first, so their loads overlap the count loads
@@ -169,22 +169,25 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
     __syncthreads();
 
     // Exclusive prefix over experts: each thread sums a run of consecutive
-    // experts, a Hillis-Steele scan combines the runs.
+    // experts; the runs are combined by a cross-lane scan in every wave and
+    // a scan of the wave totals.
     const int per = (E + kScanThreads - 1) / kScanThreads;
     int local = 0;
     for (int i = 0; i < per; ++i) {
         const int e = tid * per + i;
         if (e < E) local += total[e];
     }
-    scan[tid] = local;
-    __syncthreads();
-    for (int off = 1; off < kScanThreads; off <<= 1) {
-        const int v = tid >= off ? scan[tid - off] : 0;
-        __syncthreads();
-        scan[tid] += v;
-        __syncthreads();
+    const uint32_t lane = tid & (kWave - 1), wave = tid / kWave;
+    int incl = local;
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int u = __shfl_up(incl, off);
+        if (lane >= static_cast<uint32_t>(off)) incl += u;
     }
-    int run = scan[tid] - local;
+    if (lane == kWave - 1) scan[wave] = incl;
+    __syncthreads();
+    int wave_base = 0;
+    for (uint32_t q = 0; q < wave; ++q) wave_base += scan[q];
+    int run = wave_base + incl - local;
     for (int i = 0; i < per; ++i) {
         const int e = tid * per + i;
         if (e < E) {
@@ -300,28 +303,36 @@ __global__ __launch_bounds__(kBlock) void pack_rows(int T, int H, int K, int E, 
 
 // ---------------------------------------------------------------------------
 // De-duplicated dispatch: one row per (token, destination rank).
-//   1. dedup_tiles: one wavefront per tile of 64 tokens, lane = token.  A
-//      lane forms its token's destination mask (bit r: some expert of the
-//      token lives on rank r) and checks the ids; per destination a ballot
-//      gives the tile's count and each token's rank among the tile's tokens
-//      bound there (popcount below the lane).
+//   1. dedup_tiles: one workgroup per tile of 64 tokens stages the tile's
+//      ids in LDS; then one wavefront, lane = token, forms each token's
+//      destination mask (bit r: some expert of the token lives on rank r)
+//      and checks the ids; per destination a ballot gives the tile's count
+//      and each token's rank among the tile's tokens bound there (popcount
+//      below the lane).
 //   2. dedup_scan: one workgroup; wave r scans destination r's tile counts
 //      in tile order with cross-lane prefix sums, rewriting them into tile
 //      bases; then destination counts and offsets, and the error flag.
 //   3. dedup_rows: one wavefront per (token, column slice); lane r < P forms
 //      row_of[t, r], and the row is streamed once into each of its rows.
-__global__ __launch_bounds__(kWave) void dedup_tiles(int T, int K, int E, int P, const int32_t* __restrict__ ids,
-                                                     int32_t* __restrict__ tile_cnt, int32_t* __restrict__ lrank,
-                                                     int32_t* __restrict__ tile_err) {
+__global__ __launch_bounds__(kBlock) void dedup_tiles(int T, int K, int E, int P, const int32_t* __restrict__ ids,
+                                                      int32_t* __restrict__ tile_cnt, int32_t* __restrict__ lrank,
+                                                      int32_t* __restrict__ tile_err) {
+    __shared__ int32_t tids[kWave * 64];  // the tile's ids (K <= 64), loaded by the whole workgroup
     const int tile = blockIdx.x;
+    const int64_t t0 = static_cast<int64_t>(tile) * kWave;
+    const int nt = static_cast<int>(min<int64_t>(kWave, T - t0));
+    const int n = nt * K;
+    const int32_t* gids = ids + t0 * K;
+    for (int j = threadIdx.x; j < n; j += kBlock) tids[j] = gids[j];
+    __syncthreads();
+    if (threadIdx.x >= kWave) return;
     const uint32_t lane = threadIdx.x;
-    const int64_t t = static_cast<int64_t>(tile) * kWave + lane;
-    const bool valid = t < T;
+    const bool valid = static_cast<int>(lane) < nt;
     const int L = E / P;
     uint32_t mask = 0;
     bool bad = false;
     if (valid) {
-        const int32_t* row = ids + t * K;
+        const int32_t* row = tids + lane * K;
         for (int k = 0; k < K; ++k) {
             const int e = row[k];
             if (e < 0 || e >= E) {
@@ -334,6 +345,7 @@ __global__ __launch_bounds__(kWave) void dedup_tiles(int T, int K, int E, int P,
         }
     }
     const uint64_t below = (uint64_t(1) << lane) - 1u;
+    const int64_t t = t0 + lane;
     for (int r = 0; r < P; ++r) {
         const bool has = valid && ((mask >> r) & 1u);
         const uint64_t b = __ballot(has);
@@ -603,7 +615,7 @@ hipError_t launch_pack_dedup(int T, int H, int K, int E, int P, const uint16_t* 
                                                    align256(4 * static_cast<uint64_t>(T) * P));
     (void)hipGetLastError();
     if (ntiles > 0)
-        hipLaunchKernelGGL(dedup_tiles, dim3(ntiles), dim3(kWave), 0, stream, T, K, E, P, ids, tile_base, lrank,
+        hipLaunchKernelGGL(dedup_tiles, dim3(ntiles), dim3(kBlock), 0, stream, T, K, E, P, ids, tile_base, lrank,
                            tile_err);
     hipLaunchKernelGGL(dedup_scan, dim3(1), dim3(kScanThreads), 0, stream, ntiles, P, tile_base, tile_err, dest_counts,
                        dest_offsets, dev_status);
