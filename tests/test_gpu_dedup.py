@@ -205,3 +205,53 @@ def test_expert_parallel_dedup_round_trip():
         assert np.array_equal(to_host(back[p], np.uint16).reshape(rows_in, H)[:R], y), f"rank {p} exchange"
         assert_bits_equal(to_host(outs[p], np.uint16).reshape(T, H), oracle.unpack_dedup(y, d["row_of"]), "bf16",
                           f"rank {p} combine")
+
+
+def test_dedup_dispatch_and_combine_in_one_graph():
+    """pack_dedup and unpack_dedup captured once and replayed with new
+    routing: sizes and row indices are formed on the device each replay."""
+    T, H, K, E, P = 200, 136, 4, 32, 8
+    x = torch.empty((T, H), dtype=torch.int16, device="cuda")
+    ids = torch.empty((T, K), dtype=torch.int32, device="cuda")
+    packed = torch.empty((T * min(K, P), H), dtype=torch.int16, device="cuda")
+    out = dict(packed=packed, dest_counts=torch.empty(P, dtype=torch.int32, device="cuda"),
+               dest_offsets=torch.empty(P, dtype=torch.int32, device="cuda"),
+               row_of=torch.empty((T, P), dtype=torch.int32, device="cuda"))
+    ws = torch.empty(max(PL.purlin_pack_dedup_workspace_size(T, P), 16), dtype=torch.uint8, device="cuda")
+    comb = torch.empty((T, H), dtype=torch.int16, device="cuda")
+    st = torch.zeros(2, dtype=torch.int32, device="cuda")
+
+    def step(stream=None):
+        PL.purlin_pack_dedup(x, ids, E, P, out=out, workspace=ws, dev_status=st[0:1], stream=stream)
+        PL.purlin_unpack_dedup(packed, out["row_of"], out=comb, dev_status=st[1:2], stream=stream)
+
+    def load(seed):
+        rng = np.random.default_rng(seed)
+        xn = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
+        xn[(xn & 0x7F80) == 0x7F80] = 0x3F80  # finite values
+        idn = _distinct_ids(rng, T, K, E)
+        x.copy_(to_device(xn))
+        ids.copy_(to_device(idn))
+        return xn, idn
+
+    load(0)
+    step()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            step(stream=side)
+    for seed in (1, 2, 3):
+        xn, idn = load(seed)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        want = oracle.pack_dedup(xn, idn, E, P)
+        assert not st.any().item()
+        assert np.array_equal(to_host(out["row_of"], np.int32).reshape(T, P), want["row_of"])
+        R = len(want["packed"])
+        assert np.array_equal(to_host(packed, np.uint16).reshape(-1, H)[:R], want["packed"])
+        assert_bits_equal(to_host(comb, np.uint16).reshape(T, H), oracle.unpack_dedup(want["packed"], want["row_of"]),
+                          "bf16", f"replay seed {seed}")

@@ -336,3 +336,37 @@ def test_offsets_beyond_4GiB_per_rank():
     ag.exec(rs_out, [outs[1], torch.empty(N, dtype=torch.int16, device="cuda")])
     torch.cuda.synchronize()
     assert torch.equal(outs[1], outs[0])
+
+
+def test_plans_run_concurrently_on_two_streams():
+    """A plan is immutable: executions on different streams with distinct
+    buffers may overlap (AllReduce on one stream, AllToAll and AllGather on
+    another), each matching the oracle."""
+    P, M = 8, 65536
+    ins_a = _inputs(P, P * M, "bf16", seed=501)
+    ins_b = _inputs(P, P * M, "bf16", seed=502)
+    ar = PL.Plan("allreduce", P, P * M, "bf16", 1 << 16)
+    a2a = PL.Plan("alltoall", P, P * M, "bf16", 1 << 16)
+    ag = PL.Plan("allgather", P, P * M, "bf16", 1 << 16)
+    d_a = [to_device(a) for a in ins_a]
+    d_b = [to_device(a) for a in ins_b]
+    d_g = [to_device(a[:M]) for a in ins_b]
+    out_a = [torch.empty(P * M, dtype=torch.int16, device="cuda") for _ in range(P)]
+    out_b = [torch.empty(P * M, dtype=torch.int16, device="cuda") for _ in range(P)]
+    out_g = [torch.empty(P * M, dtype=torch.int16, device="cuda") for _ in range(P)]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            ar.exec(d_a, out_a, stream=s1)
+        with torch.cuda.stream(s2):
+            a2a.exec(d_b, out_b, stream=s2)
+            ag.exec(d_g, out_g, stream=s2)
+    torch.cuda.synchronize()
+    want_a = oracle.all_reduce(ins_a, "bf16")
+    want_b = oracle.all_to_all(ins_b, "bf16")
+    want_g = oracle.all_gather([a[:M] for a in ins_b], "bf16")
+    for r in range(P):
+        assert_bits_equal(to_host(out_a[r], np.uint16), want_a[r], "bf16", f"AllReduce rank {r}")
+        assert_bits_equal(to_host(out_b[r], np.uint16), want_b[r], "bf16", f"AllToAll rank {r}")
+        assert_bits_equal(to_host(out_g[r], np.uint16), want_g[r], "bf16", f"AllGather rank {r}")
