@@ -185,8 +185,9 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
     }
     if (lane == kWave - 1) scan[wave] = incl;
     __syncthreads();
-    int wave_base = 0;
-    for (uint32_t q = 0; q < wave; ++q) wave_base += scan[q];
+    // this wave's base: the totals of the waves before it, summed across lanes
+    int wave_base = lane < wave ? scan[lane] : 0;
+    for (int off = kWave / 2; off > 0; off >>= 1) wave_base += __shfl_xor(wave_base, off);
     int run = wave_base + incl - local;
     for (int i = 0; i < per; ++i) {
         const int e = tid * per + i;
@@ -219,11 +220,12 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
         }
     }
 
+    // rank r's rows: its experts' offsets are contiguous, so its count is
+    // the difference of two expert offsets
     const int L = E / P;
     for (int r = tid; r < P; r += kScanThreads) {
-        int sum = 0;
-        for (int e = r * L; e < (r + 1) * L; ++e) sum += total[e];
-        dest_counts[r] = sum;
+        const int end = r + 1 < P ? offs[(r + 1) * L] : offs[E - 1] + total[E - 1];
+        dest_counts[r] = end - offs[r * L];
         dest_offsets[r] = offs[r * L];
     }
 
