@@ -286,6 +286,8 @@ def main():
             "GBps_min": round(bmin / (avg_ms * 1e-3) / 1e9, 1),
             "frac_of_hbm_peak": round(bmin / (avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         }
+        if name in ("reduce_scatter", "allgather"):  # the paper's algorithm bandwidth: per-rank message / time
+            per_op[name]["algbw_GBps"] = round(N * s / (avg_ms * 1e-3) / 1e9, 1)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
 
     # dominant single-kernel op (RS, AG and combine are one launch each)
@@ -399,7 +401,8 @@ def measure_extra_ops(torch, PL, ins, rs_out, ag_out, P, N, s, reps=5):
         us = e0.elapsed_time(e1) * 1e3 / reps
         out[name] = {"avg_us": round(us, 2), "bytes_min": int(bmin), "bytes_sched": int(plan.sched_bytes),
                      "GBps_min": round(bmin / (us * 1e-6) / 1e9, 1),
-                     "frac_of_hbm_peak": round(bmin / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+                     "frac_of_hbm_peak": round(bmin / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                     "algbw_GBps": round(N * s / (us * 1e-6) / 1e9, 1)}
     return out
 
 
@@ -520,11 +523,34 @@ def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
     lat_out = [torch.empty(c2.count, dtype=torch.int16, device="cuda") for _ in range(c2.P)]
     ar2 = PL.Plan("allreduce", c2.P, c2.count, "bf16", c2.chunk)
     lat_us = graph_latency_us(ar2, lat_in, lat_out)
+    # without a graph (plan bound to its buffers once): back-to-back eager
+    # calls, and one call after the stream drained
+    run = ar2.bind(lat_in, lat_out)
+    run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(100):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    eager_us = e0.elapsed_time(e1) * 1e3 / 100
+    singles = []
+    for _ in range(20):
+        torch.cuda.synchronize()
+        e0.record()
+        run()
+        e1.record()
+        torch.cuda.synchronize()
+        singles.append(e0.elapsed_time(e1) * 1e3)
     latency = {
         "allreduce_p8_bf16_128x8192": {
             "us": round(lat_us, 2),
             "GBps_min": round(collective_bytes("allreduce", c2.P, c2.count, 2) / (lat_us * 1e-6) / 1e9, 1),
             "algbw_GBps": round(c2.count * 2 / (lat_us * 1e-6) / 1e9, 1),
+            "timing": "graph of 128 calls, 8 replays after one warm-up replay (time / 1024)",
+            "eager_back_to_back_us": round(eager_us, 2),
+            "single_call_us": round(float(np.median(singles)), 2),
         }
     }
     if sweep_sizes:

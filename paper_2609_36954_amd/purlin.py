@@ -257,6 +257,13 @@ class Plan:
         """Run a variable-size plan; ``counts`` is a device int32 tensor."""
         purlin_exec_v(self, ins, outs, counts, dev_status, stream)
 
+    def bind(self, ins, outs, counts=None, dev_status=None, stream=None):
+        """Validate the buffers once and return a callable that enqueues the
+        plan on them (on ``stream``, default: the current stream at bind
+        time) with no further Python-side work: for serving loops that run
+        the same collective on the same buffers."""
+        return BoundExec(self, ins, outs, counts, dev_status, stream)
+
     def destroy(self):
         if getattr(self, "_h", None) is not None and _lib is not None:
             _lib.purlin_plan_destroy(self._h)
@@ -267,6 +274,39 @@ class Plan:
             self.destroy()
         except Exception:
             pass
+
+
+class BoundExec:
+    """A plan bound to fixed buffers and a stream (see ``Plan.bind``).  It
+    keeps references to the tensors, so they outlive it."""
+
+    def __init__(self, plan, ins, outs, counts=None, dev_status=None, stream=None):
+        self._plan = plan
+        self._keep = (list(ins), list(outs), counts, dev_status)
+        L = lib()
+        if plan.unit is not None:
+            if counts is None:
+                raise PurlinError(PURLIN_ERR_INVALID, "a variable-size plan needs counts")
+            _require_cuda(counts, "counts", 4)
+            need = plan.P * plan.P if plan.op == "alltoallv" else plan.P
+            if counts.numel() < need:
+                raise PurlinError(PURLIN_ERR_INVALID, f"{plan.op} needs {need} counts")
+            arr = _buffer_array(plan, ins, outs)
+            args = (plan.handle, arr, _ptr(counts), _ptr(dev_status), _stream_handle(stream))
+            self._fn, self._args = L.purlin_exec_v, args
+        else:
+            if counts is not None:
+                raise PurlinError(PURLIN_ERR_INVALID, "counts are for variable-size plans")
+            if plan.count:
+                arr = _buffer_array(plan, ins, outs)
+            else:
+                arr = (ctypes.c_void_p * (2 * plan.P))()
+            self._fn, self._args = L.purlin_exec, (plan.handle, arr, _stream_handle(stream) if plan.count else None)
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st:
+            _check(st, "purlin_exec")
 
 
 def purlin_plan(op, P, count, dtype, chunk, policy=None, host_only=False):

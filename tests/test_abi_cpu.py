@@ -270,3 +270,9 @@ def test_python_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(PL, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(PL.PurlinError):
         PL.lib()
+
+
+def test_bind_checks_before_binding():
+    plan = PL.Plan("allgather", 2, 64, "bf16", 32, host_only=True)
+    with pytest.raises(PL.PurlinError):
+        plan.bind([None], [None])  # wrong number of buffers

@@ -370,3 +370,31 @@ def test_plans_run_concurrently_on_two_streams():
         assert_bits_equal(to_host(out_a[r], np.uint16), want_a[r], "bf16", f"AllReduce rank {r}")
         assert_bits_equal(to_host(out_b[r], np.uint16), want_b[r], "bf16", f"AllToAll rank {r}")
         assert_bits_equal(to_host(out_g[r], np.uint16), want_g[r], "bf16", f"AllGather rank {r}")
+
+
+def test_bound_plan_matches_exec():
+    """Plan.bind validates once and enqueues the same work as exec."""
+    P, M = 8, 4096
+    ins_np = _inputs(P, P * M, "bf16", seed=611)
+    ins = [to_device(a) for a in ins_np]
+    outs = [torch.empty(P * M, dtype=torch.int16, device="cuda") for _ in range(P)]
+    plan = PL.Plan("allreduce", P, P * M, "bf16", 4096)
+    run = plan.bind(ins, outs)
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    want = oracle.all_reduce(ins_np, "bf16")
+    for r in range(P):
+        assert_bits_equal(to_host(outs[r], np.uint16), want[r], "bf16", f"bound AllReduce rank {r}")
+    v = PL.purlin_plan_v("alltoallv", P, P * M, "bf16", 4096, unit=1)
+    counts = to_device(np.full(P * P, M, np.int32))
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    runv = v.bind(ins, outs, counts=counts, dev_status=st)
+    runv()
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    want = oracle.all_to_all(ins_np, "bf16")
+    for r in range(P):
+        assert_bits_equal(to_host(outs[r], np.uint16), want[r], "bf16", f"bound AllToAllV rank {r}")
+    with pytest.raises(PL.PurlinError):
+        v.bind(ins, outs)  # counts missing
