@@ -549,6 +549,7 @@ def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
             "GBps_min": round(collective_bytes("allreduce", c2.P, c2.count, 2) / (lat_us * 1e-6) / 1e9, 1),
             "algbw_GBps": round(c2.count * 2 / (lat_us * 1e-6) / 1e9, 1),
             "timing": "graph of 128 calls, 8 replays after one warm-up replay (time / 1024)",
+            "eager_via": "Plan.bind (buffers validated once)",
             "eager_back_to_back_us": round(eager_us, 2),
             "single_call_us": round(float(np.median(singles)), 2),
         }
