@@ -398,3 +398,25 @@ def test_bound_plan_matches_exec():
         assert_bits_equal(to_host(outs[r], np.uint16), want[r], "bf16", f"bound AllToAllV rank {r}")
     with pytest.raises(PL.PurlinError):
         v.bind(ins, outs)  # counts missing
+
+
+@pytest.mark.parametrize("op", ["allreduce", "reduce_scatter"])
+def test_repeated_runs_are_bit_identical(op):
+    """Eq. 2's fixed order: five runs, and runs with another chunk size and
+    item cut, give the same bits (no order depends on scheduling)."""
+    P, M = 8, 1 << 18
+    ins = [to_device(a) for a in _inputs(P, P * M, "bf16", seed=777)]
+    plan = PL.Plan(op, P, P * M, "bf16", 1 << 16)
+    outs = [torch.empty(plan.out_bytes // 2, dtype=torch.int16, device="cuda") for _ in range(P)]
+    plan.exec(ins, outs)
+    torch.cuda.synchronize()
+    first = [o.clone() for o in outs]
+    others = [plan] * 4 + [PL.Plan(op, P, P * M, "bf16", 4096, policy=dict(item_bytes=1024)),
+                           PL.Plan(op, P, P * M, "bf16", 3 << 20, policy=dict(ar_mode=2))]
+    for pl in others:
+        for o in outs:
+            o.fill_(0x5A5A)
+        pl.exec(ins, outs)
+        torch.cuda.synchronize()
+        for r in range(P):
+            assert torch.equal(outs[r], first[r]), f"{op} rank {r} differs between runs"
