@@ -613,22 +613,31 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
         return t.contiguous().view(torch.uint8).cpu().numpy().view(dt)
 
     log("bench: cpu baseline (oracle on a sample)")
+    t_start = time.perf_counter()
     frac = 1  # the whole of each partition of the collectives
     m = M // frac
     ok = True
     t_total, bytes_total = 0.0, 0
+    reps = 3  # every op: the median of three runs
+
+    def median_time(fn):
+        times, res = [], None
+        for _ in range(reps):
+            t = time.perf_counter()
+            res = fn()
+            times.append(time.perf_counter() - t)
+        return sorted(times)[reps // 2], res
+
     # ReduceScatter on the first m elements of every partition
     sub = [np.concatenate([a[k * M:k * M + m] for k in range(P)]) for a in ins_np]
-    t = time.perf_counter()
-    rs_want = oracle.reduce_scatter(sub, "bf16")
-    t_total += time.perf_counter() - t
+    dt, rs_want = median_time(lambda: oracle.reduce_scatter(sub, "bf16"))
+    t_total += dt
     bytes_total += collective_bytes("reduce_scatter", P, P * m, 2)
     for r in range(P):
         ok &= bool(np.array_equal(down(rs_out[r][:m], np.uint16), rs_want[r]))
     # AllGather of those
-    t = time.perf_counter()
-    ag_want = oracle.all_gather(rs_want, "bf16")
-    t_total += time.perf_counter() - t
+    dt, ag_want = median_time(lambda: oracle.all_gather(rs_want, "bf16"))
+    t_total += dt
     bytes_total += collective_bytes("allgather", P, P * m, 2)
     for r in (0, P - 1):
         got = np.concatenate([down(ag_out[r][k * M:k * M + m], np.uint16) for k in range(P)])
@@ -637,13 +646,8 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
     T = ids_np.shape[0]
     Ts = T
     H = x_np.shape[1]
-    reps = 3  # pack and combine: the median of three runs
-    times = []
-    for _ in range(reps):
-        t = time.perf_counter()
-        pw = oracle.pack(x_np, ids_np, E, P)
-        times.append(time.perf_counter() - t)
-    t_total += sorted(times)[reps // 2]
+    dt, pw = median_time(lambda: oracle.pack(x_np, ids_np, E, P))
+    t_total += dt
     bytes_total += pack_bytes(T, H, K, E, P)
     pos_want = pw["pos"]
     ok &= bool(np.array_equal(down(pack_out["pos"], np.int32).reshape(-1, K), pos_want))
@@ -652,12 +656,8 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
     rows = np.random.default_rng(0).choice(T * K, 256, replace=False)
     ok &= bool(np.array_equal(down(pack_out["packed"], np.uint16).reshape(T * K, H)[rows], pw["packed"][rows]))
     del pw
-    times = []
-    for _ in range(reps):
-        t = time.perf_counter()
-        cw = oracle.unpack(y_np, pos_want[:Ts], g_np[:Ts])
-        times.append(time.perf_counter() - t)
-    t_total += sorted(times)[reps // 2]
+    dt, cw = median_time(lambda: oracle.unpack(y_np, pos_want[:Ts], g_np[:Ts]))
+    t_total += dt
     bytes_total += unpack_bytes(Ts, H, K)
     ok &= bool(np.array_equal(down(comb_out[:Ts], np.uint16).reshape(Ts, H), cw))
     try:
@@ -669,9 +669,10 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
         "unit": "GB/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": f"the whole step: ReduceScatter+AllGather of 256 MiB/rank (P=8, bf16, one run) and "
-                  f"MoE pack and combine of all {T} tokens (median of {reps} runs)",
+        "sample": f"the whole step: ReduceScatter+AllGather of 256 MiB/rank (P=8, bf16) and MoE pack and "
+                  f"combine of all {T} tokens; each op the median of {reps} runs",
         "seconds": round(t_total, 3),
+        "cpu_seconds_spent": round(time.perf_counter() - t_start, 1),
         "host_cores_available": cores,
         "cpu": platform.processor() or platform.machine(),
         "numpy": np.__version__,
