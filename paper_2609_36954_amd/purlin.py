@@ -24,9 +24,9 @@ PURLIN_ERR_NOMEM = 3
 PURLIN_ERR_DEVICE = 4
 
 OPS = {"allreduce": 0, "reduce_scatter": 1, "allgather": 2, "alltoall": 3,
-       "broadcast": 4, "reduce": 5, "scatter": 6, "gather": 7}
+       "broadcast": 4, "reduce": 5, "scatter": 6, "gather": 7,
+       "allgatherv": 8, "reduce_scatterv": 9, "alltoallv": 10}
 ROOTED = ("broadcast", "reduce", "scatter", "gather")
-OPS.update({"allgatherv": 8, "reduce_scatterv": 9, "alltoallv": 10})
 VOPS = ("allgatherv", "reduce_scatterv", "alltoallv")
 DTYPES = {"fp32": 0, "bf16": 1}
 ELEM_BYTES = {"fp32": 4, "bf16": 2}
@@ -394,6 +394,17 @@ def purlin_exec(plan, ins, outs, stream=None):
     _check(lib().purlin_exec(plan.handle, arr, _stream_handle(stream) if plan.count else None), "purlin_exec")
 
 
+def _check_sizes(tensors, shapes):
+    """Every output the kernels write must be a contiguous device tensor
+    with at least as many elements of the right size as its shape holds."""
+    for name, (shape, dt) in shapes.items():
+        t = tensors[name]
+        need = int(np.prod(shape))
+        _require_cuda(t, name, 2 if name == "packed" else 4)
+        if t.numel() < need:
+            raise PurlinError(PURLIN_ERR_INVALID, f"{name} holds {t.numel()} elements, needs {need}")
+
+
 def purlin_pack_workspace_size(T, K, E):
     b = ctypes.c_uint64()
     _check(lib().purlin_pack_workspace_size(int(T), int(K), int(E), ctypes.byref(b)), "purlin_pack_workspace_size")
@@ -417,14 +428,16 @@ def purlin_pack(x, ids, E, P, out=None, workspace=None, dev_status=None, stream=
     _require_cuda(ids, "ids", 4)
     dev = x.device
     o = dict(out or {})
-    o.setdefault("packed", torch.empty((T * K, H), dtype=x.dtype, device=dev))
-    for name, n in (("dest_counts", P), ("dest_offsets", P), ("expert_counts", E), ("expert_offsets", E)):
-        o.setdefault(name, torch.empty(n, dtype=torch.int32, device=dev))
-    o.setdefault("pos", torch.empty((T, K), dtype=torch.int32, device=dev))
+    shapes = {"packed": ((T * K, H), x.dtype), "dest_counts": ((P,), torch.int32), "dest_offsets": ((P,), torch.int32),
+              "expert_counts": ((E,), torch.int32), "expert_offsets": ((E,), torch.int32),
+              "pos": ((T, K), torch.int32)}
+    for name, (shape, dt) in shapes.items():
+        if name not in o:  # allocate only what the caller did not supply
+            o[name] = torch.empty(shape, dtype=dt, device=dev)
+    _check_sizes(o, shapes)
     wsb = purlin_pack_workspace_size(T, K, E)
     if workspace is None:
         workspace = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
-    _require_cuda(o["packed"], "packed", 2)
     st = lib().purlin_pack(int(T), int(H), int(K), int(E), int(P), _ptr(x), _ptr(ids), _ptr(o["packed"]),
                            _ptr(o["dest_counts"]), _ptr(o["dest_offsets"]), _ptr(o["expert_counts"]),
                            _ptr(o["expert_offsets"]), _ptr(o["pos"]), _ptr(dev_status), _ptr(workspace),
@@ -444,9 +457,13 @@ def purlin_unpack(y, pos, gates, out=None, dev_status=None, stream=None):
     _require_cuda(gates, "gates", 4)
     if gates.dtype != torch.float32:
         raise PurlinError(PURLIN_ERR_INVALID, "gates must be float32")
+    if y.shape[0] < T * K or gates.numel() < T * K:
+        raise PurlinError(PURLIN_ERR_INVALID, "y needs T*K rows and gates T*K entries")
     if out is None:
         out = torch.empty((T, H), dtype=y.dtype, device=y.device)
     _require_cuda(out, "out", 2)
+    if out.numel() < T * H:
+        raise PurlinError(PURLIN_ERR_INVALID, "out holds fewer than T*H elements")
     st = lib().purlin_unpack(int(T), int(H), int(K), _ptr(y), _ptr(pos), _ptr(gates), _ptr(out), _ptr(dev_status),
                              _stream_handle(stream))
     _check(st, "purlin_unpack")
@@ -479,15 +496,12 @@ def purlin_pack_dedup(x, ids, E, P, out=None, workspace=None, dev_status=None, s
     _require_cuda(ids, "ids", 4)
     dev = x.device
     o = dict(out or {})
-    o.setdefault("packed", torch.empty((T * min(K, P), H), dtype=x.dtype, device=dev))
-    for name in ("dest_counts", "dest_offsets"):
-        o.setdefault(name, torch.empty(P, dtype=torch.int32, device=dev))
-    o.setdefault("row_of", torch.empty((T, P), dtype=torch.int32, device=dev))
-    _require_cuda(o["packed"], "packed", 2)
-    if o["packed"].numel() < T * min(K, P) * H:
-        raise PurlinError(PURLIN_ERR_INVALID, "packed holds fewer than T*min(K, P) rows")
-    if o["row_of"].numel() < T * P:
-        raise PurlinError(PURLIN_ERR_INVALID, "row_of holds fewer than T*P entries")
+    shapes = {"packed": ((T * min(K, P), H), x.dtype), "dest_counts": ((P,), torch.int32),
+              "dest_offsets": ((P,), torch.int32), "row_of": ((T, P), torch.int32)}
+    for name, (shape, dt) in shapes.items():
+        if name not in o:  # allocate only what the caller did not supply
+            o[name] = torch.empty(shape, dtype=dt, device=dev)
+    _check_sizes(o, shapes)
     wsb = purlin_pack_dedup_workspace_size(T, P)
     if workspace is None:
         workspace = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
@@ -511,6 +525,8 @@ def purlin_unpack_dedup(y, row_of, out=None, dev_status=None, stream=None):
     if out is None:
         out = torch.empty((T, H), dtype=y.dtype, device=y.device)
     _require_cuda(out, "out", 2)
+    if out.numel() < T * H:
+        raise PurlinError(PURLIN_ERR_INVALID, "out holds fewer than T*H elements")
     st = lib().purlin_unpack_dedup(int(T), int(H), int(P), int(rows), _ptr(y), _ptr(row_of), _ptr(out),
                                    _ptr(dev_status), _stream_handle(stream))
     _check(st, "purlin_unpack_dedup")

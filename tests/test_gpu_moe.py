@@ -181,3 +181,26 @@ def test_config4_pack_and_config5_combine_full_size():
     out, status = run_unpack(y, want["pos"], g)
     assert status == 0
     assert_bits_equal(out, oracle.unpack(y, want["pos"], g), "bf16", "config 5 combine")
+
+
+def test_binding_rejects_undersized_outputs_before_launch():
+    """The C ABI cannot see tensor sizes, so the binding checks every output
+    the kernels would write; nothing is enqueued on a rejection."""
+    T, H, K, E, P = 64, 32, 4, 16, 4
+    rng = np.random.default_rng(8)
+    x = to_device(rng.integers(0, 0x10000, (T, H)).astype(np.uint16))
+    ids = to_device(_distinct_ids(rng, T, K, E))
+    small = torch.empty(T * K * H - 1, dtype=torch.int16, device="cuda")
+    with pytest.raises(PL.PurlinError):
+        PL.purlin_pack(x, ids, E, P, out=dict(packed=small))
+    with pytest.raises(PL.PurlinError):
+        PL.purlin_pack(x, ids, E, P, out=dict(pos=torch.empty(T * K - 1, dtype=torch.int32, device="cuda")))
+    with pytest.raises(PL.PurlinError):
+        PL.purlin_pack_dedup(x, ids, E, P, out=dict(row_of=torch.empty(T * P - 1, dtype=torch.int32, device="cuda")))
+    r = PL.purlin_pack(x, ids, E, P)
+    g = torch.ones((T, K), dtype=torch.float32, device="cuda")
+    with pytest.raises(PL.PurlinError):
+        PL.purlin_unpack(r["packed"][: T * K - 1], r["pos"], g)
+    with pytest.raises(PL.PurlinError):
+        PL.purlin_unpack(r["packed"], r["pos"], g, out=torch.empty(T * H - 1, dtype=torch.int16, device="cuda"))
+    torch.cuda.synchronize()
