@@ -178,7 +178,7 @@ def main():
     if args.ingest_counters:
         return ingest_counters(*args.ingest_counters)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print(json.dumps({"error": "this build runs on one GPU: the P ranks are P buffers on that GPU; "
+        print(json.dumps({"error": "purlin-mi355x runs on one GPU: the P ranks are P buffers on that GPU; "
                           "--gpus above 1 is not supported"}))
         return 2
 
@@ -581,6 +581,7 @@ def emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, 
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
+        "accumulate": "f32",  # reductions and the combine add in binary32; copies move bf16 bits
         "data": "synthetic (seeded; shapes of the paper's prefill collectives and MoE dispatch/combine)",
         "config": {
             "workload": "ReduceScatter then AllGather P=8 bf16 256MiB/rank chunk 1MiB; MoE pack + combine "

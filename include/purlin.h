@@ -49,7 +49,7 @@ extern "C" {
 typedef enum purlin_status {
     PURLIN_OK = 0,
     PURLIN_ERR_INVALID = 1,     /* a bad argument; nothing was enqueued */
-    PURLIN_ERR_UNSUPPORTED = 2, /* valid request this build does not implement */
+    PURLIN_ERR_UNSUPPORTED = 2, /* valid request the library does not implement */
     PURLIN_ERR_NOMEM = 3,       /* descriptor table too large, or an allocation failed */
     PURLIN_ERR_DEVICE = 4       /* a HIP call or kernel launch failed */
 } purlin_status;

@@ -5,7 +5,7 @@ TEST INFRASTRUCTURE ONLY (see the package docstring).
 The paper names these operations only as the expert-parallel use of
 AllGather(V) / ReduceScatter(V) / AllToAll(V), "dispatch tokens and combine
 expert outputs" (Section 2, Table 2), and the variable-size layouts of
-Section 3.1 (``scatteredV``).  The contract below is this build's reading:
+Section 3.1 (``scatteredV``).  The contract below is this library's reading:
 
 Pack (dispatch), for ``ids[T, K]`` expert ids, ``E`` experts split evenly
 over ``P`` ranks (``L = E / P`` consecutive experts per rank,

@@ -7,7 +7,7 @@ AllToAll(V) (Section 2, Table 2) and says nothing of de-duplication.  This
 variant sends a token once to each rank that owns at least one of its
 experts, instead of once per (token, slot); the receiving rank applies all
 of its local experts to that one row and returns one partial output per
-(token, rank).  The contract below is this build's reading.
+(token, rank).  The contract below is this library's reading.
 
 Dispatch, for ``ids[T, K]`` expert ids, ``E`` experts split evenly over
 ``P`` ranks (``L = E / P``, ``dest(e) = e // L``):
