@@ -113,7 +113,8 @@ def unpack(y, pos, gates):
     T, K = pos.shape
     H = y.shape[1]
     acc = np.zeros((T, H), dtype=np.float32)  # +0.0
-    for k in range(K):  # slot order
-        term = np.multiply(gates[:, k:k + 1], widen(y[pos[:, k]]), dtype=np.float32)
-        acc = np.add(acc, term, dtype=np.float32)
+    with np.errstate(over="ignore", invalid="ignore"):  # IEEE overflow to inf, inf - inf = NaN
+        for k in range(K):  # slot order
+            term = np.multiply(gates[:, k:k + 1], widen(y[pos[:, k]]), dtype=np.float32)
+            acc = np.add(acc, term, dtype=np.float32)
     return narrow(acc)
