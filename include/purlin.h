@@ -395,6 +395,59 @@ PURLIN_API purlin_status purlin_pack_dedup(int T, int H, int K, int E, int P, co
 PURLIN_API purlin_status purlin_unpack_dedup(int T, int H, int P, int64_t rows, const void* y,
                                              const int32_t* row_of, void* out, int32_t* dev_status, void* stream);
 
+/* Workspace bytes purlin_ep_dispatch needs for P ranks of T tokens. */
+PURLIN_API purlin_status purlin_ep_dispatch_workspace_size(int T, int K, int E, int P, uint64_t* bytes);
+
+/* Expert-parallel dispatch over P ranks in one pass (expert parallelism's
+ * AllToAll(V) of tokens, Section 2, Table 2): the result is rank p's
+ * purlin_pack followed by the ALLTOALLV of the packed rows with counts[p][r]
+ * = rank p's dest_counts[r], but the rows go straight from x_p to the
+ * receive buffers, with no packed buffers in between.  Rank r's buffer holds
+ * the rows from rank 0, then rank 1, ..., each in its sender's pack order
+ * (expert, then token).
+ *   x        P host-held pointers to bf16 [T, H] device token rows
+ *   ids      P host-held pointers to int32 [T, K] device expert ids
+ *   recv     P host-held pointers to bf16 [capacity, H] device receive
+ *            buffers (output; rows beyond what a rank receives untouched)
+ *   counts   int32 [P * P] device (output): rows rank p sends rank r, at
+ *            counts[p*P + r]
+ *   recv_pos int32 [P, T, K] device (output): row of rank p's token t, slot
+ *            k in the buffer of the rank owning expert ids_p[t, k]:
+ *            sum_{q<p} counts[q][r] + pos_p[t,k] - dest_offsets_p[r]
+ *   dev_status int32 device (optional): 0, or 1 if an id is out of range or
+ *            repeated within a token (those slots are skipped), or if some
+ *            rank would receive more than `capacity` rows (then no row is
+ *            written).
+ *   workspace >= purlin_ep_dispatch_workspace_size bytes of device memory,
+ *            owned by the caller; its contents on entry do not matter.
+ * Limits as purlin_pack, plus P <= 16, capacity < 2^31.  Errors:
+ * PURLIN_ERR_INVALID (limits, NULL or misaligned pointer, small workspace,
+ * a receive buffer overlapping another or a token buffer),
+ * PURLIN_ERR_DEVICE. */
+PURLIN_API purlin_status purlin_ep_dispatch(int T, int H, int K, int E, int P, const void* const* x,
+                                            const int32_t* const* ids, void* const* recv, uint64_t capacity,
+                                            int32_t* counts, int32_t* recv_pos, int32_t* dev_status,
+                                            void* workspace, uint64_t workspace_bytes, void* stream);
+
+/* The matching combine: the expert outputs y_r, in rank r's receive layout,
+ * go back to their tokens and are summed in slot order as purlin_unpack
+ * does:
+ *   out_p[t, h] = narrow(+0 + g_p[t,0] * widen(y_{r0}[recv_pos[p,t,0], h]) + ...)
+ * with r_k the rank owning ids_p[t, k] -- the same bits as the reverse
+ * ALLTOALLV followed by purlin_unpack.
+ *   y        P host-held pointers to bf16 [capacity, H] device
+ *   ids, recv_pos  as given to / returned by purlin_ep_dispatch
+ *   gates    P host-held pointers to fp32 [T, K] device
+ *   out      P host-held pointers to bf16 [T, H] device (output)
+ *   dev_status int32 device (optional): 0, or 1 if some slot names an id or
+ *            a row out of range (it then contributes nothing).
+ * Errors: PURLIN_ERR_INVALID (limits, NULL or misaligned pointer, an output
+ * overlapping another or an input), PURLIN_ERR_DEVICE. */
+PURLIN_API purlin_status purlin_ep_combine(int T, int H, int K, int E, int P, const void* const* y, uint64_t capacity,
+                                           const int32_t* const* ids, const int32_t* recv_pos,
+                                           const float* const* gates, void* const* out, int32_t* dev_status,
+                                           void* stream);
+
 /* Static text for a status code ("unknown status" for others). */
 PURLIN_API const char* purlin_status_string(purlin_status status);
 

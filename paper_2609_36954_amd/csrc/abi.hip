@@ -105,6 +105,22 @@ purlin_status check_buffers(const purlin::Plan& p, void* const* bufs) {
     return PURLIN_OK;
 }
 
+// EP arguments shared by dispatch and combine: limits and the P ranks' pointers.
+bool ep_limits_ok(int T, int H, int K, int E, int P, uint64_t capacity) {
+    if (!pack_limits_ok(T, H, K, E)) return false;
+    if (P < 1 || P > PURLIN_MAX_RANKS || P > E || E % P != 0) return false;
+    if (capacity >= (uint64_t(1) << 31)) return false;
+    return purlin::ep_launch_fits(T, H, P);
+}
+
+template <class Ptr>
+bool all_aligned(Ptr const* v, int P) {
+    if (!v) return false;
+    for (int p = 0; p < P; ++p)
+        if (!v[p] || !aligned16(v[p])) return false;
+    return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -319,6 +335,61 @@ purlin_status purlin_unpack_dedup(int T, int H, int P, int64_t rows, const void*
     const hipError_t e = purlin::launch_unpack_dedup(T, H, P, rows, static_cast<const uint16_t*>(y), row_of,
                                                      static_cast<uint16_t*>(out), dev_status,
                                                      static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
+purlin_status purlin_ep_dispatch_workspace_size(int T, int K, int E, int P, uint64_t* bytes) {
+    if (!bytes || !pack_limits_ok(T, 1, K, E)) return PURLIN_ERR_INVALID;
+    if (P < 1 || P > PURLIN_MAX_RANKS || P > E || E % P != 0) return PURLIN_ERR_INVALID;
+    *bytes = purlin::ep_dispatch_workspace_bytes(T, K, E, P);
+    return PURLIN_OK;
+}
+
+purlin_status purlin_ep_dispatch(int T, int H, int K, int E, int P, const void* const* x, const int32_t* const* ids,
+                                 void* const* recv, uint64_t capacity, int32_t* counts, int32_t* recv_pos,
+                                 int32_t* dev_status, void* workspace, uint64_t workspace_bytes, void* stream) {
+    if (!ep_limits_ok(T, H, K, E, P, capacity)) return PURLIN_ERR_INVALID;
+    if (!counts || (reinterpret_cast<uintptr_t>(counts) & 3u)) return PURLIN_ERR_INVALID;
+    if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    const uint64_t need = purlin::ep_dispatch_workspace_bytes(T, K, E, P);
+    if (workspace_bytes < need || (need && (!workspace || !aligned16(workspace)))) return PURLIN_ERR_INVALID;
+    if (T > 0) {
+        if (!all_aligned(x, P) || !all_aligned(ids, P) || !all_aligned(recv, P)) return PURLIN_ERR_INVALID;
+        if (!recv_pos || (reinterpret_cast<uintptr_t>(recv_pos) & 3u)) return PURLIN_ERR_INVALID;
+        const uint64_t xb = uint64_t(T) * H * 2, rb = capacity * uint64_t(H) * 2;
+        for (int r = 0; r < P; ++r) {
+            for (int q = r + 1; q < P; ++q)
+                if (overlaps(recv[r], rb, recv[q], rb)) return PURLIN_ERR_INVALID;
+            for (int p = 0; p < P; ++p)
+                if (overlaps(recv[r], rb, x[p], xb)) return PURLIN_ERR_INVALID;
+        }
+    }
+    const hipError_t e = purlin::launch_ep_dispatch(
+        T, H, K, E, P, reinterpret_cast<const uint16_t* const*>(x), ids, reinterpret_cast<uint16_t* const*>(recv),
+        static_cast<int64_t>(capacity), counts, recv_pos, dev_status, workspace, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
+purlin_status purlin_ep_combine(int T, int H, int K, int E, int P, const void* const* y, uint64_t capacity,
+                                const int32_t* const* ids, const int32_t* recv_pos, const float* const* gates,
+                                void* const* out, int32_t* dev_status, void* stream) {
+    if (!ep_limits_ok(T, H, K, E, P, capacity)) return PURLIN_ERR_INVALID;
+    if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    if (T > 0) {
+        if (!all_aligned(ids, P) || !all_aligned(gates, P) || !all_aligned(out, P)) return PURLIN_ERR_INVALID;
+        if (capacity > 0 && !all_aligned(y, P)) return PURLIN_ERR_INVALID;
+        if (!recv_pos || (reinterpret_cast<uintptr_t>(recv_pos) & 3u)) return PURLIN_ERR_INVALID;
+        const uint64_t ob = uint64_t(T) * H * 2, yb = capacity * uint64_t(H) * 2;
+        for (int p = 0; p < P; ++p) {
+            for (int q = p + 1; q < P; ++q)
+                if (overlaps(out[p], ob, out[q], ob)) return PURLIN_ERR_INVALID;
+            for (int r = 0; r < P && capacity > 0; ++r)
+                if (overlaps(out[p], ob, y[r], yb)) return PURLIN_ERR_INVALID;
+        }
+    }
+    const hipError_t e = purlin::launch_ep_combine(
+        T, H, K, E, P, reinterpret_cast<const uint16_t* const*>(y), static_cast<int64_t>(capacity), ids, recv_pos,
+        gates, reinterpret_cast<uint16_t* const*>(out), dev_status, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
 }
 

@@ -73,4 +73,18 @@ hipError_t launch_pack_dedup(int T, int H, int K, int E, int P, const uint16_t* 
 hipError_t launch_unpack_dedup(int T, int H, int P, int64_t rows, const uint16_t* y, const int32_t* row_of,
                                uint16_t* out, int32_t* dev_status, hipStream_t stream);
 
+// Expert-parallel dispatch / combine over P ranks (per-rank pointer arrays
+// of P host-held device pointers).  The dispatch workspace holds every
+// rank's pack workspace, destination offsets, expert counts and status word.
+uint64_t ep_dispatch_workspace_bytes(int T, int K, int E, int P);
+bool ep_launch_fits(int T, int H, int P);
+
+hipError_t launch_ep_dispatch(int T, int H, int K, int E, int P, const uint16_t* const* x, const int32_t* const* ids,
+                              uint16_t* const* recv, int64_t capacity, int32_t* counts, int32_t* recv_pos,
+                              int32_t* dev_status, void* workspace, hipStream_t stream);
+
+hipError_t launch_ep_combine(int T, int H, int K, int E, int P, const uint16_t* const* y, int64_t capacity,
+                             const int32_t* const* ids, const int32_t* recv_pos, const float* const* gates,
+                             uint16_t* const* out, int32_t* dev_status, hipStream_t stream);
+
 }  // namespace purlin

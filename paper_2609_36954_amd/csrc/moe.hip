@@ -234,13 +234,13 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
 }
 
 // Stream one column slice of a token row (U * 64 16-byte vectors, U per
-// lane) through registers into every slot whose row index lane j < nslots
-// holds in `row` (-1 = no row): the row is read once from HBM.  Rows that
-// are not a multiple of 16 bytes take one slice per token, 2 bytes per lane
-// step.
-template <int U, bool NTL, bool NTS>
-__device__ __forceinline__ void copy_row_to_slots(const char* src, char* packed, uint64_t row_bytes, uint32_t slice,
-                                                  int row, int nslots, uint32_t lane) {
+// lane) through registers into every slot j < nslots: dst_of(j) gives the
+// destination row's base (wave-uniform), or null for none.  The row is read
+// once from HBM.  Rows that are not a multiple of 16 bytes take one slice
+// per token, 2 bytes per lane step.
+template <int U, bool NTL, bool NTS, class DstOf>
+__device__ __forceinline__ void copy_row_to_slots(const char* src, uint64_t row_bytes, uint32_t slice, int nslots,
+                                                  uint32_t lane, DstOf dst_of) {
     if (row_bytes % 16 == 0) {
         const uint64_t nvec = row_bytes / 16;
         const uint64_t base = static_cast<uint64_t>(slice) * U * kWave;
@@ -251,9 +251,8 @@ __device__ __forceinline__ void copy_row_to_slots(const char* src, char* packed,
             if (i < nvec) v[u] = load16<NTL>(src + i * 16);
         }
         for (int j = 0; j < nslots; ++j) {
-            const int pj = __builtin_amdgcn_readlane(row, j);
-            if (pj < 0) continue;
-            char* dst = packed + static_cast<uint64_t>(pj) * row_bytes;
+            char* dst = dst_of(j);
+            if (!dst) continue;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const uint64_t i = base + u * kWave + lane;
@@ -265,8 +264,8 @@ __device__ __forceinline__ void copy_row_to_slots(const char* src, char* packed,
         for (uint64_t h = lane; h < H; h += kWave) {
             const uint16_t v = reinterpret_cast<const uint16_t*>(src)[h];
             for (int j = 0; j < nslots; ++j) {
-                const int pj = __builtin_amdgcn_readlane(row, j);
-                if (pj >= 0) reinterpret_cast<uint16_t*>(packed + static_cast<uint64_t>(pj) * row_bytes)[h] = v;
+                char* dst = dst_of(j);
+                if (dst) reinterpret_cast<uint16_t*>(dst)[h] = v;
             }
         }
     }
@@ -300,7 +299,10 @@ __global__ __launch_bounds__(kBlock) void pack_rows(int T, int H, int K, int E, 
         if (slice == 0) pos[j] = p;
     }
     const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
-    copy_row_to_slots<U, NTL, NTS>(x + t * row_bytes, packed, row_bytes, slice, p, K, lane);
+    copy_row_to_slots<U, NTL, NTS>(x + t * row_bytes, row_bytes, slice, K, lane, [&](int j) -> char* {
+        const int pj = __builtin_amdgcn_readlane(p, j);
+        return pj < 0 ? nullptr : packed + static_cast<uint64_t>(pj) * row_bytes;
+    });
 }
 
 // ---------------------------------------------------------------------------
@@ -415,41 +417,25 @@ __global__ __launch_bounds__(kBlock) void dedup_rows(int T, int H, int P, int sl
         if (slice == 0) row_of[j] = row;
     }
     const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
-    copy_row_to_slots<U, NTL, NTS>(x + t * row_bytes, packed, row_bytes, slice, row, P, lane);
+    copy_row_to_slots<U, NTL, NTS>(x + t * row_bytes, row_bytes, slice, P, lane, [&](int j) -> char* {
+        const int rj = __builtin_amdgcn_readlane(row, j);
+        return rj < 0 ? nullptr : packed + static_cast<uint64_t>(rj) * row_bytes;
+    });
 }
 
 __global__ void set_status(int32_t* status) { *status = 0; }
 
 constexpr int kSlotGroup = 4;  // slots whose row loads are in flight together (4 measured 3% faster than 8 or 16)
 
-// One wavefront per (token, column slice) of the output row.  GATED: the
-// combine of one row per (t, k), acc (+)= g[t, k] (x) row; otherwise the
-// de-duplicated combine of one row per (t, rank), acc (+)= row, where a
-// slot of -1 means "no row".  Slots name rows in [0, rows).
-template <int U, bool NTL, bool NTS, bool GATED>
-__global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, int slices, int64_t rows,
-                                                      const char* __restrict__ y, const int32_t* __restrict__ pos,
-                                                      const float* __restrict__ gates, char* __restrict__ out,
-                                                      int32_t* __restrict__ dev_status) {
-    const uint32_t w = wave_index();
-    const uint32_t t = w / slices;
-    if (t >= static_cast<uint32_t>(T)) return;
-    const uint32_t slice = w - t * slices;
-    const uint32_t lane = lane_index();
-    int p = -1;
-    float g = 1.0f;
-    if (lane < static_cast<uint32_t>(K)) {
-        const int64_t j = static_cast<int64_t>(t) * K + lane;
-        p = pos[j];
-        if constexpr (GATED) g = gates[j];
-        const bool absent = !GATED && p == -1;
-        if (!absent && (p < 0 || p >= rows)) {
-            if (dev_status && slice == 0) atomicOr(dev_status, 1);
-        }
-        if (p < 0 || p >= rows) p = -1;
-    }
-    const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
-    char* dst = out + t * row_bytes;
+// One column slice of one output row: acc = +0, then for each slot k in
+// ascending order acc (+)= g_k (x) widen(row_k) (GATED) or acc (+)= row_k,
+// with src_of(k) the slot's source row base (wave-uniform; null = no row)
+// and g_k read from lane k of `g`; the rows of kSlotGroup slots are loaded
+// together before their terms are added.  Then one RNE narrowing and a
+// 16-byte store per vector.
+template <int U, bool NTL, bool NTS, bool GATED, class SrcOf>
+__device__ __forceinline__ void combine_slots(SrcOf src_of, float g, int K, char* dst, uint64_t row_bytes,
+                                              uint32_t slice, uint32_t lane) {
     if (row_bytes % 16 == 0) {
         const uint64_t nvec = row_bytes / 16;
         const uint64_t base = static_cast<uint64_t>(slice) * U * kWave;
@@ -460,21 +446,20 @@ __global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, int s
             for (int e = 0; e < 8; ++e) acc[u][e] = 0.0f;
         for (int k0 = 0; k0 < K; k0 += kSlotGroup) {
             u32x4 v[kSlotGroup][U];
-            int pk[kSlotGroup];
+            const char* rk[kSlotGroup];
 #pragma unroll
             for (int kk = 0; kk < kSlotGroup; ++kk) {
-                pk[kk] = (k0 + kk < K) ? __builtin_amdgcn_readlane(p, k0 + kk) : -1;
-                if (pk[kk] < 0) continue;
-                const char* row = y + static_cast<uint64_t>(pk[kk]) * row_bytes;
+                rk[kk] = (k0 + kk < K) ? src_of(k0 + kk) : nullptr;
+                if (!rk[kk]) continue;
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const uint64_t i = base + u * kWave + lane;
-                    if (i < nvec) v[kk][u] = load16<NTL>(row + i * 16);
+                    if (i < nvec) v[kk][u] = load16<NTL>(rk[kk] + i * 16);
                 }
             }
 #pragma unroll
             for (int kk = 0; kk < kSlotGroup; ++kk) {
-                if (pk[kk] < 0) continue;
+                if (!rk[kk]) continue;
                 const float gk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), k0 + kk));
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
@@ -504,19 +489,184 @@ __global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, int s
             }
         }
     } else {
-        for (uint64_t h = lane; h < static_cast<uint64_t>(H); h += kWave) {
+        const uint64_t H = row_bytes / 2;
+        for (uint64_t h = lane; h < H; h += kWave) {
             float acc = 0.0f;
             for (int k = 0; k < K; ++k) {
-                const int pk = __builtin_amdgcn_readlane(p, k);
-                if (pk < 0) continue;
+                const char* row = src_of(k);
+                if (!row) continue;
                 const float gk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), k));
-                const uint16_t hv = reinterpret_cast<const uint16_t*>(y + static_cast<uint64_t>(pk) * row_bytes)[h];
+                const uint16_t hv = reinterpret_cast<const uint16_t*>(row)[h];
                 const float v = __uint_as_float(uint32_t(hv) << 16);
                 acc = __fadd_rn(acc, GATED ? __fmul_rn(gk, v) : v);
             }
             reinterpret_cast<uint16_t*>(dst)[h] = static_cast<uint16_t>(to_bf16(acc));
         }
     }
+}
+
+// One wavefront per (token, column slice) of the output row.  GATED: the
+// combine of one row per (t, k), acc (+)= g[t, k] (x) row; otherwise the
+// de-duplicated combine of one row per (t, rank), acc (+)= row, where a
+// slot of -1 means "no row".  Slots name rows in [0, rows).
+template <int U, bool NTL, bool NTS, bool GATED>
+__global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, int slices, int64_t rows,
+                                                      const char* __restrict__ y, const int32_t* __restrict__ pos,
+                                                      const float* __restrict__ gates, char* __restrict__ out,
+                                                      int32_t* __restrict__ dev_status) {
+    const uint32_t w = wave_index();
+    const uint32_t t = w / slices;
+    if (t >= static_cast<uint32_t>(T)) return;
+    const uint32_t slice = w - t * slices;
+    const uint32_t lane = lane_index();
+    int p = -1;
+    float g = 1.0f;
+    if (lane < static_cast<uint32_t>(K)) {
+        const int64_t j = static_cast<int64_t>(t) * K + lane;
+        p = pos[j];
+        if constexpr (GATED) g = gates[j];
+        const bool absent = !GATED && p == -1;
+        if (!absent && (p < 0 || p >= rows)) {
+            if (dev_status && slice == 0) atomicOr(dev_status, 1);
+        }
+        if (p < 0 || p >= rows) p = -1;
+    }
+    const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
+    combine_slots<U, NTL, NTS, GATED>(
+        [&](int k) -> const char* {
+            const int pk = __builtin_amdgcn_readlane(p, k);
+            return pk < 0 ? nullptr : y + static_cast<uint64_t>(pk) * row_bytes;
+        },
+        g, K, out + t * row_bytes, row_bytes, slice, lane);
+}
+
+// ---------------------------------------------------------------------------
+// Expert-parallel dispatch and combine over P ranks in one pass each.  The
+// dispatch is rank p's pack followed by the AllToAllV of its packed rows,
+// without the packed buffers: once every rank's metadata is known (the
+// per-rank pack_tiles / pack_scan, which write row p of the P x P counts),
+// each token row goes straight to the receive buffer of every rank owning
+// one of its experts, at
+//     recv_row = sum_{q < p} counts[q][r] + pos_p[t, k] - dest_offsets_p[r].
+// The combine reads each slot's expert output straight from its owner's
+// buffer at that row and sums in slot order as unpack does.  On several
+// GPUs this is a push of the rows to the peers and a pull of the outputs.
+struct EpArgs {
+    const char* x[PURLIN_MAX_RANKS];        // dispatch: token rows; combine: expert outputs (receive layout)
+    const int32_t* ids[PURLIN_MAX_RANKS];
+    char* dst[PURLIN_MAX_RANKS];            // dispatch: receive buffers; combine: outputs
+    const int32_t* tile_base[PURLIN_MAX_RANKS];
+    const int32_t* lrank[PURLIN_MAX_RANKS];
+    const int32_t* dest_off[PURLIN_MAX_RANKS];
+    const float* gates[PURLIN_MAX_RANKS];
+    const int32_t* counts;  // P x P: rows rank p sends rank r
+    int32_t* recv_pos;      // [P, T, K]
+    int32_t* status;        // optional
+    int64_t capacity;       // rows per receive buffer
+    int T, H, K, E, P, slices;
+};
+
+// Every wave of rank p's token t and column slice: lane k < K forms slot k's
+// receiving rank and row (from the pack metadata and the counts staged in
+// LDS); all waves reach the same capacity verdict, so either every row is
+// written or none is.
+template <int U, bool NTL, bool NTS>
+__global__ __launch_bounds__(kBlock) void ep_dispatch_rows(EpArgs a) {
+    __shared__ int32_t m[PURLIN_MAX_RANKS * PURLIN_MAX_RANKS];
+    __shared__ int64_t before[PURLIN_MAX_RANKS * PURLIN_MAX_RANKS];  // [p][r]: rows r got from ranks < p
+    __shared__ int ok;
+    const int P = a.P;
+    for (int i = threadIdx.x; i < P * P; i += kBlock) m[i] = a.counts[i];
+    __syncthreads();
+    for (int i = threadIdx.x; i < P * P; i += kBlock) {
+        const int p = i / P, r = i - p * P;
+        int64_t b = 0;
+        for (int q = 0; q < p; ++q) b += m[q * P + r];
+        before[i] = b;
+    }
+    if (threadIdx.x == 0) {
+        bool fits = true;
+        for (int r = 0; r < P; ++r) {
+            int64_t col = 0;
+            for (int q = 0; q < P; ++q) {
+                fits = fits && m[q * P + r] >= 0;
+                col += m[q * P + r];
+            }
+            fits = fits && col <= a.capacity;
+        }
+        ok = fits;
+        if (!fits && blockIdx.x == 0 && a.status) atomicOr(a.status, 1);
+    }
+    __syncthreads();
+    if (!ok) return;
+    const uint32_t w = wave_index();
+    const uint64_t per_rank = static_cast<uint64_t>(a.T) * a.slices;
+    if (w >= per_rank * P) return;
+    const uint32_t p = static_cast<uint32_t>(w / per_rank);
+    const uint32_t rem = static_cast<uint32_t>(w - p * per_rank);
+    const uint32_t t = rem / a.slices, slice = rem - t * a.slices;
+    const uint32_t lane = lane_index();
+    const int K = a.K, E = a.E, L = a.E / P;
+    int r = 0, row = -1;
+    if (lane < static_cast<uint32_t>(K)) {
+        const int64_t j = static_cast<int64_t>(t) * K + lane;
+        const int e = a.ids[p][j];
+        const int lr = a.lrank[p][j];
+        if (e >= 0 && e < E && lr >= 0) {
+            r = e / L;
+            const int64_t q = static_cast<int64_t>(a.tile_base[p][static_cast<int64_t>(t / kPackTileTokens) * E + e]) + lr;
+            const int64_t rr = before[p * P + r] + q - a.dest_off[p][r];
+            row = (rr >= 0 && rr < a.capacity) ? static_cast<int>(rr) : -1;
+        }
+        if (slice == 0) a.recv_pos[(static_cast<int64_t>(p) * a.T + t) * K + lane] = row;
+    }
+    const uint64_t row_bytes = static_cast<uint64_t>(a.H) * 2;
+    copy_row_to_slots<U, NTL, NTS>(a.x[p] + t * row_bytes, row_bytes, slice, K, lane, [&](int k) -> char* {
+        const int rk = __builtin_amdgcn_readlane(row, k);
+        return rk < 0 ? nullptr : a.dst[__builtin_amdgcn_readlane(r, k)] + static_cast<uint64_t>(rk) * row_bytes;
+    });
+}
+
+// Rank p's token t, one column slice: slot k's expert output is row
+// recv_pos[p, t, k] of the buffer of the rank owning ids_p[t, k].
+template <int U, bool NTL, bool NTS>
+__global__ __launch_bounds__(kBlock) void ep_combine_rows(EpArgs a) {
+    const uint32_t w = wave_index();
+    const uint64_t per_rank = static_cast<uint64_t>(a.T) * a.slices;
+    if (w >= per_rank * a.P) return;
+    const uint32_t p = static_cast<uint32_t>(w / per_rank);
+    const uint32_t rem = static_cast<uint32_t>(w - p * per_rank);
+    const uint32_t t = rem / a.slices, slice = rem - t * a.slices;
+    const uint32_t lane = lane_index();
+    const int K = a.K, E = a.E, L = a.E / a.P;
+    int r = 0, row = -1;
+    float g = 0.0f;
+    if (lane < static_cast<uint32_t>(K)) {
+        const int64_t j = static_cast<int64_t>(t) * K + lane;
+        const int e = a.ids[p][j];
+        const int64_t rr = a.recv_pos[static_cast<int64_t>(p) * a.T * K + j];
+        g = a.gates[p][j];
+        if (e >= 0 && e < E && rr >= 0 && rr < a.capacity) {
+            r = e / L;
+            row = static_cast<int>(rr);
+        } else if (a.status && slice == 0) {
+            atomicOr(a.status, 1);
+        }
+    }
+    const uint64_t row_bytes = static_cast<uint64_t>(a.H) * 2;
+    combine_slots<U, NTL, NTS, true>(
+        [&](int k) -> const char* {
+            const int rk = __builtin_amdgcn_readlane(row, k);
+            return rk < 0 ? nullptr : a.x[__builtin_amdgcn_readlane(r, k)] + static_cast<uint64_t>(rk) * row_bytes;
+        },
+        g, K, a.dst[p] + t * row_bytes, row_bytes, slice, lane);
+}
+
+// Merges the ranks' routing-error words (contiguous) into the caller's status word.
+__global__ void merge_status(const int32_t* words, int n, int32_t* status) {
+    int any = 0;
+    for (int i = 0; i < n; ++i) any |= words[i];
+    *status = any ? 1 : 0;
 }
 
 // Launch shapes and cache hints, measured on MI355X: the packed rows and
@@ -650,6 +800,93 @@ hipError_t launch_unpack_dedup(int T, int H, int P, int64_t rows, const uint16_t
                            reinterpret_cast<char*>(out), dev_status);
     }
     return hipGetLastError();
+}
+
+uint64_t ep_dispatch_workspace_bytes(int T, int K, int E, int P) {
+    const uint64_t Pu = static_cast<uint64_t>(P);
+    return Pu * pack_workspace_bytes(T, K, E) + align256(4 * Pu * Pu) + align256(4 * Pu * E) + align256(4 * Pu);
+}
+
+hipError_t launch_ep_dispatch(int T, int H, int K, int E, int P, const uint16_t* const* x, const int32_t* const* ids,
+                              uint16_t* const* recv, int64_t capacity, int32_t* counts, int32_t* recv_pos,
+                              int32_t* dev_status, void* workspace, hipStream_t stream) {
+    const uint64_t Pu = static_cast<uint64_t>(P);
+    const uint64_t per = pack_workspace_bytes(T, K, E);
+    char* ws = static_cast<char*>(workspace);
+    int32_t* dest_off = reinterpret_cast<int32_t*>(ws + Pu * per);                          // [P][P]
+    int32_t* expert_counts = reinterpret_cast<int32_t*>(ws + Pu * per + align256(4 * Pu * Pu));  // [P][E]
+    int32_t* words = reinterpret_cast<int32_t*>(ws + Pu * per + align256(4 * Pu * Pu) + align256(4 * Pu * E));
+    const int ntiles = (T + kPackTileTokens - 1) / kPackTileTokens;
+    EpArgs a{};
+    (void)hipGetLastError();
+    for (int p = 0; p < P; ++p) {
+        const PackWorkspace w = pack_workspace_carve(ws + p * per, T, K, E);
+        if (ntiles > 0)
+            hipLaunchKernelGGL(pack_tiles, dim3(ntiles), dim3(kBlock), static_cast<size_t>(E) * 8, stream, T, K, E,
+                               ids[p], w.tile_base, w.lrank, w.tile_err);
+        hipLaunchKernelGGL(pack_scan, dim3(1), dim3(kScanThreads), 0, stream, ntiles, E, P, w.tile_base, w.tile_err,
+                           expert_counts + static_cast<uint64_t>(p) * E, nullptr, counts + p * P, dest_off + p * P,
+                           words + p);
+        a.x[p] = reinterpret_cast<const char*>(x[p]);
+        a.ids[p] = ids[p];
+        a.dst[p] = reinterpret_cast<char*>(recv[p]);
+        a.tile_base[p] = w.tile_base;
+        a.lrank[p] = w.lrank;
+        a.dest_off[p] = dest_off + p * P;
+    }
+    if (dev_status) hipLaunchKernelGGL(merge_status, dim3(1), dim3(1), 0, stream, words, P, dev_status);
+    if (T > 0) {
+        a.counts = counts;
+        a.recv_pos = recv_pos;
+        a.status = dev_status;
+        a.capacity = capacity;
+        a.T = T;
+        a.H = H;
+        a.K = K;
+        a.E = E;
+        a.P = P;
+        a.slices = row_slices(H, kPackUnroll);
+        const uint64_t waves = Pu * static_cast<uint64_t>(T) * a.slices;
+        const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
+        hipLaunchKernelGGL((ep_dispatch_rows<kPackUnroll, kPackNtLoad, kPackNtStore>), grid, dim3(kBlock), 0, stream,
+                           a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_ep_combine(int T, int H, int K, int E, int P, const uint16_t* const* y, int64_t capacity,
+                             const int32_t* const* ids, const int32_t* recv_pos, const float* const* gates,
+                             uint16_t* const* out, int32_t* dev_status, hipStream_t stream) {
+    EpArgs a{};
+    for (int p = 0; p < P; ++p) {
+        a.x[p] = reinterpret_cast<const char*>(y[p]);
+        a.ids[p] = ids[p];
+        a.dst[p] = reinterpret_cast<char*>(out[p]);
+        a.gates[p] = gates[p];
+    }
+    a.recv_pos = const_cast<int32_t*>(recv_pos);  // read only here
+    a.status = dev_status;
+    a.capacity = capacity;
+    a.T = T;
+    a.H = H;
+    a.K = K;
+    a.E = E;
+    a.P = P;
+    a.slices = row_slices(H, kUnpackUnroll);
+    (void)hipGetLastError();
+    if (dev_status) hipLaunchKernelGGL(set_status, dim3(1), dim3(1), 0, stream, dev_status);
+    if (T > 0) {
+        const uint64_t waves = static_cast<uint64_t>(P) * T * a.slices;
+        const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
+        hipLaunchKernelGGL((ep_combine_rows<kUnpackUnroll, kUnpackNtLoad, kUnpackNtStore>), grid, dim3(kBlock), 0,
+                           stream, a);
+    }
+    return hipGetLastError();
+}
+
+bool ep_launch_fits(int T, int H, int P) {
+    const uint64_t slices = std::max(row_slices(H, kPackUnroll), row_slices(H, kUnpackUnroll));
+    return static_cast<uint64_t>(P) * T * slices < (uint64_t(1) << 31);
 }
 
 }  // namespace purlin

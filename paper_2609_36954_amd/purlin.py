@@ -107,6 +107,10 @@ def lib():
     L.purlin_pack_dedup_workspace_size.argtypes = [i32, i32, _c_u64p]
     L.purlin_pack_dedup.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 8 + [u64, _vp]
     L.purlin_unpack_dedup.argtypes = [i32, i32, i32, ctypes.c_int64] + [_vp] * 5
+    _pa = ctypes.POINTER(_vp)
+    L.purlin_ep_dispatch_workspace_size.argtypes = [i32, i32, i32, i32, _c_u64p]
+    L.purlin_ep_dispatch.argtypes = [i32] * 5 + [_pa, _pa, _pa, u64, _vp, _vp, _vp, _vp, u64, _vp]
+    L.purlin_ep_combine.argtypes = [i32] * 5 + [_pa, u64, _pa, _vp, _pa, _pa, _vp, _vp]
     L.purlin_status_string.argtypes = [i32]
     L.purlin_status_string.restype = ctypes.c_char_p
     L.purlin_version.argtypes = []
@@ -114,7 +118,8 @@ def lib():
     for name in ("purlin_plan", "purlin_plan_ex", "purlin_plan_rooted", "purlin_plan_v", "purlin_exec_v",
                  "purlin_plan_info", "purlin_plan_descriptors", "purlin_plan_items",
                  "purlin_exec", "purlin_pack_workspace_size", "purlin_pack", "purlin_unpack",
-                 "purlin_pack_dedup_workspace_size", "purlin_pack_dedup", "purlin_unpack_dedup"):
+                 "purlin_pack_dedup_workspace_size", "purlin_pack_dedup", "purlin_unpack_dedup",
+                 "purlin_ep_dispatch_workspace_size", "purlin_ep_dispatch", "purlin_ep_combine"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -531,3 +536,94 @@ def purlin_unpack_dedup(y, row_of, out=None, dev_status=None, stream=None):
                                    _ptr(dev_status), _stream_handle(stream))
     _check(st, "purlin_unpack_dedup")
     return out
+
+
+def _ptr_array(tensors):
+    return (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
+
+
+def _rows_capacity(bufs, H, name):
+    for b in bufs:
+        _require_cuda(b, name, 2)
+    return min(b.numel() for b in bufs) // H
+
+
+def purlin_ep_dispatch_workspace_size(T, K, E, P):
+    b = ctypes.c_uint64()
+    _check(lib().purlin_ep_dispatch_workspace_size(int(T), int(K), int(E), int(P), ctypes.byref(b)),
+           "purlin_ep_dispatch_workspace_size")
+    return b.value
+
+
+def purlin_ep_dispatch(xs, idss, E, recv, counts=None, recv_pos=None, workspace=None, dev_status=None, stream=None):
+    """Expert-parallel dispatch over P = len(xs) ranks in one pass: rank p's
+    pack followed by the AllToAllV of the packed rows, written straight into
+    the receive buffers ``recv`` (P bf16 tensors of ``capacity`` rows of H).
+
+    Returns a dict with ``counts`` (int32 [P*P], rows rank p sends rank r at
+    p*P + r) and ``recv_pos`` (int32 [P, T, K]).
+    """
+    import torch
+
+    P = len(xs)
+    if len(idss) != P or len(recv) != P:
+        raise PurlinError(PURLIN_ERR_INVALID, "need P token matrices, P id matrices and P receive buffers")
+    T, H = xs[0].shape
+    K = idss[0].shape[1]
+    for x, ids in zip(xs, idss):
+        _require_cuda(x, "x", 2)
+        _require_cuda(ids, "ids", 4)
+        if tuple(x.shape) != (T, H) or tuple(ids.shape) != (T, K):
+            raise PurlinError(PURLIN_ERR_INVALID, "every rank needs x [T, H] and ids [T, K]")
+    capacity = _rows_capacity(recv, H, "recv")
+    dev = xs[0].device
+    if counts is None:
+        counts = torch.empty(P * P, dtype=torch.int32, device=dev)
+    if recv_pos is None:
+        recv_pos = torch.empty((P, T, K), dtype=torch.int32, device=dev)
+    _require_cuda(counts, "counts", 4)
+    _require_cuda(recv_pos, "recv_pos", 4)
+    if counts.numel() < P * P or recv_pos.numel() < P * T * K:
+        raise PurlinError(PURLIN_ERR_INVALID, "counts needs P*P entries and recv_pos P*T*K")
+    wsb = purlin_ep_dispatch_workspace_size(T, K, E, P)
+    if workspace is None:
+        workspace = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+    st = lib().purlin_ep_dispatch(int(T), int(H), int(K), int(E), int(P), _ptr_array(xs), _ptr_array(idss),
+                                  _ptr_array(recv), int(capacity), _ptr(counts), _ptr(recv_pos), _ptr(dev_status),
+                                  _ptr(workspace), int(workspace.numel() * workspace.element_size()),
+                                  _stream_handle(stream))
+    _check(st, "purlin_ep_dispatch")
+    return {"counts": counts, "recv_pos": recv_pos}
+
+
+def purlin_ep_combine(ys, idss, recv_pos, gatess, E, outs=None, dev_status=None, stream=None):
+    """The matching combine: P expert-output tensors ``ys`` in the receive
+    layout -> P bf16 [T, H] outputs, each slot's output weighted by its gate
+    and summed in slot order (as ``purlin_unpack``)."""
+    import torch
+
+    P = len(ys)
+    if len(idss) != P or len(gatess) != P:
+        raise PurlinError(PURLIN_ERR_INVALID, "need P expert outputs, P id matrices and P gate matrices")
+    T, K = idss[0].shape
+    H = ys[0].shape[-1]
+    capacity = _rows_capacity(ys, H, "y")
+    for ids, g in zip(idss, gatess):
+        _require_cuda(ids, "ids", 4)
+        _require_cuda(g, "gates", 4)
+        if g.dtype != torch.float32 or tuple(ids.shape) != (T, K) or g.numel() < T * K:
+            raise PurlinError(PURLIN_ERR_INVALID, "every rank needs ids [T, K] and float32 gates [T, K]")
+    _require_cuda(recv_pos, "recv_pos", 4)
+    if recv_pos.numel() < P * T * K:
+        raise PurlinError(PURLIN_ERR_INVALID, "recv_pos needs P*T*K entries")
+    if outs is None:
+        outs = [torch.empty((T, H), dtype=ys[0].dtype, device=ys[0].device) for _ in range(P)]
+    for o in outs:
+        _require_cuda(o, "out", 2)
+        if o.numel() < T * H:
+            raise PurlinError(PURLIN_ERR_INVALID, "every output needs T*H elements")
+    st = lib().purlin_ep_combine(int(T), int(H), int(K), int(E), int(P), _ptr_array(ys), int(capacity),
+                                 _ptr_array(idss), _ptr(recv_pos), _ptr_array(gatess), _ptr_array(outs),
+                                 _ptr(dev_status), _stream_handle(stream))
+    _check(st, "purlin_ep_combine")
+    return outs

@@ -276,3 +276,57 @@ def test_bind_checks_before_binding():
     plan = PL.Plan("allgather", 2, 64, "bf16", 32, host_only=True)
     with pytest.raises(PL.PurlinError):
         plan.bind([None], [None])  # wrong number of buffers
+
+
+def _arr(*ptrs):
+    return (ctypes.c_void_p * len(ptrs))(*ptrs)
+
+
+def _ep_dispatch(T=64, H=64, K=2, E=8, P=2, x=(0x100000, 0x200000), ids=(0x10000, 0x20000),
+                 recv=(0x1000000, 0x2000000), capacity=256, counts=0x3000, recv_pos=0x4000, status=None,
+                 ws=0x800000, wsb=1 << 20):
+    return PL.lib().purlin_ep_dispatch(T, H, K, E, P, _arr(*x) if x else None, _arr(*ids) if ids else None,
+                                       _arr(*recv) if recv else None, capacity, counts, recv_pos, status, ws, wsb,
+                                       None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(P=0), dict(P=17, E=34), dict(E=8, P=3), dict(K=0), dict(K=65), dict(H=0), dict(T=-1),
+    dict(capacity=1 << 31), dict(x=None), dict(ids=None), dict(recv=None), dict(counts=None),
+    dict(recv_pos=None), dict(counts=0x3002), dict(status=0x9002), dict(ws=None), dict(wsb=16),
+    dict(x=(0x100000, 0x200008)),  # misaligned rank pointer
+    dict(x=(0x100000, 0)),  # null rank pointer
+    dict(recv=(0x1000000, 0x1000000 + 256 * 64 * 2 - 16)),  # two receive buffers overlap
+    dict(recv=(0x1000000, 0x200000)),  # a receive buffer overlaps a token buffer
+])
+def test_ep_dispatch_argument_validation(kw):
+    assert _ep_dispatch(**kw) == INVALID
+
+
+def test_ep_dispatch_workspace_size():
+    L = PL.lib()
+    b = ctypes.c_uint64()
+    per = ctypes.c_uint64()
+    assert L.purlin_pack_workspace_size(4096, 8, 256, ctypes.byref(per)) == 0
+    assert L.purlin_ep_dispatch_workspace_size(4096, 8, 256, 8, ctypes.byref(b)) == 0
+    # every rank's pack workspace, then P x P offsets, P x E expert counts and P status words (256-byte pieces)
+    assert b.value == 8 * per.value + 256 + 8192 + 256
+    for args in ((4096, 8, 256, 0), (4096, 8, 256, 17), (4096, 8, 256, 3), (-1, 8, 256, 8), (4096, 0, 256, 8)):
+        assert L.purlin_ep_dispatch_workspace_size(*args, ctypes.byref(b)) == INVALID
+
+
+def _ep_combine(T=64, H=64, K=2, E=8, P=2, y=(0x1000000, 0x2000000), capacity=256, ids=(0x10000, 0x20000),
+                recv_pos=0x4000, gates=(0x30000, 0x40000), out=(0x100000, 0x200000), status=None):
+    return PL.lib().purlin_ep_combine(T, H, K, E, P, _arr(*y) if y else None, capacity, _arr(*ids) if ids else None,
+                                      recv_pos, _arr(*gates) if gates else None, _arr(*out) if out else None,
+                                      status, None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(P=0), dict(E=8, P=3), dict(K=0), dict(H=0), dict(capacity=1 << 31), dict(y=None), dict(ids=None),
+    dict(gates=None), dict(out=None), dict(recv_pos=None), dict(status=0x9002), dict(out=(0x100000, 0x100008)),
+    dict(out=(0x100000, 0x100000 + 64 * 64 * 2 - 16)),  # two outputs overlap
+    dict(out=(0x100000, 0x1000000)),  # an output overlaps an expert-output buffer
+])
+def test_ep_combine_argument_validation(kw):
+    assert _ep_combine(**kw) == INVALID

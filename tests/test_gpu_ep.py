@@ -289,3 +289,163 @@ def test_alltoallv_counts_transposed(P):
         got = to_host(outs[r].t, np.uint16)
         assert_bits_equal(got[: len(want[r])], want[r], "bf16", f"rank {r}")
         assert np.all(got[len(want[r]):].view(np.uint8) == CANARY)
+
+
+# ---------------------------------------------------------------------------
+# One-pass expert-parallel dispatch / combine (purlin_ep_dispatch / _combine)
+
+def _ep_case(P, T, H, K, E, seed):
+    rng = np.random.default_rng(seed)
+    xs = [rng.integers(0, 0x4700, (T, H)).astype(np.uint16) for _ in range(P)]  # finite values
+    idss = [_zipf_or_uniform(rng, T, K, E, seed + p) for p in range(P)]
+    gates = [rng.random((T, K)).astype(np.float32) for _ in range(P)]
+    return xs, idss, gates
+
+
+def _zipf_or_uniform(rng, T, K, E, seed):
+    if T == 0:
+        return np.zeros((0, K), np.int32)
+    if seed % 2:
+        return W.zipf_topk_ids(T, E, K, 1.1, seed)
+    return np.stack([rng.permutation(E)[:K] for _ in range(T)]).astype(np.int32)
+
+
+@pytest.mark.parametrize("P,T,H,K,E,seed", [
+    (1, 40, 32, 2, 4, 0), (2, 50, 24, 2, 8, 1), (3, 70, 7, 3, 9, 2), (4, 65, 136, 4, 16, 3),
+    (8, 200, 520, 8, 64, 5), (16, 64, 64, 4, 32, 6), (4, 0, 64, 2, 8, 7),
+])
+def test_ep_dispatch_and_combine_one_pass_match_oracle(P, T, H, K, E, seed):
+    xs_np, idss_np, gates_np = _ep_case(P, T, H, K, E, seed)
+    want = oracle.ep_dispatch(xs_np, idss_np, E, P)
+    cap = max(1, int(want["counts"].sum(axis=0).max()) + 3)
+    recv = [Guarded(cap * H * 2, torch.int16) for _ in range(P)]
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    xs = [to_device(x) for x in xs_np]
+    idss = [to_device(i) for i in idss_np]
+    got = PL.purlin_ep_dispatch(xs, idss, E, [g.t.view(cap, H) for g in recv], dev_status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    assert np.array_equal(to_host(got["counts"], np.int32).reshape(P, P), want["counts"])
+    if T:
+        assert np.array_equal(to_host(got["recv_pos"], np.int32).reshape(P, T, K), want["recv_pos"])
+    for r in range(P):
+        assert recv[r].intact()
+        host = to_host(recv[r].t, np.uint16).reshape(cap, H)
+        n = len(want["recv"][r])
+        assert np.array_equal(host[:n], want["recv"][r]), f"receive buffer {r}"
+        assert np.all(host[n:].view(np.uint8) == CANARY), "rows beyond the received count were written"
+    # combine: expert rank r marks its rows with r + 1
+    ys_np = [to_host(recv[r].t, np.uint16).reshape(cap, H) ^ np.uint16(r + 1) for r in range(P)]
+    outs = [Guarded(T * H * 2, torch.int16) for _ in range(P)]
+    PL.purlin_ep_combine([to_device(y) for y in ys_np], idss, got["recv_pos"], [to_device(g) for g in gates_np], E,
+                         outs=[o.t.view(T, H) for o in outs], dev_status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    want_out = oracle.ep_combine(ys_np, idss_np, want["recv_pos"], gates_np, E, P)
+    for p in range(P):
+        assert outs[p].intact()
+        assert_bits_equal(to_host(outs[p].t, np.uint16).reshape(T, H), want_out[p], "bf16", f"combined rank {p}")
+
+
+def test_ep_dispatch_over_capacity_writes_nothing():
+    P, T, H, K, E = 4, 64, 64, 4, 8
+    xs_np, idss_np, _ = _ep_case(P, T, H, K, E, 11)
+    need = int(oracle.ep_dispatch(xs_np, idss_np, E, P)["counts"].sum(axis=0).max())
+    cap = need - 1
+    recv = [Guarded(cap * H * 2, torch.int16) for _ in range(P)]
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    PL.purlin_ep_dispatch([to_device(x) for x in xs_np], [to_device(i) for i in idss_np], E,
+                          [g.t.view(cap, H) for g in recv], dev_status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 1
+    for g in recv:
+        assert g.intact() and bool(torch.all(g.t.view(torch.uint8) == CANARY).item())
+
+
+def test_ep_dispatch_flags_bad_routing():
+    P, T, H, K, E = 2, 70, 16, 3, 8
+    xs_np, idss_np, _ = _ep_case(P, T, H, K, E, 12)
+    idss_np[1][5, 1] = E + 2
+    idss_np[0][66, 2] = idss_np[0][66, 0]
+    cap = P * T * K
+    recv = [Guarded(cap * H * 2, torch.int16) for _ in range(P)]
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    PL.purlin_ep_dispatch([to_device(x) for x in xs_np], [to_device(i) for i in idss_np], E,
+                          [g.t.view(cap, H) for g in recv], dev_status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 1
+    assert all(g.intact() for g in recv)
+
+
+def test_ep_one_pass_full_size_equals_two_step_path():
+    """P = 8 x 4096 tokens x 7168, top-8 Zipf(1.1): the one-pass dispatch
+    and combine give the same bits as pack + AllToAllV and AllToAllV +
+    unpack (both checked against the oracle above)."""
+    P, T, H, K, E = 8, 4096, 7168, 8, 256
+    xs_np, ids_np, gates_np = _rank_inputs(P, T, H, K, E, seed=4)
+    ep = EPStep(P, T, H, K, E)
+    xs = [to_device(x) for x in xs_np]
+    ids = [to_device(i) for i in ids_np]
+    gates = [to_device(g) for g in gates_np]
+    ep.dispatch(xs, ids)
+    cap = P * T * K
+    recv1 = [torch.empty((cap, H), dtype=torch.int16, device="cuda") for _ in range(P)]
+    got = PL.purlin_ep_dispatch(xs, ids, E, recv1)
+    torch.cuda.synchronize()
+    m = to_host(ep.counts, np.int32).reshape(P, P)
+    assert np.array_equal(to_host(got["counts"], np.int32).reshape(P, P), m)
+    for r in range(P):
+        n = int(m[:, r].sum())
+        assert torch.equal(recv1[r][:n].reshape(-1), ep.recv[r][: n * H]), f"receive buffer {r}"
+        _mark(recv1[r][:n], r)
+        _mark(ep.recv[r][: n * H], r)
+    outs2 = [torch.empty((T, H), dtype=torch.int16, device="cuda") for _ in range(P)]
+    ep.combine(gates, outs2)
+    outs1 = PL.purlin_ep_combine(recv1, ids, got["recv_pos"], gates, E)
+    torch.cuda.synchronize()
+    for p in range(P):
+        assert torch.equal(outs1[p], outs2[p]), f"combined rank {p}"
+
+
+def test_ep_one_pass_in_a_graph():
+    P, T, H, K, E = 4, 96, 256, 4, 16
+    cap = P * T * K
+    xs = [torch.empty((T, H), dtype=torch.int16, device="cuda") for _ in range(P)]
+    ids = [torch.empty((T, K), dtype=torch.int32, device="cuda") for _ in range(P)]
+    gates = [torch.empty((T, K), dtype=torch.float32, device="cuda") for _ in range(P)]
+    recv = [torch.empty((cap, H), dtype=torch.int16, device="cuda") for _ in range(P)]
+    outs = [torch.empty((T, H), dtype=torch.int16, device="cuda") for _ in range(P)]
+    counts = torch.empty(P * P, dtype=torch.int32, device="cuda")
+    recv_pos = torch.empty((P, T, K), dtype=torch.int32, device="cuda")
+    ws = torch.empty(PL.purlin_ep_dispatch_workspace_size(T, K, E, P), dtype=torch.uint8, device="cuda")
+
+    def step(stream=None):
+        PL.purlin_ep_dispatch(xs, ids, E, recv, counts=counts, recv_pos=recv_pos, workspace=ws, stream=stream)
+        PL.purlin_ep_combine(recv, ids, recv_pos, gates, E, outs=outs, stream=stream)
+
+    def load(seed):
+        xs_np, ids_np, gates_np = _ep_case(P, T, H, K, E, seed)
+        for p in range(P):
+            xs[p].copy_(to_device(xs_np[p]))
+            ids[p].copy_(to_device(ids_np[p]))
+            gates[p].copy_(to_device(gates_np[p]))
+        return xs_np, ids_np, gates_np
+
+    load(1)
+    step()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            step(stream=side)
+    for seed in (2, 3, 4):
+        xs_np, ids_np, gates_np = load(seed)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        d = oracle.ep_dispatch(xs_np, ids_np, E, P)
+        want = oracle.ep_combine(d["recv"], ids_np, d["recv_pos"], gates_np, E, P)
+        for p in range(P):
+            assert_bits_equal(to_host(outs[p], np.uint16).reshape(T, H), want[p], "bf16", f"replay {seed} rank {p}")
