@@ -441,9 +441,12 @@ def measure_ep(torch, PL, W, P, T, H, E, K, reps=5):
     the packs' dest_counts (read on the device, unit = H); combine = the
     reverse AllToAllV (same counts, column-major), then P unpacks.  Receive
     buffers hold the worst case.  Routing: Zipf(1.1) top-K per rank, seeded
-    per rank.  Two variants: one row per (token, slot), and de-duplicated
+    per rank.  Three variants: one row per (token, slot); de-duplicated
     (one row per token and destination rank; its combine sums the ranks'
-    partial rows).  Event-timed on the current stream."""
+    partial rows); and one pass each way (purlin_ep_dispatch writes the rows
+    straight into the receive buffers, purlin_ep_combine reads them back from
+    there: the per-slot result without the packed buffers).  Event-timed on
+    the current stream."""
     i32 = dict(dtype=torch.int32, device="cuda")
     row = H * 2
     xs, ids, gates = [], [], []
@@ -510,9 +513,30 @@ def measure_ep(torch, PL, W, P, T, H, E, K, reps=5):
         r["rows_received_per_rank"] = [int(v) for v in m.sum(axis=0)]
         result[variant] = r
         del packs, recv, back, outs, ws
+    # one pass each way: rows straight to the receive buffers and back
+    cap = P * T * K
+    recv = [torch.empty((cap, H), dtype=torch.int16, device="cuda") for _ in range(P)]
+    outs = [torch.empty((T, H), dtype=torch.int16, device="cuda") for _ in range(P)]
+    counts = torch.empty(P * P, dtype=torch.int32, device="cuda")
+    recv_pos = torch.empty((P, T, K), dtype=torch.int32, device="cuda")
+    ws = torch.empty(PL.purlin_ep_dispatch_workspace_size(T, K, E, P), dtype=torch.uint8, device="cuda")
+    stages = [("dispatch", lambda: PL.purlin_ep_dispatch(xs, ids, E, recv, counts=counts, recv_pos=recv_pos,
+                                                         workspace=ws)),
+              ("combine", lambda: PL.purlin_ep_combine(recv, ids, recv_pos, gates, E, outs=outs))]
+    stages[0][1]()
+    torch.cuda.synchronize()
+    sent = int(counts.sum().item())
+    bmin = {"dispatch": P * T * row + sent * row + 2 * P * T * K * 4,
+            "combine": sent * row + P * T * row + 3 * P * T * K * 4}
+    r = _time_stages(torch, stages, bmin, reps)
+    r["rows_sent_total"] = sent
+    result["one_pass"] = r
+    del recv, outs, ws
     result["workload"] = {"P": P, "T_per_rank": T, "H": H, "E": E, "K": K, "routing": "Zipf(1.1) top-K"}
     result["dedup_speedup"] = round(result["per_slot"]["round_trip"]["avg_us"] /
                                     result["dedup"]["round_trip"]["avg_us"], 3)
+    result["one_pass_speedup"] = round(result["per_slot"]["round_trip"]["avg_us"] /
+                                       result["one_pass"]["round_trip"]["avg_us"], 3)
     del xs, ids, gates
     return result
 
