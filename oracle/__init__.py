@@ -21,8 +21,8 @@ Contents
 ``moe_dedup``    De-duplicated dispatch ``pack_dedup`` (one row per token and
                  destination rank) and its combine ``unpack_dedup``.
 ``ep``           Expert-parallel dispatch / combine over P ranks: pack, then
-                 AllToAllV of the rows (and back, then unpack), composed from
-                 the definitions above.
+                 AllToAllV of the rows (and back, then unpack), per slot and
+                 de-duplicated, composed from the definitions above.
 
 Representation: fp32 data is ``numpy.float32``; bf16 data is its 16-bit
 encoding held in ``numpy.uint16``.  Floating-point arithmetic is numpy
@@ -38,7 +38,7 @@ from .bf16 import narrow, widen
 from .collectives import all_gather, all_reduce, all_to_all, reduce_scatter
 from .moe import pack, unpack
 from .moe_dedup import pack_dedup, unpack_dedup
-from .ep import ep_combine, ep_dispatch
+from .ep import ep_combine, ep_combine_dedup, ep_dispatch, ep_dispatch_dedup
 from .rooted import broadcast, gather, reduce, scatter
 from .vcollectives import all_gather_v, all_to_all_v, reduce_scatter_v
 
@@ -55,6 +55,8 @@ __all__ = [
     "unpack_dedup",
     "ep_dispatch",
     "ep_combine",
+    "ep_dispatch_dedup",
+    "ep_combine_dedup",
     "broadcast",
     "gather",
     "reduce",

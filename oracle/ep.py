@@ -73,3 +73,49 @@ def ep_combine(ys, idss, recv_pos, gatess, E, P):
                 rows[t * K + k] = ys[int(ids[t, k]) // L][int(recv_pos[p, t, k])]
         outs.append(unpack(rows, np.arange(T * K, dtype=np.int64).reshape(T, K), gatess[p]))
     return outs
+
+
+def ep_dispatch_dedup(xs, idss, E, P):
+    """De-duplicated dispatch over P ranks: rank p's ``moe_dedup.pack_dedup``
+    (one row per token and owning rank), then the AllToAllV of those rows.
+    Returns ``recv`` (P arrays [R_r, H]), ``counts`` (int32 [P, P]) and
+    ``recv_row`` (int32 [P, T, P]: row of rank p's token t in rank r's
+    buffer, -1 where t has no expert on r)."""
+    from .moe_dedup import pack_dedup
+
+    packs = [pack_dedup(xs[p], idss[p], E, P) for p in range(P)]
+    H = xs[0].shape[1]
+    counts = np.array([[int(c) for c in pk["dest_counts"]] for pk in packs], dtype=np.int64)
+    flat = all_to_all_v([pk["packed"].reshape(-1) for pk in packs], (counts * H).tolist(), "bf16")
+    recv = [f.reshape(-1, H) for f in flat]
+    T = np.asarray(idss[0]).shape[0]
+    recv_row = np.full((P, T, P), -1, dtype=np.int64)
+    for p in range(P):
+        for t in range(T):
+            for r in range(P):
+                q = int(packs[p]["row_of"][t, r])
+                if q >= 0:
+                    recv_row[p, t, r] = int(counts[:p, r].sum()) + q - int(packs[p]["dest_offsets"][r])
+    return {"recv": recv, "counts": counts.astype(np.int32), "recv_row": recv_row.astype(np.int32)}
+
+
+def ep_combine_dedup(ys, recv_row, P):
+    """Partial outputs ``ys`` (P arrays, rank r's receive layout) back to
+    their tokens, summed in rank order as ``moe_dedup.unpack_dedup`` does.
+    Returns P arrays uint16 [T, H]."""
+    from .moe_dedup import unpack_dedup
+
+    outs = []
+    for p in range(P):
+        T = recv_row.shape[1]
+        H = ys[0].shape[1]
+        rows = np.zeros((T * P, H), dtype=np.uint16)  # (t, r)'s partial row, in (t, r) order
+        row_of = np.full((T, P), -1, dtype=np.int64)
+        for t in range(T):
+            for r in range(P):
+                q = int(recv_row[p, t, r])
+                if q >= 0:
+                    rows[t * P + r] = ys[r][q]
+                    row_of[t, r] = t * P + r
+        outs.append(unpack_dedup(rows, row_of))
+    return outs

@@ -92,3 +92,44 @@ def test_ep_combine_marked_experts():
         rows = np.repeat(xs[p], K, axis=0) ^ ((idss[p].reshape(-1) // L) + 1).astype(np.uint16)[:, None]
         want = oracle.unpack(rows, np.arange(T * K).reshape(T, K), gates[p])
         assert np.array_equal(outs[p], want)
+
+
+def test_ep_dispatch_dedup_hand_worked_example():
+    """P=2, E=4 (experts 0,1 on rank 0; 2,3 on rank 1), T=3, K=2.
+
+    rank 0: ids [[0,2],[1,0],[3,2]] -> ranks {0,1}, {0}, {1}: rows to 0: a0 a1; to 1: a0 a2
+    rank 1: ids [[2,3],[0,3],[1,0]] -> ranks {1}, {0,1}, {0}: rows to 0: b1 b2; to 1: b0 b1
+    rank 0 receives a0 a1 b1 b2; rank 1 receives a0 a2 b0 b1.
+    """
+    a = np.array([[1, 1], [2, 2], [3, 3]], np.uint16)
+    b = np.array([[4, 4], [5, 5], [6, 6]], np.uint16)
+    ids = [np.array([[0, 2], [1, 0], [3, 2]], np.int32), np.array([[2, 3], [0, 3], [1, 0]], np.int32)]
+    d = oracle.ep_dispatch_dedup([a, b], ids, E=4, P=2)
+    assert d["counts"].tolist() == [[2, 2], [2, 2]]
+    assert np.array_equal(d["recv"][0], np.stack([a[0], a[1], b[1], b[2]]))
+    assert np.array_equal(d["recv"][1], np.stack([a[0], a[2], b[0], b[1]]))
+    assert d["recv_row"].tolist() == [[[0, 0], [1, -1], [-1, 1]], [[-1, 2], [2, 3], [3, -1]]]
+
+
+@pytest.mark.parametrize("P,T,H,K,E,seed", [(2, 9, 3, 2, 4, 6), (4, 40, 5, 4, 16, 7), (3, 25, 2, 3, 12, 8)])
+def test_ep_dedup_rows_land_once_and_combine_equals_unpack_dedup(P, T, H, K, E, seed):
+    xs, idss, _ = _inputs(P, T, H, K, E, seed)
+    d = oracle.ep_dispatch_dedup(xs, idss, E, P)
+    L = E // P
+    for r in range(P):
+        got = sorted(int(d["recv_row"][p, t, r]) for p in range(P) for t in range(T) if d["recv_row"][p, t, r] >= 0)
+        assert got == list(range(len(d["recv"][r])))
+    for p in range(P):
+        for t in range(T):
+            owners = {int(e) // L for e in idss[p][t]}
+            for r in range(P):
+                q = int(d["recv_row"][p, t, r])
+                assert (q >= 0) == (r in owners)
+                if q >= 0:
+                    assert np.array_equal(d["recv"][r][q], xs[p][t])
+    ys = [d["recv"][r] ^ np.uint16(r + 1) for r in range(P)]  # marked partial outputs
+    outs = oracle.ep_combine_dedup(ys, d["recv_row"], P)
+    for p in range(P):
+        pk = oracle.pack_dedup(xs[p], idss[p], E, P)
+        mark = np.repeat(np.arange(P), pk["dest_counts"]).astype(np.uint16) + 1
+        assert np.array_equal(outs[p], oracle.unpack_dedup(pk["packed"] ^ mark[:, None], pk["row_of"]))
