@@ -445,8 +445,8 @@ def measure_ep(torch, PL, W, P, T, H, E, K, reps=5):
     (one row per token and destination rank; its combine sums the ranks'
     partial rows); and one pass each way (purlin_ep_dispatch writes the rows
     straight into the receive buffers, purlin_ep_combine reads them back from
-    there: the per-slot result without the packed buffers).  Event-timed on
-    the current stream."""
+    there: the per-slot result without the packed buffers), also
+    de-duplicated.  Event-timed on the current stream."""
     i32 = dict(dtype=torch.int32, device="cuda")
     row = H * 2
     xs, ids, gates = [], [], []
@@ -531,12 +531,28 @@ def measure_ep(torch, PL, W, P, T, H, E, K, reps=5):
     r = _time_stages(torch, stages, bmin, reps)
     r["rows_sent_total"] = sent
     result["one_pass"] = r
-    del recv, outs, ws
+    # de-duplicated, one pass each way
+    ws2 = torch.empty(PL.purlin_ep_dispatch_dedup_workspace_size(T, P), dtype=torch.uint8, device="cuda")
+    recv_row = torch.empty((P, T, P), dtype=torch.int32, device="cuda")
+    stages = [("dispatch", lambda: PL.purlin_ep_dispatch_dedup(xs, ids, E, recv, counts=counts, recv_row=recv_row,
+                                                               workspace=ws2)),
+              ("combine", lambda: PL.purlin_ep_combine_dedup(recv, recv_row, outs=outs))]
+    stages[0][1]()
+    torch.cuda.synchronize()
+    sent = int(counts.sum().item())
+    bmin = {"dispatch": P * T * row + sent * row + P * T * K * 4 + P * T * P * 4,
+            "combine": sent * row + P * T * row + P * T * P * 4}
+    r = _time_stages(torch, stages, bmin, reps)
+    r["rows_sent_total"] = sent
+    result["one_pass_dedup"] = r
+    del recv, outs, ws, ws2
     result["workload"] = {"P": P, "T_per_rank": T, "H": H, "E": E, "K": K, "routing": "Zipf(1.1) top-K"}
     result["dedup_speedup"] = round(result["per_slot"]["round_trip"]["avg_us"] /
                                     result["dedup"]["round_trip"]["avg_us"], 3)
     result["one_pass_speedup"] = round(result["per_slot"]["round_trip"]["avg_us"] /
                                        result["one_pass"]["round_trip"]["avg_us"], 3)
+    result["one_pass_dedup_speedup"] = round(result["per_slot"]["round_trip"]["avg_us"] /
+                                             result["one_pass_dedup"]["round_trip"]["avg_us"], 3)
     del xs, ids, gates
     return result
 

@@ -448,6 +448,35 @@ PURLIN_API purlin_status purlin_ep_combine(int T, int H, int K, int E, int P, co
                                            const float* const* gates, void* const* out, int32_t* dev_status,
                                            void* stream);
 
+/* Workspace bytes purlin_ep_dispatch_dedup needs for P ranks of T tokens. */
+PURLIN_API purlin_status purlin_ep_dispatch_dedup_workspace_size(int T, int P, uint64_t* bytes);
+
+/* The de-duplicated dispatch over P ranks in one pass: rank p's
+ * purlin_pack_dedup followed by the ALLTOALLV of its rows, without the
+ * packed buffers.  Rank r's buffer holds, from rank 0, then rank 1, ...,
+ * one row per token having an expert on r, in token order.
+ *   x, ids, recv, capacity, counts, dev_status, workspace  as
+ *            purlin_ep_dispatch (counts[p*P + r] = tokens rank p sends r)
+ *   recv_row int32 [P, T, P] device (output): row of rank p's token t in
+ *            rank r's buffer, or -1 if none of its experts is on r:
+ *            sum_{q<p} counts[q][r] + row_of_p[t,r] - dest_offsets_p[r]
+ * Limits and errors as purlin_ep_dispatch. */
+PURLIN_API purlin_status purlin_ep_dispatch_dedup(int T, int H, int K, int E, int P, const void* const* x,
+                                                  const int32_t* const* ids, void* const* recv, uint64_t capacity,
+                                                  int32_t* counts, int32_t* recv_row, int32_t* dev_status,
+                                                  void* workspace, uint64_t workspace_bytes, void* stream);
+
+/* Its combine: y_r holds rank r's partial outputs in its receive layout
+ * (gates applied on the expert side), and
+ *   out_p[t, h] = narrow(+0 + widen(y_r[recv_row[p,t,r], h]) for r = 0..P-1 with recv_row >= 0)
+ * in rank order -- the same bits as the reverse ALLTOALLV followed by
+ * purlin_unpack_dedup.  dev_status (optional): 0, or 1 if some entry is
+ * neither -1 nor a row below `capacity` (it then contributes nothing).
+ * Errors as purlin_ep_combine. */
+PURLIN_API purlin_status purlin_ep_combine_dedup(int T, int H, int P, const void* const* y, uint64_t capacity,
+                                                 const int32_t* recv_row, void* const* out, int32_t* dev_status,
+                                                 void* stream);
+
 /* Static text for a status code ("unknown status" for others). */
 PURLIN_API const char* purlin_status_string(purlin_status status);
 

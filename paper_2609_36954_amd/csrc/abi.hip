@@ -393,6 +393,62 @@ purlin_status purlin_ep_combine(int T, int H, int K, int E, int P, const void* c
     return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
 }
 
+purlin_status purlin_ep_dispatch_dedup_workspace_size(int T, int P, uint64_t* bytes) {
+    if (!bytes || T < 0 || P < 1 || P > PURLIN_MAX_RANKS) return PURLIN_ERR_INVALID;
+    *bytes = purlin::ep_dispatch_dedup_workspace_bytes(T, P);
+    return PURLIN_OK;
+}
+
+purlin_status purlin_ep_dispatch_dedup(int T, int H, int K, int E, int P, const void* const* x,
+                                       const int32_t* const* ids, void* const* recv, uint64_t capacity,
+                                       int32_t* counts, int32_t* recv_row, int32_t* dev_status, void* workspace,
+                                       uint64_t workspace_bytes, void* stream) {
+    if (!ep_limits_ok(T, H, K, E, P, capacity)) return PURLIN_ERR_INVALID;
+    if (!counts || (reinterpret_cast<uintptr_t>(counts) & 3u)) return PURLIN_ERR_INVALID;
+    if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    const uint64_t need = purlin::ep_dispatch_dedup_workspace_bytes(T, P);
+    if (workspace_bytes < need || (need && (!workspace || !aligned16(workspace)))) return PURLIN_ERR_INVALID;
+    if (T > 0) {
+        if (!all_aligned(x, P) || !all_aligned(ids, P) || !all_aligned(recv, P)) return PURLIN_ERR_INVALID;
+        if (!recv_row || (reinterpret_cast<uintptr_t>(recv_row) & 3u)) return PURLIN_ERR_INVALID;
+        const uint64_t xb = uint64_t(T) * H * 2, rb = capacity * uint64_t(H) * 2;
+        for (int r = 0; r < P; ++r) {
+            for (int q = r + 1; q < P; ++q)
+                if (overlaps(recv[r], rb, recv[q], rb)) return PURLIN_ERR_INVALID;
+            for (int p = 0; p < P; ++p)
+                if (overlaps(recv[r], rb, x[p], xb)) return PURLIN_ERR_INVALID;
+        }
+    }
+    const hipError_t e = purlin::launch_ep_dispatch_dedup(
+        T, H, K, E, P, reinterpret_cast<const uint16_t* const*>(x), ids, reinterpret_cast<uint16_t* const*>(recv),
+        static_cast<int64_t>(capacity), counts, recv_row, dev_status, workspace, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
+purlin_status purlin_ep_combine_dedup(int T, int H, int P, const void* const* y, uint64_t capacity,
+                                      const int32_t* recv_row, void* const* out, int32_t* dev_status, void* stream) {
+    if (T < 0 || H < 1 || P < 1 || P > PURLIN_MAX_RANKS) return PURLIN_ERR_INVALID;
+    if (capacity >= (uint64_t(1) << 31) || !purlin::ep_launch_fits(T, H, P)) return PURLIN_ERR_INVALID;
+    if (static_cast<int64_t>(T) * P >= (int64_t(1) << 31)) return PURLIN_ERR_INVALID;
+    if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    if (T > 0) {
+        if (!all_aligned(out, P)) return PURLIN_ERR_INVALID;
+        if (capacity > 0 && !all_aligned(y, P)) return PURLIN_ERR_INVALID;
+        if (!recv_row || (reinterpret_cast<uintptr_t>(recv_row) & 3u)) return PURLIN_ERR_INVALID;
+        const uint64_t ob = uint64_t(T) * H * 2, yb = capacity * uint64_t(H) * 2;
+        for (int p = 0; p < P; ++p) {
+            for (int q = p + 1; q < P; ++q)
+                if (overlaps(out[p], ob, out[q], ob)) return PURLIN_ERR_INVALID;
+            for (int r = 0; r < P && capacity > 0; ++r)
+                if (overlaps(out[p], ob, y[r], yb)) return PURLIN_ERR_INVALID;
+        }
+    }
+    const hipError_t e = purlin::launch_ep_combine_dedup(
+        T, H, P, reinterpret_cast<const uint16_t* const*>(y), static_cast<int64_t>(capacity), recv_row,
+        reinterpret_cast<uint16_t* const*>(out), dev_status, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
 purlin_status purlin_unpack(int T, int H, int K, const void* y, const int32_t* pos, const float* gates, void* out,
                             int32_t* dev_status, void* stream) {
     if (T < 0 || H < 1 || K < 1 || K > 64) return PURLIN_ERR_INVALID;

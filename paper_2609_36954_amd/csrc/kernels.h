@@ -87,4 +87,17 @@ hipError_t launch_ep_combine(int T, int H, int K, int E, int P, const uint16_t* 
                              const int32_t* const* ids, const int32_t* recv_pos, const float* const* gates,
                              uint16_t* const* out, int32_t* dev_status, hipStream_t stream);
 
+// The de-duplicated one-pass dispatch / combine (one row per token and
+// owning rank; recv_row is [P, T, P]).
+uint64_t ep_dispatch_dedup_workspace_bytes(int T, int P);
+
+hipError_t launch_ep_dispatch_dedup(int T, int H, int K, int E, int P, const uint16_t* const* x,
+                                    const int32_t* const* ids, uint16_t* const* recv, int64_t capacity,
+                                    int32_t* counts, int32_t* recv_row, int32_t* dev_status, void* workspace,
+                                    hipStream_t stream);
+
+hipError_t launch_ep_combine_dedup(int T, int H, int P, const uint16_t* const* y, int64_t capacity,
+                                   const int32_t* recv_row, uint16_t* const* out, int32_t* dev_status,
+                                   hipStream_t stream);
+
 }  // namespace purlin

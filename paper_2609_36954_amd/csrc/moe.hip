@@ -560,6 +560,8 @@ struct EpArgs {
     const int32_t* dest_off[PURLIN_MAX_RANKS];
     const float* gates[PURLIN_MAX_RANKS];
     const int32_t* counts;  // P x P: rows rank p sends rank r
+    const int64_t* before;  // P x P: rows rank r receives from ranks < p (ep_prefix)
+    const int32_t* fits;    // 1 if every receive buffer holds its rows (ep_prefix)
     int32_t* recv_pos;      // [P, T, K]
     int32_t* status;        // optional
     int64_t capacity;       // rows per receive buffer
@@ -567,16 +569,17 @@ struct EpArgs {
 };
 
 // Every wave of rank p's token t and column slice: lane k < K forms slot k's
-// receiving rank and row (from the pack metadata and the counts staged in
-// LDS); all waves reach the same capacity verdict, so either every row is
-// written or none is.
-template <int U, bool NTL, bool NTS>
-__global__ __launch_bounds__(kBlock) void ep_dispatch_rows(EpArgs a) {
+// receiving rank and row from the pack metadata and ep_prefix's sums; if
+// some receive buffer is too small, no wave writes anything.
+// Once per dispatch, after every rank's metadata: before[p][r] = rows rank r
+// receives from ranks < p, and whether every receive buffer holds what it
+// receives (if not, the status word is set and the rows kernel writes
+// nothing).  One workgroup; P <= 16.
+__global__ __launch_bounds__(kBlock) void ep_prefix(const int32_t* __restrict__ counts, int P, int64_t capacity,
+                                                    int64_t* __restrict__ before, int32_t* __restrict__ fits,
+                                                    int32_t* __restrict__ status) {
     __shared__ int32_t m[PURLIN_MAX_RANKS * PURLIN_MAX_RANKS];
-    __shared__ int64_t before[PURLIN_MAX_RANKS * PURLIN_MAX_RANKS];  // [p][r]: rows r got from ranks < p
-    __shared__ int ok;
-    const int P = a.P;
-    for (int i = threadIdx.x; i < P * P; i += kBlock) m[i] = a.counts[i];
+    for (int i = threadIdx.x; i < P * P; i += kBlock) m[i] = counts[i];
     __syncthreads();
     for (int i = threadIdx.x; i < P * P; i += kBlock) {
         const int p = i / P, r = i - p * P;
@@ -585,20 +588,24 @@ __global__ __launch_bounds__(kBlock) void ep_dispatch_rows(EpArgs a) {
         before[i] = b;
     }
     if (threadIdx.x == 0) {
-        bool fits = true;
+        bool ok = true;
         for (int r = 0; r < P; ++r) {
             int64_t col = 0;
             for (int q = 0; q < P; ++q) {
-                fits = fits && m[q * P + r] >= 0;
+                ok = ok && m[q * P + r] >= 0;
                 col += m[q * P + r];
             }
-            fits = fits && col <= a.capacity;
+            ok = ok && col <= capacity;
         }
-        ok = fits;
-        if (!fits && blockIdx.x == 0 && a.status) atomicOr(a.status, 1);
+        *fits = ok ? 1 : 0;
+        if (!ok && status) atomicOr(status, 1);
     }
-    __syncthreads();
-    if (!ok) return;
+}
+
+template <int U, bool NTL, bool NTS>
+__global__ __launch_bounds__(kBlock) void ep_dispatch_rows(EpArgs a) {
+    if (!*a.fits) return;  // uniform: nothing is written
+    const int P = a.P;
     const uint32_t w = wave_index();
     const uint64_t per_rank = static_cast<uint64_t>(a.T) * a.slices;
     if (w >= per_rank * P) return;
@@ -615,7 +622,7 @@ __global__ __launch_bounds__(kBlock) void ep_dispatch_rows(EpArgs a) {
         if (e >= 0 && e < E && lr >= 0) {
             r = e / L;
             const int64_t q = static_cast<int64_t>(a.tile_base[p][static_cast<int64_t>(t / kPackTileTokens) * E + e]) + lr;
-            const int64_t rr = before[p * P + r] + q - a.dest_off[p][r];
+            const int64_t rr = a.before[p * P + r] + q - a.dest_off[p][r];
             row = (rr >= 0 && rr < a.capacity) ? static_cast<int>(rr) : -1;
         }
         if (slice == 0) a.recv_pos[(static_cast<int64_t>(p) * a.T + t) * K + lane] = row;
@@ -660,6 +667,68 @@ __global__ __launch_bounds__(kBlock) void ep_combine_rows(EpArgs a) {
             return rk < 0 ? nullptr : a.x[__builtin_amdgcn_readlane(r, k)] + static_cast<uint64_t>(rk) * row_bytes;
         },
         g, K, a.dst[p] + t * row_bytes, row_bytes, slice, lane);
+}
+
+// De-duplicated, one pass: rank p's token t goes once to every rank r owning
+// one of its experts, at before[p][r] + (its row in p's de-duplicated
+// layout) - dest_offsets_p[r]; lane r < P forms that row (recv_row[p, t, r],
+// -1 for none).
+template <int U, bool NTL, bool NTS>
+__global__ __launch_bounds__(kBlock) void ep_dedup_dispatch_rows(EpArgs a) {
+    if (!*a.fits) return;  // uniform: nothing is written
+    const int P = a.P;
+    const uint32_t w = wave_index();
+    const uint64_t per_rank = static_cast<uint64_t>(a.T) * a.slices;
+    if (w >= per_rank * P) return;
+    const uint32_t p = static_cast<uint32_t>(w / per_rank);
+    const uint32_t rem = static_cast<uint32_t>(w - p * per_rank);
+    const uint32_t t = rem / a.slices, slice = rem - t * a.slices;
+    const uint32_t lane = lane_index();
+    int row = -1;
+    if (lane < static_cast<uint32_t>(P)) {
+        const int64_t j = static_cast<int64_t>(t) * P + lane;
+        const int lr = a.lrank[p][j];
+        if (lr >= 0) {
+            const int64_t rr = a.before[p * P + lane] + a.tile_base[p][static_cast<int64_t>(t / kWave) * P + lane] + lr;
+            row = (rr >= 0 && rr < a.capacity) ? static_cast<int>(rr) : -1;
+        }
+        if (slice == 0) a.recv_pos[static_cast<int64_t>(p) * a.T * P + j] = row;
+    }
+    const uint64_t row_bytes = static_cast<uint64_t>(a.H) * 2;
+    copy_row_to_slots<U, NTL, NTS>(a.x[p] + t * row_bytes, row_bytes, slice, P, lane, [&](int r) -> char* {
+        const int rr = __builtin_amdgcn_readlane(row, r);
+        return rr < 0 ? nullptr : a.dst[r] + static_cast<uint64_t>(rr) * row_bytes;
+    });
+}
+
+// Its combine: rank p's token t sums, in rank order, the partial output of
+// every rank r with recv_row[p, t, r] >= 0, read from r's buffer.
+template <int U, bool NTL, bool NTS>
+__global__ __launch_bounds__(kBlock) void ep_dedup_combine_rows(EpArgs a) {
+    const uint32_t w = wave_index();
+    const uint64_t per_rank = static_cast<uint64_t>(a.T) * a.slices;
+    if (w >= per_rank * a.P) return;
+    const uint32_t p = static_cast<uint32_t>(w / per_rank);
+    const uint32_t rem = static_cast<uint32_t>(w - p * per_rank);
+    const uint32_t t = rem / a.slices, slice = rem - t * a.slices;
+    const uint32_t lane = lane_index();
+    const int P = a.P;
+    int row = -1;
+    if (lane < static_cast<uint32_t>(P)) {
+        const int64_t rr = a.recv_pos[(static_cast<int64_t>(p) * a.T + t) * P + lane];
+        if (rr >= 0 && rr < a.capacity) {
+            row = static_cast<int>(rr);
+        } else if (rr != -1 && a.status && slice == 0) {
+            atomicOr(a.status, 1);
+        }
+    }
+    const uint64_t row_bytes = static_cast<uint64_t>(a.H) * 2;
+    combine_slots<U, NTL, NTS, false>(
+        [&](int r) -> const char* {
+            const int rr = __builtin_amdgcn_readlane(row, r);
+            return rr < 0 ? nullptr : a.x[r] + static_cast<uint64_t>(rr) * row_bytes;
+        },
+        1.0f, P, a.dst[p] + t * row_bytes, row_bytes, slice, lane);
 }
 
 // Merges the ranks' routing-error words (contiguous) into the caller's status word.
@@ -802,9 +871,17 @@ hipError_t launch_unpack_dedup(int T, int H, int P, int64_t rows, const uint16_t
     return hipGetLastError();
 }
 
+// Both one-pass dispatches end their workspace with before[P][P] (int64)
+// and the capacity verdict.
+uint64_t ep_tail_bytes(int P) {
+    const uint64_t Pu = static_cast<uint64_t>(P);
+    return align256(8 * Pu * Pu) + align256(4);
+}
+
 uint64_t ep_dispatch_workspace_bytes(int T, int K, int E, int P) {
     const uint64_t Pu = static_cast<uint64_t>(P);
-    return Pu * pack_workspace_bytes(T, K, E) + align256(4 * Pu * Pu) + align256(4 * Pu * E) + align256(4 * Pu);
+    return Pu * pack_workspace_bytes(T, K, E) + align256(4 * Pu * Pu) + align256(4 * Pu * E) + align256(4 * Pu) +
+           ep_tail_bytes(P);
 }
 
 hipError_t launch_ep_dispatch(int T, int H, int K, int E, int P, const uint16_t* const* x, const int32_t* const* ids,
@@ -816,6 +893,9 @@ hipError_t launch_ep_dispatch(int T, int H, int K, int E, int P, const uint16_t*
     int32_t* dest_off = reinterpret_cast<int32_t*>(ws + Pu * per);                          // [P][P]
     int32_t* expert_counts = reinterpret_cast<int32_t*>(ws + Pu * per + align256(4 * Pu * Pu));  // [P][E]
     int32_t* words = reinterpret_cast<int32_t*>(ws + Pu * per + align256(4 * Pu * Pu) + align256(4 * Pu * E));
+    char* tail = ws + Pu * per + align256(4 * Pu * Pu) + align256(4 * Pu * E) + align256(4 * Pu);
+    int64_t* before = reinterpret_cast<int64_t*>(tail);
+    int32_t* fits = reinterpret_cast<int32_t*>(tail + align256(8 * Pu * Pu));
     const int ntiles = (T + kPackTileTokens - 1) / kPackTileTokens;
     EpArgs a{};
     (void)hipGetLastError();
@@ -836,7 +916,10 @@ hipError_t launch_ep_dispatch(int T, int H, int K, int E, int P, const uint16_t*
     }
     if (dev_status) hipLaunchKernelGGL(merge_status, dim3(1), dim3(1), 0, stream, words, P, dev_status);
     if (T > 0) {
+        hipLaunchKernelGGL(ep_prefix, dim3(1), dim3(kBlock), 0, stream, counts, P, capacity, before, fits, dev_status);
         a.counts = counts;
+        a.before = before;
+        a.fits = fits;
         a.recv_pos = recv_pos;
         a.status = dev_status;
         a.capacity = capacity;
@@ -887,6 +970,92 @@ hipError_t launch_ep_combine(int T, int H, int K, int E, int P, const uint16_t* 
 bool ep_launch_fits(int T, int H, int P) {
     const uint64_t slices = std::max(row_slices(H, kPackUnroll), row_slices(H, kUnpackUnroll));
     return static_cast<uint64_t>(P) * T * slices < (uint64_t(1) << 31);
+}
+
+uint64_t ep_dispatch_dedup_workspace_bytes(int T, int P) {
+    const uint64_t Pu = static_cast<uint64_t>(P);
+    return Pu * pack_dedup_workspace_bytes(T, P) + align256(4 * Pu * Pu) + align256(4 * Pu) + ep_tail_bytes(P);
+}
+
+hipError_t launch_ep_dispatch_dedup(int T, int H, int K, int E, int P, const uint16_t* const* x,
+                                    const int32_t* const* ids, uint16_t* const* recv, int64_t capacity,
+                                    int32_t* counts, int32_t* recv_row, int32_t* dev_status, void* workspace,
+                                    hipStream_t stream) {
+    const uint64_t Pu = static_cast<uint64_t>(P);
+    const uint64_t per = pack_dedup_workspace_bytes(T, P);
+    const int ntiles = (T + kWave - 1) / kWave;
+    const uint64_t nt = static_cast<uint64_t>(ntiles);
+    char* ws = static_cast<char*>(workspace);
+    int32_t* dest_off = reinterpret_cast<int32_t*>(ws + Pu * per);  // [P][P]
+    int32_t* words = reinterpret_cast<int32_t*>(ws + Pu * per + align256(4 * Pu * Pu));
+    char* tail = ws + Pu * per + align256(4 * Pu * Pu) + align256(4 * Pu);
+    int64_t* before = reinterpret_cast<int64_t*>(tail);
+    int32_t* fits = reinterpret_cast<int32_t*>(tail + align256(8 * Pu * Pu));
+    EpArgs a{};
+    (void)hipGetLastError();
+    for (int p = 0; p < P; ++p) {
+        char* base = ws + p * per;
+        int32_t* tile_base = reinterpret_cast<int32_t*>(base);
+        int32_t* lrank = reinterpret_cast<int32_t*>(base + align256(4 * nt * Pu));
+        int32_t* tile_err = reinterpret_cast<int32_t*>(base + align256(4 * nt * Pu) + align256(4 * uint64_t(T) * Pu));
+        if (ntiles > 0)
+            hipLaunchKernelGGL(dedup_tiles, dim3(ntiles), dim3(kBlock), 0, stream, T, K, E, P, ids[p], tile_base, lrank,
+                               tile_err);
+        hipLaunchKernelGGL(dedup_scan, dim3(1), dim3(kScanThreads), 0, stream, ntiles, P, tile_base, tile_err,
+                           counts + p * P, dest_off + p * P, words + p);
+        a.x[p] = reinterpret_cast<const char*>(x[p]);
+        a.dst[p] = reinterpret_cast<char*>(recv[p]);
+        a.tile_base[p] = tile_base;
+        a.lrank[p] = lrank;
+        a.dest_off[p] = dest_off + p * P;
+    }
+    if (dev_status) hipLaunchKernelGGL(merge_status, dim3(1), dim3(1), 0, stream, words, P, dev_status);
+    if (T > 0) {
+        hipLaunchKernelGGL(ep_prefix, dim3(1), dim3(kBlock), 0, stream, counts, P, capacity, before, fits, dev_status);
+        a.counts = counts;
+        a.before = before;
+        a.fits = fits;
+        a.recv_pos = recv_row;
+        a.status = dev_status;
+        a.capacity = capacity;
+        a.T = T;
+        a.H = H;
+        a.K = K;
+        a.E = E;
+        a.P = P;
+        a.slices = row_slices(H, kDedupUnroll);
+        const uint64_t waves = Pu * static_cast<uint64_t>(T) * a.slices;
+        const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
+        hipLaunchKernelGGL((ep_dedup_dispatch_rows<kDedupUnroll, kPackNtLoad, kPackNtStore>), grid, dim3(kBlock), 0,
+                           stream, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_ep_combine_dedup(int T, int H, int P, const uint16_t* const* y, int64_t capacity,
+                                   const int32_t* recv_row, uint16_t* const* out, int32_t* dev_status,
+                                   hipStream_t stream) {
+    EpArgs a{};
+    for (int p = 0; p < P; ++p) {
+        a.x[p] = reinterpret_cast<const char*>(y[p]);
+        a.dst[p] = reinterpret_cast<char*>(out[p]);
+    }
+    a.recv_pos = const_cast<int32_t*>(recv_row);  // read only here
+    a.status = dev_status;
+    a.capacity = capacity;
+    a.T = T;
+    a.H = H;
+    a.P = P;
+    a.slices = row_slices(H, kUnpackUnroll);
+    (void)hipGetLastError();
+    if (dev_status) hipLaunchKernelGGL(set_status, dim3(1), dim3(1), 0, stream, dev_status);
+    if (T > 0) {
+        const uint64_t waves = static_cast<uint64_t>(P) * T * a.slices;
+        const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
+        hipLaunchKernelGGL((ep_dedup_combine_rows<kUnpackUnroll, kUnpackNtLoad, kUnpackNtStore>), grid, dim3(kBlock),
+                           0, stream, a);
+    }
+    return hipGetLastError();
 }
 
 }  // namespace purlin

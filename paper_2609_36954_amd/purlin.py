@@ -111,6 +111,9 @@ def lib():
     L.purlin_ep_dispatch_workspace_size.argtypes = [i32, i32, i32, i32, _c_u64p]
     L.purlin_ep_dispatch.argtypes = [i32] * 5 + [_pa, _pa, _pa, u64, _vp, _vp, _vp, _vp, u64, _vp]
     L.purlin_ep_combine.argtypes = [i32] * 5 + [_pa, u64, _pa, _vp, _pa, _pa, _vp, _vp]
+    L.purlin_ep_dispatch_dedup_workspace_size.argtypes = [i32, i32, _c_u64p]
+    L.purlin_ep_dispatch_dedup.argtypes = [i32] * 5 + [_pa, _pa, _pa, u64, _vp, _vp, _vp, _vp, u64, _vp]
+    L.purlin_ep_combine_dedup.argtypes = [i32] * 3 + [_pa, u64, _vp, _pa, _vp, _vp]
     L.purlin_status_string.argtypes = [i32]
     L.purlin_status_string.restype = ctypes.c_char_p
     L.purlin_version.argtypes = []
@@ -119,7 +122,8 @@ def lib():
                  "purlin_plan_info", "purlin_plan_descriptors", "purlin_plan_items",
                  "purlin_exec", "purlin_pack_workspace_size", "purlin_pack", "purlin_unpack",
                  "purlin_pack_dedup_workspace_size", "purlin_pack_dedup", "purlin_unpack_dedup",
-                 "purlin_ep_dispatch_workspace_size", "purlin_ep_dispatch", "purlin_ep_combine"):
+                 "purlin_ep_dispatch_workspace_size", "purlin_ep_dispatch", "purlin_ep_combine",
+                 "purlin_ep_dispatch_dedup_workspace_size", "purlin_ep_dispatch_dedup", "purlin_ep_combine_dedup"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -626,4 +630,74 @@ def purlin_ep_combine(ys, idss, recv_pos, gatess, E, outs=None, dev_status=None,
                                  _ptr_array(idss), _ptr(recv_pos), _ptr_array(gatess), _ptr_array(outs),
                                  _ptr(dev_status), _stream_handle(stream))
     _check(st, "purlin_ep_combine")
+    return outs
+
+
+def purlin_ep_dispatch_dedup_workspace_size(T, P):
+    b = ctypes.c_uint64()
+    _check(lib().purlin_ep_dispatch_dedup_workspace_size(int(T), int(P), ctypes.byref(b)),
+           "purlin_ep_dispatch_dedup_workspace_size")
+    return b.value
+
+
+def purlin_ep_dispatch_dedup(xs, idss, E, recv, counts=None, recv_row=None, workspace=None, dev_status=None,
+                             stream=None):
+    """De-duplicated dispatch over P = len(xs) ranks in one pass: one row per
+    token and owning rank, written straight into the receive buffers.
+
+    Returns a dict with ``counts`` (int32 [P*P]) and ``recv_row`` (int32
+    [P, T, P], -1 where a token has no expert on a rank)."""
+    import torch
+
+    P = len(xs)
+    if len(idss) != P or len(recv) != P:
+        raise PurlinError(PURLIN_ERR_INVALID, "need P token matrices, P id matrices and P receive buffers")
+    T, H = xs[0].shape
+    K = idss[0].shape[1]
+    for x, ids in zip(xs, idss):
+        _require_cuda(x, "x", 2)
+        _require_cuda(ids, "ids", 4)
+        if tuple(x.shape) != (T, H) or tuple(ids.shape) != (T, K):
+            raise PurlinError(PURLIN_ERR_INVALID, "every rank needs x [T, H] and ids [T, K]")
+    capacity = _rows_capacity(recv, H, "recv")
+    dev = xs[0].device
+    if counts is None:
+        counts = torch.empty(P * P, dtype=torch.int32, device=dev)
+    if recv_row is None:
+        recv_row = torch.empty((P, T, P), dtype=torch.int32, device=dev)
+    _require_cuda(counts, "counts", 4)
+    _require_cuda(recv_row, "recv_row", 4)
+    if counts.numel() < P * P or recv_row.numel() < P * T * P:
+        raise PurlinError(PURLIN_ERR_INVALID, "counts needs P*P entries and recv_row P*T*P")
+    wsb = purlin_ep_dispatch_dedup_workspace_size(T, P)
+    if workspace is None:
+        workspace = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+    st = lib().purlin_ep_dispatch_dedup(int(T), int(H), int(K), int(E), int(P), _ptr_array(xs), _ptr_array(idss),
+                                        _ptr_array(recv), int(capacity), _ptr(counts), _ptr(recv_row),
+                                        _ptr(dev_status), _ptr(workspace),
+                                        int(workspace.numel() * workspace.element_size()), _stream_handle(stream))
+    _check(st, "purlin_ep_dispatch_dedup")
+    return {"counts": counts, "recv_row": recv_row}
+
+
+def purlin_ep_combine_dedup(ys, recv_row, outs=None, dev_status=None, stream=None):
+    """Its combine: rank-order sum of every rank's partial output row."""
+    import torch
+
+    P = len(ys)
+    T = recv_row.shape[1]
+    H = ys[0].shape[-1]
+    capacity = _rows_capacity(ys, H, "y")
+    _require_cuda(recv_row, "recv_row", 4)
+    if recv_row.numel() < P * T * P:
+        raise PurlinError(PURLIN_ERR_INVALID, "recv_row needs P*T*P entries")
+    if outs is None:
+        outs = [torch.empty((T, H), dtype=ys[0].dtype, device=ys[0].device) for _ in range(P)]
+    for o in outs:
+        _require_cuda(o, "out", 2)
+        if o.numel() < T * H:
+            raise PurlinError(PURLIN_ERR_INVALID, "every output needs T*H elements")
+    st = lib().purlin_ep_combine_dedup(int(T), int(H), int(P), _ptr_array(ys), int(capacity), _ptr(recv_row),
+                                       _ptr_array(outs), _ptr(dev_status), _stream_handle(stream))
+    _check(st, "purlin_ep_combine_dedup")
     return outs

@@ -309,8 +309,9 @@ def test_ep_dispatch_workspace_size():
     per = ctypes.c_uint64()
     assert L.purlin_pack_workspace_size(4096, 8, 256, ctypes.byref(per)) == 0
     assert L.purlin_ep_dispatch_workspace_size(4096, 8, 256, 8, ctypes.byref(b)) == 0
-    # every rank's pack workspace, then P x P offsets, P x E expert counts and P status words (256-byte pieces)
-    assert b.value == 8 * per.value + 256 + 8192 + 256
+    # every rank's pack workspace, then P x P offsets, P x E expert counts, P status words, the P x P
+    # int64 receive prefix and the capacity verdict (256-byte pieces)
+    assert b.value == 8 * per.value + 256 + 8192 + 256 + 512 + 256
     for args in ((4096, 8, 256, 0), (4096, 8, 256, 17), (4096, 8, 256, 3), (-1, 8, 256, 8), (4096, 0, 256, 8)):
         assert L.purlin_ep_dispatch_workspace_size(*args, ctypes.byref(b)) == INVALID
 
@@ -330,3 +331,40 @@ def _ep_combine(T=64, H=64, K=2, E=8, P=2, y=(0x1000000, 0x2000000), capacity=25
 ])
 def test_ep_combine_argument_validation(kw):
     assert _ep_combine(**kw) == INVALID
+
+
+@pytest.mark.parametrize("kw", [dict(P=0), dict(E=8, P=3), dict(capacity=1 << 31), dict(recv_pos=None),
+                                dict(wsb=16), dict(recv=(0x1000000, 0x1000000))])
+def test_ep_dispatch_dedup_argument_validation(kw):
+    a = dict(T=64, H=64, K=2, E=8, P=2, x=(0x100000, 0x200000), ids=(0x10000, 0x20000),
+             recv=(0x1000000, 0x2000000), capacity=256, counts=0x3000, recv_pos=0x4000, status=None,
+             ws=0x800000, wsb=1 << 20)
+    a.update(kw)
+    st = PL.lib().purlin_ep_dispatch_dedup(a["T"], a["H"], a["K"], a["E"], a["P"], _arr(*a["x"]), _arr(*a["ids"]),
+                                           _arr(*a["recv"]), a["capacity"], a["counts"], a["recv_pos"], a["status"],
+                                           a["ws"], a["wsb"], None)
+    assert st == INVALID
+
+
+@pytest.mark.parametrize("kw", [dict(P=0), dict(P=17), dict(H=0), dict(capacity=1 << 31), dict(recv_row=None),
+                                dict(out=(0x100000, 0x100000)), dict(out=(0x100000, 0x1000000))])
+def test_ep_combine_dedup_argument_validation(kw):
+    a = dict(T=64, H=64, P=2, y=(0x1000000, 0x2000000), capacity=256, recv_row=0x4000, out=(0x100000, 0x200000))
+    a.update(kw)
+    st = PL.lib().purlin_ep_combine_dedup(a["T"], a["H"], a["P"], _arr(*a["y"]), a["capacity"], a["recv_row"],
+                                          _arr(*a["out"]), None, None)
+    assert st == INVALID
+
+
+def test_ep_dispatch_dedup_workspace_size():
+    L = PL.lib()
+    b = ctypes.c_uint64()
+    per = ctypes.c_uint64()
+    assert L.purlin_pack_dedup_workspace_size(4096, 8, ctypes.byref(per)) == 0
+    assert L.purlin_ep_dispatch_dedup_workspace_size(4096, 8, ctypes.byref(b)) == 0
+    # every rank's dedup pack workspace, then P x P offsets, P status words, the P x P int64 receive prefix
+    # and the capacity verdict (256-byte pieces)
+    assert b.value == 8 * per.value + 256 + 256 + 512 + 256
+    for args in ((4096, 0), (4096, 17), (-1, 8)):
+        assert L.purlin_ep_dispatch_dedup_workspace_size(*args, ctypes.byref(b)) == INVALID
+    assert L.purlin_ep_dispatch_dedup_workspace_size(4096, 8, None) == INVALID

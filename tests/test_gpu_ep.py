@@ -449,3 +449,85 @@ def test_ep_one_pass_in_a_graph():
         want = oracle.ep_combine(d["recv"], ids_np, d["recv_pos"], gates_np, E, P)
         for p in range(P):
             assert_bits_equal(to_host(outs[p], np.uint16).reshape(T, H), want[p], "bf16", f"replay {seed} rank {p}")
+
+
+@pytest.mark.parametrize("P,T,H,K,E,seed", [
+    (1, 40, 32, 2, 4, 0), (2, 50, 24, 2, 8, 1), (3, 70, 7, 3, 9, 2), (4, 65, 136, 4, 16, 3),
+    (8, 200, 520, 8, 64, 5), (16, 64, 64, 4, 32, 6), (4, 0, 64, 2, 8, 7),
+])
+def test_ep_dedup_one_pass_matches_oracle(P, T, H, K, E, seed):
+    xs_np, idss_np, _ = _ep_case(P, T, H, K, E, seed)
+    want = oracle.ep_dispatch_dedup(xs_np, idss_np, E, P)
+    cap = max(1, int(want["counts"].sum(axis=0).max()) + 2)
+    recv = [Guarded(cap * H * 2, torch.int16) for _ in range(P)]
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    idss = [to_device(i) for i in idss_np]
+    got = PL.purlin_ep_dispatch_dedup([to_device(x) for x in xs_np], idss, E, [g.t.view(cap, H) for g in recv],
+                                      dev_status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    assert np.array_equal(to_host(got["counts"], np.int32).reshape(P, P), want["counts"])
+    if T:
+        assert np.array_equal(to_host(got["recv_row"], np.int32).reshape(P, T, P), want["recv_row"])
+    for r in range(P):
+        assert recv[r].intact()
+        host = to_host(recv[r].t, np.uint16).reshape(cap, H)
+        n = len(want["recv"][r])
+        assert np.array_equal(host[:n], want["recv"][r]), f"receive buffer {r}"
+        assert np.all(host[n:].view(np.uint8) == CANARY)
+    ys_np = [to_host(recv[r].t, np.uint16).reshape(cap, H) ^ np.uint16(r + 1) for r in range(P)]  # partial outputs
+    outs = [Guarded(T * H * 2, torch.int16) for _ in range(P)]
+    PL.purlin_ep_combine_dedup([to_device(y) for y in ys_np], got["recv_row"], outs=[o.t.view(T, H) for o in outs],
+                               dev_status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    want_out = oracle.ep_combine_dedup(ys_np, want["recv_row"], P)
+    for p in range(P):
+        assert outs[p].intact()
+        assert_bits_equal(to_host(outs[p].t, np.uint16).reshape(T, H), want_out[p], "bf16", f"combined rank {p}")
+
+
+def test_ep_dedup_one_pass_over_capacity_writes_nothing():
+    P, T, H, K, E = 4, 64, 64, 4, 8
+    xs_np, idss_np, _ = _ep_case(P, T, H, K, E, 13)
+    cap = int(oracle.ep_dispatch_dedup(xs_np, idss_np, E, P)["counts"].sum(axis=0).max()) - 1
+    recv = [Guarded(cap * H * 2, torch.int16) for _ in range(P)]
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    PL.purlin_ep_dispatch_dedup([to_device(x) for x in xs_np], [to_device(i) for i in idss_np], E,
+                                [g.t.view(cap, H) for g in recv], dev_status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 1
+    for g in recv:
+        assert g.intact() and bool(torch.all(g.t.view(torch.uint8) == CANARY).item())
+
+
+def test_ep_dedup_one_pass_full_size_equals_two_step_path():
+    P, T, H, K, E = 8, 4096, 7168, 8, 256
+    xs_np, ids_np, _ = _rank_inputs(P, T, H, K, E, seed=4)
+    xs = [to_device(x) for x in xs_np]
+    ids = [to_device(i) for i in ids_np]
+    cap = P * T * min(K, P)
+    counts = torch.zeros((P, P), dtype=torch.int32, device="cuda")
+    packs = [PL.purlin_pack_dedup(xs[p], ids[p], E, P, out=dict(dest_counts=counts[p])) for p in range(P)]
+    fwd = PL.purlin_plan_v("alltoallv", P, T * min(K, P) * H, "bf16", 1 << 20, unit=H, out_capacity=cap * H)
+    recv2 = [torch.empty(cap * H, dtype=torch.int16, device="cuda") for _ in range(P)]
+    fwd.exec_v([pk["packed"].view(-1) for pk in packs], recv2, counts.view(-1))
+    recv1 = [torch.empty((cap, H), dtype=torch.int16, device="cuda") for _ in range(P)]
+    got = PL.purlin_ep_dispatch_dedup(xs, ids, E, recv1)
+    torch.cuda.synchronize()
+    m = to_host(counts, np.int32).reshape(P, P)
+    assert np.array_equal(to_host(got["counts"], np.int32).reshape(P, P), m)
+    for r in range(P):
+        n = int(m[:, r].sum())
+        assert torch.equal(recv1[r][:n].reshape(-1), recv2[r][: n * H]), f"receive buffer {r}"
+        _mark(recv1[r][:n], r)
+        _mark(recv2[r][: n * H], r)
+    bwd = PL.purlin_plan_v("alltoallv", P, cap * H, "bf16", 1 << 20, unit=H, out_capacity=T * min(K, P) * H,
+                           counts_transposed=True)
+    back = [torch.empty(T * min(K, P) * H, dtype=torch.int16, device="cuda") for _ in range(P)]
+    bwd.exec_v(recv2, back, counts.view(-1))
+    outs2 = [PL.purlin_unpack_dedup(back[p].view(-1, H), packs[p]["row_of"]) for p in range(P)]
+    outs1 = PL.purlin_ep_combine_dedup(recv1, got["recv_row"])
+    torch.cuda.synchronize()
+    for p in range(P):
+        assert torch.equal(outs1[p], outs2[p]), f"combined rank {p}"
