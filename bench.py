@@ -346,8 +346,9 @@ def main():
     latency = None
     if not args.no_latency:
         latency = measure_latency(torch, PL, W, graph_latency_us, args.latency_sweep)
+    ceilings = None if args.no_extra else measure_ceilings(torch, PL)
     return emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, per_op, latency, plan_ms,
-                dev_name, src_hash, extra)
+                dev_name, src_hash, extra, ceilings)
 
 
 def measure_extra_ops(torch, PL, ins, rs_out, ag_out, P, N, s, reps=5):
@@ -557,7 +558,40 @@ def measure_ep(torch, PL, W, P, T, H, E, K, reps=5):
     return result
 
 
+def measure_ceilings(torch, PL, nbytes=1 << 30, reps=20):
+    """Plain device-to-device copies of 1 GiB on the same GPU, for scale:
+    hipMemcpyAsync (torch's same-device tensor copy) and the library's plain
+    16-byte copy kernel (purlin_stream_copy).  GB/s = read + written bytes
+    / time; event-timed on the current stream after 3 untimed copies."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(7)
+    dst = torch.empty_like(src)
+    out = {}
+    for name, fn in (("hip_memcpy_dtod", lambda: dst.copy_(src)),
+                     ("plain_dwordx4_copy_kernel", lambda: PL.purlin_stream_copy(dst, src))):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        out[name] = {"avg_us": round(us, 1), "GBps": round(2 * nbytes / (us * 1e-6) / 1e9, 1),
+                     "frac_of_hbm_peak": round(2 * nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+    out["bytes_copied"] = nbytes
+    del src, dst
+    return out
+
+
 def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
+    c1 = W.COLLECTIVE_CONFIGS[1]
+    in1 = [to_dev(torch, a) for a in W.collective_inputs(c1)]
+    out1 = [torch.empty(c1.count, dtype=torch.float32, device="cuda") for _ in range(c1.P)]
+    ar1 = PL.Plan("allreduce", c1.P, c1.count, "fp32", c1.chunk)
+    lat1_us = graph_latency_us(ar1, in1, out1)
+    del in1, out1
     c2 = W.COLLECTIVE_CONFIGS[2]
     lat_in = [to_dev(torch, a) for a in W.collective_inputs(c2)]
     lat_out = [torch.empty(c2.count, dtype=torch.int16, device="cuda") for _ in range(c2.P)]
@@ -584,6 +618,12 @@ def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
         torch.cuda.synchronize()
         singles.append(e0.elapsed_time(e1) * 1e3)
     latency = {
+        "allreduce_p4_fp32_262144": {
+            "us": round(lat1_us, 2),
+            "GBps_min": round(collective_bytes("allreduce", c1.P, c1.count, 4) / (lat1_us * 1e-6) / 1e9, 1),
+            "algbw_GBps": round(c1.count * 4 / (lat1_us * 1e-6) / 1e9, 1),
+            "timing": "graph of 128 calls, 8 replays after one warm-up replay (time / 1024)",
+        },
         "allreduce_p8_bf16_128x8192": {
             "us": round(lat_us, 2),
             "GBps_min": round(collective_bytes("allreduce", c2.P, c2.count, 2) / (lat_us * 1e-6) / 1e9, 1),
@@ -608,7 +648,7 @@ def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
 
 
 def emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, per_op, latency, plan_ms, dev_name,
-         src_hash, extra):
+         src_hash, extra, ceilings=None):
     result = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -637,6 +677,7 @@ def emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, 
         "ops": per_op,
         "latency_us": latency,
         "other_ops_256MiB_per_rank": extra,
+        "copy_ceilings": ceilings,
         "plan_ms": round(plan_ms, 3),
         "device": dev_name,
         "kernel_source_hash": src_hash,
@@ -688,6 +729,7 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
     Ts = T
     H = x_np.shape[1]
     dt, pw = median_time(lambda: oracle.pack(x_np, ids_np, E, P))
+    t_pack_single = dt
     t_total += dt
     bytes_total += pack_bytes(T, H, K, E, P)
     pos_want = pw["pos"]
@@ -705,6 +747,53 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
         cores = len(os.sched_getaffinity(0))
     except AttributeError:
         cores = os.cpu_count()
+
+    # (ii) the same oracle functions over element blocks in a thread pool, one
+    # thread per core this process may run on (numpy releases the GIL inside
+    # its loops).  The per-element order is unchanged, so the results are the
+    # single-threaded ones bit for bit.  Pack's positions come from a scan over
+    # all tokens, so pack runs single-threaded in both.
+    from concurrent.futures import ThreadPoolExecutor
+
+    from oracle.collectives import rank_order_sum
+
+    nthr = max(1, min(cores, 64))
+    nblk = 4 * nthr
+
+    def cuts(n):
+        return [(n * j // nblk, n * (j + 1) // nblk) for j in range(nblk)]
+
+    def pooled(jobs):
+        with ThreadPoolExecutor(nthr) as ex:
+            return list(ex.map(lambda f: f(), jobs))
+
+    rs_jobs = [(r, lo, hi) for r in range(P) for lo, hi in cuts(m)]
+    dt_rs, rs_blocks = median_time(lambda: pooled(
+        [lambda r=r, lo=lo, hi=hi: rank_order_sum([sub[p][r * m + lo:r * m + hi] for p in range(P)], "bf16")
+         for r, lo, hi in rs_jobs]))
+    thr_ok = all(np.array_equal(b, rs_want[r][lo:hi]) for (r, lo, hi), b in zip(rs_jobs, rs_blocks))
+    del rs_blocks
+    ag_jobs = cuts(m)
+    dt_ag, ag_blocks = median_time(lambda: pooled(
+        [lambda lo=lo, hi=hi: oracle.all_gather([rs_want[p][lo:hi] for p in range(P)], "bf16") for lo, hi in ag_jobs]))
+    for (lo, hi), b in zip(ag_jobs, ag_blocks):
+        for r in (0, P - 1):
+            thr_ok &= bool(np.array_equal(b[r], ag_want[r].reshape(P, m)[:, lo:hi].reshape(-1)))
+    del ag_blocks
+    un_jobs = cuts(Ts)
+    dt_un, un_blocks = median_time(lambda: pooled(
+        [lambda lo=lo, hi=hi: oracle.unpack(y_np, pos_want[lo:hi], g_np[lo:hi]) for lo, hi in un_jobs]))
+    thr_ok &= all(np.array_equal(b, cw[lo:hi]) for (lo, hi), b in zip(un_jobs, un_blocks))
+    del un_blocks
+    t_pack = t_pack_single
+    t_threaded = dt_rs + dt_ag + t_pack + dt_un
+
+    def sha(arrays):
+        h = hashlib.sha256()
+        for a in arrays:
+            h.update(np.ascontiguousarray(a).view(np.uint8).reshape(-1))
+        return h.hexdigest()
+
     return {
         "value": round(bytes_total / t_total / 1e9, 3),
         "unit": "GB/s",
@@ -715,10 +804,39 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
         "seconds": round(t_total, 3),
         "cpu_seconds_spent": round(time.perf_counter() - t_start, 1),
         "host_cores_available": cores,
-        "cpu": platform.processor() or platform.machine(),
+        "os_cpu_count": os.cpu_count(),
+        "cpu": cpu_model(),
         "numpy": np.__version__,
         "gpu_matches_oracle_on_sample": ok,
+        "threaded": {
+            "value": round(bytes_total / t_threaded / 1e9, 3),
+            "unit": "GB/s",
+            "cores": nthr,
+            "seconds": round(t_threaded, 3),
+            "how": f"ReduceScatter, AllGather and combine over {nblk} element blocks each in a pool of {nthr} "
+                   "threads; pack single-threaded (its positions need a scan over all tokens); median of 3",
+            "identical_to_single_threaded": bool(thr_ok),
+        },
+        "input_sha256": {
+            "rs_inputs_8_ranks": sha(ins_np),
+            "moe_x": sha([x_np]),
+            "moe_ids": sha([ids_np]),
+            "moe_y": sha([y_np]),
+            "moe_gates": sha([g_np]),
+        },
     }
+
+
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo where there is one)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
 
 if __name__ == "__main__":

@@ -477,6 +477,17 @@ PURLIN_API purlin_status purlin_ep_combine_dedup(int T, int H, int P, const void
                                                  const int32_t* recv_row, void* const* out, int32_t* dev_status,
                                                  void* stream);
 
+/* Plain device-to-device copy of `bytes` bytes with no descriptors (each
+ * lane moves 16-byte vectors; one 256-thread workgroup copies 16 KiB).  Not
+ * a step of the method: it is the reference stream against which the
+ * executor's copies are measured.
+ *   dst, src  device pointers, 16-byte aligned, ranges disjoint
+ *   bytes     a multiple of 16; 0 is a no-op
+ * Asynchronous on `stream`.  PURLIN_ERR_INVALID: a null or misaligned
+ * pointer (bytes > 0), bytes not a multiple of 16, overlapping ranges;
+ * PURLIN_ERR_DEVICE: the launch failed. */
+PURLIN_API purlin_status purlin_stream_copy(void* dst, const void* src, uint64_t bytes, void* stream);
+
 /* Static text for a status code ("unknown status" for others). */
 PURLIN_API const char* purlin_status_string(purlin_status status);
 

@@ -466,6 +466,15 @@ purlin_status purlin_unpack(int T, int H, int K, const void* y, const int32_t* p
     return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
 }
 
+purlin_status purlin_stream_copy(void* dst, const void* src, uint64_t bytes, void* stream) {
+    if (bytes % 16) return PURLIN_ERR_INVALID;
+    if (bytes == 0) return PURLIN_OK;
+    if (!dst || !src || !aligned16(dst) || !aligned16(src)) return PURLIN_ERR_INVALID;
+    if (overlaps(dst, bytes, src, bytes)) return PURLIN_ERR_INVALID;
+    const hipError_t e = purlin::launch_stream_copy(dst, src, bytes, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
 const char* purlin_status_string(purlin_status status) {
     switch (status) {
         case PURLIN_OK: return "ok";

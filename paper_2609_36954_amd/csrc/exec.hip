@@ -698,6 +698,41 @@ hipError_t launch_v(purlin_op op, const purlin_desc* items, uint64_t n, int P, p
     return hipGetLastError();
 }
 
+namespace {
+
+// A plain 16-byte copy with no descriptors: each lane moves kCopyUnroll
+// vectors 256 lanes apart, one workgroup 16 KiB.  It is the reference
+// stream for the executor's copies.
+__global__ __launch_bounds__(kBlock) void stream_copy(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
+                                                     uint64_t nvec) {
+    const uint64_t base = uint64_t(blockIdx.x) * (kBlock * kCopyUnroll) + threadIdx.x;
+    u32x4 v[kCopyUnroll];
+#pragma unroll
+    for (int u = 0; u < kCopyUnroll; ++u) {
+        const uint64_t i = base + uint64_t(u) * kBlock;
+        if (i < nvec) v[u] = src[i];
+    }
+#pragma unroll
+    for (int u = 0; u < kCopyUnroll; ++u) {
+        const uint64_t i = base + uint64_t(u) * kBlock;
+        if (i < nvec) dst[i] = v[u];
+    }
+}
+
+}  // namespace
+
+hipError_t launch_stream_copy(void* dst, const void* src, uint64_t bytes, hipStream_t stream) {
+    const uint64_t nvec = bytes / 16;
+    if (nvec == 0) return hipSuccess;
+    const uint64_t per_block = uint64_t(kBlock) * kCopyUnroll;
+    const uint64_t blocks = (nvec + per_block - 1) / per_block;
+    if (blocks > 0xffffffffull) return hipErrorInvalidValue;
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(stream_copy, dim3(static_cast<uint32_t>(blocks)), dim3(kBlock), 0, stream,
+                       static_cast<const u32x4*>(src), static_cast<u32x4*>(dst), nvec);
+    return hipGetLastError();
+}
+
 hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
                         uint32_t src_step, bool nt_load, bool nt_store, purlin_dtype dtype, void* const* bufs,
                         int nbufs, hipStream_t stream) {

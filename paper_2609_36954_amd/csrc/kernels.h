@@ -14,6 +14,9 @@ namespace purlin {
 // of consume op `kind`.  The items of a REDUCE phase all sum the same `nsrc`
 // sources bufs[src_buf + p * src_step].  `bufs` holds the 2P buffer pointers.
 // nt_load / nt_store select non-temporal global loads / stores.
+// Plain copy of `bytes` (a multiple of 16) from src to dst.
+hipError_t launch_stream_copy(void* dst, const void* src, uint64_t bytes, hipStream_t stream);
+
 hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
                         uint32_t src_step, bool nt_load, bool nt_store, purlin_dtype dtype, void* const* bufs,
                         int nbufs, hipStream_t stream);

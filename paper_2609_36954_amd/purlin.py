@@ -114,6 +114,7 @@ def lib():
     L.purlin_ep_dispatch_dedup_workspace_size.argtypes = [i32, i32, _c_u64p]
     L.purlin_ep_dispatch_dedup.argtypes = [i32] * 5 + [_pa, _pa, _pa, u64, _vp, _vp, _vp, _vp, u64, _vp]
     L.purlin_ep_combine_dedup.argtypes = [i32] * 3 + [_pa, u64, _vp, _pa, _vp, _vp]
+    L.purlin_stream_copy.argtypes = [_vp, _vp, u64, _vp]
     L.purlin_status_string.argtypes = [i32]
     L.purlin_status_string.restype = ctypes.c_char_p
     L.purlin_version.argtypes = []
@@ -123,7 +124,8 @@ def lib():
                  "purlin_exec", "purlin_pack_workspace_size", "purlin_pack", "purlin_unpack",
                  "purlin_pack_dedup_workspace_size", "purlin_pack_dedup", "purlin_unpack_dedup",
                  "purlin_ep_dispatch_workspace_size", "purlin_ep_dispatch", "purlin_ep_combine",
-                 "purlin_ep_dispatch_dedup_workspace_size", "purlin_ep_dispatch_dedup", "purlin_ep_combine_dedup"):
+                 "purlin_ep_dispatch_dedup_workspace_size", "purlin_ep_dispatch_dedup", "purlin_ep_combine_dedup",
+                 "purlin_stream_copy"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -701,3 +703,16 @@ def purlin_ep_combine_dedup(ys, recv_row, outs=None, dev_status=None, stream=Non
                                        _ptr_array(outs), _ptr(dev_status), _stream_handle(stream))
     _check(st, "purlin_ep_combine_dedup")
     return outs
+
+
+def purlin_stream_copy(dst, src, stream=None):
+    """Plain copy of ``src``'s bytes into ``dst`` (the reference stream the
+    executor's copies are measured against; not a step of the method)."""
+    _require_cuda(src, "src")
+    _require_cuda(dst, "dst")
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < nbytes:
+        raise PurlinError(PURLIN_ERR_INVALID, "dst is smaller than src")
+    st = lib().purlin_stream_copy(_ptr(dst), _ptr(src), int(nbytes), _stream_handle(stream))
+    _check(st, "purlin_stream_copy")
+    return dst

@@ -368,3 +368,19 @@ def test_ep_dispatch_dedup_workspace_size():
     for args in ((4096, 0), (4096, 17), (-1, 8)):
         assert L.purlin_ep_dispatch_dedup_workspace_size(*args, ctypes.byref(b)) == INVALID
     assert L.purlin_ep_dispatch_dedup_workspace_size(4096, 8, None) == INVALID
+
+
+@pytest.mark.parametrize("dst,src,nbytes", [
+    (0x100000, 0x200000, 24),          # not a multiple of 16
+    (None, 0x200000, 64),              # null destination
+    (0x100000, None, 64),              # null source
+    (0x100008, 0x200000, 64),          # misaligned destination
+    (0x100000, 0x200008, 64),          # misaligned source
+    (0x100000, 0x100000 + 32, 64),     # overlapping ranges
+])
+def test_stream_copy_argument_validation(dst, src, nbytes):
+    assert PL.lib().purlin_stream_copy(dst, src, nbytes, None) == INVALID
+
+
+def test_stream_copy_of_nothing_is_a_no_op():
+    assert PL.lib().purlin_stream_copy(None, None, 0, None) == 0

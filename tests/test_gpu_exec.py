@@ -420,3 +420,15 @@ def test_repeated_runs_are_bit_identical(op):
         torch.cuda.synchronize()
         for r in range(P):
             assert torch.equal(outs[r], first[r]), f"{op} rank {r} differs between runs"
+
+
+@pytest.mark.parametrize("nbytes", [16, 16 * 1023, 16 * 1024, 16 * 1024 * 37 + 48, 64 << 20])
+def test_stream_copy_is_a_bit_copy(nbytes):
+    """The plain reference copy: every byte lands, the guard band after the
+    copied range stays untouched (ragged last workgroup included)."""
+    src = torch.randint(0, 256, (nbytes,), dtype=torch.uint8, device="cuda")
+    dst = torch.full((nbytes + 4096,), 0xA5, dtype=torch.uint8, device="cuda")
+    PL.purlin_stream_copy(dst, src)
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:nbytes], src)
+    assert bool((dst[nbytes:] == 0xA5).all())
