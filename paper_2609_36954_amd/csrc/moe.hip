@@ -31,6 +31,7 @@
 #include "kernels.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace purlin {
 namespace {
@@ -43,6 +44,20 @@ constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kScanThreads = 1024;
 constexpr int kMaxExperts = 4096;
 constexpr int kMaxDedupRanks = 16;
+
+// The id matrices of a metadata launch that covers several ranks at once
+// (one grid row or workgroup per rank); a single-rank launch fills entry 0.
+struct RankIds {
+    const int32_t* ids[PURLIN_MAX_RANKS];
+};
+
+// Rank p's copy of a per-rank workspace array: the ranks' workspaces lie
+// `stride` bytes apart (0 for a single rank).
+template <class V>
+__device__ __forceinline__ V* at_rank(V* base, uint64_t stride, int p) {
+    using C = typename std::conditional<std::is_const<V>::value, const char*, char*>::type;
+    return reinterpret_cast<V*>(reinterpret_cast<C>(base) + stride * static_cast<uint64_t>(p));
+}
 
 __device__ __forceinline__ uint32_t wave_index() {
     return __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
@@ -75,13 +90,18 @@ __device__ __forceinline__ uint32_t to_bf16(float f) {
     return (u & 0x7FFFFFFFu) > 0x7F800000u ? quiet_nan : rounded;
 }
 
-__global__ __launch_bounds__(kBlock) void pack_tiles(int T, int K, int E, const int32_t* __restrict__ ids,
-                                                     int32_t* __restrict__ tile_cnt, int32_t* __restrict__ lrank,
-                                                     int32_t* __restrict__ tile_err) {
+__global__ __launch_bounds__(kBlock) void pack_tiles(int T, int K, int E, RankIds rids, int32_t* __restrict__ tile_cnt,
+                                                     int32_t* __restrict__ lrank, int32_t* __restrict__ tile_err,
+                                                     uint64_t stride) {
     extern __shared__ unsigned long long masks[];  // [E]
     __shared__ int32_t tids[kPackTileTokens * 64];  // the tile's ids (K <= 64)
     __shared__ int err;
     const int tile = blockIdx.x;
+    const int rank = blockIdx.y;
+    const int32_t* ids = rids.ids[rank];
+    tile_cnt = at_rank(tile_cnt, stride, rank);
+    lrank = at_rank(lrank, stride, rank);
+    tile_err = at_rank(tile_err, stride, rank);
     const int t0 = tile * kPackTileTokens;
     const int nt = min(kPackTileTokens, T - t0);
     const int n = nt * K;
@@ -122,18 +142,28 @@ __global__ __launch_bounds__(kBlock) void pack_tiles(int T, int K, int E, const 
 // Tile counts of one work unit kept in registers between the two passes.
 constexpr int kScanBatch = 16;
 
+// One workgroup per rank (workgroup p: rank p's tile counts, expert and
+// destination outputs at p*E and p*P, status word p).
 __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int P, int32_t* __restrict__ tile_cnt,
                                                           const int32_t* __restrict__ tile_err,
                                                           int32_t* __restrict__ expert_counts,
                                                           int32_t* __restrict__ expert_offsets,
                                                           int32_t* __restrict__ dest_counts,
                                                           int32_t* __restrict__ dest_offsets,
-                                                          int32_t* __restrict__ dev_status) {
+                                                          int32_t* __restrict__ dev_status, uint64_t stride) {
     __shared__ int32_t partial[kMaxExperts];  // per work unit (expert, tile slice)
     __shared__ int32_t total[kMaxExperts];    // per expert
     __shared__ int32_t offs[kMaxExperts];     // per expert, exclusive prefix
     __shared__ int32_t scan[kScanThreads / kWave];  // wave totals
     const int tid = threadIdx.x;
+    const int rank = blockIdx.x;
+    tile_cnt = at_rank(tile_cnt, stride, rank);
+    tile_err = at_rank(tile_err, stride, rank);
+    expert_counts += static_cast<int64_t>(rank) * E;
+    if (expert_offsets) expert_offsets += static_cast<int64_t>(rank) * E;
+    dest_counts += static_cast<int64_t>(rank) * P;
+    dest_offsets += static_cast<int64_t>(rank) * P;
+    if (dev_status) dev_status += rank;
 
     // error flags first, so their loads overlap the count loads
     int any = 0;
@@ -318,11 +348,16 @@ __global__ __launch_bounds__(kBlock) void pack_rows(int T, int H, int K, int E, 
 //      bases; then destination counts and offsets, and the error flag.
 //   3. dedup_rows: one wavefront per (token, column slice); lane r < P forms
 //      row_of[t, r], and the row is streamed once into each of its rows.
-__global__ __launch_bounds__(kBlock) void dedup_tiles(int T, int K, int E, int P, const int32_t* __restrict__ ids,
+__global__ __launch_bounds__(kBlock) void dedup_tiles(int T, int K, int E, int P, RankIds rids,
                                                       int32_t* __restrict__ tile_cnt, int32_t* __restrict__ lrank,
-                                                      int32_t* __restrict__ tile_err) {
+                                                      int32_t* __restrict__ tile_err, uint64_t stride) {
     __shared__ int32_t tids[kWave * 64];  // the tile's ids (K <= 64), loaded by the whole workgroup
     const int tile = blockIdx.x;
+    const int rank = blockIdx.y;
+    const int32_t* ids = rids.ids[rank];
+    tile_cnt = at_rank(tile_cnt, stride, rank);
+    lrank = at_rank(lrank, stride, rank);
+    tile_err = at_rank(tile_err, stride, rank);
     const int64_t t0 = static_cast<int64_t>(tile) * kWave;
     const int nt = static_cast<int>(min<int64_t>(kWave, T - t0));
     const int n = nt * K;
@@ -360,13 +395,20 @@ __global__ __launch_bounds__(kBlock) void dedup_tiles(int T, int K, int E, int P
     if (lane == 0) tile_err[tile] = eb != 0 ? 1 : 0;
 }
 
+// One workgroup per rank, as pack_scan.
 __global__ __launch_bounds__(kScanThreads) void dedup_scan(int ntiles, int P, int32_t* __restrict__ tile_cnt,
                                                            const int32_t* __restrict__ tile_err,
                                                            int32_t* __restrict__ dest_counts,
                                                            int32_t* __restrict__ dest_offsets,
-                                                           int32_t* __restrict__ dev_status) {
+                                                           int32_t* __restrict__ dev_status, uint64_t stride) {
     __shared__ int32_t totals[kMaxDedupRanks];
     const uint32_t wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
+    const int rank = blockIdx.x;
+    tile_cnt = at_rank(tile_cnt, stride, rank);
+    tile_err = at_rank(tile_err, stride, rank);
+    dest_counts += static_cast<int64_t>(rank) * P;
+    dest_offsets += static_cast<int64_t>(rank) * P;
+    if (dev_status) dev_status += rank;
     int any = 0;
     for (int t = threadIdx.x; t < ntiles; t += kScanThreads) any |= tile_err[t];
     if (wave < static_cast<uint32_t>(P)) {
@@ -573,11 +615,12 @@ struct EpArgs {
 // some receive buffer is too small, no wave writes anything.
 // Once per dispatch, after every rank's metadata: before[p][r] = rows rank r
 // receives from ranks < p, and whether every receive buffer holds what it
-// receives (if not, the status word is set and the rows kernel writes
-// nothing).  One workgroup; P <= 16.
+// receives (if not, the rows kernel writes nothing).  The status word gets
+// 1 if a receive buffer is too small or a rank's routing was invalid (its
+// metadata status word `words[p]`), else 0.  One workgroup; P <= 16.
 __global__ __launch_bounds__(kBlock) void ep_prefix(const int32_t* __restrict__ counts, int P, int64_t capacity,
                                                     int64_t* __restrict__ before, int32_t* __restrict__ fits,
-                                                    int32_t* __restrict__ status) {
+                                                    const int32_t* __restrict__ words, int32_t* __restrict__ status) {
     __shared__ int32_t m[PURLIN_MAX_RANKS * PURLIN_MAX_RANKS];
     for (int i = threadIdx.x; i < P * P; i += kBlock) m[i] = counts[i];
     __syncthreads();
@@ -598,7 +641,9 @@ __global__ __launch_bounds__(kBlock) void ep_prefix(const int32_t* __restrict__ 
             ok = ok && col <= capacity;
         }
         *fits = ok ? 1 : 0;
-        if (!ok && status) atomicOr(status, 1);
+        int any = 0;
+        for (int p = 0; p < P; ++p) any |= words[p];
+        if (status) *status = (any || !ok) ? 1 : 0;
     }
 }
 
@@ -732,12 +777,6 @@ __global__ __launch_bounds__(kBlock) void ep_dedup_combine_rows(EpArgs a) {
 }
 
 // Merges the ranks' routing-error words (contiguous) into the caller's status word.
-__global__ void merge_status(const int32_t* words, int n, int32_t* status) {
-    int any = 0;
-    for (int i = 0; i < n; ++i) any |= words[i];
-    *status = any ? 1 : 0;
-}
-
 // Launch shapes and cache hints, measured on MI355X: the packed rows and
 // the expert outputs are streams far larger than the last-level cache.
 // One 16-byte vector per lane, 1 KiB column slices: many short waves hide
@@ -794,11 +833,13 @@ hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, con
     const int ntiles = (T + kPackTileTokens - 1) / kPackTileTokens;
     (void)hipGetLastError();
     if (ntiles > 0) {
-        hipLaunchKernelGGL(pack_tiles, dim3(ntiles), dim3(kBlock), static_cast<size_t>(E) * 8, stream, T, K, E, ids,
-                           ws.tile_base, ws.lrank, ws.tile_err);
+        RankIds rids{};
+        rids.ids[0] = ids;
+        hipLaunchKernelGGL(pack_tiles, dim3(ntiles), dim3(kBlock), static_cast<size_t>(E) * 8, stream, T, K, E, rids,
+                           ws.tile_base, ws.lrank, ws.tile_err, uint64_t(0));
     }
     hipLaunchKernelGGL(pack_scan, dim3(1), dim3(kScanThreads), 0, stream, ntiles, E, P, ws.tile_base, ws.tile_err,
-                       expert_counts, expert_offsets, dest_counts, dest_offsets, dev_status);
+                       expert_counts, expert_offsets, dest_counts, dest_offsets, dev_status, uint64_t(0));
     if (T > 0) {
         const int slices = row_slices(H, kPackUnroll);
         const uint64_t waves = static_cast<uint64_t>(T) * slices;
@@ -840,11 +881,14 @@ hipError_t launch_pack_dedup(int T, int H, int K, int E, int P, const uint16_t* 
     int32_t* tile_err = reinterpret_cast<int32_t*>(ws + align256(4 * static_cast<uint64_t>(ntiles) * P) +
                                                    align256(4 * static_cast<uint64_t>(T) * P));
     (void)hipGetLastError();
-    if (ntiles > 0)
-        hipLaunchKernelGGL(dedup_tiles, dim3(ntiles), dim3(kBlock), 0, stream, T, K, E, P, ids, tile_base, lrank,
-                           tile_err);
+    if (ntiles > 0) {
+        RankIds rids{};
+        rids.ids[0] = ids;
+        hipLaunchKernelGGL(dedup_tiles, dim3(ntiles), dim3(kBlock), 0, stream, T, K, E, P, rids, tile_base, lrank,
+                           tile_err, uint64_t(0));
+    }
     hipLaunchKernelGGL(dedup_scan, dim3(1), dim3(kScanThreads), 0, stream, ntiles, P, tile_base, tile_err, dest_counts,
-                       dest_offsets, dev_status);
+                       dest_offsets, dev_status, uint64_t(0));
     if (T > 0) {
         const int slices = row_slices(H, kDedupUnroll);
         const uint64_t waves = static_cast<uint64_t>(T) * slices;
@@ -898,15 +942,21 @@ hipError_t launch_ep_dispatch(int T, int H, int K, int E, int P, const uint16_t*
     int32_t* fits = reinterpret_cast<int32_t*>(tail + align256(8 * Pu * Pu));
     const int ntiles = (T + kPackTileTokens - 1) / kPackTileTokens;
     EpArgs a{};
+    RankIds rids{};
     (void)hipGetLastError();
+    // every rank's metadata in one launch of each kind (rank p's workspace
+    // at ws + p * per, its outputs at row p)
+    const PackWorkspace w0 = pack_workspace_carve(ws, T, K, E);
+    for (int p = 0; p < P; ++p) rids.ids[p] = ids[p];
+    if (ntiles > 0)
+        hipLaunchKernelGGL(pack_tiles, dim3(ntiles, P), dim3(kBlock), static_cast<size_t>(E) * 8, stream, T, K, E, rids,
+                           w0.tile_base, w0.lrank, w0.tile_err, per);
+    hipLaunchKernelGGL(pack_scan, dim3(P), dim3(kScanThreads), 0, stream, ntiles, E, P, w0.tile_base, w0.tile_err,
+                       expert_counts, static_cast<int32_t*>(nullptr), counts, dest_off, words, per);
+    hipLaunchKernelGGL(ep_prefix, dim3(1), dim3(kBlock), 0, stream, counts, P, capacity, before, fits, words,
+                       dev_status);
     for (int p = 0; p < P; ++p) {
         const PackWorkspace w = pack_workspace_carve(ws + p * per, T, K, E);
-        if (ntiles > 0)
-            hipLaunchKernelGGL(pack_tiles, dim3(ntiles), dim3(kBlock), static_cast<size_t>(E) * 8, stream, T, K, E,
-                               ids[p], w.tile_base, w.lrank, w.tile_err);
-        hipLaunchKernelGGL(pack_scan, dim3(1), dim3(kScanThreads), 0, stream, ntiles, E, P, w.tile_base, w.tile_err,
-                           expert_counts + static_cast<uint64_t>(p) * E, nullptr, counts + p * P, dest_off + p * P,
-                           words + p);
         a.x[p] = reinterpret_cast<const char*>(x[p]);
         a.ids[p] = ids[p];
         a.dst[p] = reinterpret_cast<char*>(recv[p]);
@@ -914,9 +964,7 @@ hipError_t launch_ep_dispatch(int T, int H, int K, int E, int P, const uint16_t*
         a.lrank[p] = w.lrank;
         a.dest_off[p] = dest_off + p * P;
     }
-    if (dev_status) hipLaunchKernelGGL(merge_status, dim3(1), dim3(1), 0, stream, words, P, dev_status);
     if (T > 0) {
-        hipLaunchKernelGGL(ep_prefix, dim3(1), dim3(kBlock), 0, stream, counts, P, capacity, before, fits, dev_status);
         a.counts = counts;
         a.before = before;
         a.fits = fits;
@@ -992,26 +1040,31 @@ hipError_t launch_ep_dispatch_dedup(int T, int H, int K, int E, int P, const uin
     int64_t* before = reinterpret_cast<int64_t*>(tail);
     int32_t* fits = reinterpret_cast<int32_t*>(tail + align256(8 * Pu * Pu));
     EpArgs a{};
+    RankIds rids{};
     (void)hipGetLastError();
+    // rank p's dedup workspace at ws + p * per: tile bases, local ranks, error flags
+    const uint64_t lrank_at = align256(4 * nt * Pu);
+    const uint64_t err_at = lrank_at + align256(4 * uint64_t(T) * Pu);
+    for (int p = 0; p < P; ++p) rids.ids[p] = ids[p];
+    if (ntiles > 0)
+        hipLaunchKernelGGL(dedup_tiles, dim3(ntiles, P), dim3(kBlock), 0, stream, T, K, E, P, rids,
+                           reinterpret_cast<int32_t*>(ws), reinterpret_cast<int32_t*>(ws + lrank_at),
+                           reinterpret_cast<int32_t*>(ws + err_at), per);
+    hipLaunchKernelGGL(dedup_scan, dim3(P), dim3(kScanThreads), 0, stream, ntiles, P, reinterpret_cast<int32_t*>(ws),
+                       reinterpret_cast<const int32_t*>(ws + err_at), counts, dest_off, words, per);
+    hipLaunchKernelGGL(ep_prefix, dim3(1), dim3(kBlock), 0, stream, counts, P, capacity, before, fits, words,
+                       dev_status);
     for (int p = 0; p < P; ++p) {
         char* base = ws + p * per;
         int32_t* tile_base = reinterpret_cast<int32_t*>(base);
-        int32_t* lrank = reinterpret_cast<int32_t*>(base + align256(4 * nt * Pu));
-        int32_t* tile_err = reinterpret_cast<int32_t*>(base + align256(4 * nt * Pu) + align256(4 * uint64_t(T) * Pu));
-        if (ntiles > 0)
-            hipLaunchKernelGGL(dedup_tiles, dim3(ntiles), dim3(kBlock), 0, stream, T, K, E, P, ids[p], tile_base, lrank,
-                               tile_err);
-        hipLaunchKernelGGL(dedup_scan, dim3(1), dim3(kScanThreads), 0, stream, ntiles, P, tile_base, tile_err,
-                           counts + p * P, dest_off + p * P, words + p);
+        int32_t* lrank = reinterpret_cast<int32_t*>(base + lrank_at);
         a.x[p] = reinterpret_cast<const char*>(x[p]);
         a.dst[p] = reinterpret_cast<char*>(recv[p]);
         a.tile_base[p] = tile_base;
         a.lrank[p] = lrank;
         a.dest_off[p] = dest_off + p * P;
     }
-    if (dev_status) hipLaunchKernelGGL(merge_status, dim3(1), dim3(1), 0, stream, words, P, dev_status);
     if (T > 0) {
-        hipLaunchKernelGGL(ep_prefix, dim3(1), dim3(kBlock), 0, stream, counts, P, capacity, before, fits, dev_status);
         a.counts = counts;
         a.before = before;
         a.fits = fits;
