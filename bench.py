@@ -15,8 +15,9 @@ Plans are built once per shape (host orchestration, like the paper's
 compile-time specialisation) and reused; every step re-executes them.
 
 value = algorithmic bytes of a step (reads + writes each op must make at
-least once) / wall time of a step, in GB/s (1e9 bytes/s).  Per-op times come
-from HIP events recorded on the stream the kernels run on.  The decode-size
+least once) / wall time of a step, in GB/s (1e9 bytes/s), over steps with
+nothing between the ops.  Per-op times come from as many further steps with
+HIP events recorded between the ops, on the stream the kernels run on.  The decode-size
 AllReduce (P=8, bf16, 128 x 8192 per rank) is timed separately as latency:
 128 calls captured in a graph, one warm-up replay, eight timed replays,
 time / 1024 (the paper's methodology, Section 5).
@@ -264,15 +265,23 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    # The timed steps carry no instrumentation (an event between two ops costs
+    # ~4 µs of stream time); the per-op breakdown comes from as many steps
+    # again, outside the timed region, with events between the ops.
     log(f"bench: timing {args.steps} steps")
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     for i in range(args.steps):
-        step(events[i])
+        step()
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     ms_per_step = wall * 1e3 / args.steps
+
+    log(f"bench: per-op breakdown ({args.steps} more steps, events between the ops)")
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
 
     per_op = {}
     for j, (name, bmin, bsched) in enumerate(ops):

@@ -313,6 +313,9 @@ def _zipf_or_uniform(rng, T, K, E, seed):
 @pytest.mark.parametrize("P,T,H,K,E,seed", [
     (1, 40, 32, 2, 4, 0), (2, 50, 24, 2, 8, 1), (3, 70, 7, 3, 9, 2), (4, 65, 136, 4, 16, 3),
     (8, 200, 520, 8, 64, 5), (16, 64, 64, 4, 32, 6), (4, 0, 64, 2, 8, 7),
+    (2, 4096, 16, 4, 256, 8),  # 64 token tiles per rank
+    (2, 4160, 16, 4, 256, 9),  # 65 tiles, the last one partial
+    (2, 300, 16, 4, 512, 10),  # 512 experts
 ])
 def test_ep_dispatch_and_combine_one_pass_match_oracle(P, T, H, K, E, seed):
     xs_np, idss_np, gates_np = _ep_case(P, T, H, K, E, seed)

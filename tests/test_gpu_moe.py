@@ -61,6 +61,9 @@ def check_pack(x_np, ids_np, E, P):
         (130, 64, 64, 64, 8, 7),  # K = 64 (every expert)
         (97, 16, 2, 4096, 16, 8),  # E = 4096
         (0, 64, 8, 256, 8, 9),  # no tokens
+        (4096, 24, 8, 256, 8, 12),  # 64 token tiles
+        (4097, 24, 8, 256, 8, 13),  # 65 tiles, the last one a single token
+        (300, 24, 8, 512, 8, 14),  # 512 experts
     ],
 )
 def test_pack_matches_oracle(T, H, K, E, P, seed):
@@ -78,13 +81,18 @@ def test_pack_zipf_routing_skewed():
     check_pack(x, ids, E, P)
 
 
-def test_pack_reports_bad_routing():
+@pytest.mark.parametrize("T,E", [(70, 16), (4200, 16), (70, 1024)])
+def test_pack_reports_bad_routing(T, E):
     rng = np.random.default_rng(11)
-    T, H, K, E, P = 70, 16, 4, 16, 4
+    H, K, P = 16, 4, 4
     x = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
     ids = _distinct_ids(rng, T, K, E)
     rep = ids.copy()
     rep[3, 2] = rep[3, 0]  # repeated id within a token
+    _, status = run_pack(x, rep, E, P)
+    assert status == 1
+    rep = ids.copy()
+    rep[T - 1, 1] = rep[T - 1, 0]  # ... in the last (partial) tile
     _, status = run_pack(x, rep, E, P)
     assert status == 1
     oob = ids.copy()
