@@ -351,6 +351,7 @@ def main():
         extra = measure_extra_ops(torch, PL, ins, rs_out, ag_out, P, N, s)
 
         extra["expert_parallel_p8"] = measure_ep(torch, PL, W, P, T, H, E, K)
+        extra["rank0_share"] = measure_share(torch, PL, ins, rs_out, ag_out, P, N, s)
 
     latency = None
     if not args.no_latency:
@@ -565,6 +566,37 @@ def measure_ep(torch, PL, W, P, T, H, E, K, reps=5):
                                              result["one_pass_dedup"]["round_trip"]["avg_us"], 3)
     del xs, ids, gates
     return result
+
+
+def measure_share(torch, PL, ins, rs_out, ag_out, P, N, s, reps=5):
+    """Rank 0's share of ReduceScatter, AllGather and AllReduce at 256 MiB
+    per rank (purlin_plan_share: the descriptors that write out_0, what one
+    GPU would execute with the path sharded over P GPUs).  Bytes = what the
+    share reads and writes, each byte once."""
+    out = {}
+    cases = [
+        ("reduce_scatter", PL.Plan("reduce_scatter", P, N, "bf16", 1 << 20, share=0), ins,
+         [rs_out[0]] + [None] * (P - 1)),
+        ("allgather", PL.Plan("allgather", P, N, "bf16", 1 << 20, share=0), rs_out, [ag_out[0]] + [None] * (P - 1)),
+        ("allreduce", PL.Plan("allreduce", P, N, "bf16", 1 << 20, share=0), ins, ag_out),
+    ]
+    for name, plan, i, o in cases:
+        run = plan.bind(i, o)
+        run()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            run()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        out[name] = {"avg_us": round(us, 2), "bytes": int(plan.sched_bytes),
+                     "GBps": round(plan.sched_bytes / (us * 1e-6) / 1e9, 1),
+                     "frac_of_hbm_peak": round(plan.sched_bytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+    out["what"] = ("rank 0's share (the descriptors writing out_0) at P=8, 256 MiB per rank, bf16, chunk 1 MiB; "
+                   "the other ranks' buffers stand in for peer memory")
+    return out
 
 
 def measure_ceilings(torch, PL, nbytes=1 << 30, reps=20):

@@ -192,6 +192,34 @@ PURLIN_API purlin_status purlin_plan_rooted(purlin_op op, int P, int root, uint6
                                             uint64_t chunk_bytes, const purlin_policy* policy, uint32_t flags,
                                             purlin_plan_t* out_plan);
 
+/* Rank `rank`'s share of a collective run on P GPUs: the descriptors of the
+ * full plan that write out_rank, each narrowed to that one destination.
+ * Every rank pulls what it consumes (Section 3.2: a consumer reads its
+ * peers' chunks), so on P GPUs each one would execute its own share, with
+ * the other ranks' buffers reached as peer memory; on one GPU the share is
+ * one rank's work at its real shape.
+ *   REDUCE_SCATTER  partition `rank` of every input reduced into out_rank
+ *   ALLGATHER       every rank's input copied into out_rank
+ *   ALLTOALL        partition `rank` of every input into out_rank
+ *   ALLREDUCE       compose<RS, AG>: phase 0 reduces partition `rank` into
+ *                   out_rank, phase 1 copies partition k of out_k into
+ *                   out_rank for k != rank (it reads what rank k's share
+ *                   wrote in its phase 0).  ar_mode 0 selects this form;
+ *                   ar_mode 2 has the rank reduce every partition itself;
+ *                   ar_mode 3 gives PURLIN_ERR_UNSUPPORTED.
+ *   rooted ops      as the full plan, restricted to out_rank (empty for a
+ *                   REDUCE or GATHER share of a rank that is not the root)
+ * `root` is -1 for the non-rooted collectives and the root rank for the
+ * rooted ones.  The share reads and writes only the buffers its
+ * descriptors name (purlin_exec checks those; the others may be NULL) and
+ * writes out_rank and nothing else.  The P shares together write exactly
+ * what the full plan writes.  Other arguments and errors as purlin_plan_ex
+ * and purlin_plan_rooted; PURLIN_ERR_INVALID also for rank outside [0, P)
+ * or a variable-size op. */
+PURLIN_API purlin_status purlin_plan_share(purlin_op op, int P, int root, int rank, uint64_t count,
+                                           purlin_dtype dtype, uint64_t chunk_bytes, const purlin_policy* policy,
+                                           uint32_t flags, purlin_plan_t* out_plan);
+
 /* A variable-size collective over P ranks: every input buffer holds
  * `in_capacity` elements and every output buffer `out_capacity`.  The sizes
  * are not part of the plan: purlin_exec_v reads them from device memory at

@@ -31,7 +31,7 @@ size_t fused_state_bytes(const purlin::Plan& p) {
 
 purlin_status make_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,
                         const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan, uint64_t v_unit = 0,
-                        uint64_t v_out_capacity = 0) {
+                        uint64_t v_out_capacity = 0, int share = -1) {
     if (!out_plan) return PURLIN_ERR_INVALID;
     *out_plan = nullptr;
     purlin_plan_s* h = new (std::nothrow) purlin_plan_s;
@@ -39,7 +39,7 @@ purlin_status make_plan(purlin_op op, int P, int root, uint64_t count, purlin_dt
     purlin_status st;
     try {
         st = v_unit ? purlin::build_plan_v(op, P, count, v_out_capacity, dtype, chunk, v_unit, policy, flags, h->plan)
-                    : purlin::build_plan(op, P, root, count, dtype, chunk, policy, flags, h->plan);
+                    : purlin::build_plan(op, P, root, count, dtype, chunk, policy, flags, h->plan, share);
     } catch (...) {
         st = PURLIN_ERR_NOMEM;
     }
@@ -143,6 +143,16 @@ purlin_status purlin_plan_rooted(purlin_op op, int P, int root, uint64_t count, 
         return PURLIN_ERR_INVALID;
     }
     return make_plan(op, P, root, count, dtype, chunk_bytes, policy, flags, out_plan);
+}
+
+purlin_status purlin_plan_share(purlin_op op, int P, int root, int rank, uint64_t count, purlin_dtype dtype,
+                                uint64_t chunk_bytes, const purlin_policy* policy, uint32_t flags,
+                                purlin_plan_t* out_plan) {
+    if (op < PURLIN_ALLREDUCE || op > PURLIN_GATHER || rank < 0 || rank >= P) {
+        if (out_plan) *out_plan = nullptr;
+        return PURLIN_ERR_INVALID;
+    }
+    return make_plan(op, P, root, count, dtype, chunk_bytes, policy, flags, out_plan, 0, 0, rank);
 }
 
 purlin_status purlin_plan_v(purlin_op op, int P, uint64_t in_capacity, uint64_t out_capacity, purlin_dtype dtype,

@@ -109,12 +109,13 @@ purlin_status cut_items(Plan& out, const purlin_policy& pol);
 }  // namespace
 
 purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,
-                         const purlin_policy* policy, uint32_t flags, Plan& out) {
+                         const purlin_policy* policy, uint32_t flags, Plan& out, int share) {
     if (op < PURLIN_ALLREDUCE || op > PURLIN_GATHER) return PURLIN_ERR_INVALID;
     const bool rooted = op >= PURLIN_BROADCAST;
     if (dtype != PURLIN_FP32 && dtype != PURLIN_BF16) return PURLIN_ERR_INVALID;
     if (P < 1 || P > PURLIN_MAX_RANKS) return PURLIN_ERR_INVALID;
     if (rooted ? (root < 0 || root >= P) : root != -1) return PURLIN_ERR_INVALID;
+    if (share < -1 || share >= P) return PURLIN_ERR_INVALID;
     if (count % static_cast<uint64_t>(P) != 0) return PURLIN_ERR_INVALID;
     if (flags & ~PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
     const uint64_t s = dtype == PURLIN_FP32 ? 4 : 2;
@@ -128,6 +129,14 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
     const uint64_t Cp = part ? ceil_div(part, chunk) : 0;
 
     if (pol.fanout == 0) pol.fanout = 2;
+    if (share >= 0 && op == PURLIN_ALLREDUCE) {
+        // A rank's share of an AllReduce is its ReduceScatter partition and
+        // the pulls of the others (compose<RS, AG>); the one-phase form would
+        // have every rank reduce the whole buffer, and the single-launch form
+        // coordinates ranks through counters in one GPU's memory.
+        if (pol.ar_mode == 0) pol.ar_mode = 1;
+        if (pol.ar_mode == 3) return PURLIN_ERR_UNSUPPORTED;
+    }
     if (pol.ar_mode == 0) {
         // AllReduce: in the latency regime one launch that reduces each chunk
         // once and writes it to all P outputs wins (no second launch).  When
@@ -290,6 +299,35 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
                 break;
             default:
                 return PURLIN_ERR_INVALID;
+        }
+        if (share >= 0) {
+            // Keep what writes out_share, narrowed to that destination; the
+            // buffer masks become the buffers the share reads or writes.
+            const uint32_t mine = out0 + static_cast<uint32_t>(share);
+            std::vector<purlin_desc> kept;
+            uint32_t in_mask = 0, out_mask = 0;
+            for (const purlin_desc& d : D) {
+                bool writes = false;
+                for (uint32_t j = 0; j < d.ndst; ++j) writes = writes || d.dst_buf + j * d.dst_step == mine;
+                if (!writes) continue;
+                purlin_desc n = d;
+                n.ndst = 1;
+                n.dst_buf = mine;
+                n.dst_step = 0;
+                for (uint32_t j = 0; j < n.nsrc; ++j) {
+                    const uint32_t b = n.src_buf + j * n.src_step;
+                    if (b < out0)
+                        in_mask |= 1u << b;
+                    else
+                        out_mask |= 1u << (b - out0);
+                }
+                out_mask |= 1u << share;
+                kept.push_back(n);
+            }
+            D.swap(kept);
+            out.in_mask = in_mask;
+            out.out_mask = out_mask;
+            out.share = share;
         }
         out.policy = pol;
         out.part_bytes = part;

@@ -32,6 +32,7 @@ struct Plan {
     uint32_t flags = 0;
 
     int root = -1;           // rooted collectives only
+    int share = -1;          // rank whose share this plan is, or -1 for all ranks' work
     uint32_t in_mask = 0;    // bit p: input p is read
     uint32_t out_mask = 0;   // bit r: output r is written
     uint64_t elem_bytes = 0;
@@ -70,7 +71,10 @@ purlin_status build_plan_v(purlin_op op, int P, uint64_t in_capacity, uint64_t o
                            uint64_t chunk, uint64_t unit, const purlin_policy* policy, uint32_t flags, Plan& out);
 
 // `root` is -1 for the non-rooted collectives and a rank for the rooted ones.
+// `share` >= 0 keeps only that rank's share of the work: the descriptors that
+// write its output, each narrowed to that one destination (every rank pulls
+// what it consumes).
 purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,
-                         const purlin_policy* policy, uint32_t flags, Plan& out);
+                         const purlin_policy* policy, uint32_t flags, Plan& out, int share = -1);
 
 }  // namespace purlin

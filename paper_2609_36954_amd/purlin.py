@@ -92,6 +92,7 @@ def lib():
     L.purlin_plan_ex.argtypes = [i32, i32, u64, i32, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
     L.purlin_plan_rooted.argtypes = [i32, i32, i32, u64, i32, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
     L.purlin_plan_v.argtypes = [i32, i32, u64, u64, i32, u64, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
+    L.purlin_plan_share.argtypes = [i32, i32, i32, i32, u64, i32, u64, ctypes.POINTER(Policy), u32, ctypes.POINTER(_vp)]
     L.purlin_exec_v.argtypes = [_vp, ctypes.POINTER(_vp), _vp, _vp, _vp]
     L.purlin_plan_info.argtypes = [_vp, _c_u64p, _c_u64p, _c_u64p, _c_u64p]
     L.purlin_plan_descriptors.argtypes = [_vp, ctypes.POINTER(_vp), _c_u64p, _c_u64p]
@@ -119,7 +120,8 @@ def lib():
     L.purlin_status_string.restype = ctypes.c_char_p
     L.purlin_version.argtypes = []
     L.purlin_version.restype = ctypes.c_char_p
-    for name in ("purlin_plan", "purlin_plan_ex", "purlin_plan_rooted", "purlin_plan_v", "purlin_exec_v",
+    for name in ("purlin_plan", "purlin_plan_ex", "purlin_plan_rooted", "purlin_plan_v", "purlin_plan_share",
+                 "purlin_exec_v",
                  "purlin_plan_info", "purlin_plan_descriptors", "purlin_plan_items",
                  "purlin_exec", "purlin_pack_workspace_size", "purlin_pack", "purlin_unpack",
                  "purlin_pack_dedup_workspace_size", "purlin_pack_dedup", "purlin_unpack_dedup",
@@ -174,7 +176,7 @@ class Plan:
     """A planned collective (immutable).  ``exec`` runs it on a stream."""
 
     def __init__(self, op, P, count, dtype, chunk, policy=None, host_only=False, root=None, unit=None,
-                 out_capacity=None, counts_transposed=False):
+                 out_capacity=None, counts_transposed=False, share=None):
         if op not in OPS:
             raise PurlinError(PURLIN_ERR_INVALID, f"unknown op {op!r}")
         if dtype not in DTYPES:
@@ -185,6 +187,10 @@ class Plan:
         self.root = root
         self.unit = unit
         self.host_only = bool(host_only)
+        self.share = share
+        self._used = None
+        if share is not None and op in VOPS:
+            raise PurlinError(PURLIN_ERR_INVALID, f"{op} has no rank shares")
         if (op in VOPS) != (unit is not None):
             raise PurlinError(PURLIN_ERR_INVALID, f"{op} {'needs' if op in VOPS else 'takes no'} unit")
         h = ctypes.c_void_p()
@@ -197,6 +203,13 @@ class Plan:
             flags = (PLAN_HOST_ONLY if host_only else 0) | (PLAN_COUNTS_TRANSPOSED if counts_transposed else 0)
             st = L.purlin_plan_v(OPS[op], int(P), int(count), out_cap, DTYPES[dtype], int(chunk), int(unit),
                                  ctypes.byref(pol) if pol is not None else None, flags, ctypes.byref(h))
+        elif share is not None:
+            pol = None
+            if policy is not None:
+                pol = policy if isinstance(policy, Policy) else Policy(**policy)
+            st = L.purlin_plan_share(OPS[op], int(P), -1 if root is None else int(root), int(share), int(count),
+                                     DTYPES[dtype], int(chunk), ctypes.byref(pol) if pol is not None else None,
+                                     PLAN_HOST_ONLY if host_only else 0, ctypes.byref(h))
         elif root is not None:
             pol = None
             if policy is not None:
@@ -331,6 +344,17 @@ def purlin_plan_rooted(op, P, root, count, dtype, chunk, policy=None, host_only=
 def used_buffers(plan):
     """(inputs used, outputs used) as lists of booleans, rank order."""
     P, op, root = plan.P, plan.op, plan.root
+    if getattr(plan, "share", None) is not None:  # the buffers its descriptors name
+        if plan._used is None:
+            ins, outs = [False] * P, [False] * P
+            for d in plan.descriptors():
+                for j in range(int(d["nsrc"])):
+                    b = int(d["src_buf"]) + j * int(d["src_step"])
+                    (ins if b < P else outs)[b % P] = True
+                for j in range(int(d["ndst"])):
+                    outs[int(d["dst_buf"]) + j * int(d["dst_step"]) - P] = True
+            plan._used = (ins, outs)
+        return plan._used
     ins = [True] * P
     outs = [True] * P
     if op in ("broadcast", "scatter"):

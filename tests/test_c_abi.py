@@ -58,6 +58,13 @@ int main(void) {
     if (purlin_plan_v(PURLIN_ALLGATHERV, 4, 100, 400, PURLIN_FP32, 64, 1, NULL,
                       PURLIN_PLAN_HOST_ONLY | PURLIN_PLAN_COUNTS_TRANSPOSED, &plan) != PURLIN_ERR_INVALID)
         return fail("transposed counts on a non-AllToAllV plan");
+    /* rank 3's share of a ReduceScatter: partition 3's four 64 KiB chunks, reduced into out_3 */
+    if (purlin_plan_share(PURLIN_REDUCE_SCATTER, 8, -1, 3, 1u << 20, PURLIN_BF16, 65536, NULL, PURLIN_PLAN_HOST_ONLY,
+                          &plan) != PURLIN_OK)
+        return fail("share plan");
+    if (purlin_plan_descriptors(plan, &table, &n, &stride) != PURLIN_OK || n != 4) return fail("share descriptors");
+    if (table[0].dst_buf != 8 + 3 || table[0].ndst != 1 || table[0].nsrc != 8) return fail("share destination");
+    purlin_plan_destroy(plan);
     if (purlin_plan_rooted(PURLIN_BROADCAST, 4, 4, 64, PURLIN_FP32, 64, NULL, PURLIN_PLAN_HOST_ONLY, &plan) !=
         PURLIN_ERR_INVALID)
         return fail("root out of range");

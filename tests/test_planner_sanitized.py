@@ -78,6 +78,31 @@ int main() {
                         PURLIN_OK)
                         check_bounds(p);
                 }
+    for (purlin_op op : fixed)
+        for (int P : Ps)
+            for (int share = -1; share <= P; ++share)
+                for (uint32_t mode = 0; mode <= 3; ++mode) {
+                    purlin_policy pol{};
+                    pol.ar_mode = mode;
+                    Plan p;
+                    if (build_plan(op, P, -1, 1000 * uint64_t(P), PURLIN_BF16, 96, &pol, PURLIN_PLAN_HOST_ONLY, p,
+                                   share) == PURLIN_OK) {
+                        check_bounds(p);
+                        for (const purlin_desc& d : p.items)
+                            if (share >= 0 && (d.ndst != 1 || d.dst_buf != uint32_t(P + share))) {
+                                std::printf("a share writes another rank's output\n");
+                                std::abort();
+                            }
+                    }
+                }
+    for (purlin_op op : rooted)
+        for (int P : Ps)
+            for (int share = 0; share < P; ++share) {
+                Plan p;
+                if (build_plan(op, P, P - 1, 64 * uint64_t(P), PURLIN_FP32, 32, nullptr, PURLIN_PLAN_HOST_ONLY, p,
+                               share) == PURLIN_OK)
+                    check_bounds(p);
+            }
     for (purlin_op op : vops)
         for (int P : Ps)
             for (uint64_t in_cap : {uint64_t(0), uint64_t(5), uint64_t(1000), uint64_t(70000)})
@@ -101,7 +126,9 @@ int main() {
     rejected += build_plan(PURLIN_ALLREDUCE, 8, -1, uint64_t(1) << 40, PURLIN_BF16, 2, nullptr, 0, p) != PURLIN_OK;
     rejected += build_plan_v(PURLIN_ALLTOALLV, 8, ~uint64_t(0), 64, PURLIN_BF16, 64, 1, nullptr, 0, p) != PURLIN_OK;
     rejected += build_plan_v(PURLIN_ALLGATHERV, 8, 64, 64, PURLIN_BF16, 64, 0, nullptr, 0, p) != PURLIN_OK;
-    if (rejected != 9) { std::printf("an invalid plan was accepted\n"); return 1; }
+    rejected += build_plan(PURLIN_ALLGATHER, 8, -1, 64, PURLIN_BF16, 64, nullptr, 0, p, 8) != PURLIN_OK;
+    rejected += build_plan(PURLIN_ALLGATHER, 8, -1, 64, PURLIN_BF16, 64, nullptr, 0, p, -2) != PURLIN_OK;
+    if (rejected != 11) { std::printf("an invalid plan was accepted\n"); return 1; }
     std::printf("OK %d plans\n", checked);
     return 0;
 }
