@@ -26,7 +26,11 @@ namespace {
 constexpr uint64_t kMinItem = 1024;        // one 16-byte access per lane of a 64-wide wave
 constexpr uint64_t kMaxItem = 64 * 1024;   // largest automatic work item
 constexpr uint64_t kTargetItems = 4096;    // 16 wavefronts per CU on 256 CUs
-constexpr uint64_t kStreamingBytes = 512ull << 20;  // twice the last-level cache
+// Traffic of a launch from which streaming item sizes and non-temporal hints
+// win (measured on MI355X, P = 8: between 288 MiB, where cached accesses are
+// faster, and 360 MiB, where they are 10-35% slower).
+constexpr uint64_t kStreamingBytes = 320ull << 20;
+constexpr uint64_t kAllReduceTwoPhaseBytes = 1ull << 30;  // one-phase traffic from which compose<RS, AG> wins
 constexpr uint64_t kLatencyNtStoreMin = 8ull << 20;  // written bytes per launch between which
 constexpr uint64_t kLatencyNtStoreMax = 32ull << 20; // non-temporal stores win below streaming
 
@@ -138,15 +142,15 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
         if (pol.ar_mode == 3) return PURLIN_ERR_UNSUPPORTED;
     }
     if (pol.ar_mode == 0) {
-        // AllReduce: in the latency regime one launch that reduces each chunk
-        // once and writes it to all P outputs wins (no second launch).  When
-        // the traffic streams from HBM, the two-phase compose wins although
-        // it schedules more bytes: phase 0 leaves the N*s reduced bytes in the
-        // last-level cache and phase 1's copies read them back from there,
-        // while each wave streams one direction at a time (measured on
-        // MI355X at 256 MiB per rank, P = 8).
+        // AllReduce: up to 48 MiB per rank (P = 8) one launch that reduces
+        // each chunk once and writes it to all P outputs wins (no second
+        // launch; 82 vs 128 µs at 32 MiB, 150 vs 196 µs at 48 MiB).  From
+        // 64 MiB per rank the two-phase compose wins although it schedules
+        // more bytes: phase 0 leaves the N*s reduced bytes in the last-level
+        // cache and phase 1's copies read them back from there, while each
+        // wave streams one direction at a time (measured on MI355X).
         const uint64_t one_phase_traffic = 2 * uint64_t(P) * count * s;
-        pol.ar_mode = one_phase_traffic >= kStreamingBytes ? 1 : 2;
+        pol.ar_mode = one_phase_traffic >= kAllReduceTwoPhaseBytes ? 1 : 2;
     }
 
     out = Plan{};
