@@ -18,9 +18,11 @@ value = algorithmic bytes of a step (reads + writes each op must make at
 least once) / wall time of a step, in GB/s (1e9 bytes/s), over steps with
 nothing between the ops.  Per-op times come from as many further steps with
 HIP events recorded between the ops, on the stream the kernels run on.  The decode-size
-AllReduce (P=8, bf16, 128 x 8192 per rank) is timed separately as latency:
-128 calls captured in a graph, one warm-up replay, eight timed replays,
-time / 1024 (the paper's methodology, Section 5).
+AllReduce (P=8, bf16, 128 x 8192 per rank) and the small AllReduce (P=4,
+fp32, 262144 per rank) are timed separately as latency: 128 calls captured
+in a graph, one warm-up replay, eight timed replays, time / 1024 (the
+paper's methodology, Section 5); so is the paper's latency sweep of
+AllReduce, ReduceScatter, AllGather and AllToAll at 1 KiB..512 KiB per rank.
 
 Prints ONE JSON line.
 """
@@ -168,7 +170,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--latency-sweep", action="store_true", help="also time AllReduce P=8 bf16 at 1 KiB..512 KiB per rank")
+    ap.add_argument("--no-latency-sweep", action="store_true",
+                    help="skip the sweep of AllReduce, ReduceScatter, AllGather, AllToAll at 1 KiB..512 KiB per rank")
     ap.add_argument("--no-latency", action="store_true", help="skip the graph-replayed latency measurement")
     ap.add_argument("--no-extra", action="store_true", help="skip timing the other collectives (outside the step)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -355,7 +358,7 @@ def main():
 
     latency = None
     if not args.no_latency:
-        latency = measure_latency(torch, PL, W, graph_latency_us, args.latency_sweep)
+        latency = measure_latency(torch, PL, W, graph_latency_us, not args.no_latency_sweep)
     ceilings = None if args.no_extra else measure_ceilings(torch, PL)
     return emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, per_op, latency, plan_ms,
                 dev_name, src_hash, extra, ceilings)
@@ -676,14 +679,24 @@ def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
         }
     }
     if sweep_sizes:
+        # the paper's latency sweep (Section 5): 1 KiB..512 KiB per rank (the
+        # scattered side: AllReduce/ReduceScatter/AllToAll input, AllGather
+        # output), P = 8, bf16, chunk 64 KiB; graph-replayed as above
         sweep = {}
-        for kib in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512):
-            n = kib * 1024 // 2
-            li = [torch.randn(n, device="cuda").to(torch.bfloat16).view(torch.int16) for _ in range(8)]
-            lo = [torch.empty(n, dtype=torch.int16, device="cuda") for _ in range(8)]
-            pl = PL.Plan("allreduce", 8, n, "bf16", 65536)
-            sweep[f"{kib}KiB"] = round(graph_latency_us(pl, li, lo), 2)
-        latency["allreduce_p8_bf16_sweep_us"] = sweep
+        for op in ("allreduce", "reduce_scatter", "allgather", "alltoall"):
+            row = {}
+            for kib in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512):
+                n = kib * 1024 // 2
+                li = [torch.randn(n, device="cuda").to(torch.bfloat16).view(torch.int16) for _ in range(8)]
+                lo = [torch.empty(n, dtype=torch.int16, device="cuda") for _ in range(8)]
+                if op == "reduce_scatter":
+                    lo = [t[: n // 8] for t in lo]
+                elif op == "allgather":
+                    li = [t[: n // 8] for t in li]
+                pl = PL.Plan(op, 8, n, "bf16", 65536)
+                row[f"{kib}KiB"] = round(graph_latency_us(pl, li, lo), 2)
+            sweep[op] = row
+        latency["sweep_p8_bf16_us"] = sweep
     del lat_in, lat_out
     return latency
 
