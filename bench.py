@@ -197,7 +197,7 @@ def main():
     src_hash = kernel_source_hash()
 
     # ---------------- inputs (seeded, synthetic) ----------------
-    c3 = W.COLLECTIVE_CONFIGS[3]
+    c3 = W.RS_AG_P8_BF16_256MIB
     P, N, s = c3.P, c3.count, 2
     M = N // P
     moe = W.MOE_CONFIG
@@ -630,13 +630,13 @@ def measure_ceilings(torch, PL, nbytes=1 << 30, reps=20):
 
 
 def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
-    c1 = W.COLLECTIVE_CONFIGS[1]
+    c1 = W.AR_P4_FP32_256K
     in1 = [to_dev(torch, a) for a in W.collective_inputs(c1)]
     out1 = [torch.empty(c1.count, dtype=torch.float32, device="cuda") for _ in range(c1.P)]
     ar1 = PL.Plan("allreduce", c1.P, c1.count, "fp32", c1.chunk)
     lat1_us = graph_latency_us(ar1, in1, out1)
     del in1, out1
-    c2 = W.COLLECTIVE_CONFIGS[2]
+    c2 = W.AR_P8_BF16_DECODE
     lat_in = [to_dev(torch, a) for a in W.collective_inputs(c2)]
     lat_out = [torch.empty(c2.count, dtype=torch.int16, device="cuda") for _ in range(c2.P)]
     ar2 = PL.Plan("allreduce", c2.P, c2.count, "bf16", c2.chunk)

@@ -14,19 +14,23 @@ The paper measures with real models and serving traces that are not
 available here (Section 5, "Application Performance"); these shapes stand in
 for them:
 
-=====  ==================================================================
-cfg    workload
-=====  ==================================================================
-1      AllReduce, P=4, fp32, 262144 elements per rank, U(-1, 1), chunk 16 KiB
-2      decode AllReduce, P=8, bf16 activations [128 x 8192] per rank, N(0,1),
-       chunk 64 KiB
-3      ReduceScatter then AllGather (and AllReduce as the check), P=8, bf16,
-       134217728 elements (256 MiB) per rank, N(0, 0.02), chunk 1 MiB
-4      MoE dispatch: x bf16 [4096 x 7168] N(0,1); E=256 experts over P=8
-       ranks; top-8 ids per token from Zipf(s=1.1) without repeats
-5      MoE combine: expert outputs bf16 [32768 x 7168] N(0,1) in config 4's
-       packed layout; softmax top-8 gate weights in fp32
-=====  ==================================================================
+=======================  ===================================================
+name                     workload
+=======================  ===================================================
+AR_P4_FP32_256K          AllReduce, P=4, fp32, 262144 elements per rank,
+                         U(-1, 1), chunk 16 KiB
+AR_P8_BF16_DECODE        decode AllReduce, P=8, bf16 activations
+                         [128 x 8192] per rank, N(0,1), chunk 64 KiB
+RS_AG_P8_BF16_256MIB     ReduceScatter then AllGather (and AllReduce as the
+                         check), P=8, bf16, 134217728 elements (256 MiB) per
+                         rank, N(0, 0.02), chunk 1 MiB
+MOE_CONFIG (dispatch)    x bf16 [4096 x 7168] N(0,1); E=256 experts over P=8
+                         ranks; top-8 ids per token from Zipf(s=1.1) without
+                         repeats
+MOE_CONFIG (combine)     expert outputs bf16 [32768 x 7168] N(0,1) in the
+                         dispatch's packed layout; softmax top-8 gate weights
+                         in fp32
+=======================  ===================================================
 """
 
 from dataclasses import dataclass
@@ -36,6 +40,9 @@ import numpy as np
 __all__ = [
     "CollectiveConfig",
     "MoEConfig",
+    "AR_P4_FP32_256K",
+    "AR_P8_BF16_DECODE",
+    "RS_AG_P8_BF16_256MIB",
     "COLLECTIVE_CONFIGS",
     "MOE_CONFIG",
     "rank_rngs",
@@ -76,11 +83,15 @@ class MoEConfig:
     seed_gates: int
 
 
-COLLECTIVE_CONFIGS = {
-    1: CollectiveConfig("ar_p4_fp32_256k", "allreduce", 4, 262144, "fp32", 16 * 1024, "uniform", 1.0, 1),
-    2: CollectiveConfig("ar_p8_bf16_128x8192", "allreduce", 8, 128 * 8192, "bf16", 64 * 1024, "normal", 1.0, 2),
-    3: CollectiveConfig("rs_ag_p8_bf16_256MiB", "reduce_scatter", 8, 134217728, "bf16", 1 << 20, "normal", 0.02, 3),
-}
+# AllReduce, P = 4, fp32, 262144 elements per rank, uniform in [-1, 1]
+AR_P4_FP32_256K = CollectiveConfig("ar_p4_fp32_256k", "allreduce", 4, 262144, "fp32", 16 * 1024, "uniform", 1.0, 1)
+# decode-step AllReduce, P = 8, bf16 activations [128 tokens x 8192 hidden] per rank, N(0, 1)
+AR_P8_BF16_DECODE = CollectiveConfig("ar_p8_bf16_128x8192", "allreduce", 8, 128 * 8192, "bf16", 64 * 1024, "normal",
+                                     1.0, 2)
+# prefill-size ReduceScatter then AllGather, P = 8, bf16, 256 MiB per rank, N(0, 0.02)
+RS_AG_P8_BF16_256MIB = CollectiveConfig("rs_ag_p8_bf16_256MiB", "reduce_scatter", 8, 134217728, "bf16", 1 << 20,
+                                        "normal", 0.02, 3)
+COLLECTIVE_CONFIGS = {c.name: c for c in (AR_P4_FP32_256K, AR_P8_BF16_DECODE, RS_AG_P8_BF16_256MIB)}
 
 MOE_CONFIG = MoEConfig(T=4096, H=7168, E=256, P=8, K=8, zipf_s=1.1, seed_ids=4, seed_x=40, seed_y=50, seed_gates=5)
 

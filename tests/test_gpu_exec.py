@@ -187,35 +187,35 @@ def test_graph_capture_replays_match_eager():
 # ---------------------------------------------------------------------------
 
 
-def test_config1_allreduce_p4_fp32():
-    cfg = W.COLLECTIVE_CONFIGS[1]
+def test_allreduce_p4_fp32_262144_per_rank():
+    cfg = W.AR_P4_FP32_256K
     ins = W.collective_inputs(cfg)
     want = oracle.all_reduce(ins, cfg.dtype)
     plan = PL.Plan(cfg.op, cfg.P, cfg.count, cfg.dtype, cfg.chunk)
     got = run_plan(plan, ins, cfg.dtype)
     for r in range(cfg.P):
-        assert_bits_equal(got[r], want[r], "fp32", f"config 1 rank {r}")
+        assert_bits_equal(got[r], want[r], "fp32", f"AllReduce P=4 fp32 rank {r}")
 
 
-def test_config2_allreduce_p8_bf16():
-    cfg = W.COLLECTIVE_CONFIGS[2]
+def test_decode_allreduce_p8_bf16_128x8192():
+    cfg = W.AR_P8_BF16_DECODE
     ins = W.collective_inputs(cfg)
     want = oracle.all_reduce(ins, cfg.dtype)
     for pol in (None, dict(ar_mode=1)):
         plan = PL.Plan(cfg.op, cfg.P, cfg.count, cfg.dtype, cfg.chunk, policy=pol)
         got = run_plan(plan, ins, cfg.dtype)
         for r in range(cfg.P):
-            assert_bits_equal(got[r], want[r], "bf16", f"config 2 rank {r} {pol}")
+            assert_bits_equal(got[r], want[r], "bf16", f"decode AllReduce rank {r} {pol}")
 
 
-def test_config3_reduce_scatter_then_all_gather_full_size():
+def test_reduce_scatter_then_all_gather_256MiB_per_rank():
     """256 MiB per rank, P=8, bf16, chunk 1 MiB, in the launch shapes the bench times.
 
     RS then AG must equal the AllReduce bit for bit on the whole buffer
     (compared on the device); sampled elements are checked against the
     oracle, which is elementwise across ranks.
     """
-    cfg = W.COLLECTIVE_CONFIGS[3]
+    cfg = W.RS_AG_P8_BF16_256MIB
     P, N = cfg.P, cfg.count
     M = N // P
     ins_np = W.collective_inputs(cfg)
@@ -238,9 +238,9 @@ def test_config3_reduce_scatter_then_all_gather_full_size():
     idx = np.sort(rng.choice(N, size=P * 65536, replace=False))
     want = oracle.all_reduce([a[idx] for a in ins_np], "bf16")[0]
     got_ar = to_host(ar_out[0], np.uint16)[idx]
-    assert_bits_equal(got_ar, want, "bf16", "config 3 AR sample")
+    assert_bits_equal(got_ar, want, "bf16", "AllReduce sample, 256 MiB/rank")
     rs_host = np.concatenate([to_host(t, np.uint16) for t in rs_out])
-    assert_bits_equal(rs_host[idx], want, "bf16", "config 3 RS sample")
+    assert_bits_equal(rs_host[idx], want, "bf16", "ReduceScatter sample, 256 MiB/rank")
 
 
 # ---------------------------------------------------------------------------
@@ -292,7 +292,7 @@ def test_fused_allreduce_graph_replays():
 
 
 def test_fused_allreduce_full_size_equals_two_launches():
-    cfg = W.COLLECTIVE_CONFIGS[3]
+    cfg = W.RS_AG_P8_BF16_256MIB
     P, N = cfg.P, cfg.count
     ins = [to_device(a) for a in W.collective_inputs(cfg)]
     fused = PL.Plan("allreduce", P, N, "bf16", cfg.chunk, policy=dict(ar_mode=3))

@@ -172,7 +172,7 @@ def test_pack_then_unpack_round_trip():
     assert np.array_equal(to_host(out, np.uint16).reshape(T, H), x)
 
 
-def test_config4_pack_and_config5_combine_full_size():
+def test_pack_and_combine_4096x7168_top8_of_256_full_size():
     """4096 tokens x 7168 hidden, E=256 over P=8, top-8 Zipf(1.1); then combine."""
     cfg = W.MOE_CONFIG
     ids = W.zipf_topk_ids(cfg.T, cfg.E, cfg.K, cfg.zipf_s, cfg.seed_ids)
@@ -188,7 +188,7 @@ def test_config4_pack_and_config5_combine_full_size():
     g = W.softmax_gates(cfg.T, cfg.K, cfg.seed_gates)
     out, status = run_unpack(y, want["pos"], g)
     assert status == 0
-    assert_bits_equal(out, oracle.unpack(y, want["pos"], g), "bf16", "config 5 combine")
+    assert_bits_equal(out, oracle.unpack(y, want["pos"], g), "bf16", "combine 4096 x 7168")
 
 
 def test_binding_rejects_undersized_outputs_before_launch():
