@@ -749,7 +749,17 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
         return t.contiguous().view(torch.uint8).cpu().numpy().view(dt)
 
     log("bench: cpu baseline (oracle on a sample)")
+    from paper_2609_36954_amd import workloads as W
+
     t_start = time.perf_counter()
+    max_ulp = 0
+
+    def ulp_gap(got, want):
+        """Largest distance in bf16 ulps (both as bf16 encodings)."""
+        def ordered(b):
+            b = b.astype(np.int32)
+            return np.where(b & 0x8000, 0x8000 - (b & 0x7FFF), 0x8000 + b)
+        return int(np.abs(ordered(got) - ordered(want)).max()) if got.size else 0
     frac = 1  # the whole of each partition of the collectives
     m = M // frac
     ok = True
@@ -770,7 +780,9 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
     t_total += dt
     bytes_total += collective_bytes("reduce_scatter", P, P * m, 2)
     for r in range(P):
-        ok &= bool(np.array_equal(down(rs_out[r][:m], np.uint16), rs_want[r]))
+        got = down(rs_out[r][:m], np.uint16)
+        ok &= bool(np.array_equal(got, rs_want[r]))
+        max_ulp = max(max_ulp, ulp_gap(got, rs_want[r]))
     # AllGather of those
     dt, ag_want = median_time(lambda: oracle.all_gather(rs_want, "bf16"))
     t_total += dt
@@ -796,7 +808,9 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
     dt, cw = median_time(lambda: oracle.unpack(y_np, pos_want[:Ts], g_np[:Ts]))
     t_total += dt
     bytes_total += unpack_bytes(Ts, H, K)
-    ok &= bool(np.array_equal(down(comb_out[:Ts], np.uint16).reshape(Ts, H), cw))
+    got = down(comb_out[:Ts], np.uint16).reshape(Ts, H)
+    ok &= bool(np.array_equal(got, cw))
+    max_ulp = max(max_ulp, ulp_gap(got, cw))
     try:
         cores = len(os.sched_getaffinity(0))
     except AttributeError:
@@ -842,6 +856,15 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
     t_pack = t_pack_single
     t_threaded = dt_rs + dt_ag + t_pack + dt_un
 
+    # the two small AllReduce workloads, whole, single-threaded (not in the step)
+    small = {}
+    for cfg in (W.AR_P4_FP32_256K, W.AR_P8_BF16_DECODE):
+        ins_c = W.collective_inputs(cfg)
+        es = 4 if cfg.dtype == "fp32" else 2
+        dt_c, _ = median_time(lambda: oracle.all_reduce(ins_c, cfg.dtype))
+        small[cfg.name] = {"seconds": round(dt_c, 4),
+                           "GBps": round(collective_bytes("allreduce", cfg.P, cfg.count, es) / dt_c / 1e9, 3)}
+
     def sha(arrays):
         h = hashlib.sha256()
         for a in arrays:
@@ -862,6 +885,8 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
         "cpu": cpu_model(),
         "numpy": np.__version__,
         "gpu_matches_oracle_on_sample": ok,
+        "max_bf16_ulp_on_sample": max_ulp,  # ReduceScatter and combine outputs against the oracle
+        "small_allreduce": small,
         "threaded": {
             "value": round(bytes_total / t_threaded / 1e9, 3),
             "unit": "GB/s",
