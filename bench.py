@@ -355,6 +355,7 @@ def main():
 
         extra["expert_parallel_p8"] = measure_ep(torch, PL, W, P, T, H, E, K)
         extra["rank0_share"] = measure_share(torch, PL, ins, rs_out, ag_out, P, N, s)
+        extra["workgroup_plateau"] = measure_plateau(torch, PL, ins, rs_out, ag_out, P, N, s)
 
     latency = None
     if not args.no_latency:
@@ -599,6 +600,35 @@ def measure_share(torch, PL, ins, rs_out, ag_out, P, N, s, reps=5):
                      "frac_of_hbm_peak": round(plan.sched_bytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
     out["what"] = ("rank 0's share (the descriptors writing out_0) at P=8, 256 MiB per rank, bf16, chunk 1 MiB; "
                    "the other ranks' buffers stand in for peer memory")
+    return out
+
+
+def measure_plateau(torch, PL, ins, rs_out, ag_out, P, N, s, reps=3):
+    """ReduceScatter and AllGather at 256 MiB/rank with the grid capped at
+    W workgroups (policy max_workgroups; one workgroup occupies one CU): the
+    bandwidth a collective reaches on a bounded share of the GPU, and the
+    smallest cap within 90% of the uncapped launch (the resource plateau the
+    paper measures for its copy, Section 5)."""
+    out = {}
+    for name, op, i, o in (("reduce_scatter", "reduce_scatter", ins, rs_out), ("allgather", "allgather", rs_out, ag_out)):
+        row = {}
+        for cap in (4, 8, 16, 32, 64, 128, 256, 512, 0):
+            plan = PL.Plan(op, P, N, "bf16", 1 << 20, policy={"max_workgroups": cap} if cap else None)
+            run = plan.bind(i, o)
+            run()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                run()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / reps
+            row[str(cap) if cap else "uncapped"] = round(collective_bytes(op, P, N, s) / (us * 1e-6) / 1e9, 1)
+        full = row["uncapped"]
+        knee = next((int(k) for k, v in row.items() if k != "uncapped" and v >= 0.9 * full), None)
+        out[name] = {"GBps_by_workgroups": row, "smallest_cap_within_90pct": knee}
+    out["what"] = "256 MiB/rank, P=8, bf16, chunk 1 MiB; GB/s = algorithmic bytes / time; 256 CUs on the chip"
     return out
 
 

@@ -138,7 +138,15 @@ typedef struct purlin_policy {
                             plan must not run concurrently with itself)     */
     uint32_t load_hint;  /* global loads:  0 auto, 1 cached, 2 non-temporal */
     uint32_t store_hint; /* global stores: 0 auto, 1 cached, 2 non-temporal */
-    uint32_t reserved[2];/* must be zero */
+    uint32_t max_workgroups; /* 0 = one wavefront per work item; otherwise every
+                            launch of the plan has at most this many 256-thread
+                            workgroups (4 wavefronts each) and its wavefronts
+                            stride over the items: the collective runs on a
+                            bounded share of the GPU's 256 CUs, leaving the
+                            rest to overlapped compute (the paper's
+                            resource-constrained execution, Section 5).  Not
+                            with ar_mode 3 (PURLIN_ERR_UNSUPPORTED). */
+    uint32_t reserved;   /* must be zero */
 } purlin_policy;
 
 #define PURLIN_PLAN_HOST_ONLY 1u /* build the tables on the host only (no device

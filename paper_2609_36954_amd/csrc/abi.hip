@@ -219,7 +219,8 @@ purlin_status purlin_exec_v(purlin_plan_t plan, void* const* bufs, const int32_t
         purlin::launch_v(p.op, p.d_items, ph.count, p.P, p.dtype, ph.nt_load || ph.nt_store, bufs, counts,
                          (p.flags & PURLIN_PLAN_COUNTS_TRANSPOSED) != 0, p.v_src_major, dev_status, p.in_capacity,
                          p.out_capacity, p.unit, p.chunk, p.reduce_item_bytes ? p.reduce_item_bytes : p.chunk,
-                         p.op == PURLIN_ALLTOALLV ? static_cast<uint32_t>(p.P) : 1u, static_cast<hipStream_t>(stream));
+                         p.op == PURLIN_ALLTOALLV ? static_cast<uint32_t>(p.P) : 1u, p.policy.max_workgroups,
+                         static_cast<hipStream_t>(stream));
     return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
 }
 
@@ -245,8 +246,9 @@ purlin_status purlin_exec(purlin_plan_t plan, void* const* bufs, void* stream) {
     }
     for (int i = 0; i < p.nphases; ++i) {
         const purlin::Phase& ph = p.phases[i];
-        const hipError_t e = purlin::launch_phase(p.d_items + ph.begin, ph.count, ph.kind, ph.nsrc, ph.src_buf,
-                                                  ph.src_step, ph.nt_load, ph.nt_store, p.dtype, bufs, 2 * P, s);
+        const hipError_t e =
+            purlin::launch_phase(p.d_items + ph.begin, ph.count, ph.kind, ph.nsrc, ph.src_buf, ph.src_step, ph.nt_load,
+                                 ph.nt_store, p.dtype, bufs, 2 * P, p.policy.max_workgroups, s);
         if (e != hipSuccess) return PURLIN_ERR_DEVICE;
     }
     return PURLIN_OK;

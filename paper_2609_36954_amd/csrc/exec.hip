@@ -35,6 +35,7 @@ constexpr int kWavesPerBlock = kBlock / kWave;
 struct ExecArgs {
     const purlin_desc* items;
     uint64_t n_items;
+    uint64_t wave_stride;  // wavefronts in the grid: a wave takes items w, w + stride, ...
     char* bufs[2 * PURLIN_MAX_RANKS];
     // Sources of a REDUCE phase, resolved on the host: every item of such a
     // phase names the same sources (bufs[src_buf + p * src_step]), so the
@@ -137,10 +138,11 @@ __device__ __forceinline__ void run_copy(const ExecArgs& a, const purlin_desc& d
 
 template <int U, bool NTL, bool NTS>
 __global__ __launch_bounds__(kBlock) void exec_copy(ExecArgs a) {
-    const uint32_t w = wave_index();
-    if (w >= a.n_items) return;
-    const purlin_desc d = a.items[w];
-    run_copy<U, NTL, NTS>(a, d, lane_index());
+    // one item per wave unless the grid is capped (then the waves stride)
+    for (uint64_t i = wave_index(); i < a.n_items; i += a.wave_stride) {
+        const purlin_desc d = a.items[i];
+        run_copy<U, NTL, NTS>(a, d, lane_index());
+    }
 }
 
 // Eq. 2 on one 16-byte vector of every source: 8 bf16 or 4 fp32 elements.
@@ -238,10 +240,10 @@ __device__ __forceinline__ void run_reduce(const ExecArgs& a, const purlin_desc&
 
 template <int NSRC, bool BF16, int U, bool NTL, bool NTS>
 __global__ __launch_bounds__(kBlock) void exec_reduce(ExecArgs a) {
-    const uint32_t w = wave_index();
-    if (w >= a.n_items) return;
-    const purlin_desc d = a.items[w];
-    run_reduce<NSRC, BF16, U, NTL, NTS>(a, d, lane_index());
+    for (uint64_t i = wave_index(); i < a.n_items; i += a.wave_stride) {
+        const purlin_desc d = a.items[i];
+        run_reduce<NSRC, BF16, U, NTL, NTS>(a, d, lane_index());
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -639,7 +641,7 @@ hipError_t launch_fused_allreduce(const purlin_desc* items, uint64_t n, uint64_t
 hipError_t launch_v(purlin_op op, const purlin_desc* items, uint64_t n, int P, purlin_dtype dtype, bool streaming,
                     void* const* bufs, const int32_t* counts, bool counts_transposed, bool source_major,
                     int32_t* status, uint64_t in_capacity, uint64_t out_capacity, uint64_t unit, uint64_t chunk,
-                    uint64_t item_bytes, uint32_t spaces, hipStream_t stream) {
+                    uint64_t item_bytes, uint32_t spaces, uint32_t max_workgroups, hipStream_t stream) {
     if (chunk == 0 || item_bytes == 0 || spaces == 0 || n % spaces != 0) return hipErrorInvalidValue;
     ExecArgs a{};
     a.items = items;
@@ -657,7 +659,8 @@ hipError_t launch_v(purlin_op op, const purlin_desc* items, uint64_t n, int P, p
     // least one wave: it validates the sizes and writes the status even
     // when the plan has no items (zero capacity).
     const uint64_t per_wave = op == PURLIN_REDUCE_SCATTERV ? 1 : 2;
-    const uint64_t waves = std::max<uint64_t>(1, (n + per_wave - 1) / per_wave);
+    uint64_t waves = std::max<uint64_t>(1, (n + per_wave - 1) / per_wave);
+    if (max_workgroups) waves = std::min<uint64_t>(waves, uint64_t(max_workgroups) * kWavesPerBlock);
     VGrid g{chunk, item_bytes, (chunk + item_bytes - 1) / item_bytes, n / spaces, static_cast<uint32_t>(waves)};
     const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
     const bool bf16 = dtype == PURLIN_BF16;
@@ -735,7 +738,7 @@ hipError_t launch_stream_copy(void* dst, const void* src, uint64_t bytes, hipStr
 
 hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
                         uint32_t src_step, bool nt_load, bool nt_store, purlin_dtype dtype, void* const* bufs,
-                        int nbufs, hipStream_t stream) {
+                        int nbufs, uint32_t max_workgroups, hipStream_t stream) {
     if (n == 0) return hipSuccess;
     ExecArgs a{};
     a.items = items;
@@ -748,7 +751,11 @@ hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uin
             a.srcs[p] = static_cast<char*>(bufs[b]);
         }
     }
-    const dim3 grid(static_cast<uint32_t>((n + kWavesPerBlock - 1) / kWavesPerBlock));
+    uint64_t blocks = (n + kWavesPerBlock - 1) / kWavesPerBlock;
+    if (max_workgroups) blocks = std::min<uint64_t>(blocks, max_workgroups);
+    if (blocks > 0xffffffffull) return hipErrorInvalidValue;
+    a.wave_stride = blocks * kWavesPerBlock;
+    const dim3 grid(static_cast<uint32_t>(blocks));
     (void)hipGetLastError();
     if (kind == PURLIN_KIND_COPY) {
         launch_copy(grid, stream, a, nt_load, nt_store);

@@ -19,7 +19,7 @@ hipError_t launch_stream_copy(void* dst, const void* src, uint64_t bytes, hipStr
 
 hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
                         uint32_t src_step, bool nt_load, bool nt_store, purlin_dtype dtype, void* const* bufs,
-                        int nbufs, hipStream_t stream);
+                        int nbufs, uint32_t max_workgroups, hipStream_t stream);
 
 // Device state of a single-launch AllReduce plan (zeroed at plan creation).
 struct FusedState {
@@ -42,7 +42,7 @@ hipError_t launch_fused_allreduce(const purlin_desc* items, uint64_t n, uint64_t
 hipError_t launch_v(purlin_op op, const purlin_desc* items, uint64_t n, int P, purlin_dtype dtype, bool streaming,
                     void* const* bufs, const int32_t* counts, bool counts_transposed, bool source_major,
                     int32_t* status, uint64_t in_capacity, uint64_t out_capacity, uint64_t unit, uint64_t chunk,
-                    uint64_t item_bytes, uint32_t spaces, hipStream_t stream);
+                    uint64_t item_bytes, uint32_t spaces, uint32_t max_workgroups, hipStream_t stream);
 
 struct PackWorkspace {
     int32_t* tile_base;  // [ntiles * E]: per-tile expert counts, then row bases

@@ -100,9 +100,7 @@ bool parse_policy(const purlin_policy* policy, purlin_policy& pol) {
     if (pol.item_bytes % 16 != 0) return false;
     if (pol.fanout > 2 || pol.ar_mode > 3) return false;
     if (pol.load_hint > 2 || pol.store_hint > 2) return false;
-    for (uint32_t r : pol.reserved)
-        if (r != 0) return false;
-    return true;
+    return pol.reserved == 0;
 }
 
 // Cuts out.descs into work items phase by phase, records the launches and
@@ -133,6 +131,7 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
     const uint64_t Cp = part ? ceil_div(part, chunk) : 0;
 
     if (pol.fanout == 0) pol.fanout = 2;
+    if (pol.max_workgroups && op == PURLIN_ALLREDUCE && pol.ar_mode == 3) return PURLIN_ERR_UNSUPPORTED;
     if (share >= 0 && op == PURLIN_ALLREDUCE) {
         // A rank's share of an AllReduce is its ReduceScatter partition and
         // the pulls of the others (compose<RS, AG>); the one-phase form would

@@ -70,7 +70,8 @@ class Policy(ctypes.Structure):
         ("ar_mode", ctypes.c_uint32),
         ("load_hint", ctypes.c_uint32),  # 0 auto, 1 cached, 2 non-temporal
         ("store_hint", ctypes.c_uint32),
-        ("reserved", ctypes.c_uint32 * 2),
+        ("max_workgroups", ctypes.c_uint32),  # 0 = one wavefront per work item
+        ("reserved", ctypes.c_uint32),
     ]
 
 

@@ -1,0 +1,86 @@
+"""Collectives on a bounded share of the GPU (policy max_workgroups).
+
+With the grid capped at a few workgroups every wavefront strides over many
+work items (and, for the variable-size collectives, over the active items
+of the run-time sizes).  The results must be the oracle's, bit for bit,
+whatever the cap: every op, both element types, ragged partitions.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import CANARY, Guarded, assert_bits_equal, np_dtype, to_device, to_host, torch_dtype
+from paper_2609_36954_amd import purlin as PL
+from test_gpu_exec import _inputs
+from test_planner_v import _case_counts, _oracle_v
+
+pytestmark = pytest.mark.gpu
+
+S = {"fp32": 4, "bf16": 2}
+CAPS = (1, 3, 16)
+
+
+def _want(op, ins, dtype, P, M, root):
+    if op == "allgather":
+        return oracle.all_gather([a[:M] for a in ins], dtype)
+    if op == "gather":
+        return oracle.gather([a[:M] for a in ins], root, dtype)
+    if op in PL.ROOTED:
+        return getattr(oracle, op)(ins, root, dtype)
+    return {"allreduce": oracle.all_reduce, "reduce_scatter": oracle.reduce_scatter,
+            "alltoall": oracle.all_to_all}[op](ins, dtype)
+
+
+CASES = [(op, dt, P, M) for op in ("allreduce", "reduce_scatter", "allgather", "alltoall", "broadcast", "reduce",
+                                   "scatter", "gather")
+         for dt in ("fp32", "bf16") for P, M in ((1, 999), (3, 4099), (8, 20003))]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "-".join(map(str, c)))
+def test_capped_grid_matches_oracle(case):
+    op, dtype, P, M = case
+    s = S[dtype]
+    ins_np = _inputs(P, P * M, dtype, seed=P * 7 + M)
+    root = P - 1 if op in PL.ROOTED else None
+    want = _want(op, ins_np, dtype, P, M, root)
+    modes = [{"ar_mode": 1}, {"ar_mode": 2}] if op == "allreduce" else [{}]
+    for cap in CAPS:
+        for extra in modes:
+            plan = PL.Plan(op, P, P * M, dtype, 1024 * s, root=root,
+                           policy=dict(max_workgroups=cap, item_bytes=256, **extra))
+            use_in, use_out = PL.used_buffers(plan)
+            ins = [to_device(a[: plan.in_bytes // s]) if u else None for a, u in zip(ins_np, use_in)]
+            outs = [Guarded(plan.out_bytes, torch_dtype(dtype)) if u else None for u in use_out]
+            plan.exec(ins, [o.t if o is not None else None for o in outs])
+            torch.cuda.synchronize()
+            for r in range(P):
+                if want[r] is None:
+                    continue
+                assert outs[r].intact()
+                assert_bits_equal(to_host(outs[r].t, np_dtype(dtype)), want[r], dtype, f"{op} cap={cap} {extra} r={r}")
+
+
+@pytest.mark.parametrize("op", ["allgatherv", "reduce_scatterv", "alltoallv"])
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_capped_grid_variable_sizes(op, dtype):
+    P, cap_elems, unit = 8, 6000, 3
+    rng = np.random.default_rng(11)
+    counts = _case_counts("zipf", op, P, cap_elems // unit, rng)
+    ins_np = _inputs(P, cap_elems, dtype, seed=5)
+    want = _oracle_v(op, ins_np, counts, P, dtype, unit)
+    for cap in CAPS:
+        plan = PL.Plan(op, P, cap_elems, dtype, 512, unit=unit, policy=dict(max_workgroups=cap))
+        ins = [to_device(a) for a in ins_np]
+        outs = [Guarded(plan.out_bytes, torch_dtype(dtype)) for _ in range(P)]
+        st = torch.full((4,), 7, dtype=torch.int32, device="cuda")
+        plan.exec_v(ins, [o.t for o in outs], to_device(np.asarray(counts, np.int32)), dev_status=st)
+        torch.cuda.synchronize()
+        assert int(st[0].item()) == 0
+        for r in range(P):
+            assert outs[r].intact()
+            got = to_host(outs[r].t, np_dtype(dtype))
+            n = len(want[r])
+            assert_bits_equal(got[:n], want[r], dtype, f"{op} cap={cap} rank {r}")
+            assert np.all(got[n:].view(np.uint8) == CANARY)
