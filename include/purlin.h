@@ -307,9 +307,19 @@ PURLIN_API purlin_status purlin_plan_items(purlin_plan_t plan, const purlin_desc
  * launch on `stream`; no host-device copy, no allocation, no
  * synchronisation (graph-capturable).  Errors (nothing enqueued):
  * PURLIN_ERR_INVALID for a NULL or host-only plan, NULL bufs, a NULL or
- * misaligned pointer, an input range overlapping an output range, or two
- * output ranges overlapping; PURLIN_ERR_DEVICE if a launch fails.
- * Inputs may alias each other.  For count = 0 it returns PURLIN_OK and
+ * misaligned pointer, an input range overlapping an output range other
+ * than an in-place pair (below), or two output ranges overlapping;
+ * PURLIN_ERR_DEVICE if a launch fails.  Inputs may alias each other.
+ * In place: a rank's input and output may be one buffer in the layouts
+ * where every element is read before it is rewritten by the same
+ * wavefront (or by a later phase):
+ *     ALLREDUCE, BROADCAST, REDUCE   in_r == out_r
+ *     REDUCE_SCATTER, SCATTER        out_r == in_r + r * out_bytes_per_rank
+ *     ALLGATHER, GATHER              in_r == out_r + r * in_bytes_per_rank
+ * (rooted ops: the root's own pair only; the pointers must still be
+ * 16-byte aligned, so an offset of r partitions needs out_bytes_per_rank
+ * resp. in_bytes_per_rank to be a multiple of 16); not ALLTOALL, not the
+ * variable-size collectives.  For count = 0 it returns PURLIN_OK and
  * ignores bufs.  A plan is immutable: concurrent execs on different
  * streams with distinct buffers are safe. */
 PURLIN_API purlin_status purlin_exec(purlin_plan_t plan, void* const* bufs, void* stream);

@@ -85,8 +85,38 @@ bool pack_limits_ok(int T, int H, int K, int E) {
     return static_cast<int64_t>(T) * K < (int64_t(1) << 31) && purlin::moe_launch_fits(T, H);
 }
 
+// The one input/output overlap a plan allows: rank r's in-place layout,
+// where every element is read and rewritten by the same wavefront (or, for
+// AllReduce's second phase, rewritten after the first phase has read it).
+//   ALLREDUCE, BROADCAST, REDUCE   in_r == out_r
+//   REDUCE_SCATTER, SCATTER        out_r == in_r + r * out_bytes
+//   ALLGATHER, GATHER              in_r == out_r + r * in_bytes
+// Rooted ops only for the root's own pair; ALLTOALL and the variable-size
+// ops never (an element there is rewritten before other waves read it).
+bool in_place_pair(const purlin::Plan& p, int i, int r, const void* in, const void* out) {
+    if (i != r || p.vop) return false;
+    if (p.op >= PURLIN_BROADCAST && p.op <= PURLIN_GATHER && r != p.root) return false;
+    const char* a = static_cast<const char*>(in);
+    const char* b = static_cast<const char*>(out);
+    switch (p.op) {
+        case PURLIN_ALLREDUCE:
+        case PURLIN_BROADCAST:
+        case PURLIN_REDUCE:
+            return a == b;
+        case PURLIN_REDUCE_SCATTER:
+        case PURLIN_SCATTER:
+            return b == a + uint64_t(r) * p.out_bytes;
+        case PURLIN_ALLGATHER:
+        case PURLIN_GATHER:
+            return a == b + uint64_t(r) * p.in_bytes;
+        default:
+            return false;
+    }
+}
+
 // Host-side checks shared by purlin_exec and purlin_exec_v: non-null,
-// aligned, no input/output or output/output overlap among used buffers.
+// aligned, no input/output overlap other than an in-place pair, no
+// output/output overlap among used buffers.
 purlin_status check_buffers(const purlin::Plan& p, void* const* bufs) {
     if (p.flags & PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
     if (!bufs) return PURLIN_ERR_INVALID;
@@ -96,7 +126,8 @@ purlin_status check_buffers(const purlin::Plan& p, void* const* bufs) {
         if (used(i) && (!bufs[i] || !aligned16(bufs[i]))) return PURLIN_ERR_INVALID;
     for (int i = 0; i < P; ++i)
         for (int r = 0; r < P; ++r)
-            if (used(i) && used(P + r) && overlaps(bufs[i], p.in_bytes, bufs[P + r], p.out_bytes))
+            if (used(i) && used(P + r) && overlaps(bufs[i], p.in_bytes, bufs[P + r], p.out_bytes) &&
+                !in_place_pair(p, i, r, bufs[i], bufs[P + r]))
                 return PURLIN_ERR_INVALID;
     for (int r = 0; r < P; ++r)
         for (int q = r + 1; q < P; ++q)
