@@ -15,9 +15,10 @@ Plans are built once per shape (host orchestration, like the paper's
 compile-time specialisation) and reused; every step re-executes them.
 
 value = algorithmic bytes of a step (reads + writes each op must make at
-least once) / wall time of a step, in GB/s (1e9 bytes/s), over steps with
-nothing between the ops.  Per-op times come from as many further steps with
-HIP events recorded between the ops, on the stream the kernels run on.  The decode-size
+least once) / wall time of a step, in GB/s (1e9 bytes/s); in the timed steps
+only the dominant kernel is bracketed by HIP events (its launch duration
+gives the roofline).  Per-op times come from as many steps before them, with
+HIP events recorded between all the ops, on the stream the kernels run on.  The decode-size
 AllReduce (P=8, bf16, 128 x 8192 per rank) and the small AllReduce (P=4,
 fp32, 262144 per rank) are timed separately as latency: 128 calls captured
 in a graph, one warm-up replay, eight timed replays, time / 1024 (the
@@ -52,6 +53,49 @@ KERNEL_OF_OP = {
 }
 CALIBRATION_KERNEL = "copy"  # torch's device-to-device copy of --calibrate-copy
 CALIBRATION_BYTES = 1 << 30
+
+
+class TimingEvent:
+    """A HIP event for timing only, created with hipEventDisableSystemFence:
+    recording it skips the system-scope cache write-back and invalidation
+    that a default event performs (several µs of stream time between two
+    kernels), so bracketing a kernel barely perturbs the step.  Recorded on
+    the stream the kernels run on; read after a device synchronisation.
+    The HIP runtime is the one torch loaded (same soname)."""
+
+    _hip = None
+
+    def __init__(self, torch):
+        import ctypes
+
+        if TimingEvent._hip is None:
+            h = ctypes.CDLL("libamdhip64.so.7")
+            h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            TimingEvent._hip = h
+        self._ctypes = ctypes
+        self._torch = torch
+        self.ev = ctypes.c_void_p()
+        if TimingEvent._hip.hipEventCreateWithFlags(ctypes.byref(self.ev), 0x20000000) != 0:  # hipEventDisableSystemFence
+            raise RuntimeError("hipEventCreateWithFlags failed")
+
+    def record(self):
+        st = self._ctypes.c_void_p(self._torch.cuda.current_stream().cuda_stream)
+        if TimingEvent._hip.hipEventRecord(self.ev, st) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_time(self, end):
+        """Milliseconds from this event to ``end`` (both recorded and complete)."""
+        ms = self._ctypes.c_float()
+        if TimingEvent._hip.hipEventElapsedTime(self._ctypes.byref(ms), self.ev, end.ev) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def __del__(self):
+        if TimingEvent._hip is not None and self.ev:
+            TimingEvent._hip.hipEventDestroy(self.ev)
 
 
 def log(*a):
@@ -173,6 +217,10 @@ def main():
     ap.add_argument("--no-latency-sweep", action="store_true",
                     help="skip the sweep of AllReduce, ReduceScatter, AllGather, AllToAll at 1 KiB..512 KiB per rank")
     ap.add_argument("--no-latency", action="store_true", help="skip the graph-replayed latency measurement")
+    ap.add_argument("--plateau", action="store_true",
+                    help="also time ReduceScatter and AllGather with the grid capped at 4..512 workgroups "
+                         "(off by default: the capped launches share the step's kernels and would skew their "
+                         "per-kernel profiler averages)")
     ap.add_argument("--no-extra", action="store_true", help="skip timing the other collectives (outside the step)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device-to-device tensor copy first (reference for HBM counter scaling)")
@@ -247,51 +295,45 @@ def main():
     ]
     step_bytes = sum(b for _, b, _ in ops)
 
-    def step(evs=None):
-        if evs is not None:
-            evs[0].record()
+    op_names = [name for name, _, _ in ops]
+
+    def step(evs=None, only=None):
+        """One pass of the hot path.  ``evs``: events recorded between the ops
+        (``only``: just around that op)."""
+        def mark(k):
+            if evs is not None and (only is None or k in (only, only + 1)):
+                evs[k if only is None else k - only].record()
+        mark(0)
         rs_plan.exec(ins, rs_out)
-        if evs is not None:
-            evs[1].record()
+        mark(1)
         ag_plan.exec(rs_out, ag_out)
-        if evs is not None:
-            evs[2].record()
+        mark(2)
         PL.purlin_pack(x, ids, E, P, out=pack_out, workspace=ws)
-        if evs is not None:
-            evs[3].record()
+        mark(3)
         PL.purlin_unpack(y, pack_out["pos"], g, out=comb_out)
-        if evs is not None:
-            evs[4].record()
+        mark(4)
 
     log("bench: warmup")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    # The timed steps carry no instrumentation (an event between two ops costs
-    # ~4 µs of stream time); the per-op breakdown comes from as many steps
-    # again, outside the timed region, with events between the ops.
-    log(f"bench: timing {args.steps} steps")
-    torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    for i in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    ms_per_step = wall * 1e3 / args.steps
-
-    log(f"bench: per-op breakdown ({args.steps} more steps, events between the ops)")
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    # Per-op breakdown first: as many steps as timed, HIP events between the
+    # ops (on the stream the kernels run on).  Figures are the mean over the
+    # steps, with the median beside it (a host stall that lets the stream
+    # drain inflates one step's gap).
+    log(f"bench: per-op breakdown ({args.steps} steps, events between the ops)")
+    events = [[TimingEvent(torch) for _ in range(5)] for _ in range(args.steps)]
     for i in range(args.steps):
         step(events[i])
     torch.cuda.synchronize()
-
     per_op = {}
     for j, (name, bmin, bsched) in enumerate(ops):
         ts = [events[i][j].elapsed_time(events[i][j + 1]) for i in range(args.steps)]
         avg_ms = float(np.mean(ts))
         per_op[name] = {
             "avg_us": round(avg_ms * 1e3, 2),
+            "median_us": round(float(np.median(ts)) * 1e3, 2),
             "min_us": round(float(np.min(ts)) * 1e3, 2),
             "bytes_min": int(bmin),
             "bytes_sched": int(bsched),
@@ -300,12 +342,29 @@ def main():
         }
         if name in ("reduce_scatter", "allgather"):  # the paper's algorithm bandwidth: per-rank message / time
             per_op[name]["algbw_GBps"] = round(N * s / (avg_ms * 1e-3) / 1e9, 1)
-    value = step_bytes / (ms_per_step * 1e-3) / 1e9
 
     # dominant single-kernel op (RS, AG and combine are one launch each)
     single = ["reduce_scatter", "allgather", "moe_combine"]
-    dom = max(single, key=lambda n: per_op[n]["avg_us"])
-    achieved = per_op[dom]["bytes_min"] / (per_op[dom]["avg_us"] * 1e-6) / 1e9
+    dom = max(single, key=lambda n: per_op[n]["median_us"])
+    di = op_names.index(dom)
+
+    # The timed region: exactly `steps` steps between two synchronisations,
+    # wall-clocked for the value; events only around the dominant kernel (two
+    # per step: its launch duration for the roofline, live on its stream).
+    log(f"bench: timing {args.steps} steps")
+    dom_ev = [[TimingEvent(torch) for _ in range(2)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for i in range(args.steps):
+        step(dom_ev[i], only=di)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms_per_step = wall * 1e3 / args.steps
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
+
+    dom_ts = [e[0].elapsed_time(e[1]) for e in dom_ev]
+    dom_us = float(np.mean(dom_ts)) * 1e3
+    achieved = per_op[dom]["bytes_min"] / (dom_us * 1e-6) / 1e9
     traffic = None
     tr = load_traffic(src_hash)
     if tr and dom in tr.get("ops", {}):
@@ -319,6 +378,9 @@ def main():
         "unit": "GB/s",
         "frac": round(achieved / HBM_PEAK_GBS, 4),
         "traffic": traffic,
+        "launch_us": round(dom_us, 2),
+        "launch_us_median": round(float(np.median(dom_ts)) * 1e3, 2),
+        "timing": "HIP events (no system fence) around the kernel in each timed step, on its stream",
     }
 
     # ---------------- latency: decode-size AllReduce ----------------
@@ -355,7 +417,8 @@ def main():
 
         extra["expert_parallel_p8"] = measure_ep(torch, PL, W, P, T, H, E, K)
         extra["rank0_share"] = measure_share(torch, PL, ins, rs_out, ag_out, P, N, s)
-        extra["workgroup_plateau"] = measure_plateau(torch, PL, ins, rs_out, ag_out, P, N, s)
+        if args.plateau:
+            extra["workgroup_plateau"] = measure_plateau(torch, PL, ins, rs_out, ag_out, P, N, s)
 
     latency = None
     if not args.no_latency:
