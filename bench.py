@@ -691,6 +691,29 @@ def measure_plateau(torch, PL, ins, rs_out, ag_out, P, N, s, reps=3):
         full = row["uncapped"]
         knee = next((int(k) for k, v in row.items() if k != "uncapped" and v >= 0.9 * full), None)
         out[name] = {"GBps_by_workgroups": row, "smallest_cap_within_90pct": knee}
+    # the pipeline depth of the copies (Eq. 1: bandwidth ~ bytes in flight /
+    # latency): 16-byte loads per lane in flight, on a bounded grid
+    depth = {}
+    for cap in (16, 64, 0):
+        row = {}
+        for d in (1, 2, 4, 8):
+            pol = {"copy_depth": d}
+            if cap:
+                pol["max_workgroups"] = cap
+            plan = PL.Plan("allgather", P, N, "bf16", 1 << 20, policy=pol)
+            run = plan.bind(rs_out, ag_out)
+            run()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                run()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / reps
+            row[str(d)] = round(collective_bytes("allgather", P, N, s) / (us * 1e-6) / 1e9, 1)
+        depth[str(cap) if cap else "uncapped"] = row
+    out["allgather_GBps_by_copy_depth"] = depth
     out["what"] = "256 MiB/rank, P=8, bf16, chunk 1 MiB; GB/s = algorithmic bytes / time; 256 CUs on the chip"
     return out
 

@@ -146,7 +146,13 @@ typedef struct purlin_policy {
                             rest to overlapped compute (the paper's
                             resource-constrained execution, Section 5).  Not
                             with ar_mode 3 (PURLIN_ERR_UNSUPPORTED). */
-    uint32_t reserved;   /* must be zero */
+    uint32_t copy_depth; /* copy phases of the fixed-size and rooted
+                            collectives: 16-byte loads each lane keeps in flight
+                            before it stores (the pipeline depth of Section
+                            3.3 / Eq. 1: bytes in flight per wavefront =
+                            copy_depth * 1 KiB); 0 = auto (8 on a grid capped
+                            at 128 workgroups or fewer, else 4), or 1, 2, 4, 8 */
+    uint32_t reserved[3];/* must be zero */
 } purlin_policy;
 
 #define PURLIN_PLAN_HOST_ONLY 1u /* build the tables on the host only (no device

@@ -279,7 +279,7 @@ purlin_status purlin_exec(purlin_plan_t plan, void* const* bufs, void* stream) {
         const purlin::Phase& ph = p.phases[i];
         const hipError_t e =
             purlin::launch_phase(p.d_items + ph.begin, ph.count, ph.kind, ph.nsrc, ph.src_buf, ph.src_step, ph.nt_load,
-                                 ph.nt_store, p.dtype, bufs, 2 * P, p.policy.max_workgroups, s);
+                                 ph.nt_store, p.dtype, bufs, 2 * P, p.policy.max_workgroups, p.policy.copy_depth, s);
         if (e != hipSuccess) return PURLIN_ERR_DEVICE;
     }
     return PURLIN_OK;

@@ -348,8 +348,8 @@ void launch_reduce(dim3 grid, hipStream_t stream, const ExecArgs& a, bool bf16, 
         launch_reduce_hints<NSRC, false>(grid, stream, a, ntl, nts);
 }
 
-void launch_copy(dim3 grid, hipStream_t stream, const ExecArgs& a, bool ntl, bool nts) {
-    constexpr int U = kCopyUnroll;
+template <int U>
+void launch_copy_u(dim3 grid, hipStream_t stream, const ExecArgs& a, bool ntl, bool nts) {
     if (ntl && nts)
         hipLaunchKernelGGL((exec_copy<U, true, true>), grid, dim3(kBlock), 0, stream, a);
     else if (ntl)
@@ -358,6 +358,16 @@ void launch_copy(dim3 grid, hipStream_t stream, const ExecArgs& a, bool ntl, boo
         hipLaunchKernelGGL((exec_copy<U, false, true>), grid, dim3(kBlock), 0, stream, a);
     else
         hipLaunchKernelGGL((exec_copy<U, false, false>), grid, dim3(kBlock), 0, stream, a);
+}
+
+// `depth`: 16-byte loads in flight per lane (1, 2, 4, 8; 0 = kCopyUnroll).
+void launch_copy(dim3 grid, hipStream_t stream, const ExecArgs& a, bool ntl, bool nts, uint32_t depth) {
+    switch (depth) {
+        case 1: launch_copy_u<1>(grid, stream, a, ntl, nts); break;
+        case 2: launch_copy_u<2>(grid, stream, a, ntl, nts); break;
+        case 8: launch_copy_u<8>(grid, stream, a, ntl, nts); break;
+        default: launch_copy_u<kCopyUnroll>(grid, stream, a, ntl, nts); break;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -738,7 +748,7 @@ hipError_t launch_stream_copy(void* dst, const void* src, uint64_t bytes, hipStr
 
 hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
                         uint32_t src_step, bool nt_load, bool nt_store, purlin_dtype dtype, void* const* bufs,
-                        int nbufs, uint32_t max_workgroups, hipStream_t stream) {
+                        int nbufs, uint32_t max_workgroups, uint32_t copy_depth, hipStream_t stream) {
     if (n == 0) return hipSuccess;
     ExecArgs a{};
     a.items = items;
@@ -758,7 +768,7 @@ hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uin
     const dim3 grid(static_cast<uint32_t>(blocks));
     (void)hipGetLastError();
     if (kind == PURLIN_KIND_COPY) {
-        launch_copy(grid, stream, a, nt_load, nt_store);
+        launch_copy(grid, stream, a, nt_load, nt_store, copy_depth);
     } else {
         const bool bf16 = dtype == PURLIN_BF16;
         switch (nsrc) {

@@ -19,7 +19,7 @@ hipError_t launch_stream_copy(void* dst, const void* src, uint64_t bytes, hipStr
 
 hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
                         uint32_t src_step, bool nt_load, bool nt_store, purlin_dtype dtype, void* const* bufs,
-                        int nbufs, uint32_t max_workgroups, hipStream_t stream);
+                        int nbufs, uint32_t max_workgroups, uint32_t copy_depth, hipStream_t stream);
 
 // Device state of a single-launch AllReduce plan (zeroed at plan creation).
 struct FusedState {

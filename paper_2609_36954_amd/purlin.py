@@ -71,7 +71,8 @@ class Policy(ctypes.Structure):
         ("load_hint", ctypes.c_uint32),  # 0 auto, 1 cached, 2 non-temporal
         ("store_hint", ctypes.c_uint32),
         ("max_workgroups", ctypes.c_uint32),  # 0 = one wavefront per work item
-        ("reserved", ctypes.c_uint32),
+        ("copy_depth", ctypes.c_uint32),  # 16-byte loads in flight per lane for copies (0 = auto)
+        ("reserved", ctypes.c_uint32 * 3),
     ]
 
 

@@ -90,12 +90,15 @@ def test_plan_argument_validation(args, want):
         (dict(fanout=3), INVALID),
         (dict(ar_mode=4), INVALID),
         (dict(ar_mode=3), 0),
-        (dict(reserved=1), INVALID),
+        (dict(reserved=(ctypes.c_uint32 * 3)(0, 0, 1)), INVALID),
+        (dict(copy_depth=3), INVALID),
+        (dict(copy_depth=8), 0),
         (dict(load_hint=3), INVALID),
         (dict(store_hint=3), INVALID),
         (dict(load_hint=2, store_hint=1), 0),
         (dict(item_bytes=1 << 20, fanout=1, ar_mode=1), 0),
         (dict(max_workgroups=1), 0),
+        (dict(max_workgroups=1, copy_depth=1), 0),
         (dict(max_workgroups=64, ar_mode=2), 0),
         (dict(max_workgroups=8, ar_mode=3), 2),  # the single-launch AllReduce needs one wave per item
     ],

@@ -46,6 +46,8 @@ def test_capped_grid_matches_oracle(case):
     root = P - 1 if op in PL.ROOTED else None
     want = _want(op, ins_np, dtype, P, M, root)
     modes = [{"ar_mode": 1}, {"ar_mode": 2}] if op == "allreduce" else [{}]
+    if op in ("allgather", "alltoall", "broadcast", "scatter", "gather") or op == "allreduce":
+        modes = modes + [dict(m, copy_depth=d) for m in modes[:1] for d in (1, 2, 8)]
     for cap in CAPS:
         for extra in modes:
             plan = PL.Plan(op, P, P * M, dtype, 1024 * s, root=root,
