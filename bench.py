@@ -647,6 +647,12 @@ def measure_share(torch, PL, ins, rs_out, ag_out, P, N, s, reps=5):
         ("allgather", PL.Plan("allgather", P, N, "bf16", 1 << 20, share=0), rs_out, [ag_out[0]] + [None] * (P - 1)),
         ("allreduce", PL.Plan("allreduce", P, N, "bf16", 1 << 20, share=0), ins, ag_out),
     ]
+    # push shares (the descriptors that read in_0): the copy collectives only
+    cases += [
+        ("allgather_push", PL.Plan("allgather", P, N, "bf16", 1 << 20, share=0, push=True), rs_out, ag_out),
+        ("alltoall_push", PL.Plan("alltoall", P, N, "bf16", 1 << 20, share=0, push=True), ins, ag_out),
+        ("alltoall", PL.Plan("alltoall", P, N, "bf16", 1 << 20, share=0), ins, [ag_out[0]] + [None] * (P - 1)),
+    ]
     for name, plan, i, o in cases:
         run = plan.bind(i, o)
         run()
@@ -661,8 +667,9 @@ def measure_share(torch, PL, ins, rs_out, ag_out, P, N, s, reps=5):
         out[name] = {"avg_us": round(us, 2), "bytes": int(plan.sched_bytes),
                      "GBps": round(plan.sched_bytes / (us * 1e-6) / 1e9, 1),
                      "frac_of_hbm_peak": round(plan.sched_bytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
-    out["what"] = ("rank 0's share (the descriptors writing out_0) at P=8, 256 MiB per rank, bf16, chunk 1 MiB; "
-                   "the other ranks' buffers stand in for peer memory")
+    out["what"] = ("rank 0's share at P=8, 256 MiB per rank, bf16, chunk 1 MiB: pull (the descriptors writing out_0) "
+                   "and, for the copies, push (the descriptors reading in_0); the other ranks' buffers stand in for "
+                   "peer memory")
     return out
 
 

@@ -158,6 +158,9 @@ typedef struct purlin_policy {
 #define PURLIN_PLAN_HOST_ONLY 1u /* build the tables on the host only (no device
                                     upload); such a plan can be inspected but
                                     not executed */
+#define PURLIN_PLAN_SHARE_PUSH 4u /* purlin_plan_share only: the rank's push
+                                    share (the descriptors that read its
+                                    input) instead of its pull share */
 #define PURLIN_PLAN_COUNTS_TRANSPOSED 2u /* ALLTOALLV only: read the P x P
                                     sizes column-major, counts[r*P + p] =
                                     what rank p sends to rank r.  The reverse
@@ -227,9 +230,17 @@ PURLIN_API purlin_status purlin_plan_rooted(purlin_op op, int P, int root, uint6
  * rooted ones.  The share reads and writes only the buffers its
  * descriptors name (purlin_exec checks those; the others may be NULL) and
  * writes out_rank and nothing else.  The P shares together write exactly
- * what the full plan writes.  Other arguments and errors as purlin_plan_ex
- * and purlin_plan_rooted; PURLIN_ERR_INVALID also for rank outside [0, P)
- * or a variable-size op. */
+ * what the full plan writes.
+ * With PURLIN_PLAN_SHARE_PUSH in `flags` the share is instead the
+ * descriptors that read in_rank, unchanged (multi-destination copies keep
+ * every destination): the rank pushes its data into the others' outputs.
+ * Push applies to the collectives made of copies only (ALLGATHER,
+ * ALLTOALL, BROADCAST, SCATTER, GATHER; empty for a BROADCAST or SCATTER
+ * share of a rank that is not the root); a reduction needs every rank's
+ * data in one place, so ALLREDUCE, REDUCE_SCATTER and REDUCE give
+ * PURLIN_ERR_UNSUPPORTED.  The P push shares together are the full plan.
+ * Other arguments and errors as purlin_plan_ex and purlin_plan_rooted;
+ * PURLIN_ERR_INVALID also for rank outside [0, P) or a variable-size op. */
 PURLIN_API purlin_status purlin_plan_share(purlin_op op, int P, int root, int rank, uint64_t count,
                                            purlin_dtype dtype, uint64_t chunk_bytes, const purlin_policy* policy,
                                            uint32_t flags, purlin_plan_t* out_plan);

@@ -124,7 +124,11 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
     if (rooted ? (root < 0 || root >= P) : root != -1) return PURLIN_ERR_INVALID;
     if (share < -1 || share >= P) return PURLIN_ERR_INVALID;
     if (count % static_cast<uint64_t>(P) != 0) return PURLIN_ERR_INVALID;
-    if (flags & ~PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
+    if (flags & ~(PURLIN_PLAN_HOST_ONLY | PURLIN_PLAN_SHARE_PUSH)) return PURLIN_ERR_INVALID;
+    const bool push = (flags & PURLIN_PLAN_SHARE_PUSH) != 0;
+    if (push && share < 0) return PURLIN_ERR_INVALID;
+    if (push && (op == PURLIN_ALLREDUCE || op == PURLIN_REDUCE_SCATTER || op == PURLIN_REDUCE))
+        return PURLIN_ERR_UNSUPPORTED;
     const uint64_t s = dtype == PURLIN_FP32 ? 4 : 2;
     if (chunk < s || chunk % s != 0) return PURLIN_ERR_INVALID;
     if (count > (uint64_t(1) << 58) / s) return PURLIN_ERR_INVALID;
@@ -315,7 +319,21 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
             default:
                 return PURLIN_ERR_INVALID;
         }
-        if (share >= 0) {
+        if (share >= 0 && push) {
+            // Keep the copies that read in_share, as they are.
+            std::vector<purlin_desc> kept;
+            uint32_t out_mask = 0;
+            for (const purlin_desc& d : D) {
+                if (d.kind != PURLIN_KIND_COPY || d.nsrc != 1 || d.src_buf != in0 + static_cast<uint32_t>(share))
+                    continue;
+                for (uint32_t j = 0; j < d.ndst; ++j) out_mask |= 1u << (d.dst_buf + j * d.dst_step - out0);
+                kept.push_back(d);
+            }
+            D.swap(kept);
+            out.in_mask = D.empty() ? 0u : 1u << share;
+            out.out_mask = out_mask;
+            out.share = share;
+        } else if (share >= 0) {
             // Keep what writes out_share, narrowed to that destination; the
             // buffer masks become the buffers the share reads or writes.
             const uint32_t mine = out0 + static_cast<uint32_t>(share);

@@ -34,6 +34,7 @@ KIND_COPY = 0
 KIND_REDUCE = 1
 PLAN_HOST_ONLY = 1
 PLAN_COUNTS_TRANSPOSED = 2
+PLAN_SHARE_PUSH = 4
 MAX_RANKS = 16
 
 # numpy view of purlin_desc (64 bytes, no padding)
@@ -178,7 +179,7 @@ class Plan:
     """A planned collective (immutable).  ``exec`` runs it on a stream."""
 
     def __init__(self, op, P, count, dtype, chunk, policy=None, host_only=False, root=None, unit=None,
-                 out_capacity=None, counts_transposed=False, share=None):
+                 out_capacity=None, counts_transposed=False, share=None, push=False):
         if op not in OPS:
             raise PurlinError(PURLIN_ERR_INVALID, f"unknown op {op!r}")
         if dtype not in DTYPES:
@@ -190,7 +191,10 @@ class Plan:
         self.unit = unit
         self.host_only = bool(host_only)
         self.share = share
+        self.push = bool(push)
         self._used = None
+        if push and share is None:
+            raise PurlinError(PURLIN_ERR_INVALID, "push applies to a rank's share")
         if share is not None and op in VOPS:
             raise PurlinError(PURLIN_ERR_INVALID, f"{op} has no rank shares")
         if (op in VOPS) != (unit is not None):
@@ -209,9 +213,10 @@ class Plan:
             pol = None
             if policy is not None:
                 pol = policy if isinstance(policy, Policy) else Policy(**policy)
+            flags = (PLAN_HOST_ONLY if host_only else 0) | (PLAN_SHARE_PUSH if push else 0)
             st = L.purlin_plan_share(OPS[op], int(P), -1 if root is None else int(root), int(share), int(count),
                                      DTYPES[dtype], int(chunk), ctypes.byref(pol) if pol is not None else None,
-                                     PLAN_HOST_ONLY if host_only else 0, ctypes.byref(h))
+                                     flags, ctypes.byref(h))
         elif root is not None:
             pol = None
             if policy is not None:

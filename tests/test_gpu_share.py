@@ -122,3 +122,31 @@ def test_rank0_share_at_256MiB_per_rank():
     ag.exec(ag_in, ag_out)
     got = to_host(ag_out[0], np.uint16)
     assert np.array_equal(got, np.concatenate([a[:M] for a in ins_np]))
+
+
+PUSH_CASES = [c for c in CASES if c[0] in ("allgather", "alltoall", "broadcast", "scatter", "gather")]
+
+
+@pytest.mark.parametrize("case", PUSH_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_push_shares_match_oracle(case):
+    """Every rank pushes its input into the others' outputs (the descriptors
+    that read in_rank); together the P push shares give the collective."""
+    op, dtype, P, M, ce = case
+    s = S[dtype]
+    ins_np = _inputs(P, P * M, dtype, seed=P * 37 + M)
+    for root in ([0, P - 1] if op in PL.ROOTED else [None]):
+        want = _want(op, ins_np, dtype, P, M, root)
+        shares = [PL.Plan(op, P, P * M, dtype, ce * s, root=root, share=r, push=True) for r in range(P)]
+        ins = [to_device(a[: shares[0].in_bytes // s]) for a in ins_np]
+        outs = [Guarded(shares[0].out_bytes, torch_dtype(dtype)) for _ in range(P)]
+        for o in outs:
+            o.t.view(torch.uint8).fill_(SENTINEL)
+        for r in range(P):
+            shares[r].exec(ins, [o.t for o in outs])
+        torch.cuda.synchronize()
+        for r in range(P):
+            assert outs[r].intact()
+            if want[r] is None:
+                assert bool((outs[r].t.view(torch.uint8) == SENTINEL).all())
+            else:
+                assert_bits_equal(to_host(outs[r].t, np_dtype(dtype)), want[r], dtype, f"{op} push root={root} r={r}")

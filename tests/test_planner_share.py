@@ -192,3 +192,65 @@ def test_share_rejections():
                                PL.ctypes.byref(h)) == PL.PURLIN_ERR_UNSUPPORTED
     with pytest.raises(PL.PurlinError):
         PL.Plan("alltoallv", 4, 64, "fp32", 64, unit=1, share=0, host_only=True)
+
+
+PUSH_OPS = ("allgather", "alltoall", "broadcast", "scatter", "gather")
+
+
+def _key(d):
+    return tuple(int(d[f]) for f in ("kind", "phase", "nsrc", "src_buf", "src_step", "ndst", "dst_buf", "dst_step",
+                                      "src_off", "dst_off", "bytes"))
+
+
+@pytest.mark.parametrize("op", PUSH_OPS)
+@pytest.mark.parametrize("P,M,pol", [(1, 40, {}), (3, 100, {"fanout": 1}), (8, 257, {"fanout": 2}), (5, 64, {})])
+def test_push_shares_are_the_plan_split_by_source(op, P, M, pol):
+    for root in ([0, P - 1] if op in ROOTED else [None]):
+        full = _plan(op, P, P * M, "bf16", 96, root=root, **pol)
+        shares = [PL.Plan(op, P, P * M, "bf16", 96, policy=pol or None, host_only=True, root=root, share=r, push=True)
+                  for r in range(P)]
+        for r, sh in enumerate(shares):
+            use_in, _ = PL.used_buffers(sh)
+            assert [i for i in range(P) if use_in[i]] == ([r] if sh.n_desc else [])
+            for d in sh.descriptors():
+                assert int(d["kind"]) == PL.KIND_COPY and int(d["nsrc"]) == 1 and int(d["src_buf"]) == r
+        got = sorted(_key(d) for sh in shares for d in sh.descriptors())
+        assert got == sorted(_key(d) for d in full.descriptors())
+
+
+@pytest.mark.parametrize("case", [c for c in INTERP_CASES if c[0] in PUSH_OPS], ids=lambda c: "-".join(map(str, c)))
+def test_push_shares_match_oracle(case):
+    op, dtype, P, M, ce = case
+    s = S[dtype]
+    ins = _inputs(P, P * M, dtype, seed=sum(map(ord, str(case))) % 991)
+    for root in ([0, P - 1] if op in ROOTED else [None]):
+        want = _want(op, ins, dtype, P, M, root)
+        shares = [PL.Plan(op, P, P * M, dtype, ce * s, host_only=True, root=root, share=r, push=True)
+                  for r in range(P)]
+        bufs = [np.frombuffer(a.tobytes()[:shares[0].in_bytes], dtype=np.uint8).copy() for a in ins]
+        bufs += [np.full(shares[0].out_bytes, 0xA5, dtype=np.uint8) for _ in range(P)]
+        for sh in reversed(shares):
+            items, _ = sh.items()
+            for it in items:
+                interp.apply_item(it, bufs, dtype)
+        for r in range(P):
+            if want[r] is None:
+                assert np.all(bufs[P + r] == 0xA5)
+                continue
+            bits = np.uint16 if dtype == "bf16" else np.uint32
+            assert np.array_equal(bufs[P + r].view(bits), want[r].view(bits)), (root, r)
+
+
+def test_push_share_rejections():
+    L = PL.lib()
+    h = PL.ctypes.c_void_p(1)
+    push = PL.PLAN_HOST_ONLY | PL.PLAN_SHARE_PUSH
+    for op in ("allreduce", "reduce_scatter"):
+        assert L.purlin_plan_share(PL.OPS[op], 4, -1, 0, 64, 0, 64, None, push,
+                                   PL.ctypes.byref(h)) == PL.PURLIN_ERR_UNSUPPORTED
+    assert L.purlin_plan_share(PL.OPS["reduce"], 4, 1, 0, 64, 0, 64, None, push,
+                               PL.ctypes.byref(h)) == PL.PURLIN_ERR_UNSUPPORTED
+    # the push flag belongs to shares only
+    assert L.purlin_plan_ex(PL.OPS["allgather"], 4, 64, 0, 64, None, push, PL.ctypes.byref(h)) == 1
+    with pytest.raises(PL.PurlinError):
+        PL.Plan("allgather", 4, 64, "fp32", 64, host_only=True, push=True)
