@@ -586,7 +586,8 @@ __global__ __launch_bounds__(kBlock) void unpack_rows(int T, int H, int K, int s
 // Expert-parallel dispatch and combine over P ranks in one pass each.  The
 // dispatch is rank p's pack followed by the AllToAllV of its packed rows,
 // without the packed buffers: once every rank's metadata is known (the
-// per-rank pack_tiles / pack_scan, which write row p of the P x P counts),
+// pack_tiles / pack_scan of all ranks, one launch of each with a grid row or
+// workgroup per rank; rank p's scan writes row p of the P x P counts),
 // each token row goes straight to the receive buffer of every rank owning
 // one of its experts, at
 //     recv_row = sum_{q < p} counts[q][r] + pos_p[t, k] - dest_offsets_p[r].
@@ -610,9 +611,6 @@ struct EpArgs {
     int T, H, K, E, P, slices;
 };
 
-// Every wave of rank p's token t and column slice: lane k < K forms slot k's
-// receiving rank and row from the pack metadata and ep_prefix's sums; if
-// some receive buffer is too small, no wave writes anything.
 // Once per dispatch, after every rank's metadata: before[p][r] = rows rank r
 // receives from ranks < p, and whether every receive buffer holds what it
 // receives (if not, the rows kernel writes nothing).  The status word gets
@@ -647,6 +645,9 @@ __global__ __launch_bounds__(kBlock) void ep_prefix(const int32_t* __restrict__ 
     }
 }
 
+// Every wave of rank p's token t and column slice: lane k < K forms slot k's
+// receiving rank and row from the pack metadata and ep_prefix's sums; if
+// some receive buffer is too small, no wave writes anything.
 template <int U, bool NTL, bool NTS>
 __global__ __launch_bounds__(kBlock) void ep_dispatch_rows(EpArgs a) {
     if (!*a.fits) return;  // uniform: nothing is written
