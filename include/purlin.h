@@ -338,13 +338,16 @@ PURLIN_API purlin_status purlin_plan_items(purlin_plan_t plan, const purlin_desc
  * resp. in_bytes_per_rank to be a multiple of 16); not ALLTOALL, not the
  * variable-size collectives.  For count = 0 it returns PURLIN_OK and
  * ignores bufs.  A plan is immutable: concurrent execs on different
- * streams with distinct buffers are safe. */
+ * streams with distinct buffers are safe (except for a single-launch
+ * AllReduce plan, ar_mode 3, whose per-chunk counters belong to the plan:
+ * run it on one stream at a time). */
 PURLIN_API purlin_status purlin_exec(purlin_plan_t plan, void* const* bufs, void* stream);
 
 /* Device error word of a plan (0 = none).  Only single-launch AllReduce
  * plans (ar_mode 3) can set it: a copy that waited longer than a fixed bound
  * for its chunk gives up and sets it, so a launch always completes.
- * Synchronous: waits for the device to finish the plan's queued work. */
+ * Synchronous: waits for all work queued on the device (a device-wide
+ * synchronisation), then reads the word. */
 PURLIN_API purlin_status purlin_plan_device_error(purlin_plan_t plan, uint32_t* error);
 
 /* Free a plan (NULL-safe).  Does not synchronise: the caller keeps the plan
