@@ -212,3 +212,32 @@ def test_binding_rejects_undersized_outputs_before_launch():
     with pytest.raises(PL.PurlinError):
         PL.purlin_unpack(r["packed"], r["pos"], g, out=torch.empty(T * H - 1, dtype=torch.int16, device="cuda"))
     torch.cuda.synchronize()
+
+
+def test_pack_and_combine_beyond_4GiB():
+    """40960 tokens x 7168, top-8 of 256: the packed matrix is 4.7 GB, so row
+    offsets pass 2^32 bytes in pack and combine.  Positions and counts are
+    compared with the oracle's (computed on 8 columns of the same tokens),
+    sampled rows bit for bit, and the combine of the packed rows with gates
+    1/8 returns every token exactly (K equal rows weighted 1/K)."""
+    T, H, K, E, P = 40960, 7168, 8, 256, 8
+    ids = W.zipf_topk_ids(T, E, K, 1.1, seed=31).astype(np.int32)
+    rng = np.random.default_rng(31)
+    x_d = torch.randn(T, H, device="cuda").to(torch.bfloat16).view(torch.int16)
+    r = PL.purlin_pack(x_d, to_device(ids), E, P)
+    torch.cuda.synchronize()
+    want = oracle.pack(np.zeros((T, 8), np.uint16), ids, E, P)
+    assert np.array_equal(to_host(r["pos"], np.int32).reshape(T, K), want["pos"])
+    assert np.array_equal(to_host(r["dest_counts"], np.int32), want["dest_counts"])
+    assert np.array_equal(to_host(r["expert_offsets"], np.int32), want["expert_offsets"])
+    assert int(want["pos"].max()) * H * 2 > (1 << 32)
+    # the rows that land past 4 GiB and a random sample
+    far = np.argwhere(want["pos"].astype(np.int64) * H * 2 >= (1 << 32))
+    pick = np.concatenate([far[rng.choice(len(far), 128, replace=False)],
+                           np.argwhere(want["pos"] >= 0)[rng.choice(T * K, 128, replace=False)]])
+    for t, k in pick:
+        assert torch.equal(r["packed"][int(want["pos"][t, k])], x_d[t]), (t, k)
+    g = torch.full((T, K), 1.0 / K, device="cuda")
+    out = PL.purlin_unpack(r["packed"], r["pos"], g)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(T, H), x_d)
