@@ -747,3 +747,18 @@ def purlin_stream_copy(dst, src, stream=None):
     st = lib().purlin_stream_copy(_ptr(dst), _ptr(src), int(nbytes), _stream_handle(stream))
     _check(st, "purlin_stream_copy")
     return dst
+
+
+# Short names: plan(...) -> Plan; pack(...) -> (packed, dest_counts,
+# dest_offsets, expert_counts, pos); unpack(...) -> out.
+def plan(op, P, count, dtype, chunk, **kw):
+    return Plan(op, P, count, dtype, chunk, **kw)
+
+
+def pack(x, ids, E, P, **kw):
+    r = purlin_pack(x, ids, E, P, **kw)
+    return r["packed"], r["dest_counts"], r["dest_offsets"], r["expert_counts"], r["pos"]
+
+
+def unpack(y, pos, gates, **kw):
+    return purlin_unpack(y, pos, gates, **kw)

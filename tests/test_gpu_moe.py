@@ -241,3 +241,22 @@ def test_pack_and_combine_beyond_4GiB():
     out = PL.purlin_unpack(r["packed"], r["pos"], g)
     torch.cuda.synchronize()
     assert torch.equal(out.view(T, H), x_d)
+
+
+def test_short_names():
+    """plan / pack / unpack: the same calls under the wrapper's short names."""
+    rng = np.random.default_rng(40)
+    T, H, K, E, P = 100, 64, 4, 16, 4
+    x = to_device(rng.integers(0, 0x7F00, (T, H)).astype(np.uint16))
+    ids = to_device(_distinct_ids(rng, T, K, E))
+    packed, dest_counts, dest_offsets, expert_counts, pos = PL.pack(x, ids, E, P)
+    out = PL.unpack(packed, pos, torch.full((T, K), 1.0 / K, device="cuda"))
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(T, H), x.view(T, H))
+    assert int(dest_counts.sum().item()) == T * K and int(expert_counts.sum().item()) == T * K
+    pl = PL.plan("allreduce", 2, 64, "fp32", 64)
+    a = [torch.ones(64, device="cuda"), torch.full((64,), 2.0, device="cuda")]
+    o = [torch.empty(64, device="cuda") for _ in range(2)]
+    pl.exec(a, o)
+    torch.cuda.synchronize()
+    assert bool((o[0] == 3).all()) and bool((o[1] == 3).all())
