@@ -224,6 +224,9 @@ def main():
     ap.add_argument("--no-latency-sweep", action="store_true",
                     help="skip the sweep of AllReduce, ReduceScatter, AllGather, AllToAll at 1 KiB..512 KiB per rank")
     ap.add_argument("--no-latency", action="store_true", help="skip the graph-replayed latency measurement")
+    ap.add_argument("--bandwidth-sweep", action="store_true",
+                    help="also time AllReduce, ReduceScatter, AllGather and AllToAll at 1 MiB..1 GiB per rank "
+                         "(the paper's bandwidth range; 16 GiB of buffers)")
     ap.add_argument("--plateau", action="store_true",
                     help="also time ReduceScatter and AllGather with the grid capped at 4..512 workgroups "
                          "(off by default: the capped launches share the step's kernels and would skew their "
@@ -426,6 +429,8 @@ def main():
         extra["rank0_share"] = measure_share(torch, PL, ins, rs_out, ag_out, P, N, s)
         if args.plateau:
             extra["workgroup_plateau"] = measure_plateau(torch, PL, ins, rs_out, ag_out, P, N, s)
+        if args.bandwidth_sweep:
+            extra["bandwidth_sweep"] = measure_bandwidth_sweep(torch, PL)
 
     latency = None
     if not args.no_latency:
@@ -677,6 +682,40 @@ def measure_share(torch, PL, ins, rs_out, ag_out, P, N, s, reps=5):
     out["what"] = ("rank 0's share at P=8, 256 MiB per rank, bf16, chunk 1 MiB: pull (the descriptors writing out_0) "
                    "and, for the copies, push (the descriptors reading in_0); the other ranks' buffers stand in for "
                    "peer memory")
+    return out
+
+
+def measure_bandwidth_sweep(torch, PL, P=8, reps=5):
+    """The paper's bandwidth range (Section 5: 1 MiB..1 GiB per rank), P=8,
+    bf16, chunk 1 MiB, for the four collectives: µs, algorithmic GB/s and
+    the paper's algorithm bandwidth (per-rank message / time)."""
+    s = 2
+    big = (1 << 30) // s
+    ins = [torch.empty(big, dtype=torch.int16, device="cuda").fill_(0x3F80) for _ in range(P)]
+    outs = [torch.empty(big, dtype=torch.int16, device="cuda") for _ in range(P)]
+    out = {}
+    for op in ("allreduce", "reduce_scatter", "allgather", "alltoall"):
+        row = {}
+        for mib in (1, 4, 16, 64, 256, 1024):
+            n = (mib << 20) // s
+            i = [t[: n // P] for t in ins] if op == "allgather" else [t[:n] for t in ins]
+            o = [t[: n // P] for t in outs] if op == "reduce_scatter" else [t[:n] for t in outs]
+            run = PL.Plan(op, P, n, "bf16", 1 << 20).bind(i, o)
+            run()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                run()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / reps
+            b = collective_bytes(op, P, n, s)
+            row[f"{mib}MiB"] = {"us": round(us, 1), "GBps": round(b / (us * 1e-6) / 1e9, 1),
+                                "algbw_GBps": round(n * s / (us * 1e-6) / 1e9, 1)}
+        out[op] = row
+    del ins, outs
+    torch.cuda.empty_cache()
     return out
 
 
