@@ -75,16 +75,20 @@ purlin_desc make_desc(uint32_t kind, uint32_t phase, uint32_t nsrc, uint32_t src
 //    512 MiB per rank at P = 8): 2 KiB items, measured 3-6% faster than
 //    the sizes above there (and slower below it).  The waves in flight
 //    then cover a narrower span of every destination buffer at a time.
+//    Variable-size plans keep the sizes above: their waves also map each
+//    item onto the run-time sizes, and 2 KiB items made the AllToAllV
+//    exchanges 18-50% slower.
 //  - Smaller phases (latency regime): aim at kTargetItems items of at
 //    least one wave-wide 16-byte access per lane.
 // Never above kMaxItem, and large enough to keep the item count under
 // PURLIN_MAX_ITEMS.
-uint64_t auto_item_bytes(uint64_t phase_bytes, uint64_t traffic, uint32_t kind, uint32_t nsrc, uint32_t ndst) {
+uint64_t auto_item_bytes(uint64_t phase_bytes, uint64_t traffic, uint32_t kind, uint32_t nsrc, uint32_t ndst,
+                         bool variable) {
     uint64_t item;
     if (traffic >= kStreamingBytes) {
         if (kind == PURLIN_KIND_REDUCE)
             item = pow2_floor(std::max<uint64_t>(1, (32 * 1024) / std::max<uint32_t>(1, nsrc)));
-        else if (traffic >= kLargeCopyBytes)
+        else if (traffic >= kLargeCopyBytes && !variable)
             item = 2048;
         else if (ndst > 1)
             item = std::min<uint64_t>(32 * 1024, pow2_floor(std::max<uint64_t>(1, (256 * 1024) / ndst)));
@@ -409,7 +413,7 @@ purlin_status cut_items(Plan& out, const purlin_policy& pol) {
     for (uint32_t ph = 0; ph < 2; ++ph) {
         PhaseShape& sh = shape[ph];
         if (sh.ndesc == 0) continue;
-        sh.item = pol.item_bytes ? pol.item_bytes : auto_item_bytes(sh.bytes, sh.traffic, sh.kind, sh.nsrc, sh.ndst);
+        sh.item = pol.item_bytes ? pol.item_bytes : auto_item_bytes(sh.bytes, sh.traffic, sh.kind, sh.nsrc, sh.ndst, out.vop);
         for (const purlin_desc& d : out.descs)
             if (d.phase == ph) items_total += ceil_div(d.bytes, sh.item);
         if (items_total > PURLIN_MAX_ITEMS) return PURLIN_ERR_NOMEM;

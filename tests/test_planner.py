@@ -354,3 +354,33 @@ def test_fused_allreduce_claim_order(case):
     for r in range(P):
         got = bufs[P + r].view(np.uint16 if dtype == "bf16" else np.uint32)
         assert np.array_equal(got, want[r].view(got.dtype))
+
+
+# ---------------------------------------------------------------------------
+# automatic work-item sizes by regime (P = 8, bf16, chunk 1 MiB)
+# ---------------------------------------------------------------------------
+
+MiB = 1 << 20
+
+
+@pytest.mark.parametrize("op,mib_per_rank,want", [
+    ("reduce_scatter", 256, 4096),     # 8-way reduce: 32 KiB read per item
+    ("reduce_scatter", 1024, 4096),
+    ("allgather", 256, 32 * 1024),     # one read, 8 writes per item; 2.25 GiB moved
+    ("allgather", 512, 2048),          # 4.5 GiB moved: the large-copy size
+    ("alltoall", 128, 4096),           # one-to-one, 2 GiB moved
+    ("alltoall", 256, 2048),           # 4 GiB moved
+])
+def test_automatic_item_size(op, mib_per_rank, want):
+    N = mib_per_rank * MiB // 2
+    items, _ = PL.Plan(op, 8, N, "bf16", MiB, host_only=True).items()
+    assert int(items["bytes"].max()) == want
+
+
+@pytest.mark.parametrize("op", ["alltoallv", "allgatherv"])
+def test_variable_size_plans_keep_the_streaming_item_size(op):
+    # the same traffic as the fixed-size AllToAll at 256 MiB/rank, but the
+    # waves of a variable-size launch also map items onto run-time sizes
+    N = 256 * MiB // 2
+    items, _ = PL.Plan(op, 8, N, "bf16", MiB, unit=1, host_only=True).items()
+    assert int(items["bytes"].max()) > 2048
