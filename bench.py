@@ -948,6 +948,7 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
     dt, rs_want = median_time(lambda: oracle.reduce_scatter(sub, "bf16"))
     t_total += dt
     bytes_total += collective_bytes("reduce_scatter", P, P * m, 2)
+    per_op = {"reduce_scatter": {"bytes": collective_bytes("reduce_scatter", P, P * m, 2), "seconds": dt}}
     for r in range(P):
         got = down(rs_out[r][:m], np.uint16)
         ok &= bool(np.array_equal(got, rs_want[r]))
@@ -956,6 +957,7 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
     dt, ag_want = median_time(lambda: oracle.all_gather(rs_want, "bf16"))
     t_total += dt
     bytes_total += collective_bytes("allgather", P, P * m, 2)
+    per_op["allgather"] = {"bytes": collective_bytes("allgather", P, P * m, 2), "seconds": dt}
     for r in (0, P - 1):
         got = np.concatenate([down(ag_out[r][k * M:k * M + m], np.uint16) for k in range(P)])
         ok &= bool(np.array_equal(got, ag_want[r]))
@@ -967,6 +969,7 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
     t_pack_single = dt
     t_total += dt
     bytes_total += pack_bytes(T, H, K, E, P)
+    per_op["moe_pack"] = {"bytes": pack_bytes(T, H, K, E, P), "seconds": dt}
     pos_want = pw["pos"]
     ok &= bool(np.array_equal(down(pack_out["pos"], np.int32).reshape(-1, K), pos_want))
     for key in ("dest_counts", "dest_offsets", "expert_counts", "expert_offsets"):
@@ -977,6 +980,7 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
     dt, cw = median_time(lambda: oracle.unpack(y_np, pos_want[:Ts], g_np[:Ts]))
     t_total += dt
     bytes_total += unpack_bytes(Ts, H, K)
+    per_op["moe_combine"] = {"bytes": unpack_bytes(Ts, H, K), "seconds": dt}
     got = down(comb_out[:Ts], np.uint16).reshape(Ts, H)
     ok &= bool(np.array_equal(got, cw))
     max_ulp = max(max_ulp, ulp_gap(got, cw))
@@ -1024,6 +1028,14 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
     del un_blocks
     t_pack = t_pack_single
     t_threaded = dt_rs + dt_ag + t_pack + dt_un
+    for name, dt_thr in (("reduce_scatter", dt_rs), ("allgather", dt_ag), ("moe_pack", t_pack),
+                         ("moe_combine", dt_un)):
+        e = per_op[name]
+        e["seconds_threaded"] = dt_thr
+        e["GBps"] = round(e["bytes"] / e["seconds"] / 1e9, 3)
+        e["GBps_threaded"] = round(e["bytes"] / dt_thr / 1e9, 3)
+        e["seconds"] = round(e["seconds"], 4)
+        e["seconds_threaded"] = round(dt_thr, 4)
 
     # the two small AllReduce workloads, whole, single-threaded (not in the step)
     small = {}
@@ -1056,6 +1068,7 @@ def cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_o
         "gpu_matches_oracle_on_sample": ok,
         "max_bf16_ulp_on_sample": max_ulp,  # ReduceScatter and combine outputs against the oracle
         "small_allreduce": small,
+        "per_op": per_op,  # single-threaded and pooled seconds of each op's sample (pack single-threaded in both)
         "threaded": {
             "value": round(bytes_total / t_threaded / 1e9, 3),
             "unit": "GB/s",
