@@ -237,10 +237,13 @@ purlin_status purlin_exec_v(purlin_plan_t plan, void* const* bufs, const int32_t
     if (p.flags & PURLIN_PLAN_HOST_ONLY) return PURLIN_ERR_INVALID;
     if (!counts || (reinterpret_cast<uintptr_t>(counts) & 3u)) return PURLIN_ERR_INVALID;
     if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    void* const no_bufs[2 * PURLIN_MAX_RANKS] = {};
     if (p.items.empty()) {
-        // zero capacity: no buffer is touched (bufs is ignored), but the sizes
-        // are still checked on the device when a status word is given
+        // zero capacity: no buffer is touched (bufs is ignored and may be
+        // NULL), but the sizes are still checked on the device when a status
+        // word is given
         if (!dev_status) return PURLIN_OK;
+        bufs = no_bufs;
     } else {
         const purlin_status st = check_buffers(p, bufs);
         if (st != PURLIN_OK) return st;

@@ -174,3 +174,23 @@ def test_v_small_sizes_in_a_large_capacity(op):
     for r in range(P):
         assert_bits_equal(got[r][: len(want[r])], want[r], "bf16", f"{op} rank {r}")
         assert np.all(got[r][len(want[r]):].view(np.uint8) == CANARY)
+
+
+@pytest.mark.parametrize("op", ["allgatherv", "reduce_scatterv", "alltoallv"])
+def test_v_zero_capacity_accepts_null_buffers(op):
+    """A zero-capacity plan ignores bufs, so a C caller may pass NULL."""
+    import ctypes
+    P = 4
+    plan = PL.Plan(op, P, 0, "bf16", 256, unit=1)
+    n = P * P if op == "alltoallv" else P
+    for counts, want in (([0] * n, 0), ([1] + [0] * (n - 1), 1)):
+        dev_counts = to_device(np.asarray(counts, np.int32))
+        st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+        rc = PL.lib().purlin_exec_v(plan.handle, None, ctypes.c_void_p(dev_counts.data_ptr()),
+                                    ctypes.c_void_p(st.data_ptr()), ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        assert rc == 0
+        torch.cuda.synchronize()
+        assert int(st.item()) == want
+    # without a status word nothing is launched at all
+    rc = PL.lib().purlin_exec_v(plan.handle, None, ctypes.c_void_p(dev_counts.data_ptr()), None, None)
+    assert rc == 0
