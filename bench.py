@@ -49,6 +49,7 @@ KERNEL_SOURCES = ["paper_2609_36954_amd/csrc/exec.hip", "paper_2609_36954_amd/cs
 KERNEL_OF_OP = {
     "reduce_scatter": "exec_reduce<8, true",
     "allgather": "exec_copy<",
+    "moe_pack": "::pack_rows<",  # the rows kernel (not unpack_rows); the metadata launches move ~0.3 MiB
     "moe_combine": "unpack_rows<",
 }
 CALIBRATION_KERNEL = "copy"  # torch's device-to-device copy of --calibrate-copy
@@ -162,8 +163,9 @@ def _counter_means(d, counter):
     return {k: v[0] / v[1] for k, v in sums.items()}, {k: v[2] for k, v in sums.items()}
 
 
-def ingest_counters(fetch_dir, write_dir):
-    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) -> HBM bytes per launch.
+def ingest_counters(fetch_dir, write_dir, path=None):
+    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) -> HBM bytes per launch,
+    written to ``path`` (default profiles/traffic.json).
 
     Each counter is scaled by what it reads for a plain 1 GiB device copy
     (reads 1 GiB, writes 1 GiB), run in the same process."""
@@ -194,7 +196,8 @@ def ingest_counters(fetch_dir, write_dir):
         out["ops"][op] = {"kernel": kf, "fetch_KiB": fetch[kf], "write_KiB": write[kw],
                           "hbm_read_bytes": round(fb), "hbm_write_bytes": round(wb),
                           "hbm_bytes_per_launch": round(fb + wb)}
-    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if path is None:
+        path = os.path.join(ROOT, "profiles", "traffic.json")
     os.makedirs(os.path.dirname(path), exist_ok=True)
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
