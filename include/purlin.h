@@ -282,8 +282,9 @@ PURLIN_API purlin_status purlin_plan_v(purlin_op op, int P, uint64_t in_capacity
  * sets it to 1 (else 0).  One launch of a fixed number of wavefronts that
  * stride over the work items below the run-time sizes, so capacity left
  * unused costs no work.  A plan of zero capacity ignores bufs, which may
- * then be NULL (the sizes are still checked when dev_status is given).  Host-side errors as for
- * purlin_exec, plus PURLIN_ERR_INVALID for a non-V plan or NULL counts.
+ * then be NULL (the sizes are still checked when dev_status is given).
+ * Host-side errors as for purlin_exec, plus PURLIN_ERR_INVALID for a non-V
+ * plan or NULL counts.
  * purlin_exec rejects V plans. */
 PURLIN_API purlin_status purlin_exec_v(purlin_plan_t plan, void* const* bufs, const int32_t* counts,
                                        int32_t* dev_status, void* stream);
