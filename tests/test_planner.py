@@ -384,3 +384,20 @@ def test_variable_size_plans_keep_the_streaming_item_size(op):
     N = 256 * MiB // 2
     items, _ = PL.Plan(op, 8, N, "bf16", MiB, unit=1, host_only=True).items()
     assert int(items["bytes"].max()) > 2048
+
+
+@pytest.mark.parametrize("P,mib_per_rank,dtype,two_phase", [
+    (8, 48, "bf16", False),   # one-phase traffic 768 MiB: reduce once, write all 8 outputs
+    (8, 64, "bf16", True),    # 1 GiB: compose<RS, AG> in two launches
+    (8, 256, "bf16", True),
+    (4, 1, "fp32", False),    # the small fp32 AllReduce
+    (8, 2, "bf16", False),    # the decode AllReduce
+])
+def test_automatic_allreduce_mode(P, mib_per_rank, dtype, two_phase):
+    s = S[dtype]
+    N = mib_per_rank * MiB // s
+    items, pb = PL.Plan("allreduce", P, N, dtype, MiB, host_only=True).items()
+    assert (pb[1] < pb[2]) == two_phase
+    phase0 = items[:pb[1]]
+    assert np.all(phase0["kind"] == PL.KIND_REDUCE)
+    assert np.all(phase0["ndst"] == (1 if two_phase else P))
