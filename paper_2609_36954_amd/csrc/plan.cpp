@@ -31,6 +31,7 @@ constexpr uint64_t kTargetItems = 4096;    // 16 wavefronts per CU on 256 CUs
 // faster, and 360 MiB, where they are 10-35% slower).
 constexpr uint64_t kStreamingBytes = 320ull << 20;
 constexpr uint64_t kAllReduceTwoPhaseBytes = 1ull << 30;
+constexpr uint64_t kLastLevelCacheBytes = 256ull << 20;  // MI355X Infinity Cache (256 MB)
 constexpr uint64_t kLargeCopyBytes = 4ull << 30;  // copy-phase traffic from which 2 KiB items win  // one-phase traffic from which compose<RS, AG> wins
 constexpr uint64_t kLatencyNtStoreMin = 8ull << 20;  // written bytes per launch between which
 constexpr uint64_t kLatencyNtStoreMax = 32ull << 20; // non-temporal stores win below streaming
@@ -174,9 +175,13 @@ purlin_status build_plan(purlin_op op, int P, int root, uint64_t count, purlin_d
         // 64 MiB per rank the two-phase compose wins although it schedules
         // more bytes: phase 0 leaves the N*s reduced bytes in the last-level
         // cache and phase 1's copies read them back from there, while each
-        // wave streams one direction at a time (measured on MI355X).
+        // wave streams one direction at a time (744 vs 801 µs at 256 MiB).
+        // Once those bytes no longer fit that cache, phase 1 reads them from
+        // HBM and the one-phase form is ahead again (1662 vs 1677 µs at
+        // 512 MiB per rank, 3299 vs 3372 µs at 1 GiB; measured on MI355X).
         const uint64_t one_phase_traffic = 2 * uint64_t(P) * count * s;
-        pol.ar_mode = one_phase_traffic >= kAllReduceTwoPhaseBytes ? 1 : 2;
+        const bool reduced_fits_cache = count * s <= kLastLevelCacheBytes;
+        pol.ar_mode = one_phase_traffic >= kAllReduceTwoPhaseBytes && reduced_fits_cache ? 1 : 2;
     }
 
     out = Plan{};

@@ -389,11 +389,14 @@ def test_variable_size_plans_keep_the_streaming_item_size(op):
 @pytest.mark.parametrize("P,mib_per_rank,dtype,two_phase", [
     (8, 48, "bf16", False),   # one-phase traffic 768 MiB: reduce once, write all 8 outputs
     (8, 64, "bf16", True),    # 1 GiB: compose<RS, AG> in two launches
-    (8, 256, "bf16", True),
+    (8, 256, "bf16", True),   # the reduced 256 MiB still fits the last-level cache
+    (8, 512, "bf16", False),  # it no longer does: phase 1 would read it from HBM
     (4, 1, "fp32", False),    # the small fp32 AllReduce
     (8, 2, "bf16", False),    # the decode AllReduce
 ])
 def test_automatic_allreduce_mode(P, mib_per_rank, dtype, two_phase):
+    """Two launches (compose<RS, AG>) from 1 GiB of one-phase traffic while
+    the reduced buffer fits the 256 MB last-level cache; otherwise one."""
     s = S[dtype]
     N = mib_per_rank * MiB // s
     items, pb = PL.Plan("allreduce", P, N, dtype, MiB, host_only=True).items()
