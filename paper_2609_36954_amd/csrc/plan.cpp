@@ -30,9 +30,9 @@ constexpr uint64_t kTargetItems = 4096;    // 16 wavefronts per CU on 256 CUs
 // win (measured on MI355X, P = 8: between 288 MiB, where cached accesses are
 // faster, and 360 MiB, where they are 10-35% slower).
 constexpr uint64_t kStreamingBytes = 320ull << 20;
-constexpr uint64_t kAllReduceTwoPhaseBytes = 1ull << 30;
-constexpr uint64_t kLastLevelCacheBytes = 256ull << 20;  // MI355X Infinity Cache (256 MB)
-constexpr uint64_t kLargeCopyBytes = 4ull << 30;  // copy-phase traffic from which 2 KiB items win  // one-phase traffic from which compose<RS, AG> wins
+constexpr uint64_t kAllReduceTwoPhaseBytes = 1ull << 30;  // one-phase traffic from which compose<RS, AG> wins
+constexpr uint64_t kLastLevelCacheBytes = 256ull << 20;    // MI355X Infinity Cache (256 MB)
+constexpr uint64_t kLargeCopyBytes = 4ull << 30;           // copy-phase traffic from which 2 KiB items win
 constexpr uint64_t kLatencyNtStoreMin = 8ull << 20;  // written bytes per launch between which
 constexpr uint64_t kLatencyNtStoreMax = 32ull << 20; // non-temporal stores win below streaming
 
