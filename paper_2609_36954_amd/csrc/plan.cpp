@@ -72,9 +72,10 @@ purlin_desc make_desc(uint32_t kind, uint32_t phase, uint32_t nsrc, uint32_t src
 //    (32 KiB to each of 8 destinations) and a one-to-one copy item of 4 KiB
 //    run fastest; larger items leave too few wavefronts, smaller ones pay
 //    per-item overhead.
-//  - Copy phases that move 4 GiB or more (AllGather and AllToAll from
-//    512 MiB per rank at P = 8): 2 KiB items, measured 3-6% faster than
-//    the sizes above there (and slower below it).  The waves in flight
+//  - Copy phases that move 4 GiB or more (at P = 8: AllGather from
+//    512 MiB per rank, AllToAll from 256 MiB): 2 KiB items, measured 3-6%
+//    faster than the sizes above from 512 MiB per rank (and 10% slower for
+//    AllGather at 256 MiB).  The waves in flight
 //    then cover a narrower span of every destination buffer at a time.
 //    Variable-size plans keep the sizes above: their waves also map each
 //    item onto the run-time sizes, and 2 KiB items made the AllToAllV
