@@ -137,7 +137,9 @@ typedef struct purlin_policy {
                             counters with epochs, Section 3.2 and 4.2; such a
                             plan must not run concurrently with itself)     */
     uint32_t load_hint;  /* global loads:  0 auto, 1 cached, 2 non-temporal */
-    uint32_t store_hint; /* global stores: 0 auto, 1 cached, 2 non-temporal */
+    uint32_t store_hint; /* global stores: 0 auto, 1 cached, 2 non-temporal
+                            (variable-size plans apply one setting to loads
+                            and stores: non-temporal if either hint is) */
     uint32_t max_workgroups; /* 0 = one wavefront per work item; otherwise every
                             launch of the plan has at most this many 256-thread
                             workgroups (4 wavefronts each) and its wavefronts
