@@ -368,6 +368,8 @@ MiB = 1 << 20
     ("reduce_scatter", 1024, 4096),
     ("allgather", 256, 32 * 1024),     # one read, 8 writes per item; 2.25 GiB moved
     ("allgather", 512, 2048),          # 4.5 GiB moved: the large-copy size
+    ("alltoall", 16, 4096),            # one-to-one below the streaming threshold: still 4 KiB
+    ("allgather", 32, 8192),           # multi-destination below it: 32 MiB of items / 4096
     ("alltoall", 128, 4096),           # one-to-one, 2 GiB moved
     ("alltoall", 256, 2048),           # 4 GiB moved
 ])
