@@ -321,7 +321,11 @@ PURLIN_API purlin_status purlin_plan_descriptors(purlin_plan_t plan, const purli
 PURLIN_API purlin_status purlin_plan_items(purlin_plan_t plan, const purlin_desc** items, uint64_t* n,
                                 uint64_t phase_begin[3]);
 
-/* Run the plan: bufs[] holds 2P device pointers, in_0..in_{P-1} then
+/* Run the plan (Section 3.2, Listing 2: every chunk descriptor is consumed
+ * by its copy or reduce op, Section 3.3, Listing 3 and Eq. 2, at the
+ * address the layout rule gives; an AllReduce runs its ReduceScatter phase
+ * before its AllGather phase, Section 3.1).
+ * bufs[] holds 2P device pointers, in_0..in_{P-1} then
  * out_0..out_{P-1}, sized per purlin_plan_info (entries a rooted plan does
  * not use are ignored).  Each phase is one kernel
  * launch on `stream`; no host-device copy, no allocation, no

@@ -5,6 +5,7 @@ import pytest
 import torch
 
 import oracle
+from case_seed import case_seed
 from gpu_util import CANARY, Guarded, assert_bits_equal, np_dtype, to_device, to_host, torch_dtype
 from paper_2609_36954_amd import purlin as PL
 from paper_2609_36954_amd import workloads as W
@@ -34,7 +35,7 @@ CASES = [(op, dt, P, kind, unit) for op in ("allgatherv", "reduce_scatterv", "al
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "-".join(map(str, c)))
 def test_v_matches_oracle(case):
     op, dtype, P, kind, unit = case
-    rng = np.random.default_rng(abs(hash(case)) % 10000)
+    rng = np.random.default_rng(case_seed(case))
     cap = 6000
     s = S[dtype]
     counts = _case_counts(kind, op, P, cap // unit, rng)
