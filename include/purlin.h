@@ -397,6 +397,29 @@ PURLIN_API purlin_status purlin_pack(int T, int H, int K, int E, int P, const vo
                           int32_t* dev_status, void* workspace, uint64_t workspace_bytes,
                           void* stream);
 
+/* Bytes of the per-GPU workspace that purlin_pack_static uses instead of a
+ * caller-supplied one. */
+#define PURLIN_STATIC_SCRATCH_BYTES (4u << 20)
+
+/* purlin_pack without the workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same arguments, outputs, bits
+ * and errors as purlin_pack; the workspace is a library-owned array of
+ * PURLIN_STATIC_SCRATCH_BYTES in device memory, one copy per GPU, held until
+ * the process ends.  The call allocates nothing: on its first call on a
+ * device (the current one, which `stream` must belong to) it looks that
+ * copy's address up once.
+ *   Limit: purlin_pack_workspace_size(T, K, E) <= PURLIN_STATIC_SCRATCH_BYTES
+ *   (about 87 K tokens at K = 8, E = 256), else PURLIN_ERR_INVALID.
+ *   Every call on one GPU shares its array: calls that may overlap on one
+ *   GPU (different streams without ordering between them) race; order them
+ *   on one stream.  PURLIN_ERR_UNSUPPORTED for a device index >= 64,
+ *   PURLIN_ERR_DEVICE if the address lookup or a launch fails. */
+PURLIN_API purlin_status purlin_pack_static(int T, int H, int K, int E, int P, const void* x, const int32_t* ids,
+                                            void* packed, int32_t* dest_counts, int32_t* dest_offsets,
+                                            int32_t* expert_counts, int32_t* expert_offsets, int32_t* pos,
+                                            int32_t* dev_status, void* stream);
+
 /* MoE combine (unpack), the inverse of purlin_pack weighted by gates:
  *   acc = +0.0f;
  *   for k = 0 .. K-1:  acc = acc + (gates[t,k] * widen(y[pos[t,k], h]));

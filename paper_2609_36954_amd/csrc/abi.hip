@@ -3,7 +3,9 @@
 // and the launches.  Status codes only: no exception crosses the ABI.
 
 #include <algorithm>
+#include <atomic>
 #include <cstdint>
+#include <mutex>
 #include <new>
 
 #include "kernels.h"
@@ -13,6 +15,12 @@
 struct purlin_plan_s {
     purlin::Plan plan;
 };
+
+// Workspace of the entry points that allocate nothing (purlin_pack_static):
+// one copy per GPU, zero at load, held until the process ends.  In host
+// code `scratch` names a host-side stand-in, never the device memory: the
+// device address comes from hipGetSymbolAddress (static_scratch below).
+static __device__ __align__(256) unsigned char scratch[PURLIN_STATIC_SCRATCH_BYTES];
 
 namespace {
 
@@ -79,6 +87,11 @@ purlin_status make_plan(purlin_op op, int P, int root, uint64_t count, purlin_dt
     *out_plan = h;
     return PURLIN_OK;
 }
+
+// Per-device address of `scratch` (below), looked up once per device.
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+std::mutex g_scratch_mu;
 
 bool pack_limits_ok(int T, int H, int K, int E) {
     if (T < 0 || H < 1 || K < 1 || K > 64 || E < 1 || E > 4096) return false;
@@ -150,6 +163,59 @@ bool all_aligned(Ptr const* v, int P) {
     for (int p = 0; p < P; ++p)
         if (!v[p] || !aligned16(v[p])) return false;
     return true;
+}
+
+// Every purlin_pack argument but the workspace.
+purlin_status check_pack_args(int T, int H, int K, int E, int P, const void* x, const int32_t* ids,
+                              const void* packed, const int32_t* dest_counts, const int32_t* dest_offsets,
+                              const int32_t* expert_counts, const int32_t* expert_offsets, const int32_t* pos,
+                              const int32_t* dev_status) {
+    if (!pack_limits_ok(T, H, K, E)) return PURLIN_ERR_INVALID;
+    if (P < 1 || P > E || E % P != 0) return PURLIN_ERR_INVALID;
+    if (!dest_counts || !dest_offsets || !expert_counts) return PURLIN_ERR_INVALID;
+    if (!aligned16(dest_counts) || !aligned16(dest_offsets) || !aligned16(expert_counts)) return PURLIN_ERR_INVALID;
+    if (expert_offsets && !aligned16(expert_offsets)) return PURLIN_ERR_INVALID;
+    if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    if (T > 0) {
+        if (!x || !ids || !packed || !pos) return PURLIN_ERR_INVALID;
+        if (!aligned16(x) || !aligned16(ids) || !aligned16(packed) || !aligned16(pos)) return PURLIN_ERR_INVALID;
+        const uint64_t xb = uint64_t(T) * H * 2, pb = xb * K;
+        if (overlaps(x, xb, packed, pb)) return PURLIN_ERR_INVALID;
+    }
+    return PURLIN_OK;
+}
+
+// purlin_pack after validation, with a workspace of at least
+// pack_workspace_bytes(T, K, E) bytes.
+purlin_status launch_pack_checked(int T, int H, int K, int E, int P, const void* x, const int32_t* ids, void* packed,
+                                  int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts,
+                                  int32_t* expert_offsets, int32_t* pos, int32_t* dev_status, void* workspace,
+                                  void* stream) {
+    const purlin::PackWorkspace ws = purlin::pack_workspace_carve(workspace, T, K, E);
+    const hipError_t e = purlin::launch_pack(T, H, K, E, P, static_cast<const uint16_t*>(x), ids,
+                                             static_cast<uint16_t*>(packed), dest_counts, dest_offsets,
+                                             expert_counts, expert_offsets, pos, dev_status, ws,
+                                             static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
+// This device's address of `scratch`: looked up on the first call on each
+// device (with that device current), then reused.
+purlin_status static_scratch(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return PURLIN_ERR_DEVICE;
+    if (dev < 0 || dev >= kMaxDevices) return PURLIN_ERR_UNSUPPORTED;
+    void* p = g_scratch_addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch_addr[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return PURLIN_ERR_DEVICE;
+            g_scratch_addr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return PURLIN_OK;
 }
 
 }  // namespace
@@ -317,26 +383,28 @@ purlin_status purlin_pack(int T, int H, int K, int E, int P, const void* x, cons
                           int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts,
                           int32_t* expert_offsets, int32_t* pos, int32_t* dev_status, void* workspace,
                           uint64_t workspace_bytes, void* stream) {
-    if (!pack_limits_ok(T, H, K, E)) return PURLIN_ERR_INVALID;
-    if (P < 1 || P > E || E % P != 0) return PURLIN_ERR_INVALID;
-    if (!dest_counts || !dest_offsets || !expert_counts) return PURLIN_ERR_INVALID;
-    if (!aligned16(dest_counts) || !aligned16(dest_offsets) || !aligned16(expert_counts)) return PURLIN_ERR_INVALID;
-    if (expert_offsets && !aligned16(expert_offsets)) return PURLIN_ERR_INVALID;
-    if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    const purlin_status st =
+        check_pack_args(T, H, K, E, P, x, ids, packed, dest_counts, dest_offsets, expert_counts, expert_offsets, pos,
+                        dev_status);
+    if (st != PURLIN_OK) return st;
     const uint64_t need = purlin::pack_workspace_bytes(T, K, E);
     if (workspace_bytes < need || (need && (!workspace || !aligned16(workspace)))) return PURLIN_ERR_INVALID;
-    if (T > 0) {
-        if (!x || !ids || !packed || !pos) return PURLIN_ERR_INVALID;
-        if (!aligned16(x) || !aligned16(ids) || !aligned16(packed) || !aligned16(pos)) return PURLIN_ERR_INVALID;
-        const uint64_t xb = uint64_t(T) * H * 2, pb = xb * K;
-        if (overlaps(x, xb, packed, pb)) return PURLIN_ERR_INVALID;
-    }
-    const purlin::PackWorkspace ws = purlin::pack_workspace_carve(workspace, T, K, E);
-    const hipError_t e = purlin::launch_pack(T, H, K, E, P, static_cast<const uint16_t*>(x), ids,
-                                             static_cast<uint16_t*>(packed), dest_counts, dest_offsets,
-                                             expert_counts, expert_offsets, pos, dev_status, ws,
-                                             static_cast<hipStream_t>(stream));
-    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+    return launch_pack_checked(T, H, K, E, P, x, ids, packed, dest_counts, dest_offsets, expert_counts,
+                               expert_offsets, pos, dev_status, workspace, stream);
+}
+
+purlin_status purlin_pack_static(int T, int H, int K, int E, int P, const void* x, const int32_t* ids, void* packed,
+                                 int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts,
+                                 int32_t* expert_offsets, int32_t* pos, int32_t* dev_status, void* stream) {
+    purlin_status st = check_pack_args(T, H, K, E, P, x, ids, packed, dest_counts, dest_offsets, expert_counts,
+                                       expert_offsets, pos, dev_status);
+    if (st != PURLIN_OK) return st;
+    if (purlin::pack_workspace_bytes(T, K, E) > PURLIN_STATIC_SCRATCH_BYTES) return PURLIN_ERR_INVALID;
+    void* ws = nullptr;
+    st = static_scratch(&ws);
+    if (st != PURLIN_OK) return st;
+    return launch_pack_checked(T, H, K, E, P, x, ids, packed, dest_counts, dest_offsets, expert_counts,
+                               expert_offsets, pos, dev_status, ws, stream);
 }
 
 purlin_status purlin_pack_dedup_workspace_size(int T, int P, uint64_t* bytes) {

@@ -107,6 +107,7 @@ def lib():
     L.purlin_plan_destroy.restype = None
     L.purlin_pack_workspace_size.argtypes = [i32, i32, i32, _c_u64p]
     L.purlin_pack.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 10 + [u64, _vp]
+    L.purlin_pack_static.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 10
     L.purlin_unpack.argtypes = [i32, i32, i32] + [_vp] * 6
     L.purlin_pack_dedup_workspace_size.argtypes = [i32, i32, _c_u64p]
     L.purlin_pack_dedup.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 8 + [u64, _vp]
@@ -486,6 +487,33 @@ def purlin_pack(x, ids, E, P, out=None, workspace=None, dev_status=None, stream=
                            int(workspace.numel() * workspace.element_size()), _stream_handle(stream))
     _check(st, "purlin_pack")
     return o
+
+
+def purlin_pack_static(x, ids, E, P, out, dev_status=None, stream=None):
+    """``purlin_pack`` through the entry point that allocates nothing: its
+    workspace is the library's per-GPU array.  ``out`` must supply every
+    output tensor (keys as returned by ``purlin_pack``)."""
+    T, H = x.shape
+    K = ids.shape[1]
+    if ids.shape[0] != T:
+        raise PurlinError(PURLIN_ERR_INVALID, "x and ids disagree on T")
+    _require_cuda(x, "x", 2)
+    _require_cuda(ids, "ids", 4)
+    import torch
+
+    shapes = {"packed": ((T * K, H), x.dtype), "dest_counts": ((P,), torch.int32), "dest_offsets": ((P,), torch.int32),
+              "expert_counts": ((E,), torch.int32), "expert_offsets": ((E,), torch.int32),
+              "pos": ((T, K), torch.int32)}
+    missing = [name for name in shapes if name not in out]
+    if missing:
+        raise PurlinError(PURLIN_ERR_INVALID, f"out lacks {', '.join(missing)}")
+    _check_sizes(out, shapes)
+    st = lib().purlin_pack_static(int(T), int(H), int(K), int(E), int(P), _ptr(x), _ptr(ids), _ptr(out["packed"]),
+                                  _ptr(out["dest_counts"]), _ptr(out["dest_offsets"]), _ptr(out["expert_counts"]),
+                                  _ptr(out["expert_offsets"]), _ptr(out["pos"]), _ptr(dev_status),
+                                  _stream_handle(stream))
+    _check(st, "purlin_pack_static")
+    return out
 
 
 def purlin_unpack(y, pos, gates, out=None, dev_status=None, stream=None):

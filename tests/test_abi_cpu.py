@@ -212,6 +212,22 @@ def test_pack_argument_validation(kw):
     assert _pack(**kw) == INVALID
 
 
+def _pack_static(T=64, H=64, K=2, E=8, P=2, x=0x1000, ids=0x2000, packed=0x3000, dc=0x4000, do=0x5000, ec=0x6000,
+                 eo=None, pos=0x7000, status=None):
+    return PL.lib().purlin_pack_static(T, H, K, E, P, x, ids, packed, dc, do, ec, eo, pos, status, None)
+
+
+@pytest.mark.parametrize(
+    "kw",
+    [dict(K=0), dict(E=8, P=3), dict(T=-1), dict(x=None), dict(pos=None), dict(x=0x1008), dict(status=0x9002),
+     dict(x=0x3000, packed=0x3000),
+     dict(T=131072, H=8, K=8, E=256, P=8, x=0x10000000, packed=0x20000000)],  # workspace beyond the static array
+)
+def test_pack_static_argument_validation(kw):
+    """Rejected on the host before the device is touched (no GPU here)."""
+    assert _pack_static(**kw) == INVALID
+
+
 def _unpack(T=64, H=64, K=2, y=0x100000, pos=0x2000, gates=0x3000, out=0x4000, status=None):
     return PL.lib().purlin_unpack(T, H, K, y, pos, gates, out, status, None)
 

@@ -1,0 +1,107 @@
+"""purlin_pack_static, the pack entry point that allocates nothing, against purlin_pack.
+
+Both are called through the C ABI on the same seeded inputs; every output
+(rows, counts, offsets, positions, status word) must be bit-identical to
+purlin_pack's, and to the oracle.  Two calls in a row, the second on a
+smaller input, so the shared per-GPU workspace holds the first call's
+contents when the second starts.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import Guarded, to_device, to_host
+from paper_2609_36954_amd import purlin as PL
+from paper_2609_36954_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _outputs(T, H, K, E, P):
+    g = {
+        "packed": Guarded(T * K * H * 2, torch.int16),
+        "dest_counts": Guarded(P * 4, torch.int32),
+        "dest_offsets": Guarded(P * 4, torch.int32),
+        "expert_counts": Guarded(E * 4, torch.int32),
+        "expert_offsets": Guarded(E * 4, torch.int32),
+        "pos": Guarded(T * K * 4, torch.int32),
+    }
+    out = {k: v.t for k, v in g.items()}
+    out["packed"] = out["packed"].view(T * K, H)
+    out["pos"] = out["pos"].view(T, K)
+    return g, out
+
+
+def _host(g, T, H, K):
+    h = {k: to_host(v.t, np.uint16 if k == "packed" else np.int32) for k, v in g.items()}
+    h["packed"] = h["packed"].reshape(T * K, H)
+    h["pos"] = h["pos"].reshape(T, K)
+    return h
+
+
+def _run(fn, x_np, ids_np, E, P):
+    T, H = x_np.shape
+    K = ids_np.shape[1]
+    g, out = _outputs(T, H, K, E, P)
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    x, ids = to_device(x_np), to_device(ids_np)
+    if fn == "static":
+        PL.purlin_pack_static(x, ids, E, P, out=out, dev_status=st)
+    else:
+        PL.purlin_pack(x, ids, E, P, out=out, dev_status=st)
+    torch.cuda.synchronize()
+    assert all(v.intact() for v in g.values()), f"{fn}: write outside an output buffer"
+    return _host(g, T, H, K), int(st[0].item())
+
+
+# (T, H, K, E, P, seed): the first spans 64 token tiles of the metadata
+# (several tiles per expert, skewed Zipf routing); the second is smaller in
+# every dimension, with a ragged last tile.
+CALLS = [(4096, 1024, 8, 256, 8, 41), (130, 264, 4, 64, 4, 42)]
+
+
+def test_pack_static_matches_pack_on_two_calls_in_a_row():
+    for T, H, K, E, P, seed in CALLS:
+        ids_np = W.zipf_topk_ids(T, E, K, 1.1, seed)
+        x_np = W.normal_bf16(np.random.default_rng(seed + 100), T * H).reshape(T, H)
+        print(f"pack_static T={T} H={H} K={K} E={E} P={P} seed={seed}", flush=True)
+        got, st_got = _run("static", x_np, ids_np, E, P)
+        want, st_want = _run("pack", x_np, ids_np, E, P)
+        assert st_got == st_want == 0
+        for key in want:
+            assert np.array_equal(got[key], want[key]), f"{key} differs from purlin_pack (T={T})"
+        ref = oracle.pack(x_np, ids_np, E, P)
+        for key in ("dest_counts", "dest_offsets", "expert_counts", "expert_offsets", "pos", "packed"):
+            assert np.array_equal(got[key], ref[key]), f"{key} differs from the oracle (T={T})"
+
+
+def test_pack_static_flags_bad_routing_like_pack():
+    T, H, K, E, P = 200, 64, 4, 32, 4
+    ids_np = W.zipf_topk_ids(T, E, K, 1.1, 43)
+    ids_np[17, 2] = ids_np[17, 0]  # repeated within a token
+    ids_np[150, 1] = E + 5  # out of range
+    x_np = W.normal_bf16(np.random.default_rng(44), T * H).reshape(T, H)
+    got, st_got = _run("static", x_np, ids_np, E, P)
+    want, st_want = _run("pack", x_np, ids_np, E, P)
+    assert st_got == st_want == 1
+    assert np.array_equal(got["pos"], want["pos"])
+
+
+def test_pack_static_rejects_a_workspace_beyond_its_array():
+    T, H, K, E, P = 131072, 8, 8, 256, 8  # needs about 6 MiB of workspace
+    assert PL.purlin_pack_workspace_size(T, K, E) > 4 << 20
+    x = torch.zeros((T, H), dtype=torch.int16, device="cuda")
+    ids = torch.zeros((T, K), dtype=torch.int32, device="cuda")
+    out = {
+        "packed": torch.empty((T * K, H), dtype=torch.int16, device="cuda"),
+        "dest_counts": torch.empty(P, dtype=torch.int32, device="cuda"),
+        "dest_offsets": torch.empty(P, dtype=torch.int32, device="cuda"),
+        "expert_counts": torch.empty(E, dtype=torch.int32, device="cuda"),
+        "expert_offsets": torch.empty(E, dtype=torch.int32, device="cuda"),
+        "pos": torch.empty((T, K), dtype=torch.int32, device="cuda"),
+    }
+    with pytest.raises(PL.PurlinError) as e:
+        PL.purlin_pack_static(x, ids, E, P, out=out)
+    assert e.value.status == PL.PURLIN_ERR_INVALID
