@@ -398,24 +398,7 @@ def main():
 
     # ---------------- latency: decode-size AllReduce ----------------
     def graph_latency_us(plan, lin, lout, calls=128, reps=8):
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            plan.exec(lin, lout, stream=side)
-        torch.cuda.synchronize()
-        gph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(gph, stream=side):
-            for _ in range(calls):
-                plan.exec(lin, lout, stream=side)
-        gph.replay()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(reps):
-            gph.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / (calls * reps)
+        return graph_call_us(torch, lambda st: plan.exec(lin, lout, stream=st), calls, reps)
 
     # ---------------- CPU baseline: the oracle on a bounded sample ----------------
     # (first: it compares the step's own outputs, which the later measurements overwrite)
@@ -441,6 +424,31 @@ def main():
     ceilings = None if args.no_extra else measure_ceilings(torch, PL)
     return emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, per_op, latency, plan_ms,
                 dev_name, src_hash, extra, ceilings)
+
+
+def graph_call_us(torch, enqueue, calls=128, reps=8):
+    """The paper's small-message timing (Section 5): `calls` calls captured
+    in one graph on a side stream, one warm-up replay, then `reps` timed
+    replays; returns µs per call (elapsed / (calls * reps)).  `enqueue(st)`
+    issues one call on stream `st`."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        enqueue(side)
+    torch.cuda.synchronize()
+    gph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gph, stream=side):
+        for _ in range(calls):
+            enqueue(side)
+    gph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        gph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / (calls * reps)
 
 
 def measure_extra_ops(torch, PL, ins, rs_out, ag_out, P, N, s, reps=5):
@@ -775,33 +783,69 @@ def measure_plateau(torch, PL, ins, rs_out, ag_out, P, N, s, reps=3):
 
 
 def measure_ceilings(torch, PL, nbytes=1 << 30, reps=20):
-    """Plain device-to-device copies of 1 GiB on the same GPU, for scale:
-    hipMemcpyAsync (torch's same-device tensor copy) and the library's plain
-    16-byte copy kernel (purlin_stream_copy).  GB/s = read + written bytes
-    / time; event-timed on the current stream after 3 untimed copies."""
+    """Reference streams on the same GPU, for scale: hipMemcpyAsync (torch's
+    same-device tensor copy), the library's plain copy kernel
+    (purlin_stream_copy) and its descriptor-free streams (purlin_stream):
+    read-only and write-only 1 GiB, a 1 GiB copy, 8 sources of 256 MiB
+    XOR-ed into one (ReduceScatter's 8-to-1 mix) and one 256 MiB source
+    written to 8 destinations (AllGather's 1-to-8 mix).  Each purlin_stream
+    mix runs with the four load/store cache-hint combinations; the mix's
+    figure is the best of them (all four are kept under "by_hints").
+    GB/s = bytes read + written / time, HIP events without a system fence
+    around `reps` back-to-back calls on the current stream, after 3 untimed
+    calls."""
+    part = nbytes // 4
     src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(7)
     dst = torch.empty_like(src)
-    out = {}
-    for name, fn in (("hip_memcpy_dtod", lambda: dst.copy_(src)),
-                     ("plain_dwordx4_copy_kernel", lambda: PL.purlin_stream_copy(dst, src))):
+    srcs8 = [torch.empty(part, dtype=torch.uint8, device="cuda").fill_(p) for p in range(8)]
+    dsts8 = [torch.empty(part, dtype=torch.uint8, device="cuda") for _ in range(8)]
+    sink = torch.empty(16, dtype=torch.uint8, device="cuda")
+
+    def timed(fn, moved):
         for _ in range(3):
             fn()
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0, e1 = TimingEvent(torch), TimingEvent(torch)
         e0.record()
         for _ in range(reps):
             fn()
         e1.record()
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) * 1e3 / reps
-        out[name] = {"avg_us": round(us, 1), "GBps": round(2 * nbytes / (us * 1e-6) / 1e9, 1),
-                     "frac_of_hbm_peak": round(2 * nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+        return {"avg_us": round(us, 1), "bytes": int(moved), "GBps": round(moved / (us * 1e-6) / 1e9, 1),
+                "frac_of_hbm_peak": round(moved / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+
+    out = {"hip_memcpy_dtod": timed(lambda: dst.copy_(src), 2 * nbytes),
+           "plain_dwordx4_copy_kernel": timed(lambda: PL.purlin_stream_copy(dst, src), 2 * nbytes)}
+    mixes = (
+        ("read_only", [], [src], nbytes),
+        ("write_only", [dst], [], nbytes),
+        ("copy_1to1", [dst], [src], 2 * nbytes),
+        ("reduce_shape_8to1", [dsts8[0]], srcs8, 9 * part),
+        ("gather_shape_1to8", dsts8, [srcs8[0]], 9 * part),
+    )
+    for name, ds, ss, moved in mixes:
+        by = {}
+        for ntl in (False, True):
+            for nts in (False, True):
+                if (not ss and ntl) or (not ds and nts):
+                    continue  # the hint has nothing to act on
+                key = ("nt" if ntl else "cached") + "_loads_" + ("nt" if nts else "cached") + "_stores"
+                by[key] = timed(lambda ds=ds, ss=ss, ntl=ntl, nts=nts: PL.purlin_stream(ds, ss, sink=sink, nt_load=ntl,
+                                                                                      nt_store=nts), moved)
+        best = max(by, key=lambda k: by[k]["GBps"])
+        out[name] = dict(by[best], hints=best, by_hints=by)
     out["bytes_copied"] = nbytes
-    del src, dst
+    del src, dst, srcs8, dsts8, sink
     return out
 
 
 def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
+    # The floor: the smallest launch the library makes (a 16-byte copy, one
+    # wavefront's worth of a workgroup), timed like the collectives below.
+    a16 = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    b16 = torch.empty_like(a16)
+    floor_us = graph_call_us(torch, lambda st: PL.purlin_stream_copy(b16, a16, stream=st))
     c1 = W.AR_P4_FP32_256K
     in1 = [to_dev(torch, a) for a in W.collective_inputs(c1)]
     out1 = [torch.empty(c1.count, dtype=torch.float32, device="cuda") for _ in range(c1.P)]
@@ -834,14 +878,18 @@ def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
         torch.cuda.synchronize()
         singles.append(e0.elapsed_time(e1) * 1e3)
     latency = {
+        "launch_floor_us": round(floor_us, 2),
+        "launch_floor": "purlin_stream_copy of 16 bytes, graph of 128 calls, 8 replays (time / 1024)",
         "allreduce_p4_fp32_262144": {
             "us": round(lat1_us, 2),
+            "over_floor_us": round(lat1_us - floor_us, 2),
             "GBps_min": round(collective_bytes("allreduce", c1.P, c1.count, 4) / (lat1_us * 1e-6) / 1e9, 1),
             "algbw_GBps": round(c1.count * 4 / (lat1_us * 1e-6) / 1e9, 1),
             "timing": "graph of 128 calls, 8 replays after one warm-up replay (time / 1024)",
         },
         "allreduce_p8_bf16_128x8192": {
             "us": round(lat_us, 2),
+            "over_floor_us": round(lat_us - floor_us, 2),
             "GBps_min": round(collective_bytes("allreduce", c2.P, c2.count, 2) / (lat_us * 1e-6) / 1e9, 1),
             "algbw_GBps": round(c2.count * 2 / (lat_us * 1e-6) / 1e9, 1),
             "timing": "graph of 128 calls, 8 replays after one warm-up replay (time / 1024)",
@@ -869,6 +917,8 @@ def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
                 row[f"{kib}KiB"] = round(graph_latency_us(pl, li, lo), 2)
             sweep[op] = row
         latency["sweep_p8_bf16_us"] = sweep
+        latency["sweep_p8_bf16_over_floor_us"] = {op: {k: round(v - floor_us, 2) for k, v in row.items()}
+                                                  for op, row in sweep.items()}
     del lat_in, lat_out
     return latency
 

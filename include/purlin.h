@@ -584,6 +584,29 @@ PURLIN_API purlin_status purlin_ep_combine_dedup(int T, int H, int P, const void
  * PURLIN_ERR_DEVICE: the launch failed. */
 PURLIN_API purlin_status purlin_stream_copy(void* dst, const void* src, uint64_t bytes, void* stream);
 
+/* Reference stream of n sources to m destinations with no descriptors:
+ * for every 16-byte vector i < bytes / 16,
+ *     v = src[0][i] ^ src[1][i] ^ ... ^ src[nsrc-1][i]   ({i, i, i, i} as
+ *                                                        32-bit words if nsrc = 0)
+ *     dst[j][i] = v  for every j < ndst
+ * With ndst = 0 the sources are only read, and `sink` (16 bytes of device
+ * memory) may receive an unspecified vector.  `hints`: PURLIN_STREAM_NT_LOAD
+ * and / or PURLIN_STREAM_NT_STORE select non-temporal loads / stores.  Not a step of the method:
+ * the streams (read-only, write-only, 1:1, 8-to-1, 1-to-8) are the access
+ * mixes the executor's kernels are measured against.
+ *   dst   ndst device pointers, 16-byte aligned, pairwise disjoint ranges
+ *   src   nsrc device pointers, 16-byte aligned (may alias each other)
+ *   bytes a multiple of 16; 0 is a no-op
+ * 0 <= nsrc, ndst <= 16, nsrc + ndst >= 1.  Asynchronous on `stream`.
+ * PURLIN_ERR_INVALID: counts out of range, bytes not a multiple of 16, a
+ * NULL or misaligned pointer, a destination overlapping a source or
+ * another destination, ndst = 0 without a sink, unknown hint bits;
+ * PURLIN_ERR_DEVICE: the launch failed. */
+#define PURLIN_STREAM_NT_LOAD 1u
+#define PURLIN_STREAM_NT_STORE 2u
+PURLIN_API purlin_status purlin_stream(void* const* dst, int ndst, const void* const* src, int nsrc, uint64_t bytes,
+                                       void* sink, uint32_t hints, void* stream);
+
 /* Static text for a status code ("unknown status" for others). */
 PURLIN_API const char* purlin_status_string(purlin_status status);
 

@@ -589,6 +589,28 @@ purlin_status purlin_stream_copy(void* dst, const void* src, uint64_t bytes, voi
     return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
 }
 
+purlin_status purlin_stream(void* const* dst, int ndst, const void* const* src, int nsrc, uint64_t bytes, void* sink,
+                            uint32_t hints, void* stream) {
+    if (hints & ~uint32_t(PURLIN_STREAM_NT_LOAD | PURLIN_STREAM_NT_STORE)) return PURLIN_ERR_INVALID;
+    if (nsrc < 0 || ndst < 0 || nsrc > PURLIN_MAX_RANKS || ndst > PURLIN_MAX_RANKS || nsrc + ndst == 0)
+        return PURLIN_ERR_INVALID;
+    if (bytes % 16) return PURLIN_ERR_INVALID;
+    if (bytes == 0) return PURLIN_OK;
+    if ((nsrc && !src) || (ndst && !dst)) return PURLIN_ERR_INVALID;
+    if (ndst == 0 && (!sink || !aligned16(sink))) return PURLIN_ERR_INVALID;
+    for (int p = 0; p < nsrc; ++p)
+        if (!src[p] || !aligned16(src[p])) return PURLIN_ERR_INVALID;
+    for (int j = 0; j < ndst; ++j) {
+        if (!dst[j] || !aligned16(dst[j])) return PURLIN_ERR_INVALID;
+        for (int p = 0; p < nsrc; ++p)
+            if (overlaps(dst[j], bytes, src[p], bytes)) return PURLIN_ERR_INVALID;
+        for (int k = 0; k < j; ++k)
+            if (overlaps(dst[j], bytes, dst[k], bytes)) return PURLIN_ERR_INVALID;
+    }
+    const hipError_t e = purlin::launch_stream(dst, ndst, src, nsrc, bytes, sink, hints, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
 const char* purlin_status_string(purlin_status status) {
     switch (status) {
         case PURLIN_OK: return "ok";

@@ -732,6 +732,73 @@ __global__ __launch_bounds__(kBlock) void stream_copy(const u32x4* __restrict__ 
     }
 }
 
+// Reference streams (not steps of the method): every 16-byte vector i of
+// the range is the XOR of the NS sources' vectors i (NS = 0: the vector
+// {i, i, i, i}), stored to each of the ND destinations; with ND = 0 the
+// vectors are only read (a store to `sink` that the data cannot trigger in
+// practice keeps the loads alive).  A workgroup moves U * 256 vectors
+// (U = 2 with 8 or more sources, else 4), every load of a lane in flight
+// before its stores; NTL / NTS select the non-temporal forms.
+struct StreamArgs {
+    const u32x4* src[PURLIN_MAX_RANKS];
+    u32x4* dst[PURLIN_MAX_RANKS];
+    u32x4* sink;
+    uint64_t nvec;
+    int nsrc, ndst;
+};
+
+constexpr int stream_unroll(int nsrc) { return nsrc >= 8 ? 2 : 4; }
+
+// NS, ND < 0: counts taken from the arguments.  U vectors per lane.  The
+// cache hints are template parameters: a run-time choice between the two
+// load forms can be folded into one plain load by the compiler.
+template <int NS, int ND, int U, bool NTL, bool NTS>
+__global__ __launch_bounds__(kBlock) void stream_nm(StreamArgs a) {
+    const int ns = NS >= 0 ? NS : a.nsrc, nd = ND >= 0 ? ND : a.ndst;
+    const uint64_t base = uint64_t(blockIdx.x) * (kBlock * U) + threadIdx.x;
+    u32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const uint64_t i = base + uint64_t(u) * kBlock;
+        v[u] = u32x4{uint32_t(i), uint32_t(i), uint32_t(i), uint32_t(i)};
+        if (ns > 0 && i < a.nvec) {
+            v[u] = load16<NTL>(reinterpret_cast<const char*>(a.src[0] + i));
+            for (int p = 1; p < ns; ++p) v[u] ^= load16<NTL>(reinterpret_cast<const char*>(a.src[p] + i));
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const uint64_t i = base + uint64_t(u) * kBlock;
+        if (i >= a.nvec) continue;
+        if (nd == 0) {
+            if (v[u][0] == 0x9E3779B9u && v[u][1] == 0x7F4A7C15u && v[u][2] == 0xF39CC060u) *a.sink = v[u];
+        } else {
+            for (int j = 0; j < nd; ++j) store16<NTS>(reinterpret_cast<char*>(a.dst[j] + i), v[u]);
+        }
+    }
+}
+
+// One purlin_stream launch: the kernel instantiated for its source and
+// destination counts (the measured mixes) or the generic one.
+template <bool NTL, bool NTS>
+void launch_stream_mix(const StreamArgs& a, dim3 grid, hipStream_t stream) {
+    const int ns = a.nsrc, nd = a.ndst;
+    if (ns == 1 && nd == 0)
+        hipLaunchKernelGGL((stream_nm<1, 0, stream_unroll(1), NTL, NTS>), grid, dim3(kBlock), 0, stream, a);
+    else if (ns == 0 && nd == 1)
+        hipLaunchKernelGGL((stream_nm<0, 1, stream_unroll(0), NTL, NTS>), grid, dim3(kBlock), 0, stream, a);
+    else if (ns == 1 && nd == 1)
+        hipLaunchKernelGGL((stream_nm<1, 1, stream_unroll(1), NTL, NTS>), grid, dim3(kBlock), 0, stream, a);
+    else if (ns == 8 && nd == 1)
+        hipLaunchKernelGGL((stream_nm<8, 1, stream_unroll(8), NTL, NTS>), grid, dim3(kBlock), 0, stream, a);
+    else if (ns == 1 && nd == 8)
+        hipLaunchKernelGGL((stream_nm<1, 8, stream_unroll(1), NTL, NTS>), grid, dim3(kBlock), 0, stream, a);
+    else if (ns >= 8)
+        hipLaunchKernelGGL((stream_nm<-1, -1, stream_unroll(8), NTL, NTS>), grid, dim3(kBlock), 0, stream, a);
+    else
+        hipLaunchKernelGGL((stream_nm<-1, -1, stream_unroll(1), NTL, NTS>), grid, dim3(kBlock), 0, stream, a);
+}
+
 }  // namespace
 
 hipError_t launch_stream_copy(void* dst, const void* src, uint64_t bytes, hipStream_t stream) {
@@ -743,6 +810,30 @@ hipError_t launch_stream_copy(void* dst, const void* src, uint64_t bytes, hipStr
     (void)hipGetLastError();
     hipLaunchKernelGGL(stream_copy, dim3(static_cast<uint32_t>(blocks)), dim3(kBlock), 0, stream,
                        static_cast<const u32x4*>(src), static_cast<u32x4*>(dst), nvec);
+    return hipGetLastError();
+}
+
+hipError_t launch_stream(void* const* dst, int ndst, const void* const* src, int nsrc, uint64_t bytes, void* sink,
+                         uint32_t hints, hipStream_t stream) {
+    StreamArgs a{};
+    for (int p = 0; p < nsrc; ++p) a.src[p] = static_cast<const u32x4*>(src[p]);
+    for (int j = 0; j < ndst; ++j) a.dst[j] = static_cast<u32x4*>(dst[j]);
+    a.sink = static_cast<u32x4*>(sink);
+    a.nvec = bytes / 16;
+    a.nsrc = nsrc;
+    a.ndst = ndst;
+    if (a.nvec == 0) return hipSuccess;
+    const uint64_t per_block = uint64_t(kBlock) * stream_unroll(nsrc);
+    const uint64_t blocks = (a.nvec + per_block - 1) / per_block;
+    if (blocks > 0xffffffffull) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<uint32_t>(blocks));
+    (void)hipGetLastError();
+    switch (hints & (PURLIN_STREAM_NT_LOAD | PURLIN_STREAM_NT_STORE)) {
+        case 0: launch_stream_mix<false, false>(a, grid, stream); break;
+        case PURLIN_STREAM_NT_LOAD: launch_stream_mix<true, false>(a, grid, stream); break;
+        case PURLIN_STREAM_NT_STORE: launch_stream_mix<false, true>(a, grid, stream); break;
+        default: launch_stream_mix<true, true>(a, grid, stream); break;
+    }
     return hipGetLastError();
 }
 

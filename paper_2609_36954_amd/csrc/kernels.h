@@ -16,6 +16,9 @@ namespace purlin {
 // nt_load / nt_store select non-temporal global loads / stores.
 // Plain copy of `bytes` (a multiple of 16) from src to dst.
 hipError_t launch_stream_copy(void* dst, const void* src, uint64_t bytes, hipStream_t stream);
+// Reference stream: dst_j[i] = XOR_p src_p[i] per 16-byte vector (see purlin_stream).
+hipError_t launch_stream(void* const* dst, int ndst, const void* const* src, int nsrc, uint64_t bytes, void* sink,
+                         uint32_t hints, hipStream_t stream);
 
 hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
                         uint32_t src_step, bool nt_load, bool nt_store, purlin_dtype dtype, void* const* bufs,

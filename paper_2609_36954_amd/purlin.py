@@ -120,6 +120,7 @@ def lib():
     L.purlin_ep_dispatch_dedup.argtypes = [i32] * 5 + [_pa, _pa, _pa, u64, _vp, _vp, _vp, _vp, u64, _vp]
     L.purlin_ep_combine_dedup.argtypes = [i32] * 3 + [_pa, u64, _vp, _pa, _vp, _vp]
     L.purlin_stream_copy.argtypes = [_vp, _vp, u64, _vp]
+    L.purlin_stream.argtypes = [ctypes.POINTER(_vp), i32, ctypes.POINTER(_vp), i32, u64, _vp, u32, _vp]
     L.purlin_status_string.argtypes = [i32]
     L.purlin_status_string.restype = ctypes.c_char_p
     L.purlin_version.argtypes = []
@@ -775,6 +776,26 @@ def purlin_stream_copy(dst, src, stream=None):
     st = lib().purlin_stream_copy(_ptr(dst), _ptr(src), int(nbytes), _stream_handle(stream))
     _check(st, "purlin_stream_copy")
     return dst
+
+
+def purlin_stream(dsts, srcs, nbytes=None, sink=None, nt_load=False, nt_store=False, stream=None):
+    """Reference stream: every destination receives the XOR of the sources,
+    16 bytes at a time (no sources: a counting pattern; no destinations:
+    read only, ``sink`` a 16-byte device tensor; ``nt_load`` / ``nt_store``:
+    non-temporal loads / stores).  Not a step of the method:
+    the access mixes the executor's kernels are measured against."""
+    for t in list(dsts) + list(srcs) + ([sink] if sink is not None else []):
+        _require_cuda(t, "stream buffer")
+    if nbytes is None:
+        nbytes = min(t.numel() * t.element_size() for t in list(dsts) + list(srcs))
+    for t in list(dsts) + list(srcs):
+        if t.numel() * t.element_size() < nbytes:
+            raise PurlinError(PURLIN_ERR_INVALID, "a stream buffer is smaller than nbytes")
+    d = (_vp * max(1, len(dsts)))(*[t.data_ptr() for t in dsts])
+    s = (_vp * max(1, len(srcs)))(*[t.data_ptr() for t in srcs])
+    hints = (1 if nt_load else 0) | (2 if nt_store else 0)
+    st = lib().purlin_stream(d, len(dsts), s, len(srcs), int(nbytes), _ptr(sink), hints, _stream_handle(stream))
+    _check(st, "purlin_stream")
 
 
 # Short names: plan(...) -> Plan; pack(...) -> (packed, dest_counts,

@@ -228,6 +228,33 @@ def test_pack_static_argument_validation(kw):
     assert _pack_static(**kw) == INVALID
 
 
+def _stream(dsts=(0x100000,), srcs=(0x200000,), nbytes=4096, sink=None, nd=None, ns=None, hints=0):
+    d = (ctypes.c_void_p * max(1, len(dsts)))(*dsts)
+    s = (ctypes.c_void_p * max(1, len(srcs)))(*srcs)
+    return PL.lib().purlin_stream(d, len(dsts) if nd is None else nd, s, len(srcs) if ns is None else ns, nbytes, sink,
+                                  hints, None)
+
+
+@pytest.mark.parametrize(
+    "kw",
+    [dict(dsts=(), srcs=()),  # nothing to do
+     dict(nd=17), dict(ns=-1),
+     dict(nbytes=4100),  # not a multiple of 16
+     dict(dsts=(0x100008,)),  # misaligned
+     dict(srcs=(0,)),  # null source
+     dict(dsts=(), srcs=(0x200000,)),  # read only without a sink
+     dict(dsts=(0x200800,)),  # destination overlaps the source
+     dict(dsts=(0x100000, 0x100800), srcs=()),  # destinations overlap
+     dict(hints=4)],  # unknown hint bit
+)
+def test_stream_argument_validation(kw):
+    assert _stream(**kw) == INVALID
+
+
+def test_stream_zero_bytes_is_a_no_op():
+    assert _stream(nbytes=0) == 0
+
+
 def _unpack(T=64, H=64, K=2, y=0x100000, pos=0x2000, gates=0x3000, out=0x4000, status=None):
     return PL.lib().purlin_unpack(T, H, K, y, pos, gates, out, status, None)
 

@@ -64,6 +64,11 @@ def check_pack(x_np, ids_np, E, P):
         (4096, 24, 8, 256, 8, 12),  # 64 token tiles
         (4097, 24, 8, 256, 8, 13),  # 65 tiles, the last one a single token
         (300, 24, 8, 512, 8, 14),  # 512 experts
+        (32768, 8, 1, 16, 4, 15),  # one slot: 512 token tiles
+        (1023, 40, 32, 128, 8, 16),  # K = 32: 32736 ids
+        (2500, 48, 13, 200, 8, 17),  # K = 13, E = 200, ragged last tile
+        (32769, 8, 1, 16, 4, 18),  # 513 tiles, the last one a single token
+        (100, 24, 4, 264, 8, 19),  # E = 264
     ],
 )
 def test_pack_matches_oracle(T, H, K, E, P, seed):
@@ -73,15 +78,16 @@ def test_pack_matches_oracle(T, H, K, E, P, seed):
     check_pack(x, ids, E, P)
 
 
-def test_pack_zipf_routing_skewed():
+@pytest.mark.parametrize("T", [1000, 4096, 4100])
+def test_pack_zipf_routing_skewed(T):
     rng = np.random.default_rng(10)
-    T, H, E, P, K = 1000, 256, 256, 8, 8
+    H, E, P, K = 256, 256, 8, 8
     ids = W.zipf_topk_ids(T, E, K, 1.1, seed=10)
     x = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
     check_pack(x, ids, E, P)
 
 
-@pytest.mark.parametrize("T,E", [(70, 16), (4200, 16), (70, 1024)])
+@pytest.mark.parametrize("T,E", [(70, 16), (4200, 16), (70, 1024), (8000, 256), (9000, 256)])
 def test_pack_reports_bad_routing(T, E):
     rng = np.random.default_rng(11)
     H, K, P = 16, 4, 4

@@ -56,10 +56,10 @@ def _run(fn, x_np, ids_np, E, P):
     return _host(g, T, H, K), int(st[0].item())
 
 
-# (T, H, K, E, P, seed): the first spans 64 token tiles of the metadata
-# (several tiles per expert, skewed Zipf routing); the second is smaller in
-# every dimension, with a ragged last tile.
-CALLS = [(4096, 1024, 8, 256, 8, 41), (130, 264, 4, 64, 4, 42)]
+# (T, H, K, E, P, seed): the second call is smaller in every dimension but
+# E, with a ragged last token tile; the third is the 4096-token, top-8 of
+# 256 experts routing table.
+CALLS = [(5000, 256, 8, 288, 8, 41), (1200, 200, 6, 512, 8, 42), (4096, 1024, 8, 256, 8, 43)]
 
 
 def test_pack_static_matches_pack_on_two_calls_in_a_row():
