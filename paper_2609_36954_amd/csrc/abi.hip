@@ -37,6 +37,39 @@ size_t fused_state_bytes(const purlin::Plan& p) {
     return sizeof(purlin::FusedState) + sizeof(uint64_t) * p.chunks_per_part * static_cast<uint64_t>(p.P);
 }
 
+// Device copies of a plan: its work items and, for a single-launch
+// AllReduce, its zeroed state.  The uploads run on a private non-blocking
+// stream that is drained before returning: no other stream, and no capture
+// in progress on another stream, is waited for or disturbed.
+purlin_status upload_plan(purlin::Plan& pl) {
+    const size_t bytes = pl.items.size() * sizeof(purlin_desc);
+    if (hipMalloc(reinterpret_cast<void**>(&pl.d_items), bytes) != hipSuccess) {
+        pl.d_items = nullptr;
+        return PURLIN_ERR_NOMEM;
+    }
+    const size_t sb = pl.fused ? fused_state_bytes(pl) : 0;
+    if (sb && hipMalloc(&pl.d_state, sb) != hipSuccess) {
+        pl.d_state = nullptr;
+        (void)hipFree(pl.d_items);
+        pl.d_items = nullptr;
+        return PURLIN_ERR_NOMEM;
+    }
+    hipStream_t s = nullptr;
+    bool ok = hipStreamCreateWithFlags(&s, hipStreamNonBlocking) == hipSuccess;
+    ok = ok && hipMemcpyAsync(pl.d_items, pl.items.data(), bytes, hipMemcpyHostToDevice, s) == hipSuccess;
+    ok = ok && (!sb || hipMemsetAsync(pl.d_state, 0, sb, s) == hipSuccess);
+    ok = ok && hipStreamSynchronize(s) == hipSuccess;
+    if (s) (void)hipStreamDestroy(s);
+    if (!ok) {
+        if (pl.d_state) (void)hipFree(pl.d_state);
+        (void)hipFree(pl.d_items);
+        pl.d_state = nullptr;
+        pl.d_items = nullptr;
+        return PURLIN_ERR_DEVICE;
+    }
+    return PURLIN_OK;
+}
+
 purlin_status make_plan(purlin_op op, int P, int root, uint64_t count, purlin_dtype dtype, uint64_t chunk,
                         const purlin_policy* policy, uint32_t flags, purlin_plan_t* out_plan, uint64_t v_unit = 0,
                         uint64_t v_out_capacity = 0, int share = -1) {
@@ -57,31 +90,10 @@ purlin_status make_plan(purlin_op op, int P, int root, uint64_t count, purlin_dt
     }
     purlin::Plan& pl = h->plan;
     if (!(flags & PURLIN_PLAN_HOST_ONLY) && !pl.items.empty()) {
-        const size_t bytes = pl.items.size() * sizeof(purlin_desc);
-        if (hipMalloc(reinterpret_cast<void**>(&pl.d_items), bytes) != hipSuccess) {
-            pl.d_items = nullptr;
+        const purlin_status dst = upload_plan(pl);
+        if (dst != PURLIN_OK) {
             delete h;
-            return PURLIN_ERR_NOMEM;
-        }
-        if (hipMemcpy(pl.d_items, pl.items.data(), bytes, hipMemcpyHostToDevice) != hipSuccess) {
-            (void)hipFree(pl.d_items);
-            delete h;
-            return PURLIN_ERR_DEVICE;
-        }
-        if (pl.fused) {
-            const size_t sb = fused_state_bytes(pl);
-            if (hipMalloc(&pl.d_state, sb) != hipSuccess) {
-                pl.d_state = nullptr;
-                (void)hipFree(pl.d_items);
-                delete h;
-                return PURLIN_ERR_NOMEM;
-            }
-            if (hipMemset(pl.d_state, 0, sb) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
-                (void)hipFree(pl.d_state);
-                (void)hipFree(pl.d_items);
-                delete h;
-                return PURLIN_ERR_DEVICE;
-            }
+            return dst;
         }
     }
     *out_plan = h;
