@@ -397,6 +397,29 @@ PURLIN_API purlin_status purlin_pack(int T, int H, int K, int E, int P, const vo
                           int32_t* dev_status, void* workspace, uint64_t workspace_bytes,
                           void* stream);
 
+/* purlin_pack in two calls, so that the metadata, which reads only ids, can
+ * run earlier or on another stream than the rows (Section 2, Table 2: the
+ * dispatch; the counts are the scatteredV sizes of Section 3.1).
+ * purlin_pack_meta computes dest_counts, dest_offsets, expert_counts,
+ * expert_offsets and dev_status exactly as purlin_pack does, and leaves in
+ * `workspace` what purlin_pack_rows needs; purlin_pack_rows then writes
+ * packed and pos, bit-identical to purlin_pack.  Arguments have
+ * purlin_pack's meaning and limits; the rows call must use the same T, K,
+ * E and workspace, and must start after the metadata call has finished
+ * (same stream, or an event between the streams); the workspace must not
+ * be reused by another metadata call before the rows call has finished.
+ * A rows call without a matching metadata call writes unspecified rows of
+ * packed and pos, never outside them.  Errors: PURLIN_ERR_INVALID (limits,
+ * NULL or misaligned pointer, small workspace, x overlapping packed),
+ * PURLIN_ERR_DEVICE. */
+PURLIN_API purlin_status purlin_pack_meta(int T, int K, int E, int P, const int32_t* ids, int32_t* dest_counts,
+                                          int32_t* dest_offsets, int32_t* expert_counts, int32_t* expert_offsets,
+                                          int32_t* dev_status, void* workspace, uint64_t workspace_bytes,
+                                          void* stream);
+PURLIN_API purlin_status purlin_pack_rows(int T, int H, int K, int E, const void* x, const int32_t* ids,
+                                          void* packed, int32_t* pos, const void* workspace,
+                                          uint64_t workspace_bytes, void* stream);
+
 /* Bytes of the per-GPU workspace that purlin_pack_static uses instead of a
  * caller-supplied one. */
 #define PURLIN_STATIC_SCRATCH_BYTES (4u << 20)

@@ -405,6 +405,43 @@ purlin_status purlin_pack(int T, int H, int K, int E, int P, const void* x, cons
                                expert_offsets, pos, dev_status, workspace, stream);
 }
 
+purlin_status purlin_pack_meta(int T, int K, int E, int P, const int32_t* ids, int32_t* dest_counts,
+                               int32_t* dest_offsets, int32_t* expert_counts, int32_t* expert_offsets,
+                               int32_t* dev_status, void* workspace, uint64_t workspace_bytes, void* stream) {
+    if (T < 0 || K < 1 || K > 64 || E < 1 || E > 4096 || static_cast<int64_t>(T) * K >= (int64_t(1) << 31))
+        return PURLIN_ERR_INVALID;
+    if (P < 1 || P > E || E % P != 0) return PURLIN_ERR_INVALID;
+    if (!dest_counts || !dest_offsets || !expert_counts) return PURLIN_ERR_INVALID;
+    if (!aligned16(dest_counts) || !aligned16(dest_offsets) || !aligned16(expert_counts)) return PURLIN_ERR_INVALID;
+    if (expert_offsets && !aligned16(expert_offsets)) return PURLIN_ERR_INVALID;
+    if (dev_status && (reinterpret_cast<uintptr_t>(dev_status) & 3u)) return PURLIN_ERR_INVALID;
+    if (T > 0 && (!ids || !aligned16(ids))) return PURLIN_ERR_INVALID;
+    const uint64_t need = purlin::pack_workspace_bytes(T, K, E);
+    if (workspace_bytes < need || (need && (!workspace || !aligned16(workspace)))) return PURLIN_ERR_INVALID;
+    const purlin::PackWorkspace ws = purlin::pack_workspace_carve(workspace, T, K, E);
+    const hipError_t e = purlin::launch_pack_meta(T, K, E, P, ids, dest_counts, dest_offsets, expert_counts,
+                                                  expert_offsets, dev_status, ws, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
+purlin_status purlin_pack_rows(int T, int H, int K, int E, const void* x, const int32_t* ids, void* packed,
+                               int32_t* pos, const void* workspace, uint64_t workspace_bytes, void* stream) {
+    if (!pack_limits_ok(T, H, K, E)) return PURLIN_ERR_INVALID;
+    if (T > 0) {
+        if (!x || !ids || !packed || !pos) return PURLIN_ERR_INVALID;
+        if (!aligned16(x) || !aligned16(ids) || !aligned16(packed) || !aligned16(pos)) return PURLIN_ERR_INVALID;
+        const uint64_t xb = uint64_t(T) * H * 2, pb = xb * K;
+        if (overlaps(x, xb, packed, pb)) return PURLIN_ERR_INVALID;
+    }
+    const uint64_t need = purlin::pack_workspace_bytes(T, K, E);
+    if (workspace_bytes < need || (need && (!workspace || !aligned16(workspace)))) return PURLIN_ERR_INVALID;
+    const purlin::PackWorkspace ws = purlin::pack_workspace_carve(const_cast<void*>(workspace), T, K, E);
+    const hipError_t e = purlin::launch_pack_rows(T, H, K, E, static_cast<const uint16_t*>(x), ids,
+                                                  static_cast<uint16_t*>(packed), pos, ws,
+                                                  static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
 purlin_status purlin_pack_static(int T, int H, int K, int E, int P, const void* x, const int32_t* ids, void* packed,
                                  int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts,
                                  int32_t* expert_offsets, int32_t* pos, int32_t* dev_status, void* stream) {

@@ -64,6 +64,15 @@ hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, con
                        int32_t* expert_offsets, int32_t* pos, int32_t* dev_status, const PackWorkspace& ws,
                        hipStream_t stream);
 
+// The two halves of launch_pack: the metadata (reads ids only; fills the
+// workspace and the count/offset outputs) and the rows (reads x, ids and
+// the workspace; writes packed and pos).
+hipError_t launch_pack_meta(int T, int K, int E, int P, const int32_t* ids, int32_t* dest_counts,
+                            int32_t* dest_offsets, int32_t* expert_counts, int32_t* expert_offsets, int32_t* dev_status,
+                            const PackWorkspace& ws, hipStream_t stream);
+hipError_t launch_pack_rows(int T, int H, int K, int E, const uint16_t* x, const int32_t* ids, uint16_t* packed,
+                            int32_t* pos, const PackWorkspace& ws, hipStream_t stream);
+
 hipError_t launch_unpack(int T, int H, int K, const uint16_t* y, const int32_t* pos, const float* gates,
                          uint16_t* out, int32_t* dev_status, hipStream_t stream);
 

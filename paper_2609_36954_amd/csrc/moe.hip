@@ -828,9 +828,9 @@ PackWorkspace pack_workspace_carve(void* base, int T, int K, int E) {
     return ws;
 }
 
-hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, const int32_t* ids, uint16_t* packed,
-                       int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts, int32_t* expert_offsets,
-                       int32_t* pos, int32_t* dev_status, const PackWorkspace& ws, hipStream_t stream) {
+hipError_t launch_pack_meta(int T, int K, int E, int P, const int32_t* ids, int32_t* dest_counts,
+                            int32_t* dest_offsets, int32_t* expert_counts, int32_t* expert_offsets, int32_t* dev_status,
+                            const PackWorkspace& ws, hipStream_t stream) {
     const int ntiles = (T + kPackTileTokens - 1) / kPackTileTokens;
     (void)hipGetLastError();
     if (ntiles > 0) {
@@ -841,6 +841,12 @@ hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, con
     }
     hipLaunchKernelGGL(pack_scan, dim3(1), dim3(kScanThreads), 0, stream, ntiles, E, P, ws.tile_base, ws.tile_err,
                        expert_counts, expert_offsets, dest_counts, dest_offsets, dev_status, uint64_t(0));
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_rows(int T, int H, int K, int E, const uint16_t* x, const int32_t* ids, uint16_t* packed,
+                            int32_t* pos, const PackWorkspace& ws, hipStream_t stream) {
+    (void)hipGetLastError();
     if (T > 0) {
         const int slices = row_slices(H, kPackUnroll);
         const uint64_t waves = static_cast<uint64_t>(T) * slices;
@@ -850,6 +856,15 @@ hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, con
                            reinterpret_cast<char*>(packed));
     }
     return hipGetLastError();
+}
+
+hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, const int32_t* ids, uint16_t* packed,
+                       int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts, int32_t* expert_offsets,
+                       int32_t* pos, int32_t* dev_status, const PackWorkspace& ws, hipStream_t stream) {
+    const hipError_t e = launch_pack_meta(T, K, E, P, ids, dest_counts, dest_offsets, expert_counts, expert_offsets,
+                                          dev_status, ws, stream);
+    if (e != hipSuccess) return e;
+    return launch_pack_rows(T, H, K, E, x, ids, packed, pos, ws, stream);
 }
 
 hipError_t launch_unpack(int T, int H, int K, const uint16_t* y, const int32_t* pos, const float* gates, uint16_t* out,

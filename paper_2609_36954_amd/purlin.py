@@ -108,6 +108,8 @@ def lib():
     L.purlin_pack_workspace_size.argtypes = [i32, i32, i32, _c_u64p]
     L.purlin_pack.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 10 + [u64, _vp]
     L.purlin_pack_static.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 10
+    L.purlin_pack_meta.argtypes = [i32, i32, i32, i32] + [_vp] * 7 + [u64, _vp]
+    L.purlin_pack_rows.argtypes = [i32, i32, i32, i32] + [_vp] * 5 + [u64, _vp]
     L.purlin_unpack.argtypes = [i32, i32, i32] + [_vp] * 6
     L.purlin_pack_dedup_workspace_size.argtypes = [i32, i32, _c_u64p]
     L.purlin_pack_dedup.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 8 + [u64, _vp]
@@ -488,6 +490,45 @@ def purlin_pack(x, ids, E, P, out=None, workspace=None, dev_status=None, stream=
                            int(workspace.numel() * workspace.element_size()), _stream_handle(stream))
     _check(st, "purlin_pack")
     return o
+
+
+def purlin_pack_meta(ids, E, P, out, workspace, dev_status=None, stream=None):
+    """The metadata half of ``purlin_pack``: fills ``out``'s dest_counts,
+    dest_offsets, expert_counts and expert_offsets (and ``dev_status``) and
+    leaves the row positions' inputs in ``workspace``."""
+    import torch
+
+    T, K = ids.shape
+    if T:
+        _require_cuda(ids, "ids", 4)
+    shapes = {"dest_counts": ((P,), torch.int32), "dest_offsets": ((P,), torch.int32),
+              "expert_counts": ((E,), torch.int32), "expert_offsets": ((E,), torch.int32)}
+    _check_sizes(out, shapes)
+    st = lib().purlin_pack_meta(int(T), int(K), int(E), int(P), _ptr(ids), _ptr(out["dest_counts"]),
+                                _ptr(out["dest_offsets"]), _ptr(out["expert_counts"]), _ptr(out["expert_offsets"]),
+                                _ptr(dev_status), _ptr(workspace), int(workspace.numel() * workspace.element_size()),
+                                _stream_handle(stream))
+    _check(st, "purlin_pack_meta")
+    return out
+
+
+def purlin_pack_rows(x, ids, E, out, workspace, stream=None):
+    """The rows half of ``purlin_pack`` (after ``purlin_pack_meta`` on the
+    same workspace has finished): fills ``out``'s packed and pos."""
+    import torch
+
+    T, H = x.shape
+    K = ids.shape[1]
+    if ids.shape[0] != T:
+        raise PurlinError(PURLIN_ERR_INVALID, "x and ids disagree on T")
+    _require_cuda(x, "x", 2)
+    _require_cuda(ids, "ids", 4)
+    _check_sizes(out, {"packed": ((T * K, H), x.dtype), "pos": ((T, K), torch.int32)})
+    st = lib().purlin_pack_rows(int(T), int(H), int(K), int(E), _ptr(x), _ptr(ids), _ptr(out["packed"]),
+                                _ptr(out["pos"]), _ptr(workspace), int(workspace.numel() * workspace.element_size()),
+                                _stream_handle(stream))
+    _check(st, "purlin_pack_rows")
+    return out
 
 
 def purlin_pack_static(x, ids, E, P, out, dev_status=None, stream=None):

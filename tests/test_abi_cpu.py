@@ -212,6 +212,33 @@ def test_pack_argument_validation(kw):
     assert _pack(**kw) == INVALID
 
 
+def _pack_meta(T=64, K=2, E=8, P=2, ids=0x2000, dc=0x4000, do=0x5000, ec=0x6000, eo=None, status=None, ws=0x8000,
+               wsb=1 << 20):
+    return PL.lib().purlin_pack_meta(T, K, E, P, ids, dc, do, ec, eo, status, ws, wsb, None)
+
+
+def _pack_rows(T=64, H=64, K=2, E=8, x=0x1000, ids=0x2000, packed=0x100000, pos=0x7000, ws=0x8000, wsb=1 << 20):
+    return PL.lib().purlin_pack_rows(T, H, K, E, x, ids, packed, pos, ws, wsb, None)
+
+
+@pytest.mark.parametrize(
+    "kw",
+    [dict(K=0), dict(K=65), dict(E=0), dict(E=4097), dict(E=8, P=3), dict(P=0), dict(T=-1), dict(ids=None),
+     dict(ids=0x2004), dict(dc=None), dict(ec=0x6008), dict(status=0x9002), dict(ws=None), dict(wsb=16)],
+)
+def test_pack_meta_argument_validation(kw):
+    assert _pack_meta(**kw) == INVALID
+
+
+@pytest.mark.parametrize(
+    "kw",
+    [dict(K=0), dict(H=0), dict(T=-1), dict(x=None), dict(ids=None), dict(packed=None), dict(pos=None),
+     dict(x=0x1008), dict(ws=None), dict(wsb=16), dict(x=0x100000)],  # the last: x overlaps packed
+)
+def test_pack_rows_argument_validation(kw):
+    assert _pack_rows(**kw) == INVALID
+
+
 def _pack_static(T=64, H=64, K=2, E=8, P=2, x=0x1000, ids=0x2000, packed=0x3000, dc=0x4000, do=0x5000, ec=0x6000,
                  eo=None, pos=0x7000, status=None):
     return PL.lib().purlin_pack_static(T, H, K, E, P, x, ids, packed, dc, do, ec, eo, pos, status, None)

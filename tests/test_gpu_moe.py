@@ -110,6 +110,41 @@ def test_pack_reports_bad_routing(T, E):
     assert status == 0
 
 
+@pytest.mark.parametrize("T,H,K,E,P,seed", [(4096, 512, 8, 256, 8, 21), (333, 1000, 6, 120, 4, 22), (0, 64, 8, 256, 8, 23)])
+def test_pack_split_on_two_streams_matches_pack(T, H, K, E, P, seed):
+    """purlin_pack_meta on a side stream, an event, purlin_pack_rows on the
+    current stream: every output equals purlin_pack's and the oracle's."""
+    rng = np.random.default_rng(seed)
+    ids_np = W.zipf_topk_ids(T, E, K, 1.1, seed) if T else np.zeros((0, K), np.int32)
+    x_np = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
+    want, status = run_pack(x_np, ids_np, E, P)
+    assert status == 0
+    x, ids = to_device(x_np), to_device(ids_np)
+    ws = torch.empty(max(16, PL.purlin_pack_workspace_size(T, K, E)), dtype=torch.uint8, device="cuda")
+    g = {"packed": Guarded(T * K * H * 2, torch.int16), "pos": Guarded(T * K * 4, torch.int32),
+         "dest_counts": Guarded(P * 4, torch.int32), "dest_offsets": Guarded(P * 4, torch.int32),
+         "expert_counts": Guarded(E * 4, torch.int32), "expert_offsets": Guarded(E * 4, torch.int32)}
+    out = {k: v.t for k, v in g.items()}
+    out["packed"] = out["packed"].view(T * K, H)
+    out["pos"] = out["pos"].view(T, K)
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    PL.purlin_pack_meta(ids, E, P, out, ws, dev_status=st, stream=side)
+    done = torch.cuda.Event()
+    done.record(side)
+    torch.cuda.current_stream().wait_event(done)
+    PL.purlin_pack_rows(x, ids, E, out, ws)
+    torch.cuda.synchronize()
+    assert all(v.intact() for v in g.values())
+    assert int(st[0].item()) == 0
+    for key in want:
+        got = to_host(g[key].t, np.uint16 if key == "packed" else np.int32).reshape(want[key].shape)
+        assert np.array_equal(got, want[key]), key
+    ref = oracle.pack(x_np, ids_np, E, P)
+    assert np.array_equal(want["packed"], ref["packed"]) and np.array_equal(want["pos"], ref["pos"])
+
+
 def run_unpack(y_np, pos_np, g_np, status=True):
     T, K = pos_np.shape
     H = y_np.shape[1]
