@@ -165,9 +165,10 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
     dest_offsets += static_cast<int64_t>(rank) * P;
     if (dev_status) dev_status += rank;
 
-    // error flags first, so their loads overlap the count loads
-    int any = 0;
-    for (int t = tid; t < ntiles; t += kScanThreads) any |= tile_err[t];
+    // error flags: one per thread when the tiles fit one pass (its load is
+    // only consumed at the end, so it overlaps the count loads), else a loop
+    int err0 = 0;
+    if (ntiles <= kScanThreads && tid < ntiles) err0 = tile_err[tid];
 
     // Work units: tpe threads per expert when E is small, each owning a
     // contiguous slice of tiles; one unit per expert when E >= 1024.  A
@@ -259,6 +260,9 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
         dest_offsets[r] = offs[r * L];
     }
 
+    int any = err0;
+    if (ntiles > kScanThreads)
+        for (int t = tid; t < ntiles; t += kScanThreads) any |= tile_err[t];
     any = __syncthreads_or(any);
     if (tid == 0 && dev_status) *dev_status = any ? 1 : 0;
 }
