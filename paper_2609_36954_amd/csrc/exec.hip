@@ -207,7 +207,12 @@ __device__ __forceinline__ void run_reduce(const ExecArgs& a, const purlin_desc&
     const char* src[NSRC];
 #pragma unroll
     for (int p = 0; p < NSRC; ++p) src[p] = a.srcs[p] + d.src_off;
-    if (((d.src_off | d.dst_off) & 15) != 0) {
+    // Unaligned items, and bf16 items of fewer than 12 vectors, go element
+    // by element: a wavefront with at most 8 of its lanes active runs the
+    // bf16 widening and rounding about 0.8 us slower (measured on MI355X,
+    // P = 8: 128-byte items 2.5 us, 192-byte items 1.8 us per graph-replayed
+    // call; the same 128 bytes over 16 or 64 lanes 1.65 us).
+    if (((d.src_off | d.dst_off) & 15) != 0 || (BF16 && d.bytes < 12 * 16)) {
         reduce_elems<NSRC, BF16>(a, d, src, 0, d.bytes, lane);
         return;
     }
