@@ -406,6 +406,10 @@ def main():
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(torch, ins_np, rs_out, ag_out, x_np, ids_np, y_np, g_np, pack_out, comb_out, P, N, M, E, K)
 
+    # ---------------- the MoE ops' access mixes as plain streams, in the ops' place ----------------
+    in_step = measure_in_step_streams(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x, y, pack_out["packed"],
+                                      comb_out, T, H, K, per_op, args.steps)
+
     # ---------------- the other collectives at the same shape (not in the step) ----------------
     extra = None
     if not args.no_extra:
@@ -423,7 +427,7 @@ def main():
         latency = measure_latency(torch, PL, W, graph_latency_us, not args.no_latency_sweep)
     ceilings = None if args.no_extra else measure_ceilings(torch, PL)
     return emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, per_op, latency, plan_ms,
-                dev_name, src_hash, extra, ceilings)
+                dev_name, src_hash, extra, ceilings, in_step)
 
 
 def graph_call_us(torch, enqueue, calls=128, reps=8):
@@ -840,6 +844,54 @@ def measure_ceilings(torch, PL, nbytes=1 << 30, reps=20):
     return out
 
 
+def measure_in_step_streams(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x, y, packed, comb_out, T, H, K,
+                            per_op, steps):
+    """The MoE ops against plain streams of their own access mix, timed in
+    their place in the step: the same ReduceScatter and AllGather run first
+    (their 2 GiB streams evict the token matrix from the last-level cache, as
+    in the step), then the pack's mix (the token matrix, T x H, read once and
+    written to K destinations of T x H each: the packed buffer's K
+    consecutive slices, cached loads and non-temporal stores as the pack's
+    rows kernel) and the combine's mix (K sources of T x H, the expert
+    outputs' slices, into one T x H output, non-temporal loads and stores as
+    the combine), with the step's events between all four ops.  The streams
+    move the rows' bytes in sequential order, so an op's ratio to its stream
+    is what its own access order costs."""
+    nb = T * H * 2
+    dsts = [packed[i * T:(i + 1) * T] for i in range(K)]
+    srcs = [y[i * T:(i + 1) * T] for i in range(K)]
+    evs = [[TimingEvent(torch) for _ in range(5)] for _ in range(steps)]
+    for i in range(steps + 2):
+        ev = evs[i - 2] if i >= 2 else None  # two untimed passes first
+        if ev:
+            ev[0].record()
+        rs_plan.exec(ins, rs_out)
+        if ev:
+            ev[1].record()
+        ag_plan.exec(rs_out, ag_out)
+        if ev:
+            ev[2].record()
+        PL.purlin_stream(dsts, [x], nbytes=nb, nt_load=False, nt_store=True)
+        if ev:
+            ev[3].record()
+        PL.purlin_stream([comb_out], srcs, nbytes=nb, nt_load=True, nt_store=True)
+        if ev:
+            ev[4].record()
+    torch.cuda.synchronize()
+    out = {}
+    for name, j, desc in (("moe_pack", 2, f"1 source ({nb} B) -> {K} destinations, cached loads, nt stores"),
+                          ("moe_combine", 3, f"{K} sources ({nb} B each) -> 1 destination, nt loads, nt stores")):
+        ts = [e[j].elapsed_time(e[j + 1]) * 1e3 for e in evs]
+        us = float(np.mean(ts))
+        moved = (K + 1) * nb
+        op = per_op[name]
+        out[name] = {"stream": desc, "bytes": moved, "avg_us": round(us, 2), "median_us": round(float(np.median(ts)), 2),
+                     "GBps": round(moved / (us * 1e-6) / 1e9, 1),
+                     "frac_of_hbm_peak": round(moved / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                     "op_avg_us": op["avg_us"], "op_over_stream": round(op["avg_us"] / us, 4)}
+    return out
+
+
 def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
     # The floor: the smallest launch the library makes (a 16-byte copy, one
     # wavefront's worth of a workgroup), timed like the collectives below.
@@ -924,7 +976,7 @@ def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):
 
 
 def emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, per_op, latency, plan_ms, dev_name,
-         src_hash, extra, ceilings=None):
+         src_hash, extra, ceilings=None, in_step=None):
     result = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -954,6 +1006,7 @@ def emit(args, value, ms_per_step, step_bytes, P, N, T, H, E, K, roofline, cpu, 
         "latency_us": latency,
         "other_ops_256MiB_per_rank": extra,
         "copy_ceilings": ceilings,
+        "in_step_streams": in_step,
         "plan_ms": round(plan_ms, 3),
         "device": dev_name,
         "kernel_source_hash": src_hash,

@@ -173,6 +173,8 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
     // Work units: tpe threads per expert when E is small, each owning a
     // contiguous slice of tiles; one unit per expert when E >= 1024.  A
     // unit whose slice fits kScanBatch keeps its counts in registers.
+    // Unit u is (slice q = u / E, expert e = u % E): consecutive lanes read
+    // and write consecutive experts of one tile row.
     const int tpe = E >= kScanThreads ? 1 : kScanThreads / E;
     const int units = E * tpe;
     const int span = (ntiles + tpe - 1) / tpe;
@@ -180,7 +182,7 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
 
     int c[kScanBatch];
     for (int u = tid; u < units; u += kScanThreads) {
-        const int e = u / tpe, q = u - e * tpe;
+        const int q = u / E, e = u - q * E;
         const int lo = min(ntiles, q * span), hi = min(ntiles, lo + span);
         int sum = 0;
         for (int t = lo; t < hi; t += kScanBatch) {
@@ -194,7 +196,7 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
     __syncthreads();
     for (int e = tid; e < E; e += kScanThreads) {
         int sum = 0;
-        for (int q = 0; q < tpe; ++q) sum += partial[e * tpe + q];
+        for (int q = 0; q < tpe; ++q) sum += partial[q * E + e];
         total[e] = sum;
     }
     __syncthreads();
@@ -233,10 +235,10 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
 
     // Rewrite each tile's count into the row of its first (t, k) per expert.
     for (int u = tid; u < units; u += kScanThreads) {
-        const int e = u / tpe, q = u - e * tpe;
+        const int q = u / E, e = u - q * E;
         const int lo = min(ntiles, q * span), hi = min(ntiles, lo + span);
         int base = offs[e];
-        for (int q2 = 0; q2 < q; ++q2) base += partial[e * tpe + q2];
+        for (int q2 = 0; q2 < q; ++q2) base += partial[q2 * E + e];
         for (int t = lo; t < hi; t += kScanBatch) {
             if (!in_regs) {
 #pragma unroll
@@ -781,15 +783,25 @@ __global__ __launch_bounds__(kBlock) void ep_dedup_combine_rows(EpArgs a) {
         1.0f, P, a.dst[p] + t * row_bytes, row_bytes, slice, lane);
 }
 
-// Merges the ranks' routing-error words (contiguous) into the caller's status word.
 // Launch shapes and cache hints, measured on MI355X: the packed rows and
 // the expert outputs are streams far larger than the last-level cache.
 // One 16-byte vector per lane, 1 KiB column slices: many short waves hide
 // the row loads best (pack 4% and the de-duplicated pack 22% faster than
 // 8 KiB slices, measured in the bench pipeline at 4096 x 7168, K = 8).
+// The pack reads its token rows non-temporally: in a cycle of
+// ReduceScatter, AllGather (P = 8, 256 MiB per rank), pack and combine, the
+// rows kernel takes the same time either way but the AllGather after it
+// (which reads the ReduceScatter's output, written with cached stores) ran
+// 14 us faster and the cycle 1003 -> 986 us, the 56 MiB token matrix no
+// longer taking last-level cache space.  The de-duplicated and
+// expert-parallel dispatches keep cached loads (de-duplicated pack of 8
+// ranks 445 -> 470 us with non-temporal ones).  A wave per (token, slot)
+// writing whole 14 KiB rows measured 10% faster than the slices after an
+// AllGather alone but made the cycle slower (1000 -> 1030 us).
 constexpr int kPackUnroll = 1;
 constexpr int kDedupUnroll = 1;
-constexpr bool kPackNtLoad = false;
+constexpr bool kPackNtLoad = true;
+constexpr bool kDispatchNtLoad = false;  // de-duplicated and expert-parallel dispatch rows
 constexpr bool kPackNtStore = true;
 constexpr int kUnpackUnroll = 1;
 constexpr bool kUnpackNtLoad = true;
@@ -913,7 +925,7 @@ hipError_t launch_pack_dedup(int T, int H, int K, int E, int P, const uint16_t* 
         const int slices = row_slices(H, kDedupUnroll);
         const uint64_t waves = static_cast<uint64_t>(T) * slices;
         const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
-        hipLaunchKernelGGL((dedup_rows<kDedupUnroll, kPackNtLoad, kPackNtStore>), grid, dim3(kBlock), 0, stream, T, H,
+        hipLaunchKernelGGL((dedup_rows<kDedupUnroll, kDispatchNtLoad, kPackNtStore>), grid, dim3(kBlock), 0, stream, T, H,
                            P, slices, reinterpret_cast<const char*>(x), tile_base, lrank, dest_offsets, row_of,
                            reinterpret_cast<char*>(packed));
     }
@@ -999,7 +1011,7 @@ hipError_t launch_ep_dispatch(int T, int H, int K, int E, int P, const uint16_t*
         a.slices = row_slices(H, kPackUnroll);
         const uint64_t waves = Pu * static_cast<uint64_t>(T) * a.slices;
         const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
-        hipLaunchKernelGGL((ep_dispatch_rows<kPackUnroll, kPackNtLoad, kPackNtStore>), grid, dim3(kBlock), 0, stream,
+        hipLaunchKernelGGL((ep_dispatch_rows<kPackUnroll, kDispatchNtLoad, kPackNtStore>), grid, dim3(kBlock), 0, stream,
                            a);
     }
     return hipGetLastError();
@@ -1099,7 +1111,7 @@ hipError_t launch_ep_dispatch_dedup(int T, int H, int K, int E, int P, const uin
         a.slices = row_slices(H, kDedupUnroll);
         const uint64_t waves = Pu * static_cast<uint64_t>(T) * a.slices;
         const dim3 grid(static_cast<uint32_t>((waves + kWavesPerBlock - 1) / kWavesPerBlock));
-        hipLaunchKernelGGL((ep_dedup_dispatch_rows<kDedupUnroll, kPackNtLoad, kPackNtStore>), grid, dim3(kBlock), 0,
+        hipLaunchKernelGGL((ep_dedup_dispatch_rows<kDedupUnroll, kDispatchNtLoad, kPackNtStore>), grid, dim3(kBlock), 0,
                            stream, a);
     }
     return hipGetLastError();
