@@ -230,6 +230,8 @@ def main():
     ap.add_argument("--bandwidth-sweep", action="store_true",
                     help="also time AllReduce, ReduceScatter, AllGather and AllToAll at 1 MiB..1 GiB per rank "
                          "(the paper's bandwidth range; 16 GiB of buffers)")
+    ap.add_argument("--sweep-only", action="store_true",
+                    help="only the bandwidth sweep (its kernels alone, for counter runs)")
     ap.add_argument("--plateau", action="store_true",
                     help="also time ReduceScatter and AllGather with the grid capped at 4..512 workgroups "
                          "(off by default: the capped launches share the step's kernels and would skew their "
@@ -254,6 +256,9 @@ def main():
 
     PL.lib()  # fail loudly if the HIP library is missing
     torch.cuda.set_device(0)
+    if args.sweep_only:
+        print(json.dumps(measure_bandwidth_sweep(torch, PL)), flush=True)
+        return 0
     dev_name = torch.cuda.get_device_name(0)
     src_hash = kernel_source_hash()
 
