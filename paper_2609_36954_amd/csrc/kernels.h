@@ -64,12 +64,14 @@ hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, con
                        int32_t* expert_offsets, int32_t* pos, int32_t* dev_status, const PackWorkspace& ws,
                        hipStream_t stream);
 
-// The two halves of launch_pack: the metadata (reads ids only; fills the
-// workspace and the count/offset outputs) and the rows (reads x, ids and
-// the workspace; writes packed and pos).
+// The two halves of launch_pack: the metadata (reads ids; fills the
+// workspace and the count/offset outputs; given the token matrix, also
+// reads it ahead into the caches) and the rows (reads x, ids and the
+// workspace; writes packed and pos).
 hipError_t launch_pack_meta(int T, int K, int E, int P, const int32_t* ids, int32_t* dest_counts,
                             int32_t* dest_offsets, int32_t* expert_counts, int32_t* expert_offsets, int32_t* dev_status,
-                            const PackWorkspace& ws, hipStream_t stream);
+                            const PackWorkspace& ws, hipStream_t stream, const void* prefetch = nullptr,
+                            uint64_t prefetch_bytes = 0);
 hipError_t launch_pack_rows(int T, int H, int K, int E, const uint16_t* x, const int32_t* ids, uint16_t* packed,
                             int32_t* pos, const PackWorkspace& ws, hipStream_t stream);
 

@@ -90,12 +90,50 @@ __device__ __forceinline__ uint32_t to_bf16(float f) {
     return (u & 0x7FFFFFFFu) > 0x7F800000u ? quiet_nan : rounded;
 }
 
+// A byte range that extra workgroups of a metadata launch read through the
+// caches and drop: the token matrix, read while the latency-bound metadata
+// leaves HBM idle, so that the rows kernel after it finds the matrix in the
+// last-level cache and streams its writes alone.  `blocks` workgroups
+// (after the launch's own) read [lo, hi) of `base`.
+struct Prefetch {
+    const char* base;
+    uint64_t lo, hi;
+    uint32_t blocks;
+};
+
+// Workgroup `part` of `parts` reads its share of p's range, 16-byte loads,
+// four in flight per thread; the values only feed an empty asm statement,
+// which keeps the loads without storing anything.
+__device__ __forceinline__ void prefetch_part(const Prefetch& p, uint32_t part) {
+    const uint64_t v0 = p.lo / 16, v1 = p.hi / 16;
+    const uint64_t per = (v1 - v0 + p.blocks - 1) / p.blocks;
+    const uint64_t lo = v0 + per * part, hi = min(v1, lo + per);
+    const uint32_t nt = blockDim.x;
+    u32x4 acc = {0u, 0u, 0u, 0u};
+    for (uint64_t i = lo + threadIdx.x; i < hi; i += 4ull * nt) {
+        u32x4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const uint64_t j = i + static_cast<uint64_t>(u) * nt;
+            v[u] = j < hi ? load16<false>(p.base + j * 16) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc ^= v[u];
+    }
+    __asm__ volatile("" : : "v"(acc));
+}
+
 __global__ __launch_bounds__(kBlock) void pack_tiles(int T, int K, int E, RankIds rids, int32_t* __restrict__ tile_cnt,
                                                      int32_t* __restrict__ lrank, int32_t* __restrict__ tile_err,
-                                                     uint64_t stride) {
+                                                     uint64_t stride, Prefetch pf) {
     extern __shared__ unsigned long long masks[];  // [E]
     __shared__ int32_t tids[kPackTileTokens * 64];  // the tile's ids (K <= 64)
     __shared__ int err;
+    const uint32_t ntiles = gridDim.x - pf.blocks;
+    if (blockIdx.x >= ntiles) {
+        prefetch_part(pf, blockIdx.x - ntiles);
+        return;
+    }
     const int tile = blockIdx.x;
     const int rank = blockIdx.y;
     const int32_t* ids = rids.ids[rank];
@@ -150,7 +188,13 @@ __global__ __launch_bounds__(kScanThreads) void pack_scan(int ntiles, int E, int
                                                           int32_t* __restrict__ expert_offsets,
                                                           int32_t* __restrict__ dest_counts,
                                                           int32_t* __restrict__ dest_offsets,
-                                                          int32_t* __restrict__ dev_status, uint64_t stride) {
+                                                          int32_t* __restrict__ dev_status, uint64_t stride,
+                                                          Prefetch pf) {
+    const uint32_t nscan = gridDim.x - pf.blocks;
+    if (blockIdx.x >= nscan) {
+        prefetch_part(pf, blockIdx.x - nscan);
+        return;
+    }
     __shared__ int32_t partial[kMaxExperts];  // per work unit (expert, tile slice)
     __shared__ int32_t total[kMaxExperts];    // per expert
     __shared__ int32_t offs[kMaxExperts];     // per expert, exclusive prefix
@@ -800,6 +844,11 @@ __global__ __launch_bounds__(kBlock) void ep_dedup_combine_rows(EpArgs a) {
 // AllGather alone but made the cycle slower (1000 -> 1030 us).
 constexpr int kPackUnroll = 1;
 constexpr int kDedupUnroll = 1;
+// Token matrices read ahead by the pack's metadata launches: from 8 MiB
+// (below, the rows kernel is latency-bound) to 128 MiB (half the 256 MB
+// last-level cache, so the matrix survives until the rows kernel reads it).
+constexpr uint64_t kPrefetchMinBytes = uint64_t(8) << 20;
+constexpr uint64_t kPrefetchMaxBytes = uint64_t(128) << 20;
 constexpr bool kPackNtLoad = true;
 constexpr bool kDispatchNtLoad = false;  // de-duplicated and expert-parallel dispatch rows
 constexpr bool kPackNtStore = true;
@@ -846,17 +895,39 @@ PackWorkspace pack_workspace_carve(void* base, int T, int K, int E) {
 
 hipError_t launch_pack_meta(int T, int K, int E, int P, const int32_t* ids, int32_t* dest_counts,
                             int32_t* dest_offsets, int32_t* expert_counts, int32_t* expert_offsets, int32_t* dev_status,
-                            const PackWorkspace& ws, hipStream_t stream) {
+                            const PackWorkspace& ws, hipStream_t stream, const void* prefetch,
+                            uint64_t prefetch_bytes) {
     const int ntiles = (T + kPackTileTokens - 1) / kPackTileTokens;
+    // The token matrix, when given and of a size the last-level cache holds
+    // well, is read by extra workgroups of both launches: the first 2/5 with
+    // the tiles, the rest with the scan, one pass of four 16-byte loads per
+    // thread.  Measured on MI355X in the bench step (4096 x 7168 bf16,
+    // after a 2 GiB AllGather): rows kernel 103 -> 89 us, tiles 4.6 -> 8.5
+    // us, scan 6.7 -> 13.5 us, the pack 115 -> 111 us (the metadata's
+    // dependent loads slow down under the read traffic, so the matrix's
+    // 8-9 us of reading is only partly hidden); the whole matrix read with
+    // the tiles instead: 15.4 + 7.3 + 92.7 us.
+    Prefetch pt{}, ps{};
+    if (prefetch && ntiles > 0 && prefetch_bytes >= kPrefetchMinBytes && prefetch_bytes <= kPrefetchMaxBytes) {
+        const uint64_t cut = prefetch_bytes * 2 / 5 / 16 * 16;
+        const auto blocks = [](uint64_t bytes, uint32_t threads, uint32_t most) {
+            const uint64_t per = static_cast<uint64_t>(threads) * 64;  // four 16-byte loads per thread
+            return static_cast<uint32_t>(std::min<uint64_t>(most, (bytes + per - 1) / per));
+        };
+        pt = Prefetch{static_cast<const char*>(prefetch), 0, cut, blocks(cut, kBlock, 4096)};
+        ps = Prefetch{static_cast<const char*>(prefetch), cut, prefetch_bytes / 16 * 16,
+                      blocks(prefetch_bytes - cut, kScanThreads, 768)};
+    }
     (void)hipGetLastError();
     if (ntiles > 0) {
         RankIds rids{};
         rids.ids[0] = ids;
-        hipLaunchKernelGGL(pack_tiles, dim3(ntiles), dim3(kBlock), static_cast<size_t>(E) * 8, stream, T, K, E, rids,
-                           ws.tile_base, ws.lrank, ws.tile_err, uint64_t(0));
+        hipLaunchKernelGGL(pack_tiles, dim3(ntiles + pt.blocks), dim3(kBlock), static_cast<size_t>(E) * 8, stream, T,
+                           K, E, rids, ws.tile_base, ws.lrank, ws.tile_err, uint64_t(0), pt);
     }
-    hipLaunchKernelGGL(pack_scan, dim3(1), dim3(kScanThreads), 0, stream, ntiles, E, P, ws.tile_base, ws.tile_err,
-                       expert_counts, expert_offsets, dest_counts, dest_offsets, dev_status, uint64_t(0));
+    hipLaunchKernelGGL(pack_scan, dim3(1 + ps.blocks), dim3(kScanThreads), 0, stream, ntiles, E, P, ws.tile_base,
+                       ws.tile_err, expert_counts, expert_offsets, dest_counts, dest_offsets, dev_status, uint64_t(0),
+                       ps);
     return hipGetLastError();
 }
 
@@ -878,7 +949,7 @@ hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, con
                        int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts, int32_t* expert_offsets,
                        int32_t* pos, int32_t* dev_status, const PackWorkspace& ws, hipStream_t stream) {
     const hipError_t e = launch_pack_meta(T, K, E, P, ids, dest_counts, dest_offsets, expert_counts, expert_offsets,
-                                          dev_status, ws, stream);
+                                          dev_status, ws, stream, x, static_cast<uint64_t>(T) * H * 2);
     if (e != hipSuccess) return e;
     return launch_pack_rows(T, H, K, E, x, ids, packed, pos, ws, stream);
 }
@@ -982,9 +1053,9 @@ hipError_t launch_ep_dispatch(int T, int H, int K, int E, int P, const uint16_t*
     for (int p = 0; p < P; ++p) rids.ids[p] = ids[p];
     if (ntiles > 0)
         hipLaunchKernelGGL(pack_tiles, dim3(ntiles, P), dim3(kBlock), static_cast<size_t>(E) * 8, stream, T, K, E, rids,
-                           w0.tile_base, w0.lrank, w0.tile_err, per);
+                           w0.tile_base, w0.lrank, w0.tile_err, per, Prefetch{});
     hipLaunchKernelGGL(pack_scan, dim3(P), dim3(kScanThreads), 0, stream, ntiles, E, P, w0.tile_base, w0.tile_err,
-                       expert_counts, static_cast<int32_t*>(nullptr), counts, dest_off, words, per);
+                       expert_counts, static_cast<int32_t*>(nullptr), counts, dest_off, words, per, Prefetch{});
     hipLaunchKernelGGL(ep_prefix, dim3(1), dim3(kBlock), 0, stream, counts, P, capacity, before, fits, words,
                        dev_status);
     for (int p = 0; p < P; ++p) {
