@@ -17,11 +17,16 @@
 //      expert totals, exclusive prefix over experts, destination
 //      counts/offsets, and the error flag.  The per-tile counts are
 //      rewritten in place into each tile's first row per expert.
-//   3. pack_rows: one wavefront per token.  Lane k forms pos[t, k]; the wave
-//      then streams the token row once from HBM through registers and
-//      writes it to its K packed rows with 16-byte stores.
-// Unpack is one launch, one wavefront per token, slots in groups of 4 with
-// all their 16-byte row loads in flight before the FP32 accumulation.
+//   3. pack_rows: one wavefront per (token, 1 KiB column slice).  Lane k
+//      forms pos[t, k]; the wave then streams its slice of the token row
+//      through registers and writes it to the K packed rows with 16-byte
+//      stores.
+// Extra workgroups of the first two launches read the token matrix ahead
+// (when it is 8-128 MiB), so that the rows kernel finds it in the
+// last-level cache.
+// Unpack is one launch, one wavefront per (token, slice), slots in groups
+// of 4 with all their 16-byte row loads in flight before the FP32
+// accumulation.
 //
 // The de-duplicated variants (one row per token and destination rank) use
 // the same structure with destinations in place of experts: pack_dedup is
