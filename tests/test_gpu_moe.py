@@ -69,6 +69,9 @@ def check_pack(x_np, ids_np, E, P):
         (2500, 48, 13, 200, 8, 17),  # K = 13, E = 200, ragged last tile
         (32769, 8, 1, 16, 4, 18),  # 513 tiles, the last one a single token
         (100, 24, 4, 264, 8, 19),  # E = 264
+        (600, 7171, 8, 256, 8, 24),  # 8.2 MiB token matrix read ahead, odd rows (element path)
+        (4100, 1030, 8, 256, 8, 25),  # 8.1 MiB read ahead, rows not a multiple of 16 bytes
+        (8192, 8192, 2, 64, 8, 26),  # 128 MiB: the largest matrix read ahead
     ],
 )
 def test_pack_matches_oracle(T, H, K, E, P, seed):
