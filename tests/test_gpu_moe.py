@@ -148,6 +148,69 @@ def test_pack_split_on_two_streams_matches_pack(T, H, K, E, P, seed):
     assert np.array_equal(want["packed"], ref["packed"]) and np.array_equal(want["pos"], ref["pos"])
 
 
+@pytest.mark.parametrize("fill", [0xFF, 0x00, 0x5A])
+def test_pack_on_uncleared_workspace_and_again(fill):
+    """The workspace's contents on entry do not matter: filled with a byte
+    pattern, then reused for a second routing; each call matches the oracle."""
+    T, H, K, E, P = 1000, 256, 8, 256, 8
+    ws = torch.full((PL.purlin_pack_workspace_size(T, K, E),), fill, dtype=torch.uint8, device="cuda")
+    for seed in (31, 32):
+        rng = np.random.default_rng(seed)
+        ids_np = W.zipf_topk_ids(T, E, K, 1.1, seed)
+        x_np = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
+        st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+        r = PL.purlin_pack(to_device(x_np), to_device(ids_np), E, P, workspace=ws, dev_status=st)
+        torch.cuda.synchronize()
+        assert int(st[0].item()) == 0
+        want = oracle.pack(x_np, ids_np, E, P)
+        for key in ("dest_counts", "dest_offsets", "expert_counts", "expert_offsets", "pos"):
+            assert np.array_equal(to_host(r[key], np.int32).reshape(want[key].shape), want[key]), (seed, key)
+        assert np.array_equal(to_host(r["packed"], np.uint16).reshape(T * K, H), want["packed"]), seed
+
+
+def test_pack_in_a_graph_replayed_with_new_routing():
+    """One purlin_pack captured in a graph, replayed three times with new
+    tokens and routing loaded eagerly between the replays: every replay
+    matches the oracle."""
+    T, H, K, E, P = 4096, 512, 8, 256, 8
+    x = torch.empty((T, H), dtype=torch.int16, device="cuda")
+    ids = torch.empty((T, K), dtype=torch.int32, device="cuda")
+    ws = torch.empty(PL.purlin_pack_workspace_size(T, K, E), dtype=torch.uint8, device="cuda")
+    out = dict(packed=torch.empty((T * K, H), dtype=torch.int16, device="cuda"),
+               dest_counts=torch.empty(P, dtype=torch.int32, device="cuda"),
+               dest_offsets=torch.empty(P, dtype=torch.int32, device="cuda"),
+               expert_counts=torch.empty(E, dtype=torch.int32, device="cuda"),
+               expert_offsets=torch.empty(E, dtype=torch.int32, device="cuda"),
+               pos=torch.empty((T, K), dtype=torch.int32, device="cuda"))
+
+    def load(seed):
+        rng = np.random.default_rng(seed)
+        ids_np = W.zipf_topk_ids(T, E, K, 1.1, seed)
+        x_np = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
+        x.copy_(to_device(x_np))
+        ids.copy_(to_device(ids_np))
+        return x_np, ids_np
+
+    load(40)
+    PL.purlin_pack(x, ids, E, P, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            PL.purlin_pack(x, ids, E, P, out=out, workspace=ws, stream=side)
+    for rep, seed in enumerate((41, 42, 43)):
+        x_np, ids_np = load(seed)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        want = oracle.pack(x_np, ids_np, E, P)
+        for key in ("dest_counts", "dest_offsets", "expert_counts", "pos"):
+            assert np.array_equal(to_host(out[key], np.int32).reshape(want[key].shape), want[key]), (rep, key)
+        assert np.array_equal(to_host(out["packed"], np.uint16).reshape(T * K, H), want["packed"]), rep
+
+
 def run_unpack(y_np, pos_np, g_np, status=True):
     T, K = pos_np.shape
     H = y_np.shape[1]
