@@ -49,7 +49,7 @@ KERNEL_SOURCES = ["paper_2609_36954_amd/csrc/exec.hip", "paper_2609_36954_amd/cs
 KERNEL_OF_OP = {
     "reduce_scatter": "exec_reduce<8, true",
     "allgather": "exec_copy<",
-    "moe_pack": "::pack_rows<",  # the rows kernel (not unpack_rows); the metadata launches move ~0.3 MiB
+    "moe_pack": "::pack_onepass<",  # the single-launch pack (the three-launch form: pack_tiles, pack_scan, pack_rows)
     "moe_combine": "unpack_rows<",
 }
 CALIBRATION_KERNEL = "copy"  # torch's device-to-device copy of --calibrate-copy

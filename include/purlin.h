@@ -361,6 +361,16 @@ PURLIN_API purlin_status purlin_plan_device_error(purlin_plan_t plan, uint32_t* 
  * alive until work queued with it has finished. */
 PURLIN_API void purlin_plan_destroy(purlin_plan_t plan);
 
+/* Whether purlin_pack runs in one launch for this shape (*single = 1) or in
+ * three (*single = 0: per-tile metadata, its scan, then the rows).  The
+ * one-launch form applies when every workgroup can count all T*K ids itself
+ * and hold its tokens' rows in registers: rows a multiple of 16 bytes
+ * (H % 8 == 0), 4 <= T*K <= 32768, E <= 1024, and at most 512 workgroups of
+ * at most 64 tokens and 1024 (t, k) pairs each.  Both forms give the same
+ * results (the definition below); the workspace is sized for either.
+ * PURLIN_ERR_INVALID for NULL `single` or shapes purlin_pack rejects. */
+PURLIN_API purlin_status purlin_pack_single_launch(int T, int H, int K, int E, int* single);
+
 /* Workspace bytes purlin_pack needs for T tokens, K slots, E experts. */
 PURLIN_API purlin_status purlin_pack_workspace_size(int T, int K, int E, uint64_t* bytes);
 

@@ -391,6 +391,12 @@ purlin_status purlin_pack_workspace_size(int T, int K, int E, uint64_t* bytes) {
     return PURLIN_OK;
 }
 
+purlin_status purlin_pack_single_launch(int T, int H, int K, int E, int* single) {
+    if (!single || !pack_limits_ok(T, H, K, E)) return PURLIN_ERR_INVALID;
+    *single = purlin::pack_onepass_tokens(T, H, K, E) > 0 ? 1 : 0;
+    return PURLIN_OK;
+}
+
 purlin_status purlin_pack(int T, int H, int K, int E, int P, const void* x, const int32_t* ids, void* packed,
                           int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts,
                           int32_t* expert_offsets, int32_t* pos, int32_t* dev_status, void* workspace,

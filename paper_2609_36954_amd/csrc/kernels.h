@@ -59,6 +59,10 @@ uint64_t pack_workspace_bytes(int T, int K, int E);
 bool moe_launch_fits(int T, int H);  // the pack/unpack grids for T tokens of H elements are launchable
 PackWorkspace pack_workspace_carve(void* base, int T, int K, int E);
 
+// Tokens per workgroup of the one-pass pack for this shape, or 0 when
+// launch_pack takes the three launches (metadata tiles, scan, rows).
+int pack_onepass_tokens(int T, int H, int K, int E);
+
 hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, const int32_t* ids,
                        uint16_t* packed, int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts,
                        int32_t* expert_offsets, int32_t* pos, int32_t* dev_status, const PackWorkspace& ws,

@@ -391,6 +391,225 @@ __global__ __launch_bounds__(kBlock) void pack_rows(int T, int H, int K, int E, 
 }
 
 // ---------------------------------------------------------------------------
+// The whole pack in one launch, for routings small enough that every
+// workgroup can count all of them itself (T*K <= kOneMaxIds, E <=
+// kOneMaxExperts) and hold its own tokens' rows in registers.  Workgroup b
+// owns tokens [b*tw, b*tw + tw) and never waits for another workgroup:
+//   1. it loads every id (4 to a vector) and its own ids;
+//   2. it counts every id into LDS, split at its first token: before[e] =
+//      ids of e in earlier tokens, after[e] = the rest (lane l adds into copy
+//      l % C of the counters, C up to 16, so the routings' popular experts
+//      do not serialise one LDS word: with Zipf(1.1) routing over 256
+//      experts, expert 0 is in 86% of the tokens); it marks its own tokens
+//      in one 64-bit mask per expert; then it issues the loads of its rows of
+//      x (kOneVec 16-byte vectors per thread, non-temporal), which arrive
+//      while it finishes the metadata;
+//   3. expert totals, their exclusive prefix over experts, and the positions
+//      of its own (t, k): offset[e] + before[e] + earlier own tokens of e;
+//   4. it writes each vector of its rows to the K packed rows of its token,
+//      each as soon as that vector has arrived.
+// Workgroup 0 also writes the counts and offsets and, after its rows, checks
+// every token for repeated ids and writes the status word (it has seen every
+// id, so it knows of out-of-range ones).  Ranks follow from counts, so the
+// result is the same whatever the order of the LDS atomics.
+constexpr int kOneThreads = 1024;
+constexpr int kOneVec = 16;                               // x vectors per thread: 64 VGPRs
+constexpr int kOneIdVec = 8;                              // id vectors (4 ids) per thread
+constexpr int kOneMaxIds = kOneIdVec * 4 * kOneThreads;  // 32768
+constexpr int kOneMaxExperts = kOneThreads;              // one expert per thread in the scan
+constexpr int kOneMaxOwn = kOneThreads;                  // own (t, k) pairs: one per thread
+constexpr int kOneUnrolledSlots = 8;                     // K up to this: the store loop unrolled
+constexpr int kOneMaxCopies = 16;                        // counter copies (lanes modulo)
+constexpr uint32_t kOneCopyBytes = 40u << 10;            // LDS for the counter copies (64 KiB in all)
+
+template <int KMAX, bool NTL, bool NTS>
+__global__ __launch_bounds__(kOneThreads) void pack_onepass(int T, int K, int E, int P, int tw, uint32_t nvec,
+                                                            int copies, const char* __restrict__ x,
+                                                            const int32_t* __restrict__ ids,
+                                                            char* __restrict__ packed, int32_t* __restrict__ pos,
+                                                            int32_t* __restrict__ expert_counts,
+                                                            int32_t* __restrict__ expert_offsets,
+                                                            int32_t* __restrict__ dest_counts,
+                                                            int32_t* __restrict__ dest_offsets,
+                                                            int32_t* __restrict__ dev_status) {
+    // Counter copy c holds before[] at [c*S, c*S + E) and after[] at
+    // [c*S + E, c*S + 2E); S = 2E + 1 is odd, so one expert's copies lie in
+    // different LDS banks.
+    extern __shared__ int32_t hist[];
+    __shared__ int32_t cnt[2 * kOneMaxExperts];  // summed copies: before[e], then after[e]
+    __shared__ int32_t offs[kOneMaxExperts];
+    __shared__ unsigned long long masks[kOneMaxExperts];
+    __shared__ int32_t own_pos[kOneMaxOwn];
+    __shared__ int32_t wave_tot[kOneThreads / kWave];
+    __shared__ int bad_any;
+
+    const int tid = threadIdx.x;
+    const int t0 = static_cast<int>(blockIdx.x) * tw;
+    const int nt = min(tw, T - t0);
+    const int n = T * K;
+    const int first = t0 * K;  // this workgroup's first (t, k)
+    const int nown = nt * K;
+    const uint64_t row_bytes = static_cast<uint64_t>(nvec) * 16;
+    const int S = 2 * E + 1;
+
+    // 1. loads of the ids.  Every load is issued unconditionally (indexes
+    // clamped into range, n >= 4), so the code is straight-line and each
+    // use waits only for its own load.
+    const int n4 = n / 4;
+    u32x4 idv[kOneIdVec];
+#pragma unroll
+    for (int q = 0; q < kOneIdVec; ++q) {
+        const int j = min(tid + q * kOneThreads, n4 - 1);
+        idv[q] = *reinterpret_cast<const u32x4*>(ids + 4 * j);
+    }
+    const int tail = n - 4 * n4;
+    const int tail_e = ids[min(4 * n4 + tid, n - 1)];
+    const int own_e = ids[first + min(tid, nown - 1)];
+    for (int i = tid; i < copies * S; i += kOneThreads) hist[i] = 0;
+    for (int e = tid; e < E; e += kOneThreads) masks[e] = 0ull;
+    if (tid == 0) bad_any = 0;
+    __syncthreads();
+
+    // 2. count every id, split at this workgroup's first token
+    bool bad = false;
+    int32_t* h = hist + (tid & (copies - 1)) * S;
+#pragma unroll
+    for (int q = 0; q < kOneIdVec; ++q) {
+        const int j = tid + q * kOneThreads;
+        if (j < n4) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int e = static_cast<int>(idv[q][r]);
+                if (e < 0 || e >= E)
+                    bad = true;
+                else
+                    atomicAdd(&h[(4 * j + r >= first ? E : 0) + e], 1);
+            }
+        }
+    }
+    if (tid < tail) {
+        if (tail_e < 0 || tail_e >= E)
+            bad = true;
+        else
+            atomicAdd(&h[(4 * n4 + tid >= first ? E : 0) + tail_e], 1);
+    }
+    const int tl = tid / K;  // own token of (t, k) = (t0 + tl, tid % K)
+    const bool own_ok = tid < nown && own_e >= 0 && own_e < E;
+    if (own_ok) {
+        const unsigned long long bit = 1ull << tl;
+        if (atomicOr(&masks[own_e], bit) & bit) bad = true;  // repeated within the token
+    }
+    // the rows: issued after the counting in program order (a wave whose
+    // loads cannot all issue at once would otherwise stall the counting
+    // behind them)
+    __asm__ volatile("" ::: "memory");
+    const uint32_t nv = static_cast<uint32_t>(nt) * nvec;
+    const char* xs = x + static_cast<uint64_t>(t0) * row_bytes;
+    u32x4 v[kOneVec];
+#pragma unroll
+    for (int u = 0; u < kOneVec; ++u) {
+        const uint32_t i = min(static_cast<uint32_t>(u * kOneThreads + tid), nv - 1);
+        v[u] = load16<NTL>(xs + static_cast<uint64_t>(i) * 16);
+    }
+    if (bad) bad_any = 1;  // every writer stores the same value
+    __syncthreads();
+    for (int e = tid; e < E; e += kOneThreads) {
+        int before = 0, after = 0;
+        for (int c = 0; c < copies; ++c) {
+            before += hist[c * S + e];
+            after += hist[c * S + E + e];
+        }
+        cnt[e] = before;
+        cnt[E + e] = after;
+    }
+    __syncthreads();
+
+    // 3. expert totals and their exclusive prefix: one expert per thread
+    const int tot = tid < E ? cnt[tid] + cnt[E + tid] : 0;
+    const uint32_t lane = tid & (kWave - 1), wave = tid / kWave;
+    int incl = tot;
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int w = __shfl_up(incl, off);
+        if (lane >= static_cast<uint32_t>(off)) incl += w;
+    }
+    if (lane == kWave - 1) wave_tot[wave] = incl;
+    __syncthreads();
+    int wave_base = lane < wave ? wave_tot[lane] : 0;
+    for (int off = kWave / 2; off > 0; off >>= 1) wave_base += __shfl_xor(wave_base, off);
+    const int excl = wave_base + incl - tot;
+    if (tid < E) offs[tid] = excl;
+    if (blockIdx.x == 0 && tid < E) {
+        expert_counts[tid] = tot;
+        if (expert_offsets) expert_offsets[tid] = excl;
+    }
+    __syncthreads();
+    if (blockIdx.x == 0 && tid < P) {
+        const int L = E / P;
+        const int end = tid + 1 < P ? offs[(tid + 1) * L] : offs[E - 1] + cnt[E - 1] + cnt[2 * E - 1];
+        dest_counts[tid] = end - offs[tid * L];
+        dest_offsets[tid] = offs[tid * L];
+    }
+    if (tid < nown) {
+        int p = -1;
+        if (own_ok) {
+            const int64_t q = static_cast<int64_t>(offs[own_e]) + cnt[own_e] +
+                              __popcll(masks[own_e] & ((1ull << tl) - 1ull));
+            p = q < n ? static_cast<int>(q) : -1;
+        }
+        own_pos[tid] = p;
+        pos[first + tid] = p;
+    }
+    __syncthreads();
+
+    // 4. every vector of the rows to its token's K packed rows.  With
+    // KMAX > 0 (K <= KMAX) the slots are unrolled, so the code stays
+    // straight-line and each vector's stores wait only for that vector.
+    uint32_t tok = static_cast<uint32_t>(tid) / nvec, col = static_cast<uint32_t>(tid) - tok * nvec;
+    const uint32_t step_tok = kOneThreads / nvec, step_col = kOneThreads - step_tok * nvec;
+#pragma unroll
+    for (int u = 0; u < kOneVec; ++u) {
+        const uint32_t i = static_cast<uint32_t>(u * kOneThreads + tid);
+        const bool live = i < nv;
+        const int32_t* pk = own_pos + min(tok, static_cast<uint32_t>(nt - 1)) * K;
+        char* dst = packed + col * 16ull;
+        if constexpr (KMAX > 0) {
+            int pv[KMAX];
+#pragma unroll
+            for (int k = 0; k < KMAX; ++k) pv[k] = k < K ? pk[k] : -1;
+#pragma unroll
+            for (int k = 0; k < KMAX; ++k)
+                if (live && pv[k] >= 0) store16<NTS>(dst + static_cast<uint64_t>(pv[k]) * row_bytes, v[u]);
+        } else if (live) {
+            for (int k = 0; k < K; ++k) {
+                const int p = pk[k];
+                if (p >= 0) store16<NTS>(dst + static_cast<uint64_t>(p) * row_bytes, v[u]);
+            }
+        }
+        tok += step_tok;
+        col += step_col;
+        if (col >= nvec) {
+            col -= nvec;
+            ++tok;
+        }
+    }
+
+    // workgroup 0: ids repeated within any token, then the status word
+    if (blockIdx.x == 0 && dev_status) {
+        bool dup = false;
+        for (int t = tid; t < T; t += kOneThreads) {
+            const int32_t* row = ids + static_cast<int64_t>(t) * K;
+            for (int k = 1; k < K; ++k) {
+                const int e = row[k];
+                for (int k2 = 0; k2 < k; ++k2)
+                    if (row[k2] == e) dup = true;
+            }
+        }
+        const int any = __syncthreads_or(dup || bad_any);
+        if (tid == 0) *dev_status = any ? 1 : 0;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // De-duplicated dispatch: one row per (token, destination rank).
 //   1. dedup_tiles: one workgroup per tile of 64 tokens stages the tile's
 //      ids in LDS; then one wavefront, lane = token, forms each token's
@@ -854,6 +1073,10 @@ constexpr int kDedupUnroll = 1;
 // last-level cache, so the matrix survives until the rows kernel reads it).
 constexpr uint64_t kPrefetchMinBytes = uint64_t(8) << 20;
 constexpr uint64_t kPrefetchMaxBytes = uint64_t(128) << 20;
+// The one-pass pack: a grid of one workgroup per compute unit of MI355X
+// (256); at most two rounds of it.
+constexpr int kOneGroups = 256;
+constexpr int kOneMaxGroups = 2 * kOneGroups;
 constexpr bool kPackNtLoad = true;
 constexpr bool kDispatchNtLoad = false;  // de-duplicated and expert-parallel dispatch rows
 constexpr bool kPackNtStore = true;
@@ -950,9 +1173,38 @@ hipError_t launch_pack_rows(int T, int H, int K, int E, const uint16_t* x, const
     return hipGetLastError();
 }
 
+int pack_onepass_tokens(int T, int H, int K, int E) {
+    const uint64_t row_bytes = static_cast<uint64_t>(H) * 2;
+    if (T < 1 || row_bytes % 16 != 0 || E > kOneMaxExperts) return 0;
+    if (static_cast<int64_t>(T) * K > kOneMaxIds || T * K < 4) return 0;
+    const uint64_t nvec = row_bytes / 16;
+    const uint64_t most = static_cast<uint64_t>(kOneVec) * kOneThreads;  // x vectors a workgroup holds
+    if (nvec > most) return 0;
+    // as many workgroups as compute units, fewer tokens each when the rows
+    // do not fit the registers, the token masks (64 bits) or the position
+    // table (then the grid runs in more than one round)
+    const uint64_t tw = std::min<uint64_t>({(static_cast<uint64_t>(T) + kOneGroups - 1) / kOneGroups, most / nvec,
+                                            uint64_t(64), static_cast<uint64_t>(kOneMaxOwn / K)});
+    if (tw < 1 || (static_cast<uint64_t>(T) + tw - 1) / tw > kOneMaxGroups) return 0;
+    return static_cast<int>(tw);
+}
+
 hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, const int32_t* ids, uint16_t* packed,
                        int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts, int32_t* expert_offsets,
                        int32_t* pos, int32_t* dev_status, const PackWorkspace& ws, hipStream_t stream) {
+    if (const int tw = pack_onepass_tokens(T, H, K, E)) {
+        (void)hipGetLastError();
+        const uint32_t nvec = static_cast<uint32_t>(static_cast<uint64_t>(H) * 2 / 16);
+        const auto kernel = K <= kOneUnrolledSlots ? pack_onepass<kOneUnrolledSlots, kPackNtLoad, kPackNtStore>
+                                                   : pack_onepass<0, kPackNtLoad, kPackNtStore>;
+        int copies = kOneMaxCopies;
+        while (copies > 1 && static_cast<uint64_t>(copies) * (2 * E + 1) * 4 > kOneCopyBytes) copies /= 2;
+        const size_t lds = static_cast<size_t>(copies) * (2 * E + 1) * 4;
+        hipLaunchKernelGGL(kernel, dim3((T + tw - 1) / tw), dim3(kOneThreads), lds, stream, T, K, E, P, tw, nvec,
+                           copies, reinterpret_cast<const char*>(x), ids, reinterpret_cast<char*>(packed), pos,
+                           expert_counts, expert_offsets, dest_counts, dest_offsets, dev_status);
+        return hipGetLastError();
+    }
     const hipError_t e = launch_pack_meta(T, K, E, P, ids, dest_counts, dest_offsets, expert_counts, expert_offsets,
                                           dev_status, ws, stream, x, static_cast<uint64_t>(T) * H * 2);
     if (e != hipSuccess) return e;

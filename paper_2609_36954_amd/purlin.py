@@ -106,6 +106,7 @@ def lib():
     L.purlin_plan_destroy.argtypes = [_vp]
     L.purlin_plan_destroy.restype = None
     L.purlin_pack_workspace_size.argtypes = [i32, i32, i32, _c_u64p]
+    L.purlin_pack_single_launch.argtypes = [i32, i32, i32, i32, ctypes.POINTER(ctypes.c_int)]
     L.purlin_pack.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 10 + [u64, _vp]
     L.purlin_pack_static.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 10
     L.purlin_pack_meta.argtypes = [i32, i32, i32, i32] + [_vp] * 7 + [u64, _vp]
@@ -130,7 +131,7 @@ def lib():
     for name in ("purlin_plan", "purlin_plan_ex", "purlin_plan_rooted", "purlin_plan_v", "purlin_plan_share",
                  "purlin_exec_v",
                  "purlin_plan_info", "purlin_plan_descriptors", "purlin_plan_items",
-                 "purlin_exec", "purlin_pack_workspace_size", "purlin_pack", "purlin_unpack",
+                 "purlin_exec", "purlin_pack_workspace_size", "purlin_pack_single_launch", "purlin_pack", "purlin_unpack",
                  "purlin_pack_dedup_workspace_size", "purlin_pack_dedup", "purlin_unpack_dedup",
                  "purlin_ep_dispatch_workspace_size", "purlin_ep_dispatch", "purlin_ep_combine",
                  "purlin_ep_dispatch_dedup_workspace_size", "purlin_ep_dispatch_dedup", "purlin_ep_combine_dedup",
@@ -455,6 +456,14 @@ def purlin_pack_workspace_size(T, K, E):
     b = ctypes.c_uint64()
     _check(lib().purlin_pack_workspace_size(int(T), int(K), int(E), ctypes.byref(b)), "purlin_pack_workspace_size")
     return b.value
+
+
+def purlin_pack_single_launch(T, H, K, E):
+    """True when ``purlin_pack`` runs in one launch for this shape."""
+    v = ctypes.c_int(0)
+    _check(lib().purlin_pack_single_launch(int(T), int(H), int(K), int(E), ctypes.byref(v)),
+           "purlin_pack_single_launch")
+    return bool(v.value)
 
 
 def purlin_pack(x, ids, E, P, out=None, workspace=None, dev_status=None, stream=None):

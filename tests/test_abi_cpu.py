@@ -179,6 +179,47 @@ def test_pack_workspace_size():
     assert L.purlin_pack_workspace_size(4096, 8, 256, None) == INVALID
 
 
+@pytest.mark.parametrize(
+    "T,H,K,E,single",
+    [
+        (4096, 7168, 8, 256, True),  # the MoE dispatch of the bench: 256 workgroups of 16 tokens
+        (1, 8, 4, 4, True),  # T*K = 4, the smallest
+        (1, 8, 3, 4, False),  # T*K = 3
+        (32768, 8, 1, 16, True),  # T*K = 32768, the largest
+        (32769, 8, 1, 16, False),
+        (4097, 8, 8, 256, False),  # 32776 ids
+        (100, 24, 4, 1024, True),  # E = 1024, the largest
+        (100, 24, 4, 1025, False),
+        (65, 7, 3, 9, False),  # rows not a multiple of 16 bytes
+        (4100, 1030, 8, 256, False),
+        (0, 64, 8, 256, False),  # no tokens
+        (4700, 7168, 4, 256, True),  # 18 tokens per workgroup (registers): 262 workgroups, two rounds
+        (9000, 7168, 2, 256, True),  # 18 per workgroup: 500 workgroups
+        (9300, 7168, 2, 256, False),  # 517 workgroups
+        (300, 131072, 8, 256, True),  # one 256 KiB row per workgroup, 300 workgroups
+        (300, 131080, 8, 256, False),  # a row beyond a workgroup's registers
+        (16384, 16, 2, 256, True),  # 64 tokens per workgroup
+        (16448, 16, 1, 256, True),  # 65 per compute unit: 64 per workgroup, 257 workgroups
+        (512, 16, 64, 256, True),  # 2 tokens x 64 slots per workgroup
+        (8192, 16, 4, 256, True),  # 32 tokens x 4 slots per workgroup
+        (1024, 16, 32, 256, True),  # 4 tokens x 32 slots
+        (4096, 16, 64, 256, False),  # 262144 ids
+    ],
+)
+def test_pack_single_launch_shapes(T, H, K, E, single):
+    assert PL.purlin_pack_single_launch(T, H, K, E) is single
+
+
+def test_pack_single_launch_rejects_bad_shapes():
+    L = PL.lib()
+    v = ctypes.c_int(7)
+    assert L.purlin_pack_single_launch(4096, 7168, 8, 256, None) == INVALID
+    assert L.purlin_pack_single_launch(-1, 64, 8, 256, ctypes.byref(v)) == INVALID
+    assert L.purlin_pack_single_launch(64, 64, 65, 256, ctypes.byref(v)) == INVALID
+    assert L.purlin_pack_single_launch(64, 64, 8, 4097, ctypes.byref(v)) == INVALID
+    assert v.value == 7
+
+
 def _pack(T=64, H=64, K=2, E=8, P=2, x=0x1000, ids=0x2000, packed=0x3000, dc=0x4000, do=0x5000, ec=0x6000, eo=None,
           pos=0x7000, status=None, ws=0x8000, wsb=1 << 20):
     return PL.lib().purlin_pack(T, H, K, E, P, x, ids, packed, dc, do, ec, eo, pos, status, ws, wsb, None)

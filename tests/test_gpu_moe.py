@@ -72,9 +72,19 @@ def check_pack(x_np, ids_np, E, P):
         (600, 7171, 8, 256, 8, 24),  # 8.2 MiB token matrix read ahead, odd rows (element path)
         (4100, 1030, 8, 256, 8, 25),  # 8.1 MiB read ahead, rows not a multiple of 16 bytes
         (8192, 8192, 2, 64, 8, 26),  # 128 MiB: the largest matrix read ahead
+        # one launch: limits and ragged edges
+        (1, 8, 4, 4, 2, 27),  # T*K = 4, the smallest
+        (2499, 48, 13, 200, 8, 28),  # 32487 ids: three after the last 4-id vector
+        (100, 24, 4, 1024, 8, 29),  # E = 1024, the largest
+        (16448, 16, 1, 256, 4, 30),  # 64 tokens per workgroup, 257 workgroups (two rounds)
+        (4700, 7168, 4, 256, 8, 31),  # 18 rows per workgroup (registers), 262 workgroups
+        (260, 131072, 8, 256, 8, 32),  # one 256 KiB row per workgroup: 16 vectors per thread
+        (512, 8200, 64, 256, 8, 33),  # rows of 1025 vectors (more than the threads), K = 64
+        (8000, 24, 4, 1000, 8, 34),  # 32 tokens per workgroup, 250 workgroups
     ],
 )
 def test_pack_matches_oracle(T, H, K, E, P, seed):
+    print(f"pack T={T} H={H} K={K} E={E} P={P} one launch={PL.purlin_pack_single_launch(T, H, K, E)}", flush=True)
     rng = np.random.default_rng(seed)
     ids = _distinct_ids(rng, T, K, E)
     x = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
@@ -109,6 +119,10 @@ def test_pack_reports_bad_routing(T, E):
     got, status = run_pack(x, oob, E, P)
     assert status == 1
     assert got["pos"][66, 1] == -1
+    oob[T - 1, 3] = -5  # negative, in the last token
+    got, status = run_pack(x, oob, E, P)
+    assert status == 1
+    assert got["pos"][66, 1] == -1 and got["pos"][T - 1, 3] == -1
     _, status = run_pack(x, ids, E, P)
     assert status == 0
 
@@ -282,6 +296,7 @@ def test_pack_then_unpack_round_trip():
 def test_pack_and_combine_4096x7168_top8_of_256_full_size():
     """4096 tokens x 7168 hidden, E=256 over P=8, top-8 Zipf(1.1); then combine."""
     cfg = W.MOE_CONFIG
+    assert PL.purlin_pack_single_launch(cfg.T, cfg.H, cfg.K, cfg.E)
     ids = W.zipf_topk_ids(cfg.T, cfg.E, cfg.K, cfg.zipf_s, cfg.seed_ids)
     x = W.moe_tokens(cfg)
     got, status = run_pack(x, ids, cfg.E, cfg.P)

@@ -56,13 +56,15 @@ def _run(fn, x_np, ids_np, E, P):
     return _host(g, T, H, K), int(st[0].item())
 
 
-# (T, H, K, E, P, seed): the second call is smaller in every dimension but
-# E, with a ragged last token tile; the third is the 4096-token, top-8 of
-# 256 experts routing table.
-CALLS = [(5000, 256, 8, 288, 8, 41), (1200, 200, 6, 512, 8, 42), (4096, 1024, 8, 256, 8, 43)]
+# (T, H, K, E, P, seed): the first two calls take the three launches that
+# use the static workspace, the second smaller in T and H, with a ragged
+# last token tile; the third is the 4096-token, top-8 of 256 experts
+# routing table, which runs in one launch without a workspace.
+CALLS = [(5000, 256, 8, 288, 8, 41), (4200, 200, 8, 512, 8, 42), (4096, 1024, 8, 256, 8, 43)]
 
 
 def test_pack_static_matches_pack_on_two_calls_in_a_row():
+    assert [PL.purlin_pack_single_launch(T, H, K, E) for T, H, K, E, _, _ in CALLS] == [False, False, True]
     for T, H, K, E, P, seed in CALLS:
         ids_np = W.zipf_topk_ids(T, E, K, 1.1, seed)
         x_np = W.normal_bf16(np.random.default_rng(seed + 100), T * H).reshape(T, H)
