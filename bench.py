@@ -415,6 +415,10 @@ def main():
     in_step = measure_in_step_streams(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x, y, pack_out["packed"],
                                       comb_out, T, H, K, per_op, args.steps)
 
+    # ---------------- how the chip's dies share the pack's time ----------------
+    in_step["xcd_balance"] = measure_xcd_balance(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x, ids, y, g,
+                                                 pack_out, comb_out, T, H, E, K, P)
+
     # ---------------- the other collectives at the same shape (not in the step) ----------------
     extra = None
     if not args.no_extra:
@@ -895,6 +899,66 @@ def measure_in_step_streams(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x,
                      "frac_of_hbm_peak": round(moved / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
                      "op_avg_us": op["avg_us"], "op_over_stream": round(op["avg_us"] / us, 4)}
     return out
+
+
+def _xcd_summary(PL, rate, recs):
+    fin = PL.xcd_finish_times(rate, recs)
+    ends = [fin[k]["end_us"] for k in sorted(fin)]
+    return {"span_us": round(max(ends), 2),
+            "xcd_end_us": {str(k): round(fin[k]["end_us"], 2) for k in sorted(fin)},
+            "xcd_meta_us": {str(k): round(fin[k]["meta_us"], 2) for k in sorted(fin)},
+            "mean_xcd_end_us": round(float(np.mean(ends)), 2),
+            "first_to_last_xcd": round(max(ends) - min(ends), 2)}
+
+
+def measure_xcd_balance(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x, ids, y, g, pack_out, comb_out, T, H,
+                        E, K, P, reps=6):
+    """When each of the chip's XCDs (accelerator dies; workgroup b runs on XCD
+    b % 8) finishes its share of the pack, in the pack's place in the step
+    (after the same ReduceScatter and AllGather; the one-launch pack with its
+    timing record, purlin_pack_timed), and of plain streams of the pack's and
+    the combine's access mix of the same size run back to back.  Each
+    workgroup's end is the wall clock once all its stores have completed; an
+    XCD's end is its last workgroup's; times from the first workgroup's
+    entry, the median over `reps` runs per XCD."""
+    log("bench: XCD finishing times")
+    if not PL.purlin_pack_single_launch(T, H, K, E):
+        return None
+    runs = []
+    rec = None
+    for i in range(reps + 1):
+        rs_plan.exec(ins, rs_out)
+        ag_plan.exec(rs_out, ag_out)
+        rec, groups = PL.purlin_pack_timed(x, ids, E, P, pack_out, rec=rec)
+        PL.purlin_unpack(y, pack_out["pos"], g, out=comb_out)
+        torch.cuda.synchronize()
+        if i:  # the first run is a warm-up
+            runs.append(_xcd_summary(PL, *PL._timed_records(rec, groups)))
+    out = {"pack_in_step": _median_runs(runs)}
+    nb = T * H * 2
+    dsts = [pack_out["packed"][i * T:(i + 1) * T] for i in range(K)]
+    srcs = [y[i * T:(i + 1) * T] for i in range(K)]
+    for name, dd, ss, ntl, nts in (("stream_1to8_pack_size", dsts, [x], False, True),
+                                   ("stream_8to1_combine_size", [comb_out], srcs, True, True),
+                                   ("stream_write_only_packed_size", [pack_out["packed"]], [], False, True)):
+        nbytes = nb * K if name.startswith("stream_write") else nb
+        runs = []
+        for i in range(reps + 1):
+            r = PL.purlin_stream_timed(dd, ss, nbytes=nbytes, nt_load=ntl, nt_store=nts)
+            if i:
+                runs.append(_xcd_summary(PL, *r))
+        out[name] = _median_runs(runs)
+    return out
+
+
+def _median_runs(runs):
+    """Per-field medians of several _xcd_summary results."""
+    m = {k: round(float(np.median([r[k] for r in runs])), 2) for k in ("span_us", "mean_xcd_end_us",
+                                                                        "first_to_last_xcd")}
+    for key in ("xcd_end_us", "xcd_meta_us"):
+        m[key] = {x: round(float(np.median([r[key][x] for r in runs])), 2) for x in runs[0][key]}
+    m["runs"] = len(runs)
+    return m
 
 
 def measure_latency(torch, PL, W, graph_latency_us, sweep_sizes):

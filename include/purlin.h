@@ -640,6 +640,33 @@ PURLIN_API purlin_status purlin_stream_copy(void* dst, const void* src, uint64_t
 PURLIN_API purlin_status purlin_stream(void* const* dst, int ndst, const void* const* src, int nsrc, uint64_t bytes,
                                        void* sink, uint32_t hints, void* stream);
 
+/* Measurement entry points: purlin_stream and the one-launch purlin_pack,
+ * each also recording when every workgroup ran and on which XCD (the
+ * chip's accelerator dies; the hardware hands workgroup b to XCD b % 8), so
+ * that a kernel's time can be split into its dies' finishing times.  Not
+ * steps of the method.  `rec` (device, 16-byte aligned, rec_entries
+ * uint64 entries, at least 4 * (groups + 1)) receives
+ *   rec[0] = the wall-clock rate in kHz, rec[1] = groups,
+ *   rec[4(b+1) + 0..3] = {XCD id, wall clock at entry, wall clock when the
+ *                        workgroup's metadata was done (its entry for a
+ *                        stream), wall clock once all its stores completed}
+ * for every workgroup b.  The recording adds one wait and one barrier at the
+ * end of each workgroup.  `groups` (host, optional) receives the number of
+ * workgroups; with rec = NULL nothing is launched (a size query).
+ * purlin_stream_timed: arguments and errors as purlin_stream, plus
+ * PURLIN_ERR_INVALID for a short, misaligned or overlapping rec.
+ * purlin_pack_timed: arguments, results and errors as purlin_pack (no
+ * workspace), for shapes purlin_pack_single_launch accepts; other shapes
+ * give PURLIN_ERR_UNSUPPORTED. */
+PURLIN_API purlin_status purlin_stream_timed(void* const* dst, int ndst, const void* const* src, int nsrc,
+                                             uint64_t bytes, void* sink, uint32_t hints, uint64_t* rec,
+                                             uint64_t rec_entries, uint64_t* groups, void* stream);
+PURLIN_API purlin_status purlin_pack_timed(int T, int H, int K, int E, int P, const void* x, const int32_t* ids,
+                                           void* packed, int32_t* dest_counts, int32_t* dest_offsets,
+                                           int32_t* expert_counts, int32_t* expert_offsets, int32_t* pos,
+                                           int32_t* dev_status, uint64_t* rec, uint64_t rec_entries,
+                                           uint64_t* groups, void* stream);
+
 /* Static text for a status code ("unknown status" for others). */
 PURLIN_API const char* purlin_status_string(purlin_status status);
 

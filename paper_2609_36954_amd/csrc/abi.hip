@@ -666,6 +666,60 @@ purlin_status purlin_stream(void* const* dst, int ndst, const void* const* src, 
     return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
 }
 
+purlin_status purlin_stream_timed(void* const* dst, int ndst, const void* const* src, int nsrc, uint64_t bytes,
+                                  void* sink, uint32_t hints, uint64_t* rec, uint64_t rec_entries, uint64_t* groups,
+                                  void* stream) {
+    if (nsrc < 0 || nsrc > PURLIN_MAX_RANKS || bytes % 16) return PURLIN_ERR_INVALID;
+    const uint64_t g = purlin::stream_groups(nsrc, bytes);
+    if (groups) *groups = g;
+    if (!rec) return PURLIN_OK;
+    if (g == 0) return purlin_stream(dst, ndst, src, nsrc, bytes, sink, hints, stream);
+    if (!aligned16(rec) || rec_entries < purlin::kRecPerGroup * (g + 1)) return PURLIN_ERR_INVALID;
+    if (overlaps(rec, rec_entries * 8, sink, 16)) return PURLIN_ERR_INVALID;
+    for (int j = 0; j < ndst && dst; ++j)
+        if (overlaps(rec, rec_entries * 8, dst[j], bytes)) return PURLIN_ERR_INVALID;
+    // the stream's own checks, then the timed launch
+    if (hints & ~uint32_t(PURLIN_STREAM_NT_LOAD | PURLIN_STREAM_NT_STORE)) return PURLIN_ERR_INVALID;
+    if (ndst < 0 || ndst > PURLIN_MAX_RANKS || nsrc + ndst == 0) return PURLIN_ERR_INVALID;
+    if ((nsrc && !src) || (ndst && !dst)) return PURLIN_ERR_INVALID;
+    if (ndst == 0 && (!sink || !aligned16(sink))) return PURLIN_ERR_INVALID;
+    for (int p = 0; p < nsrc; ++p)
+        if (!src[p] || !aligned16(src[p])) return PURLIN_ERR_INVALID;
+    for (int j = 0; j < ndst; ++j) {
+        if (!dst[j] || !aligned16(dst[j])) return PURLIN_ERR_INVALID;
+        for (int p = 0; p < nsrc; ++p)
+            if (overlaps(dst[j], bytes, src[p], bytes)) return PURLIN_ERR_INVALID;
+        for (int k = 0; k < j; ++k)
+            if (overlaps(dst[j], bytes, dst[k], bytes)) return PURLIN_ERR_INVALID;
+    }
+    const hipError_t e =
+        purlin::launch_stream(dst, ndst, src, nsrc, bytes, sink, hints, static_cast<hipStream_t>(stream), rec);
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
+purlin_status purlin_pack_timed(int T, int H, int K, int E, int P, const void* x, const int32_t* ids, void* packed,
+                                int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts,
+                                int32_t* expert_offsets, int32_t* pos, int32_t* dev_status, uint64_t* rec,
+                                uint64_t rec_entries, uint64_t* groups, void* stream) {
+    if (!pack_limits_ok(T, H, K, E)) return PURLIN_ERR_INVALID;
+    const int tw = purlin::pack_onepass_tokens(T, H, K, E);
+    if (tw == 0) return PURLIN_ERR_UNSUPPORTED;
+    const uint64_t g = (static_cast<uint64_t>(T) + tw - 1) / tw;
+    if (groups) *groups = g;
+    if (!rec) return PURLIN_OK;
+    const purlin_status st = check_pack_args(T, H, K, E, P, x, ids, packed, dest_counts, dest_offsets, expert_counts,
+                                             expert_offsets, pos, dev_status);
+    if (st != PURLIN_OK) return st;
+    if (!aligned16(rec) || rec_entries < purlin::kRecPerGroup * (g + 1)) return PURLIN_ERR_INVALID;
+    if (overlaps(rec, rec_entries * 8, packed, uint64_t(T) * K * H * 2)) return PURLIN_ERR_INVALID;
+    const purlin::PackWorkspace ws{};  // the one-launch form uses none
+    const hipError_t e = purlin::launch_pack(T, H, K, E, P, static_cast<const uint16_t*>(x), ids,
+                                             static_cast<uint16_t*>(packed), dest_counts, dest_offsets,
+                                             expert_counts, expert_offsets, pos, dev_status, ws,
+                                             static_cast<hipStream_t>(stream), rec);
+    return e == hipSuccess ? PURLIN_OK : PURLIN_ERR_DEVICE;
+}
+
 const char* purlin_status_string(purlin_status status) {
     switch (status) {
         case PURLIN_OK: return "ok";

@@ -758,6 +758,8 @@ struct StreamArgs {
     u32x4* sink;
     uint64_t nvec;
     int nsrc, ndst;
+    uint64_t* rec;  // timing records, or null
+    uint64_t rate_khz;
 };
 
 constexpr int stream_unroll(int nsrc) { return nsrc >= 8 ? 2 : 4; }
@@ -768,6 +770,7 @@ constexpr int stream_unroll(int nsrc) { return nsrc >= 8 ? 2 : 4; }
 template <int NS, int ND, int U, bool NTL, bool NTS>
 __global__ __launch_bounds__(kBlock) void stream_nm(StreamArgs a) {
     const int ns = NS >= 0 ? NS : a.nsrc, nd = ND >= 0 ? ND : a.ndst;
+    const uint64_t t_entry = a.rec ? wall_clock64() : 0;
     const uint64_t base = uint64_t(blockIdx.x) * (kBlock * U) + threadIdx.x;
     u32x4 v[U];
 #pragma unroll
@@ -787,6 +790,21 @@ __global__ __launch_bounds__(kBlock) void stream_nm(StreamArgs a) {
             if (v[u][0] == 0x9E3779B9u && v[u][1] == 0x7F4A7C15u && v[u][2] == 0xF39CC060u) *a.sink = v[u];
         } else {
             for (int j = 0; j < nd; ++j) store16<NTS>(reinterpret_cast<char*>(a.dst[j] + i), v[u]);
+        }
+    }
+    if (a.rec) {
+        __builtin_amdgcn_s_waitcnt(0);  // this thread's loads and stores have completed
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint64_t* r = a.rec + kRecPerGroup * (uint64_t(blockIdx.x) + 1);
+            r[0] = xcc_id();
+            r[1] = t_entry;
+            r[2] = t_entry;
+            r[3] = wall_clock64();
+            if (blockIdx.x == 0) {
+                a.rec[0] = a.rate_khz;
+                a.rec[1] = gridDim.x;
+            }
         }
     }
 }
@@ -826,9 +844,23 @@ hipError_t launch_stream_copy(void* dst, const void* src, uint64_t bytes, hipStr
     return hipGetLastError();
 }
 
+uint64_t stream_groups(int nsrc, uint64_t bytes) {
+    const uint64_t per_block = uint64_t(kBlock) * stream_unroll(nsrc);
+    return (bytes / 16 + per_block - 1) / per_block;
+}
+
+uint64_t wall_clock_khz() {
+    int dev = 0, khz = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess) return 0;
+    return khz > 0 ? static_cast<uint64_t>(khz) : 0;
+}
+
 hipError_t launch_stream(void* const* dst, int ndst, const void* const* src, int nsrc, uint64_t bytes, void* sink,
-                         uint32_t hints, hipStream_t stream) {
+                         uint32_t hints, hipStream_t stream, uint64_t* rec) {
     StreamArgs a{};
+    a.rec = rec;
+    a.rate_khz = rec ? wall_clock_khz() : 0;
     for (int p = 0; p < nsrc; ++p) a.src[p] = static_cast<const u32x4*>(src[p]);
     for (int j = 0; j < ndst; ++j) a.dst[j] = static_cast<u32x4*>(dst[j]);
     a.sink = static_cast<u32x4*>(sink);

@@ -10,6 +10,19 @@
 
 namespace purlin {
 
+// Timing records of the measurement entry points (purlin_stream_timed,
+// purlin_pack_timed): entry 0..3 = {wall-clock rate in kHz, workgroups, 0,
+// 0}; then per workgroup b, entries 4(b+1)..: {XCD (the XCC id register),
+// wall clock at entry, wall clock when its metadata was done (its entry for
+// a stream), wall clock once all its stores have completed}.
+constexpr uint64_t kRecPerGroup = 4;
+
+__device__ __forceinline__ uint32_t xcc_id() {
+    uint32_t v;
+    __asm__ volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+    return v & 0xFu;
+}
+
 // Launch one phase: `n` work items starting at device pointer `items`, all
 // of consume op `kind`.  The items of a REDUCE phase all sum the same `nsrc`
 // sources bufs[src_buf + p * src_step].  `bufs` holds the 2P buffer pointers.
@@ -18,7 +31,11 @@ namespace purlin {
 hipError_t launch_stream_copy(void* dst, const void* src, uint64_t bytes, hipStream_t stream);
 // Reference stream: dst_j[i] = XOR_p src_p[i] per 16-byte vector (see purlin_stream).
 hipError_t launch_stream(void* const* dst, int ndst, const void* const* src, int nsrc, uint64_t bytes, void* sink,
-                         uint32_t hints, hipStream_t stream);
+                         uint32_t hints, hipStream_t stream, uint64_t* rec = nullptr);
+// Workgroups of one launch_stream grid.
+uint64_t stream_groups(int nsrc, uint64_t bytes);
+// The wall-clock rate of the current device in kHz (0 if unknown).
+uint64_t wall_clock_khz();
 
 hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uint32_t nsrc, uint32_t src_buf,
                         uint32_t src_step, bool nt_load, bool nt_store, purlin_dtype dtype, void* const* bufs,
@@ -66,7 +83,7 @@ int pack_onepass_tokens(int T, int H, int K, int E);
 hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, const int32_t* ids,
                        uint16_t* packed, int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts,
                        int32_t* expert_offsets, int32_t* pos, int32_t* dev_status, const PackWorkspace& ws,
-                       hipStream_t stream);
+                       hipStream_t stream, uint64_t* rec = nullptr);
 
 // The two halves of launch_pack: the metadata (reads ids; fills the
 // workspace and the count/offset outputs; given the token matrix, also

@@ -431,7 +431,8 @@ __global__ __launch_bounds__(kOneThreads) void pack_onepass(int T, int K, int E,
                                                             int32_t* __restrict__ expert_offsets,
                                                             int32_t* __restrict__ dest_counts,
                                                             int32_t* __restrict__ dest_offsets,
-                                                            int32_t* __restrict__ dev_status) {
+                                                            int32_t* __restrict__ dev_status, uint64_t* rec,
+                                                            uint64_t rate_khz) {
     // Counter copy c holds before[] at [c*S, c*S + E) and after[] at
     // [c*S + E, c*S + 2E); S = 2E + 1 is odd, so one expert's copies lie in
     // different LDS banks.
@@ -443,6 +444,7 @@ __global__ __launch_bounds__(kOneThreads) void pack_onepass(int T, int K, int E,
     __shared__ int32_t wave_tot[kOneThreads / kWave];
     __shared__ int bad_any;
 
+    const uint64_t t_entry = rec ? wall_clock64() : 0;
     const int tid = threadIdx.x;
     const int t0 = static_cast<int>(blockIdx.x) * tw;
     const int nt = min(tw, T - t0);
@@ -561,6 +563,8 @@ __global__ __launch_bounds__(kOneThreads) void pack_onepass(int T, int K, int E,
     }
     __syncthreads();
 
+    const uint64_t t_meta = rec ? wall_clock64() : 0;
+
     // 4. every vector of the rows to its token's K packed rows.  With
     // KMAX > 0 (K <= KMAX) the slots are unrolled, so the code stays
     // straight-line and each vector's stores wait only for that vector.
@@ -606,6 +610,21 @@ __global__ __launch_bounds__(kOneThreads) void pack_onepass(int T, int K, int E,
         }
         const int any = __syncthreads_or(dup || bad_any);
         if (tid == 0) *dev_status = any ? 1 : 0;
+    }
+    if (rec) {
+        __builtin_amdgcn_s_waitcnt(0);  // this thread's stores have completed
+        __syncthreads();
+        if (tid == 0) {
+            uint64_t* r = rec + kRecPerGroup * (uint64_t(blockIdx.x) + 1);
+            r[0] = xcc_id();
+            r[1] = t_entry;
+            r[2] = t_meta;
+            r[3] = wall_clock64();
+            if (blockIdx.x == 0) {
+                rec[0] = rate_khz;
+                rec[1] = gridDim.x;
+            }
+        }
     }
 }
 
@@ -1191,7 +1210,8 @@ int pack_onepass_tokens(int T, int H, int K, int E) {
 
 hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, const int32_t* ids, uint16_t* packed,
                        int32_t* dest_counts, int32_t* dest_offsets, int32_t* expert_counts, int32_t* expert_offsets,
-                       int32_t* pos, int32_t* dev_status, const PackWorkspace& ws, hipStream_t stream) {
+                       int32_t* pos, int32_t* dev_status, const PackWorkspace& ws, hipStream_t stream,
+                       uint64_t* rec) {
     if (const int tw = pack_onepass_tokens(T, H, K, E)) {
         (void)hipGetLastError();
         const uint32_t nvec = static_cast<uint32_t>(static_cast<uint64_t>(H) * 2 / 16);
@@ -1202,7 +1222,8 @@ hipError_t launch_pack(int T, int H, int K, int E, int P, const uint16_t* x, con
         const size_t lds = static_cast<size_t>(copies) * (2 * E + 1) * 4;
         hipLaunchKernelGGL(kernel, dim3((T + tw - 1) / tw), dim3(kOneThreads), lds, stream, T, K, E, P, tw, nvec,
                            copies, reinterpret_cast<const char*>(x), ids, reinterpret_cast<char*>(packed), pos,
-                           expert_counts, expert_offsets, dest_counts, dest_offsets, dev_status);
+                           expert_counts, expert_offsets, dest_counts, dest_offsets, dev_status, rec,
+                           rec ? wall_clock_khz() : 0);
         return hipGetLastError();
     }
     const hipError_t e = launch_pack_meta(T, K, E, P, ids, dest_counts, dest_offsets, expert_counts, expert_offsets,

@@ -124,6 +124,9 @@ def lib():
     L.purlin_ep_combine_dedup.argtypes = [i32] * 3 + [_pa, u64, _vp, _pa, _vp, _vp]
     L.purlin_stream_copy.argtypes = [_vp, _vp, u64, _vp]
     L.purlin_stream.argtypes = [ctypes.POINTER(_vp), i32, ctypes.POINTER(_vp), i32, u64, _vp, u32, _vp]
+    L.purlin_stream_timed.argtypes = [ctypes.POINTER(_vp), i32, ctypes.POINTER(_vp), i32, u64, _vp, u32, _vp, u64,
+                                      _c_u64p, _vp]
+    L.purlin_pack_timed.argtypes = [i32, i32, i32, i32, i32] + [_vp] * 10 + [u64, _c_u64p, _vp]
     L.purlin_status_string.argtypes = [i32]
     L.purlin_status_string.restype = ctypes.c_char_p
     L.purlin_version.argtypes = []
@@ -135,7 +138,7 @@ def lib():
                  "purlin_pack_dedup_workspace_size", "purlin_pack_dedup", "purlin_unpack_dedup",
                  "purlin_ep_dispatch_workspace_size", "purlin_ep_dispatch", "purlin_ep_combine",
                  "purlin_ep_dispatch_dedup_workspace_size", "purlin_ep_dispatch_dedup", "purlin_ep_combine_dedup",
-                 "purlin_stream_copy"):
+                 "purlin_stream_copy", "purlin_stream_timed", "purlin_pack_timed"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -846,6 +849,84 @@ def purlin_stream(dsts, srcs, nbytes=None, sink=None, nt_load=False, nt_store=Fa
     hints = (1 if nt_load else 0) | (2 if nt_store else 0)
     st = lib().purlin_stream(d, len(dsts), s, len(srcs), int(nbytes), _ptr(sink), hints, _stream_handle(stream))
     _check(st, "purlin_stream")
+
+
+def _timed_records(rec, groups):
+    """Host copy of a timing record: (rate_khz, per-workgroup int64 array
+    [groups, 4] of XCD id, entry, metadata done, end in wall-clock ticks)."""
+    import numpy as np
+
+    a = rec[: 4 * (groups + 1)].cpu().numpy().astype(np.int64)
+    return int(a[0]), a[4:].reshape(groups, 4)
+
+
+def xcd_finish_times(rate_khz, per_group):
+    """Per-XCD summary of a timing record: microseconds from the first
+    workgroup's entry to the last completion of each XCD, and the same for
+    the metadata phase (the last workgroup of the XCD to finish it)."""
+    import numpy as np
+
+    t0 = per_group[:, 1].min()
+    us = 1e3 / rate_khz
+    out = {}
+    for k in sorted(set(per_group[:, 0].tolist())):
+        sel = per_group[:, 0] == k
+        out[int(k)] = {"groups": int(sel.sum()), "end_us": float((per_group[sel, 3].max() - t0) * us),
+                       "meta_us": float((per_group[sel, 2].max() - t0) * us)}
+    return out
+
+
+def purlin_stream_timed(dsts, srcs, nbytes=None, sink=None, nt_load=False, nt_store=False, stream=None):
+    """``purlin_stream`` with a timing record per workgroup; returns
+    (rate_khz, records [groups, 4]) after the stream's device work has
+    finished (the call synchronises its stream)."""
+    import torch
+
+    for t in list(dsts) + list(srcs) + ([sink] if sink is not None else []):
+        _require_cuda(t, "stream buffer")
+    if nbytes is None:
+        nbytes = min(t.numel() * t.element_size() for t in list(dsts) + list(srcs))
+    for t in list(dsts) + list(srcs):
+        if t.numel() * t.element_size() < nbytes:
+            raise PurlinError(PURLIN_ERR_INVALID, "a stream buffer is smaller than nbytes")
+    d = (_vp * max(1, len(dsts)))(*[t.data_ptr() for t in dsts])
+    s = (_vp * max(1, len(srcs)))(*[t.data_ptr() for t in srcs])
+    hints = (1 if nt_load else 0) | (2 if nt_store else 0)
+    g = ctypes.c_uint64(0)
+    _check(lib().purlin_stream_timed(d, len(dsts), s, len(srcs), int(nbytes), _ptr(sink), hints, None, 0,
+                                     ctypes.byref(g), None), "purlin_stream_timed")
+    dev = (list(dsts) + list(srcs))[0].device
+    rec = torch.zeros(4 * (g.value + 1), dtype=torch.int64, device=dev)
+    _check(lib().purlin_stream_timed(d, len(dsts), s, len(srcs), int(nbytes), _ptr(sink), hints, _ptr(rec),
+                                     rec.numel(), None, _stream_handle(stream)), "purlin_stream_timed")
+    torch.cuda.synchronize(dev)
+    return _timed_records(rec, g.value)
+
+
+def purlin_pack_timed(x, ids, E, P, out, dev_status=None, rec=None, stream=None):
+    """The one-launch ``purlin_pack`` with a timing record per workgroup, into
+    ``rec`` (a device int64 tensor of at least 4 * (groups + 1) entries, or
+    None to allocate one).  Returns (rec, groups); read it with
+    ``_timed_records(rec, groups)`` once the stream has finished."""
+    import torch
+
+    T, H = x.shape
+    K = ids.shape[1]
+    _require_cuda(x, "x", 2)
+    _require_cuda(ids, "ids", 4)
+    shapes = {"packed": ((T * K, H), x.dtype), "dest_counts": ((P,), torch.int32), "dest_offsets": ((P,), torch.int32),
+              "expert_counts": ((E,), torch.int32), "expert_offsets": ((E,), torch.int32),
+              "pos": ((T, K), torch.int32)}
+    _check_sizes(out, shapes)
+    g = ctypes.c_uint64(0)
+    args = [int(T), int(H), int(K), int(E), int(P), _ptr(x), _ptr(ids), _ptr(out["packed"]), _ptr(out["dest_counts"]),
+            _ptr(out["dest_offsets"]), _ptr(out["expert_counts"]), _ptr(out["expert_offsets"]), _ptr(out["pos"]),
+            _ptr(dev_status)]
+    _check(lib().purlin_pack_timed(*args, None, 0, ctypes.byref(g), None), "purlin_pack_timed")
+    if rec is None:
+        rec = torch.zeros(4 * (g.value + 1), dtype=torch.int64, device=x.device)
+    _check(lib().purlin_pack_timed(*args, _ptr(rec), rec.numel(), None, _stream_handle(stream)), "purlin_pack_timed")
+    return rec, g.value
 
 
 # Short names: plan(...) -> Plan; pack(...) -> (packed, dest_counts,

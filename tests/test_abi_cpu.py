@@ -501,3 +501,20 @@ def test_stream_copy_argument_validation(dst, src, nbytes):
 
 def test_stream_copy_of_nothing_is_a_no_op():
     assert PL.lib().purlin_stream_copy(None, None, 0, None) == 0
+
+
+def test_timed_entry_points_size_queries():
+    """With rec = NULL the timed entry points only report their grid size."""
+    L = PL.lib()
+    g = ctypes.c_uint64(0)
+    # one-launch pack of the bench's shape: 256 workgroups of 16 tokens
+    assert L.purlin_pack_timed(4096, 7168, 8, 256, 8, *([None] * 10), 0, ctypes.byref(g), None) == 0
+    assert g.value == 256
+    assert L.purlin_pack_timed(4100, 1030, 8, 256, 8, *([None] * 10), 0, ctypes.byref(g), None) == UNSUPPORTED
+    assert L.purlin_pack_timed(4096, 7168, 65, 256, 8, *([None] * 10), 0, ctypes.byref(g), None) == INVALID
+    # stream: 256 threads x 4 vectors of 16 bytes per workgroup (2 with 8 or more sources)
+    assert L.purlin_stream_timed(None, 1, None, 1, 1 << 30, None, 0, None, 0, ctypes.byref(g), None) == 0
+    assert g.value == (1 << 30) // (256 * 4 * 16)
+    assert L.purlin_stream_timed(None, 1, None, 8, 1 << 30, None, 0, None, 0, ctypes.byref(g), None) == 0
+    assert g.value == (1 << 30) // (256 * 2 * 16)
+    assert L.purlin_stream_timed(None, 1, None, 1, 17, None, 0, None, 0, ctypes.byref(g), None) == INVALID
