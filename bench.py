@@ -905,6 +905,7 @@ def _xcd_summary(PL, rate, recs):
     fin = PL.xcd_finish_times(rate, recs)
     ends = [fin[k]["end_us"] for k in sorted(fin)]
     return {"span_us": round(max(ends), 2),
+            "xcd_is_group_mod_8": float(np.mean(recs[:, 0] == np.arange(recs.shape[0]) % 8)),
             "xcd_end_us": {str(k): round(fin[k]["end_us"], 2) for k in sorted(fin)},
             "xcd_meta_us": {str(k): round(fin[k]["meta_us"], 2) for k in sorted(fin)},
             "mean_xcd_end_us": round(float(np.mean(ends)), 2),
@@ -955,6 +956,7 @@ def _median_runs(runs):
     """Per-field medians of several _xcd_summary results."""
     m = {k: round(float(np.median([r[k] for r in runs])), 2) for k in ("span_us", "mean_xcd_end_us",
                                                                         "first_to_last_xcd")}
+    m["xcd_is_group_mod_8"] = min(r["xcd_is_group_mod_8"] for r in runs)
     for key in ("xcd_end_us", "xcd_meta_us"):
         m[key] = {x: round(float(np.median([r[key][x] for r in runs])), 2) for x in runs[0][key]}
     m["runs"] = len(runs)
