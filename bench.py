@@ -901,11 +901,19 @@ def measure_in_step_streams(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x,
     return out
 
 
+def _round_robin_fraction(recs):
+    """Fraction of workgroups b on XCD (b + c) % 8 for the dispatch's most
+    common offset c: the hardware deals consecutive workgroups to consecutive
+    XCDs, starting where the previous dispatch stopped."""
+    off = (recs[:, 0] - np.arange(recs.shape[0])) % 8
+    return float(np.bincount(off.astype(np.int64), minlength=8).max() / len(off))
+
+
 def _xcd_summary(PL, rate, recs):
     fin = PL.xcd_finish_times(rate, recs)
     ends = [fin[k]["end_us"] for k in sorted(fin)]
     return {"span_us": round(max(ends), 2),
-            "xcd_is_group_mod_8": float(np.mean(recs[:, 0] == np.arange(recs.shape[0]) % 8)),
+            "xcd_round_robin": _round_robin_fraction(recs),
             "xcd_end_us": {str(k): round(fin[k]["end_us"], 2) for k in sorted(fin)},
             "xcd_meta_us": {str(k): round(fin[k]["meta_us"], 2) for k in sorted(fin)},
             "mean_xcd_end_us": round(float(np.mean(ends)), 2),
@@ -914,8 +922,8 @@ def _xcd_summary(PL, rate, recs):
 
 def measure_xcd_balance(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x, ids, y, g, pack_out, comb_out, T, H,
                         E, K, P, reps=6):
-    """When each of the chip's XCDs (accelerator dies; workgroup b runs on XCD
-    b % 8) finishes its share of the pack, in the pack's place in the step
+    """When each of the chip's XCDs (accelerator dies, dealt consecutive
+    workgroups round-robin) finishes its share of the pack, in the pack's place in the step
     (after the same ReduceScatter and AllGather; the one-launch pack with its
     timing record, purlin_pack_timed), and of plain streams of the pack's and
     the combine's access mix of the same size run back to back.  Each
@@ -956,7 +964,7 @@ def _median_runs(runs):
     """Per-field medians of several _xcd_summary results."""
     m = {k: round(float(np.median([r[k] for r in runs])), 2) for k in ("span_us", "mean_xcd_end_us",
                                                                         "first_to_last_xcd")}
-    m["xcd_is_group_mod_8"] = min(r["xcd_is_group_mod_8"] for r in runs)
+    m["xcd_round_robin"] = min(r["xcd_round_robin"] for r in runs)
     for key in ("xcd_end_us", "xcd_meta_us"):
         m[key] = {x: round(float(np.median([r[key][x] for r in runs])), 2) for x in runs[0][key]}
     m["runs"] = len(runs)

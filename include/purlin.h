@@ -642,8 +642,9 @@ PURLIN_API purlin_status purlin_stream(void* const* dst, int ndst, const void* c
 
 /* Measurement entry points: purlin_stream and the one-launch purlin_pack,
  * each also recording when every workgroup ran and on which XCD (the
- * chip's accelerator dies; the hardware hands workgroup b to XCD b % 8), so
- * that a kernel's time can be split into its dies' finishing times.  Not
+ * chip's accelerator dies, which the hardware deals consecutive workgroups
+ * to round-robin), so that a kernel's time can be split into its dies'
+ * finishing times.  Not
  * steps of the method.  `rec` (device, 16-byte aligned, rec_entries
  * uint64 entries, at least 4 * (groups + 1)) receives
  *   rec[0] = the wall-clock rate in kHz, rec[1] = groups,
