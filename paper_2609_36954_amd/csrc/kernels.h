@@ -43,9 +43,13 @@ hipError_t launch_phase(const purlin_desc* items, uint64_t n, uint32_t kind, uin
 
 // Device state of a single-launch AllReduce plan (zeroed at plan creation).
 struct FusedState {
-    uint64_t tickets;  // items claimed over all launches: launch e's waves take [e*n, (e+1)*n)
-    uint32_t error;    // set if a wait gave up (bounded spin)
-    uint32_t pad[5];
+    // Items claimed over all launches, one counter per partition of the
+    // waves (workgroup index mod 8), each on its own 128-byte line: the
+    // waves of partition k claim the items of partition k, nk per launch,
+    // so launch e's tickets of counter k are [e*nk, (e+1)*nk).
+    uint64_t tickets[8 * 16];
+    uint32_t error;  // set if a wait gave up (bounded spin)
+    uint32_t pad[31];
 };
 
 // One launch for a whole AllReduce: items [0, n_reduce) reduce partition k

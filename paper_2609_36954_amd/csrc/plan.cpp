@@ -112,15 +112,15 @@ uint64_t auto_item_bytes(uint64_t phase_bytes, uint64_t traffic, uint32_t kind, 
 }
 
 // Work-item size of a single-launch AllReduce (both of its phases): a
-// quarter of a chunk, so a chunk is published by four reduce items.  Every
-// item pays an agent-scope release (reduce) or acquire (copy), which writes
-// back or invalidates an L2; measured on MI355X (P = 8, bf16), a quarter
-// chunk was fastest: 44.5 µs with 16 KiB items vs 73.4 µs with whole 64 KiB
-// chunks and 244 µs with the streaming sizes at 128 x 8192 per rank;
-// 1160 µs with 256 KiB items vs 1360 µs with whole 1 MiB chunks and 3785 µs
-// at 256 MiB per rank.
+// quarter of a chunk, at most 32 KiB.  Every item claims a ticket, and a
+// reduced chunk is published to its copies with write-through stores and a
+// counter; measured on MI355X (P = 8, bf16), per call: at 256 MiB per rank
+// 810 µs with 32 KiB items, 833 µs with 4 KiB and 1090 µs with quarter
+// chunks of 256 KiB; at 128 x 8192 per rank (64 KiB chunks) 22.7 µs with
+// quarter chunks, 26 µs with 4 KiB and 34 µs with 32 KiB items.
+constexpr uint64_t kFusedMaxItem = 32 * 1024;
 uint64_t fused_item_bytes(uint64_t chunk, uint64_t phase_bytes) {
-    uint64_t item = std::max<uint64_t>(16, chunk / 4 / 16 * 16);
+    uint64_t item = std::max<uint64_t>(16, std::min(kFusedMaxItem, chunk / 4) / 16 * 16);
     const uint64_t floor_for_cap = ceil_div(phase_bytes, PURLIN_MAX_ITEMS / 2);
     if (item < floor_for_cap) item = ceil_div(floor_for_cap, 16) * 16;
     return item;

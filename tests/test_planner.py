@@ -357,6 +357,67 @@ def test_fused_allreduce_claim_order(case):
         assert np.array_equal(got, want[r].view(got.dtype))
 
 
+def _partition_of(i):
+    """The kernel's partition of item (or wave) i: its workgroup of 4 waves, mod 8."""
+    return (i // 4) % 8
+
+
+@pytest.mark.parametrize("n", [1, 3, 4, 5, 31, 32, 33, 64, 100, 1000, 4099])
+def test_fused_partition_sizes_and_ticket_to_item_map(n):
+    """Partition k holds nk = 4 * (n // 32) + min(max(n % 32 - 4k, 0), 4)
+    items, as many as it has waves, and the j-th ticket of partition k names
+    its j-th item in table order: ((j // 4) * 8 + k) * 4 + j % 4."""
+    for k in range(8):
+        items = [i for i in range(n) if _partition_of(i) == k]
+        nk = 4 * (n // 32) + min(max(n % 32 - 4 * k, 0), 4)
+        assert len(items) == nk
+        assert [((j // 4) * 8 + k) * 4 + j % 4 for j in range(nk)] == items
+
+
+@pytest.mark.parametrize("case", FUSED_CASES[::3], ids=lambda c: "-".join(map(str, c)))
+def test_fused_allreduce_partitioned_claims_never_deadlock(case):
+    """The waves of each of the 8 partitions claim that partition's items in
+    table order.  Run the partitions round-robin, a copy item blocking its
+    partition until every reduce item of its chunk has run: some partition
+    can always move (no deadlock), and the result is the oracle's."""
+    P, M, dtype, chunk_elems, item = case
+    s = S[dtype]
+    plan = host_plan("allreduce", P, P * M, dtype, chunk_elems * s, ar_mode=3, fanout=2, item_bytes=item)
+    items, pb = plan.items()
+    n, n_reduce = len(items), int(pb[1])
+    need = {}
+    for it in items[:n_reduce]:
+        key = (int(it["part"]), int(it["chunk"]))
+        need[key] = need.get(key, 0) + 1
+    queues = [[i for i in range(n) if _partition_of(i) == k] for k in range(8)]
+    for q in queues:  # within a partition every reduce item precedes every copy item
+        kinds = [int(items[i]["kind"]) for i in q]
+        assert kinds == sorted(kinds, key=lambda kd: kd != PL.KIND_REDUCE)
+    ins = _inputs(P, P * M, dtype, seed=P + M + 1)
+    want = oracle.all_reduce(ins, dtype)
+    bufs = [np.frombuffer(a.tobytes(), np.uint8).copy() for a in ins] + [np.zeros(plan.out_bytes, np.uint8) for _ in range(P)]
+    done = {}
+    heads = [0] * 8
+    while any(heads[k] < len(queues[k]) for k in range(8)):
+        moved = False
+        for k in range(8):
+            if heads[k] == len(queues[k]):
+                continue
+            it = items[queues[k][heads[k]]]
+            key = (int(it["part"]), int(it["chunk"]))
+            if it["kind"] != PL.KIND_REDUCE and done.get(key, 0) < need[key]:
+                continue  # waits for its chunk
+            interp.apply_item(it, bufs, dtype)
+            if it["kind"] == PL.KIND_REDUCE:
+                done[key] = done.get(key, 0) + 1
+            heads[k] += 1
+            moved = True
+        assert moved, "every partition waits"
+    for r in range(P):
+        got = bufs[P + r].view(np.uint16 if dtype == "bf16" else np.uint32)
+        assert np.array_equal(got, want[r].view(got.dtype))
+
+
 # ---------------------------------------------------------------------------
 # automatic work-item sizes by regime (P = 8, bf16, chunk 1 MiB)
 # ---------------------------------------------------------------------------
