@@ -49,8 +49,18 @@ def run_pack_dedup(x_np, ids_np, E, P):
     (200, 1000, 6, 96, 16, 6),
     (100, 64, 8, 8, 8, 7),  # E = P: nothing to de-duplicate
     (129, 64, 1, 32, 4, 8),  # K = 1
+    # K of 4 to 64, P = 16, larger shapes
+    (1, 8, 4, 4, 2, 9),
+    (2047, 48, 16, 64, 16, 10),  # K = 16, P = 16
+    (512, 16, 64, 64, 16, 11),  # K = 64
+    (8192, 16, 4, 64, 16, 12),
+    (4700, 7168, 4, 256, 8, 13),  # 64 MiB token matrix
+    (300, 520, 8, 64, 4, 14),
+    (1000, 64, 32, 128, 8, 15),  # K = 32
+    (64, 128, 8, 8, 8, 16),  # E = P
 ])
 def test_pack_dedup_matches_oracle(T, H, K, E, P, seed):
+    print(f"pack_dedup T={T} H={H} K={K} E={E} P={P}", flush=True)
     rng = np.random.default_rng(seed)
     x = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
     ids = _distinct_ids(rng, T, K, E)
@@ -84,6 +94,41 @@ def test_pack_dedup_flags_bad_routing_and_stays_in_bounds():
     ids[10, 0] = -1
     _, status = run_pack_dedup(rng.integers(0, 0x10000, (T, H)).astype(np.uint16), ids, E, P)
     assert status == 1
+
+
+@pytest.mark.parametrize("T,K,E,P", [(70, 4, 8, 4), (4096, 8, 256, 8)])
+def test_pack_dedup_flags_bad_routing_and_ignores_bad_ids(T, K, E, P):
+    """Out-of-range ids (positive, negative) are ignored and flagged, a
+    repeated id is flagged; the destination sets (and so every output) are
+    those of the ids with the bad ones left out."""
+    H = 16
+    rng = np.random.default_rng(T + K)
+    ids = _distinct_ids(rng, T, K, E)
+    x = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
+    bad = ids.copy()
+    bad[5, 1] = E + 3
+    bad[10, 0] = -1
+    bad[T - 1, 2] = bad[T - 1, 0]  # repeated in the last token: the same set
+    got, status = run_pack_dedup(x, bad, E, P)
+    assert status == 1
+    # the same destination sets without the bad ids: drop them, pad with a kept id of the token
+    L = E // P
+    want_sets = [set(int(e) // L for e in row if 0 <= e < E) for row in bad]
+    counts = np.zeros(P, np.int64)
+    row_of = np.full((T, P), -1, np.int64)
+    for r in range(P):
+        for t in range(T):
+            if r in want_sets[t]:
+                row_of[t, r] = counts[r]
+                counts[r] += 1
+    offs = np.concatenate([[0], np.cumsum(counts)[:-1]])
+    row_of = np.where(row_of >= 0, row_of + offs[None, :], -1)
+    assert np.array_equal(got["dest_counts"], counts)
+    assert np.array_equal(got["row_of"], row_of)
+    for t in (0, 5, 10, T - 1):
+        for r in range(P):
+            if row_of[t, r] >= 0:
+                assert np.array_equal(got["packed"][row_of[t, r]], x[t])
 
 
 def run_unpack_dedup(y_np, row_of_np):
