@@ -738,7 +738,42 @@ def measure_bandwidth_sweep(torch, PL, P=8, reps=5):
             row[f"{mib}MiB"] = {"us": round(us, 1), "GBps": round(b / (us * 1e-6) / 1e9, 1),
                                 "algbw_GBps": round(n * s / (us * 1e-6) / 1e9, 1)}
         out[op] = row
-    del ins, outs
+        log(f"bandwidth sweep: {op} done")
+    # The same calls on fresh buffers.  Above, every call reuses the buffers
+    # of the call before, and at 256 MiB/rank the smaller side of a
+    # ReduceScatter or AllGather (its output or its input, 256 MiB in all)
+    # is then partly still in the 256 MB last-level cache.  Here the calls
+    # rotate over four sets of that side and two of the full-size outputs.
+    small = [[torch.empty(big // P, dtype=torch.int16, device="cuda").fill_(0x3F80) for _ in range(P)]
+             for _ in range(4)]
+    outs2 = [torch.empty(big, dtype=torch.int16, device="cuda") for _ in range(P)]
+    cold = {}
+    for op in ("allreduce", "reduce_scatter", "allgather", "alltoall"):
+        row = {}
+        for mib in (256, 1024):
+            n = (mib << 20) // s
+            runs = []
+            for j in range(4):
+                sm = [t[: n // P] for t in small[j]]
+                full_out = [t[:n] for t in (outs if j % 2 == 0 else outs2)]
+                i = sm if op == "allgather" else [t[:n] for t in ins]
+                o = sm if op == "reduce_scatter" else full_out
+                runs.append(PL.Plan(op, P, n, "bf16", 1 << 20).bind(i, o))
+            runs[0]()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for r in range(2 * len(runs)):
+                runs[r % len(runs)]()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / (2 * len(runs))
+            b = collective_bytes(op, P, n, s)
+            row[f"{mib}MiB"] = {"us": round(us, 1), "GBps": round(b / (us * 1e-6) / 1e9, 1)}
+        cold[op] = row
+        log(f"bandwidth sweep, fresh buffers: {op} done")
+    out["fresh_buffers"] = cold
+    del ins, outs, outs2, small
     torch.cuda.empty_cache()
     return out
 

@@ -480,11 +480,19 @@ purlin_status cut_items(Plan& out, const purlin_policy& pol) {
         // than the 256 MB last-level cache gains from non-temporal
         // accesses; which side gains was measured on MI355X: reads for
         // many-to-one (reduce), writes for one-to-many (multi-destination
-        // copy), both for one-to-one copies.  Phases whose traffic fits
-        // the cache keep cached accesses so repeated calls hit it.
-        uint64_t traffic = 0, max_ndst = 0;
+        // copy), both for one-to-one copies.  A reduce also writes
+        // non-temporally once its output is larger than that cache: the
+        // output can no longer stay there for a next reader, and cached
+        // stores of it run slower (P = 8, bf16, fresh output buffers: 1 GiB
+        // per rank 72.2% of 8 TB/s against 68.7%, one-phase AllReduce 68.8
+        // against 65.9%; at 256 MiB per rank the ReduceScatter's output
+        // stays cached for the AllGather that reads it).  Phases whose
+        // traffic fits the cache keep cached accesses so repeated calls hit
+        // it.
+        uint64_t traffic = 0, written = 0, max_ndst = 0;
         for (uint64_t i = phase.begin; i < out.items.size(); ++i) {
             traffic += (uint64_t(out.items[i].nsrc) + out.items[i].ndst) * out.items[i].bytes;
+            written += uint64_t(out.items[i].ndst) * out.items[i].bytes;
             max_ndst = std::max<uint64_t>(max_ndst, out.items[i].ndst);
         }
         const bool streaming = traffic >= kStreamingBytes;
@@ -492,6 +500,7 @@ purlin_status cut_items(Plan& out, const purlin_policy& pol) {
         if (streaming) {
             if (phase.kind == PURLIN_KIND_REDUCE) {
                 auto_nt_load = true;
+                auto_nt_store = written > kLastLevelCacheBytes;
             } else if (max_ndst > 1) {
                 auto_nt_store = true;
             } else {
@@ -507,9 +516,6 @@ purlin_status cut_items(Plan& out, const purlin_policy& pol) {
             // launch latency and larger ones gain nothing.  Loads stay
             // cached.  (Variable-size launches tie both hints together and
             // keep the cached form here.)
-            uint64_t written = 0;
-            for (uint64_t i = phase.begin; i < out.items.size(); ++i)
-                written += uint64_t(out.items[i].ndst) * out.items[i].bytes;
             auto_nt_store = written >= kLatencyNtStoreMin && written <= kLatencyNtStoreMax;
         }
         phase.nt_load = pol.load_hint ? pol.load_hint == 2 : auto_nt_load;
