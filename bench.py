@@ -773,6 +773,33 @@ def measure_bandwidth_sweep(torch, PL, P=8, reps=5):
         cold[op] = row
         log(f"bandwidth sweep, fresh buffers: {op} done")
     out["fresh_buffers"] = cold
+    # Reference streams of the same access mixes at 1 GiB per buffer (the
+    # best of the four load/store hint pairs): what each mix reaches at that
+    # size without descriptors.
+    G = big * s
+    mixes = {}
+    for name, d, src in (("8_to_8", outs, ins), ("1_to_8", outs, ins[:1]), ("8_to_1", outs[:1], ins),
+                         ("1_to_1", outs[:1], ins[:1])):
+        best = None
+        for ntl in (False, True):
+            for nts in (False, True):
+                fn = lambda: PL.purlin_stream(d, src, nbytes=G, nt_load=ntl, nt_store=nts)
+                fn()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(3):
+                    fn()
+                e1.record()
+                torch.cuda.synchronize()
+                us = e0.elapsed_time(e1) * 1e3 / 3
+                if best is None or us < best[0]:
+                    best = (us, ntl, nts)
+        us, ntl, nts = best
+        mixes[name] = {"us": round(us, 1), "GBps": round((len(d) + len(src)) * G / (us * 1e-6) / 1e9, 1),
+                       "hints": f"{'nt' if ntl else 'cached'} loads {'nt' if nts else 'cached'} stores"}
+    out["stream_ceilings_1GiB"] = mixes
+    log("bandwidth sweep: 1 GiB reference streams done")
     del ins, outs, outs2, small
     torch.cuda.empty_cache()
     return out

@@ -135,7 +135,12 @@ typedef struct purlin_policy {
                             phases of 1 in one launch: a chunk's copies start
                             when its reduction has finished (per-chunk
                             counters with epochs, Section 3.2 and 4.2; such a
-                            plan must not run concurrently with itself)     */
+                            plan must not run concurrently with itself).
+                            Mode 3 demonstrates the in-kernel notify/consume:
+                            it is never chosen automatically and measured
+                            slower than mode 1 at every size on MI355X
+                            (P = 8, bf16: 1.08x its time at 256 MiB per
+                            rank, 1.4x at 32 MiB, 2.8x at 2 MiB). */
     uint32_t load_hint;  /* global loads:  0 auto, 1 cached, 2 non-temporal */
     uint32_t store_hint; /* global stores: 0 auto, 1 cached, 2 non-temporal
                             (variable-size plans apply one setting to loads

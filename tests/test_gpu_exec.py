@@ -341,6 +341,41 @@ def test_offsets_beyond_4GiB_per_rank():
     assert torch.equal(outs[1], outs[0])
 
 
+def test_collectives_at_1GiB_per_rank():
+    """P = 8, bf16, 1 GiB per rank, chunk 1 MiB: the bandwidth sweep's
+    largest calls, in the launch shapes it times (the reduces' outputs are
+    larger than the last-level cache and written non-temporally).  Inputs are
+    drawn on the device with a seeded torch generator; sampled elements of
+    every ReduceScatter and AllReduce output are checked against the oracle,
+    and RS then AG must equal the AllReduce bit for bit on every rank."""
+    P, N = 8, (1 << 30) // 2
+    M = N // P
+    g = torch.Generator(device="cuda").manual_seed(57)
+    ins = [(torch.randn(N, device="cuda", generator=g) * 0.02).to(torch.bfloat16).view(torch.int16) for _ in range(P)]
+    rs_out = [torch.empty(M, dtype=torch.int16, device="cuda") for _ in range(P)]
+    ar_out = [torch.empty(N, dtype=torch.int16, device="cuda") for _ in range(P)]
+    PL.Plan("reduce_scatter", P, N, "bf16", 1 << 20).exec(ins, rs_out)
+    PL.Plan("allreduce", P, N, "bf16", 1 << 20).exec(ins, ar_out)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(58)
+    # random elements, both ends, and both sides of every partition boundary
+    edges = ((np.arange(1, P) * M)[:, None] + np.arange(-64, 64)[None, :]).ravel()
+    idx = np.unique(np.concatenate([rng.integers(0, N, 1 << 17), np.arange(4096), np.arange(N - 4096, N), edges]))
+    idx_t = torch.from_numpy(idx).to("cuda")
+    sample = [to_host(t[idx_t], np.uint16) for t in ins]
+    want = oracle.all_reduce([np.concatenate([x, np.zeros((-len(x)) % P, np.uint16)]) for x in sample], "bf16")[0][: len(idx)]
+    rs_cat = torch.cat(rs_out)
+    assert_bits_equal(to_host(rs_cat[idx_t], np.uint16), want, "bf16", "ReduceScatter, 1 GiB/rank, sampled")
+    for r in range(P):
+        assert_bits_equal(to_host(ar_out[r][idx_t], np.uint16), want, "bf16", f"AllReduce rank {r}, 1 GiB/rank, sampled")
+    del ins, rs_cat
+    ag_out = [torch.empty(N, dtype=torch.int16, device="cuda") for _ in range(P)]
+    PL.Plan("allgather", P, N, "bf16", 1 << 20).exec(rs_out, ag_out)
+    torch.cuda.synchronize()
+    for r in range(P):
+        assert torch.equal(ag_out[r], ar_out[r]), f"RS then AG differs from AR at rank {r}, 1 GiB/rank"
+
+
 def test_plans_run_concurrently_on_two_streams():
     """A plan is immutable: executions on different streams with distinct
     buffers may overlap (AllReduce on one stream, AllToAll and AllGather on
