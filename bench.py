@@ -415,6 +415,10 @@ def main():
     in_step = measure_in_step_streams(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x, y, pack_out["packed"],
                                       comb_out, T, H, K, per_op, args.steps)
 
+    # ---------------- the pack's status word (repeated and out-of-range ids) ----------------
+    in_step["pack_status_word"] = measure_pack_status_in_step(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x, ids,
+                                                              y, g, pack_out, comb_out, ws, E, P, args.steps)
+
     # ---------------- how the chip's dies share the pack's time ----------------
     in_step["xcd_balance"] = measure_xcd_balance(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x, ids, y, g,
                                                  pack_out, comb_out, T, H, E, K, P)
@@ -960,6 +964,32 @@ def measure_in_step_streams(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x,
                      "GBps": round(moved / (us * 1e-6) / 1e9, 1),
                      "frac_of_hbm_peak": round(moved / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
                      "op_avg_us": op["avg_us"], "op_over_stream": round(op["avg_us"] / us, 4)}
+    return out
+
+
+def measure_pack_status_in_step(torch, PL, rs_plan, ag_plan, ins, rs_out, ag_out, x, ids, y, g, pack_out, comb_out,
+                                ws, E, P, steps):
+    """The pack in its step place with and without the status word
+    (dev_status: every token checked for repeated ids, every id for range),
+    alternating step by step, events around the pack only."""
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    ts = {False: [], True: []}
+    for i in range(2 * steps + 2):
+        with_status = bool(i % 2)
+        ev = [TimingEvent(torch) for _ in range(2)]
+        rs_plan.exec(ins, rs_out)
+        ag_plan.exec(rs_out, ag_out)
+        ev[0].record()
+        PL.purlin_pack(x, ids, E, P, out=pack_out, workspace=ws, dev_status=st if with_status else None)
+        ev[1].record()
+        PL.purlin_unpack(y, pack_out["pos"], g, out=comb_out)
+        torch.cuda.synchronize()
+        if i >= 2:  # one untimed pass of each first
+            ts[with_status].append(ev[0].elapsed_time(ev[1]) * 1e3)
+    out = {name: {"avg_us": round(float(np.mean(ts[k])), 2), "median_us": round(float(np.median(ts[k])), 2)}
+           for name, k in (("without_status", False), ("with_status", True))}
+    out["status"] = int(st.item())
+    out["cost_us"] = round(out["with_status"]["avg_us"] - out["without_status"]["avg_us"], 2)
     return out
 
 

@@ -408,9 +408,10 @@ __global__ __launch_bounds__(kBlock) void pack_rows(int T, int H, int K, int E, 
 //      of its own (t, k): offset[e] + before[e] + earlier own tokens of e;
 //   4. it writes each vector of its rows to the K packed rows of its token,
 //      each as soon as that vector has arrived.
-// Workgroup 0 also writes the counts and offsets and, after its rows, checks
-// every token for repeated ids and writes the status word (it has seen every
-// id, so it knows of out-of-range ones).  Ranks follow from counts, so the
+// Workgroup 0 also writes the counts and offsets, checks every token for
+// repeated ids (before its stores, whose queue its loads would otherwise
+// wait behind; after them for K > 8) and writes the status word (it has seen
+// every id, so it knows of out-of-range ones).  Ranks follow from counts, so the
 // result is the same whatever the order of the LDS atomics.
 constexpr int kOneThreads = 1024;
 constexpr int kOneVec = 16;                               // x vectors per thread: 64 VGPRs
@@ -421,6 +422,35 @@ constexpr int kOneMaxOwn = kOneThreads;                  // own (t, k) pairs: on
 constexpr int kOneUnrolledSlots = 8;                     // K up to this: the store loop unrolled
 constexpr int kOneMaxCopies = 16;                        // counter copies (lanes modulo)
 constexpr uint32_t kOneCopyBytes = 40u << 10;            // LDS for the counter copies (64 KiB in all)
+
+constexpr int kDupTokens = 4;  // tokens per thread and round of the repeated-id check
+
+// The ids of tokens t, t + kOneThreads, ... (kDupTokens of them, indexes
+// clamped to the last token) into registers, all loads issued together.
+template <int KMAX>
+__device__ __forceinline__ void load_token_ids(int (&e)[kDupTokens][KMAX], const int32_t* __restrict__ ids, int T,
+                                               int K, int t) {
+#pragma unroll
+    for (int i = 0; i < kDupTokens; ++i) {
+        const int32_t* row = ids + static_cast<int64_t>(min(t + i * kOneThreads, T - 1)) * K;
+#pragma unroll
+        for (int k = 0; k < KMAX; ++k) e[i][k] = k < K ? row[k] : 0;
+    }
+}
+
+// Whether any of those tokens holds an id twice among its K slots.
+template <int KMAX>
+__device__ __forceinline__ bool repeated_id(const int (&e)[kDupTokens][KMAX], int K) {
+    bool dup = false;
+#pragma unroll
+    for (int i = 0; i < kDupTokens; ++i)
+#pragma unroll
+        for (int k = 1; k < KMAX; ++k)
+#pragma unroll
+            for (int k2 = 0; k2 < k; ++k2)
+                if (k < K && e[i][k] == e[i][k2]) dup = true;
+    return dup;
+}
 
 template <int KMAX, bool NTL, bool NTS>
 __global__ __launch_bounds__(kOneThreads) void pack_onepass(int T, int K, int E, int P, int tw, uint32_t nvec,
@@ -467,6 +497,15 @@ __global__ __launch_bounds__(kOneThreads) void pack_onepass(int T, int K, int E,
     const int tail = n - 4 * n4;
     const int tail_e = ids[min(4 * n4 + tid, n - 1)];
     const int own_e = ids[first + min(tid, nown - 1)];
+    // Workgroup 0 checks every token for repeated ids (the status word).
+    // With K <= KMAX the ids of a thread's first kDupTokens tokens are
+    // loaded here, with the others, so that they arrive before any store is
+    // queued behind which they would wait (later rounds, T > 4096, are
+    // loaded after the counting, still before the stores).
+    const bool dup_check = blockIdx.x == 0 && dev_status != nullptr && K > 1;
+    int dupv[kDupTokens][KMAX > 0 ? KMAX : 1];
+    if constexpr (KMAX > 0)
+        if (dup_check) load_token_ids<KMAX>(dupv, ids, T, K, tid);
     for (int i = tid; i < copies * S; i += kOneThreads) hist[i] = 0;
     for (int e = tid; e < E; e += kOneThreads) masks[e] = 0ull;
     if (tid == 0) bad_any = 0;
@@ -500,6 +539,15 @@ __global__ __launch_bounds__(kOneThreads) void pack_onepass(int T, int K, int E,
     if (own_ok) {
         const unsigned long long bit = 1ull << tl;
         if (atomicOr(&masks[own_e], bit) & bit) bad = true;  // repeated within the token
+    }
+    if constexpr (KMAX > 0) {
+        if (dup_check) {
+            if (repeated_id<KMAX>(dupv, K)) bad = true;
+            for (int tb = tid + kDupTokens * kOneThreads; tb < T; tb += kDupTokens * kOneThreads) {
+                load_token_ids<KMAX>(dupv, ids, T, K, tb);
+                if (repeated_id<KMAX>(dupv, K)) bad = true;
+            }
+        }
     }
     // the rows: issued after the counting in program order (a wave whose
     // loads cannot all issue at once would otherwise stall the counting
@@ -597,15 +645,19 @@ __global__ __launch_bounds__(kOneThreads) void pack_onepass(int T, int K, int E,
         }
     }
 
-    // workgroup 0: ids repeated within any token, then the status word
+    // workgroup 0: the status word.  With K <= KMAX its repeated-id check
+    // ran before the stores (above); for larger K every token's row is
+    // checked here, after the workgroup's rows.
     if (blockIdx.x == 0 && dev_status) {
         bool dup = false;
-        for (int t = tid; t < T; t += kOneThreads) {
-            const int32_t* row = ids + static_cast<int64_t>(t) * K;
-            for (int k = 1; k < K; ++k) {
-                const int e = row[k];
-                for (int k2 = 0; k2 < k; ++k2)
-                    if (row[k2] == e) dup = true;
+        if constexpr (KMAX == 0) {
+            for (int t = tid; t < T; t += kOneThreads) {
+                const int32_t* row = ids + static_cast<int64_t>(t) * K;
+                for (int k = 1; k < K; ++k) {
+                    const int e = row[k];
+                    for (int k2 = 0; k2 < k; ++k2)
+                        if (row[k2] == e) dup = true;
+                }
             }
         }
         const int any = __syncthreads_or(dup || bad_any);

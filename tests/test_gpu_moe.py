@@ -127,6 +127,29 @@ def test_pack_reports_bad_routing(T, E):
     assert status == 0
 
 
+@pytest.mark.parametrize("T,K,E", [(4096, 8, 256), (500, 6, 64), (2000, 3, 16), (8192, 4, 64), (300, 12, 64)])
+def test_pack_one_launch_reports_repeated_ids(T, K, E):
+    """The one-launch form checks every token for repeated ids (loaded a
+    round of tokens at a time for K <= 8, a plain loop above): a repeat in
+    any slot pair of any token, including the first and last token and
+    tokens on either side of a round, sets the status word; distinct ids
+    leave it 0."""
+    H, P = 8, 4
+    assert PL.purlin_pack_single_launch(T, H, K, E)
+    rng = np.random.default_rng(1000 + T + K)
+    x = rng.integers(0, 0x10000, (T, H)).astype(np.uint16)
+    ids = _distinct_ids(rng, T, K, E)
+    _, status = run_pack(x, ids, E, P)
+    assert status == 0
+    cases = [(0, 1, 0), (T // 2, K - 1, 0), (T - 1, K - 1, K - 2), (min(T - 1, 4095), K - 1, 1), (min(T - 1, 4096), 1, 0)]
+    for t, k, k2 in cases:
+        rep = ids.copy()
+        rep[t, k] = rep[t, k2]
+        print(f"repeat at token {t}: slot {k} = slot {k2}", flush=True)
+        _, status = run_pack(x, rep, E, P)
+        assert status == 1
+
+
 @pytest.mark.parametrize("T,H,K,E,P,seed", [(4096, 512, 8, 256, 8, 21), (333, 1000, 6, 120, 4, 22), (0, 64, 8, 256, 8, 23)])
 def test_pack_split_on_two_streams_matches_pack(T, H, K, E, P, seed):
     """purlin_pack_meta on a side stream, an event, purlin_pack_rows on the
