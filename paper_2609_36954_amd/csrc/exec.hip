@@ -540,11 +540,21 @@ __device__ __forceinline__ uint64_t active_items(const VGrid& g, uint64_t extent
     return min(g.per_space, (o / g.chunk) * g.per_chunk + (o % g.chunk) / g.item + 1);
 }
 
+// The first item of wave w is item w (when the run-time sizes make it
+// active): its descriptor is loaded before the sizes are known, so that the
+// wave's data loads wait on one memory round trip, not two.
+__device__ __forceinline__ purlin_desc first_item(const ExecArgs& a, uint32_t w) {
+    purlin_desc d{};
+    if (w < a.n_items) d = a.items[w];
+    return d;
+}
+
 template <bool STREAM>
 __global__ __launch_bounds__(kBlock) void exec_allgatherv(ExecArgs a, VArgs v, VGrid g) {
     const uint32_t w = wave_index();
     if (w >= g.waves) return;
     const uint32_t lane = lane_index();
+    const purlin_desc d0 = first_item(a, w);
     int64_t c;
     const bool ok = load_counts(v, lane, static_cast<int64_t>(v.in_cap), static_cast<int64_t>(v.out_cap), c);
     report(v, w, lane, ok);
@@ -554,7 +564,7 @@ __global__ __launch_bounds__(kBlock) void exec_allgatherv(ExecArgs a, VArgs v, V
     for (uint32_t p = 0; p < v.P; ++p) total += readlane64(c, p);
     const uint64_t n = active_items(g, uint64_t(total) * s);
     for (uint64_t i = w; i < n; i += g.waves) {
-        const purlin_desc d = a.items[i];
+        const purlin_desc d = i == w ? d0 : a.items[i];
         const int64_t lo_v = static_cast<int64_t>(d.src_off / s), hi_v = lo_v + static_cast<int64_t>(d.bytes / s);
         int64_t off = 0;
         for (uint32_t p = 0; p < v.P; ++p) {
@@ -581,6 +591,7 @@ __global__ __launch_bounds__(kBlock) void exec_reducescatterv(ExecArgs a, VArgs 
     const uint32_t w = wave_index();
     if (w >= g.waves) return;
     const uint32_t lane = lane_index();
+    const purlin_desc d0 = first_item(a, w);
     int64_t c;
     const bool ok = load_counts(v, lane, static_cast<int64_t>(v.out_cap), static_cast<int64_t>(v.in_cap), c);
     report(v, w, lane, ok);
@@ -590,7 +601,7 @@ __global__ __launch_bounds__(kBlock) void exec_reducescatterv(ExecArgs a, VArgs 
     for (uint32_t r = 0; r < v.P; ++r) total += readlane64(c, r);
     const uint64_t n = active_items(g, uint64_t(total) * s);
     for (uint64_t i = w; i < n; i += g.waves) {
-        const purlin_desc d = a.items[i];
+        const purlin_desc d = i == w ? d0 : a.items[i];
         const int64_t lo_v = static_cast<int64_t>(d.src_off / s), hi_v = lo_v + static_cast<int64_t>(d.bytes / s);
         int64_t off = 0;
         for (uint32_t r = 0; r < v.P; ++r) {
